@@ -1,0 +1,206 @@
+/*
+ * oscars.h - C ABI of the Oscars local-SGD hot path on one MI355X (gfx950).
+ *
+ * The method (Huang, "Oscars: Adaptive Semi-Synchronous Parallel Model for
+ * Distributed Deep Learning with Global View", arXiv 2102.08550):
+ *   - Problem Formulation, Eq. 1-3: a common barrier T and per-worker local
+ *     step counts tau_i = floor(T / t_i^iter) chosen to minimise the largest
+ *     idle time max_i mod(T, t_i^iter) under a bound M on the step spread;
+ *   - Approach, Algorithm 1 (Load-Balance): the scan that finds T*;
+ *   - Approach, Eq. 4: each worker runs tau_i local SGD steps
+ *     x <- x - eta g(x); at its tau_i-th step the models of all N workers are
+ *     averaged with weight 1/N and every worker continues from the average.
+ *
+ * Here the N workers are K simulated replicas that live side by side in one
+ * GPU's memory; the parameter server's aggregation is a K-way reduction kernel.
+ *
+ * Conventions for every function:
+ *   - returns an oscars_status (0 = OSCARS_OK, < 0 = error); never throws;
+ *   - arguments are validated before anything is changed or enqueued; on an
+ *     OSCARS_E_INVALID / OSCARS_E_INFEASIBLE return nothing was modified;
+ *   - device pointers are HIP device memory owned by the caller; host arrays
+ *     are only read (or written, for outputs) during the call;
+ *   - GPU work is enqueued on the given HIP stream (NULL = the null stream)
+ *     and the call returns without waiting, unless stated otherwise;
+ *   - on OSCARS_E_HIP the contents of device outputs are unspecified and
+ *     oscars_last_hip_error() gives the HIP error code;
+ *   - a context is not thread-safe; distinct contexts are independent.
+ */
+#ifndef OSCARS_H
+#define OSCARS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t oscars_status;
+
+enum {
+  OSCARS_OK = 0,
+  OSCARS_E_INVALID = -1,    /* bad argument: null, out of range, misaligned  */
+  OSCARS_E_NOMEM = -2,      /* host or device allocation failed              */
+  OSCARS_E_HIP = -3,        /* a HIP runtime call or kernel launch failed    */
+  OSCARS_E_INFEASIBLE = -4, /* Algorithm 1: constraint false at T = max t    */
+  OSCARS_E_STATE = -5       /* call not valid in the context's current state */
+};
+
+enum { OSCARS_FP32 = 0, OSCARS_BF16 = 1 };
+
+/* Largest number of replicas one aggregation accepts. */
+#define OSCARS_MAX_K 64
+/* Largest mini-batch size and layer width the local-step kernels accept. */
+#define OSCARS_MAX_BATCH 1024
+#define OSCARS_MAX_WIDTH 65536
+#define OSCARS_MAX_LAYERS 16
+
+/* Opaque context: model shape, K, device workspace, per-worker cursors. */
+typedef struct oscars_ctx oscars_ctx;
+
+/*
+ * Model: a fully connected ReLU network with a softmax cross-entropy loss.
+ *   n_layers  L >= 1 (L = 1 is softmax regression);
+ *   dims      host [L + 1]: dims[0] = input width d, dims[L] = classes C,
+ *             every entry in [1, OSCARS_MAX_WIDTH]; d must be a multiple of 8;
+ *   dtype     OSCARS_FP32: inputs, weights and arithmetic in fp32;
+ *             OSCARS_BF16: bf16 inputs and weights in the products, fp32
+ *             accumulation, fp32 master parameters.
+ * Flat parameter layout of one replica (what oscars_num_params counts):
+ *   [W_1 (dims[1] x dims[0], row-major), b_1 (dims[1]), W_2, b_2, ...],
+ *   each segment starting on a 64-element (256-byte) boundary; the padding
+ *   between segments is zero and stays zero.
+ */
+typedef struct {
+  int32_t n_layers;
+  const int32_t* dims;
+  int32_t dtype;
+} oscars_model;
+
+/*
+ * Training data and the workers' shards (Introduction: each worker of a
+ * parameter server holds different training data).
+ *   x        device [n_rows][d]: fp32, or bf16 bit patterns for OSCARS_BF16;
+ *            16-byte aligned;
+ *   y        device [n_rows] int32 labels in [0, C);
+ *   n_rows   number of rows;
+ *   offsets  host [K + 1], non-decreasing, offsets[0] = 0,
+ *            offsets[K] = n_rows; worker k owns rows [offsets[k], offsets[k+1]),
+ *            which must not be empty;
+ *   seed     seed of the mini-batch sampler (see oscars_sample_indices).
+ */
+typedef struct {
+  const void* x;
+  const int32_t* y;
+  int64_t n_rows;
+  const int64_t* offsets;
+  uint64_t seed;
+} oscars_shards;
+
+/* Create a context for K replicas of `model`, mini-batches up to max_batch.
+ * Allocates the device workspace (activations, bf16 weight copies, index
+ * tables) on the current HIP device.  `hip_stream` (a hipStream_t, NULL =
+ * null stream) is the stream oscars_local_steps enqueues on. */
+oscars_status oscars_create(oscars_ctx** out, const oscars_model* model, int32_t K,
+                            int32_t max_batch, void* hip_stream);
+/* Free the workspace.  NULL is allowed.  Waits for the context's stream. */
+void oscars_destroy(oscars_ctx* ctx);
+/* Replace the stream later calls enqueue on. */
+oscars_status oscars_set_stream(oscars_ctx* ctx, void* hip_stream);
+/* Padded flat length of one replica (the stride between replicas). */
+int64_t oscars_num_params(const oscars_ctx* ctx);
+/* Element offsets of W_l and b_l (l = 1..L) in the flat layout. */
+oscars_status oscars_layer_offsets(const oscars_ctx* ctx, int32_t l, int64_t* w_off,
+                                   int64_t* b_off);
+
+/* Algorithm 1 (Approach; Problem Formulation Eq. 1-3), host only.
+ *   t_iter  host [N] per-worker iteration times in integer ticks, >= 1;
+ *   M       bound on floor(T/min t) - floor(T/max t), >= 1;
+ *   T_star  out: chosen barrier;  tau  out host [N]: floor(T_star / t_iter[i]).
+ * Scans T = max t, max t + 1, ... while the constraint holds, keeps the first
+ * T of least maximal wait, and stops early at the first zero wait.
+ * OSCARS_E_INFEASIBLE if the constraint already fails at T = max t. */
+oscars_status oscars_load_balance(const int64_t* t_iter, int32_t N, int64_t M, int64_t* T_star,
+                                  int32_t* tau);
+
+/* Eq. 4 weights, host only: w[k] = 1/K as fp32 for every k.  `staleness`
+ * (host [K], may be NULL) is accepted and has no effect: the update rule
+ * averages uniformly. */
+oscars_status oscars_paper_weights(const int32_t* staleness, int32_t K, float* w);
+
+/* Contiguous shards, host only: offsets[k] = floor(k * n_rows / K), k = 0..K. */
+oscars_status oscars_shard_offsets(int64_t n_rows, int32_t K, int64_t* offsets);
+
+/* Mini-batch rows of worker k, host only.  Worker k draws its shard without
+ * replacement, epoch by epoch; sample number p = step * batch + b lies in
+ * epoch e = p / n_k at position p mod n_k; the epoch-e order is a Durstenfeld
+ * shuffle of 0..n_k-1 (i from n_k-1 down to 1, j = r mod (i+1)) driven by
+ * SplitMix64 started at seed ^ ((k << 32) | e).
+ *   rows_out  host [steps][batch]: global row indices for steps
+ *             first_step .. first_step + steps - 1. */
+oscars_status oscars_sample_indices(const oscars_shards* shards, int32_t K, int32_t k,
+                                    int64_t first_step, int32_t steps, int32_t batch,
+                                    int64_t* rows_out);
+
+/* Local SGD of Eq. 4 (second branch) for every worker, batched on the GPU.
+ *   replicas  device [K][oscars_num_params] fp32 master parameters, one replica
+ *             per worker, 16-byte aligned; updated in place;
+ *   shards    training data and shards (K + 1 offsets);
+ *   tau       host [K]: worker k runs tau[k] >= 0 steps (0 leaves replica k
+ *             untouched); at most 4096;
+ *   lr        learning rate eta, finite and > 0;
+ *   batch     mini-batch size, 1 <= batch <= max_batch of the context.
+ * Worker k continues its sample stream where its previous call stopped (its
+ * cursor advances by tau[k]).  Replicas with tau[k] <= j get no work in step j. */
+oscars_status oscars_local_steps(oscars_ctx* ctx, float* replicas, const oscars_shards* shards,
+                                 const int32_t* tau, float lr, int32_t batch);
+
+/* Mean training loss of each worker over its steps in the last
+ * oscars_local_steps call (NaN for a worker that ran no step).  Waits for the
+ * context's stream.  losses: host [K]. */
+oscars_status oscars_round_losses(oscars_ctx* ctx, float* losses);
+
+/* Parameter-server aggregation (Approach, Eq. 4, first branch).
+ *   global    device [n] fp32 out: g[i] = sum_k w_k * replicas[k * ld + i],
+ *             summed as a balanced pairwise tree over P = next power of two
+ *             >= K leaves (leaf k = fl(w_k * x_k[i]) for k < K, +0 otherwise;
+ *             each node fl(left + right)); with K a power of two and
+ *             w_k = 1/K the result is exact up to that tree's roundings;
+ *   replicas  device [K][ld] fp32; if broadcast != 0 every replica is
+ *             overwritten with g after the reduction (replicas[k*ld + i] = g[i]
+ *             for i < n); otherwise only read;
+ *   weights   host [K] fp32 (oscars_paper_weights gives the paper's 1/K);
+ *   K         1 <= K <= OSCARS_MAX_K;  n >= 1;  ld >= n, ld % 4 == 0;
+ *   global and replicas 16-byte aligned and not overlapping. */
+oscars_status oscars_aggregate(float* global, float* replicas, const float* weights, int32_t K,
+                               int64_t n, int64_t ld, int32_t broadcast, void* hip_stream);
+
+/* Resume support: per-worker count of local steps done so far. host [K]. */
+oscars_status oscars_get_cursors(const oscars_ctx* ctx, int64_t* steps_done);
+oscars_status oscars_set_cursors(oscars_ctx* ctx, const int64_t* steps_done);
+
+/* Per-kernel timing with HIP events recorded on the context's stream around
+ * every launch of the selected kernel kinds (bit mask of 1 << OSCARS_KERNEL_*).
+ * oscars_profile_end waits for the stream and returns, per kind, the summed
+ * milliseconds and the number of launches since oscars_profile_begin
+ * (host [OSCARS_KERNEL_COUNT] each). */
+enum {
+  OSCARS_KERNEL_CAST = 0,
+  OSCARS_KERNEL_FWD = 1,
+  OSCARS_KERNEL_SOFTMAX = 2,
+  OSCARS_KERNEL_DGRAD = 3,
+  OSCARS_KERNEL_WGRAD = 4,
+  OSCARS_KERNEL_COUNT = 5
+};
+oscars_status oscars_profile_begin(oscars_ctx* ctx, uint32_t kind_mask);
+oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches);
+
+const char* oscars_status_str(oscars_status s);
+/* HIP error code of the last OSCARS_E_HIP in this thread (0 if none). */
+int32_t oscars_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OSCARS_H */

@@ -1,0 +1,283 @@
+"""Oscars local-SGD hot path on MI355X (gfx950): Python binding.
+
+A thin ctypes layer over the C ABI declared in ``include/oscars.h``.  It only
+marshals arguments (torch tensors become device pointers, the current torch
+stream becomes the HIP stream); every step of the hot path runs in the HIP
+library ``_lib/liboscars.so``.  If that library is missing the import of this
+package fails: there is no CPU fallback.
+
+Build with ``python paper_2102_08550_amd/build.py`` (or
+``__graft_entry__.build()``).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "liboscars.so")
+
+OK, E_INVALID, E_NOMEM, E_HIP, E_INFEASIBLE, E_STATE = 0, -1, -2, -3, -4, -5
+FP32, BF16 = 0, 1
+MAX_K = 64
+KERNEL_CAST, KERNEL_FWD, KERNEL_SOFTMAX, KERNEL_DGRAD, KERNEL_WGRAD = range(5)
+KERNEL_NAMES = ("cast_bf16", "gemm_fwd", "softmax_ce", "gemm_dgrad", "gemm_wgrad_update")
+
+_i32, _i64, _u32, _u64, _f32, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
+                                     ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p)
+_P = ctypes.POINTER
+
+
+class OscarsError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {_lib().oscars_status_str(status).decode()} (status {status}"
+                         + (f", hip error {_lib().oscars_last_hip_error()}" if status == E_HIP
+                            else "") + ")")
+
+
+class _Model(ctypes.Structure):
+    _fields_ = [("n_layers", _i32), ("dims", _P(_i32)), ("dtype", _i32)]
+
+
+class _Shards(ctypes.Structure):
+    _fields_ = [("x", _vp), ("y", _vp), ("n_rows", _i64), ("offsets", _P(_i64)), ("seed", _u64)]
+
+
+_LIB = None
+
+# name -> (restype, argtypes)
+_SIGS = {
+    "oscars_create": (_i32, [_P(_vp), _P(_Model), _i32, _i32, _vp]),
+    "oscars_destroy": (None, [_vp]),
+    "oscars_set_stream": (_i32, [_vp, _vp]),
+    "oscars_num_params": (_i64, [_vp]),
+    "oscars_layer_offsets": (_i32, [_vp, _i32, _P(_i64), _P(_i64)]),
+    "oscars_load_balance": (_i32, [_P(_i64), _i32, _i64, _P(_i64), _P(_i32)]),
+    "oscars_paper_weights": (_i32, [_P(_i32), _i32, _P(_f32)]),
+    "oscars_shard_offsets": (_i32, [_i64, _i32, _P(_i64)]),
+    "oscars_sample_indices": (_i32, [_P(_Shards), _i32, _i32, _i64, _i32, _i32, _P(_i64)]),
+    "oscars_local_steps": (_i32, [_vp, _vp, _P(_Shards), _P(_i32), _f32, _i32]),
+    "oscars_round_losses": (_i32, [_vp, _P(_f32)]),
+    "oscars_aggregate": (_i32, [_vp, _vp, _P(_f32), _i32, _i64, _i64, _i32, _vp]),
+    "oscars_get_cursors": (_i32, [_vp, _P(_i64)]),
+    "oscars_set_cursors": (_i32, [_vp, _P(_i64)]),
+    "oscars_profile_begin": (_i32, [_vp, _u32]),
+    "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
+    "oscars_status_str": (ctypes.c_char_p, [_i32]),
+    "oscars_last_hip_error": (_i32, []),
+}
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"HIP library not built: {LIB_PATH} is missing "
+                              "(run python paper_2102_08550_amd/build.py)")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = lib
+    return _LIB
+
+
+_lib()  # fail at import time when the library is absent
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise OscarsError(status, what)
+
+
+def _arr(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(_P(np.ctypeslib.as_ctypes_type(dtype)))
+
+
+def _stream_handle(stream=None) -> Optional[int]:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dev_ptr(t, dtype=None, what="tensor") -> int:
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{what} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} must have dtype {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+# ---------------------------------------------------------------- host-only calls
+
+def load_balance(t_iter: Sequence[int], M: int) -> Tuple[int, List[int]]:
+    """Algorithm 1: (T*, tau) for integer iteration times t_iter and bound M."""
+    t, tp = _arr(t_iter, np.int64)
+    tau = np.zeros(len(t), np.int32)
+    T = _i64(0)
+    _check(_lib().oscars_load_balance(tp, len(t), int(M), ctypes.byref(T),
+                                      tau.ctypes.data_as(_P(_i32))), "oscars_load_balance")
+    return int(T.value), tau.tolist()
+
+
+def paper_weights(K: int, staleness: Optional[Sequence[int]] = None) -> np.ndarray:
+    w = np.zeros(K, np.float32)
+    st = None
+    if staleness is not None:
+        st, stp = _arr(staleness, np.int32)
+    else:
+        stp = None
+    _check(_lib().oscars_paper_weights(stp, int(K), w.ctypes.data_as(_P(_f32))),
+           "oscars_paper_weights")
+    return w
+
+
+def shard_offsets(n_rows: int, K: int) -> List[int]:
+    off = np.zeros(K + 1, np.int64)
+    _check(_lib().oscars_shard_offsets(int(n_rows), int(K), off.ctypes.data_as(_P(_i64))),
+           "oscars_shard_offsets")
+    return off.tolist()
+
+
+def _shards(x_ptr, y_ptr, n_rows, offsets, seed):
+    off, offp = _arr(offsets, np.int64)
+    sh = _Shards(x_ptr, y_ptr, int(n_rows), offp, ctypes.c_uint64(seed & (2**64 - 1)).value)
+    return sh, off  # keep `off` alive with the struct
+
+
+def sample_indices(n_rows: int, offsets: Sequence[int], seed: int, k: int, first_step: int,
+                   steps: int, batch: int) -> np.ndarray:
+    sh, keep = _shards(None, None, n_rows, offsets, seed)
+    out = np.zeros((steps, batch), np.int64)
+    _check(_lib().oscars_sample_indices(ctypes.byref(sh), len(offsets) - 1, int(k),
+                                        int(first_step), int(steps), int(batch),
+                                        out.ctypes.data_as(_P(_i64))), "oscars_sample_indices")
+    return out
+
+
+# ---------------------------------------------------------------- GPU calls
+
+def aggregate(global_, replicas, weights: Sequence[float], K: int, n: int, ld: int,
+              broadcast: bool = False, stream=None):
+    """global_[i] = pairwise-tree sum_k w_k replicas[k*ld + i]; optional broadcast."""
+    import torch
+    gp = _dev_ptr(global_, torch.float32, "global")
+    rp = _dev_ptr(replicas, torch.float32, "replicas")
+    if global_.numel() < n or replicas.numel() < (K - 1) * ld + n:
+        raise ValueError("buffers smaller than K, n, ld imply")
+    w, wp = _arr(weights, np.float32)
+    if len(w) != K:
+        raise ValueError("one weight per replica")
+    _check(_lib().oscars_aggregate(gp, rp, wp, int(K), int(n), int(ld), int(bool(broadcast)),
+                                   _stream_handle(stream)), "oscars_aggregate")
+
+
+class Context:
+    """K replicas of a ReLU MLP (dims = (d, h_1, ..., C)) and their workspace."""
+
+    def __init__(self, dims: Sequence[int], dtype: int, K: int, max_batch: int, stream=None):
+        self.dims = [int(v) for v in dims]
+        self.dtype = int(dtype)
+        self.K = int(K)
+        self._dims_arr, dp = _arr(self.dims, np.int32)
+        model = _Model(len(self.dims) - 1, dp, self.dtype)
+        h = _vp()
+        _check(_lib().oscars_create(ctypes.byref(h), ctypes.byref(model), self.K, int(max_batch),
+                                    _stream_handle(stream)), "oscars_create")
+        self._h = h
+        self.n_pad = int(_lib().oscars_num_params(h))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _lib().oscars_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_stream(self, stream=None):
+        _check(_lib().oscars_set_stream(self._h, _stream_handle(stream)), "oscars_set_stream")
+
+    def layer_offsets(self, l: int) -> Tuple[int, int]:
+        w, b = _i64(0), _i64(0)
+        _check(_lib().oscars_layer_offsets(self._h, int(l), ctypes.byref(w), ctypes.byref(b)),
+               "oscars_layer_offsets")
+        return int(w.value), int(b.value)
+
+    def pack(self, layers) -> np.ndarray:
+        """Flat padded float32 vector from [(W, b), ...] in this model's layout."""
+        flat = np.zeros(self.n_pad, np.float32)
+        for l, (W, b) in enumerate(layers, start=1):
+            wo, bo = self.layer_offsets(l)
+            flat[wo:wo + W.size] = np.asarray(W, np.float32).ravel()
+            flat[bo:bo + b.size] = np.asarray(b, np.float32)
+        return flat
+
+    def unpack(self, flat: np.ndarray):
+        out = []
+        for l in range(1, len(self.dims)):
+            wo, bo = self.layer_offsets(l)
+            i, o = self.dims[l - 1], self.dims[l]
+            out.append((flat[wo:wo + o * i].reshape(o, i), flat[bo:bo + o]))
+        return out
+
+    def local_steps(self, replicas, x, y, offsets: Sequence[int], seed: int, tau: Sequence[int],
+                    lr: float, batch: int):
+        import torch
+        rp = _dev_ptr(replicas, torch.float32, "replicas")
+        if replicas.numel() < self.K * self.n_pad:
+            raise ValueError("replicas must hold K * n_pad floats")
+        xdt = torch.bfloat16 if self.dtype == BF16 else torch.float32
+        if x.dtype == torch.int16 or x.dtype == torch.uint16:
+            xdt = x.dtype  # bf16 bit patterns
+        xp = _dev_ptr(x, xdt, "x")
+        yp = _dev_ptr(y, torch.int32, "y")
+        if x.dim() != 2 or x.shape[1] != self.dims[0] or y.numel() != x.shape[0]:
+            raise ValueError("x must be [n_rows][d] and y [n_rows]")
+        sh, keep = _shards(xp, yp, x.shape[0], offsets, seed)
+        t, tp = _arr(tau, np.int32)
+        if len(t) != self.K or len(offsets) != self.K + 1:
+            raise ValueError("tau needs K entries and offsets K + 1")
+        _check(_lib().oscars_local_steps(self._h, rp, ctypes.byref(sh), tp, float(lr), int(batch)),
+               "oscars_local_steps")
+
+    def round_losses(self) -> np.ndarray:
+        out = np.zeros(self.K, np.float32)
+        _check(_lib().oscars_round_losses(self._h, out.ctypes.data_as(_P(_f32))),
+               "oscars_round_losses")
+        return out
+
+    def cursors(self) -> List[int]:
+        out = np.zeros(self.K, np.int64)
+        _check(_lib().oscars_get_cursors(self._h, out.ctypes.data_as(_P(_i64))),
+               "oscars_get_cursors")
+        return out.tolist()
+
+    def set_cursors(self, steps_done: Sequence[int]):
+        a, ap = _arr(steps_done, np.int64)
+        _check(_lib().oscars_set_cursors(self._h, ap), "oscars_set_cursors")
+
+    def profile_begin(self, kinds: Sequence[int]):
+        mask = 0
+        for k in kinds:
+            mask |= 1 << int(k)
+        _check(_lib().oscars_profile_begin(self._h, mask), "oscars_profile_begin")
+
+    def profile_end(self):
+        ms = (ctypes.c_double * 5)()
+        n = (_i64 * 5)()
+        _check(_lib().oscars_profile_end(self._h, ms, n), "oscars_profile_end")
+        return {KERNEL_NAMES[i]: (ms[i], n[i]) for i in range(5)}

@@ -1,0 +1,71 @@
+// Launchers of the hot-path kernels (device code in kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace oscars {
+
+enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };
+
+// One grouped GEMM launch over `n_slots` replicas (grid z = slot).  Slot z
+// works on replica order[z].  Every "per-slot" pointer below is the slot-0
+// address; the kernel adds z times the matching stride.
+//
+//   FWD   C[b][o] = A[b][:] . W[o][:] + bias[o]  (ReLU if relu), stored to out
+//         A: activations [M=B][K=in] (row stride a_ld), or dataset rows
+//            x[gather[b]] when gather != nullptr; W: [N=out][K=in].
+//   DGRAD C[b][i] = sum_o D[b][o] W[o][i], zeroed where mask[b][i] <= 0
+//         D: [M=B][K=out] (a_ld), W: [K=out][N=in] (b_ld = in).
+//   WGRAD dW[o][i] = sum_b D[b][o] A[b][i];  W <- W - lr dW (fp32 master),
+//         bias <- bias - lr sum_b D[b][o]; bf16 copy of W refreshed if any.
+//         D: [K=B][M=out] (a_ld), A: [K=B][N=in] (b_ld) or x[gather[b]].
+struct GemmArgs {
+  int M, N, K;
+  // operand A (FWD: activations / x; DGRAD: delta; WGRAD: delta)
+  const void* a;
+  int64_t a_ld, a_slot;
+  // operand B (FWD, DGRAD: weights; WGRAD: activations / x)
+  const void* b;
+  int64_t b_ld, b_slot;
+  int b_by_order;  // b's slot offset uses order[z] (fp32 masters) instead of z
+  // row gather of the dataset operand (FWD: A rows; WGRAD: B rows)
+  const int32_t* gather;
+  int64_t gather_slot;
+  // outputs / epilogue inputs
+  void* out;  // FWD: activations or logits; DGRAD: delta of the layer below
+  int64_t out_ld, out_slot;
+  const void* mask;  // DGRAD: activations of the layer below
+  int64_t mask_ld, mask_slot;
+  float* master;  // fp32 replicas (bias for FWD; W and bias for WGRAD)
+  int64_t master_slot;  // replica stride
+  int64_t w_off, b_off;  // W_l and b_l offsets within a replica
+  uint16_t* wcopy;  // WGRAD, bf16 models: slot-indexed bf16 weight copies
+  int64_t wcopy_slot;
+  const int32_t* order;  // [slots] replica id of each slot
+  float lr;
+  int relu;  // FWD: apply ReLU
+  int out_bf16;  // FWD / DGRAD: store bf16 (else fp32)
+};
+
+hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s);
+
+// Softmax cross-entropy on logits [slot][B][ld]: delta = (softmax - onehot)/B
+// stored as bf16 or fp32 into delta [slot][B][ld] (columns C..ld-1 zeroed),
+// per-row loss into loss[slot][B].
+hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
+                             const int32_t* y, const int32_t* gather, int64_t gather_slot,
+                             void* delta, bool delta_bf16, float* loss, int64_t loss_slot,
+                             int n_slots, hipStream_t s);
+
+// wcopy[z][i] = bf16(master[order[z]][i]) for i < n, z < n_slots.
+hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int32_t* order,
+                            uint16_t* wcopy, int64_t wcopy_slot, int64_t n, int n_slots,
+                            hipStream_t s);
+
+// Pairwise-tree weighted K-way reduction with optional broadcast.
+hipError_t launch_aggregate(float* g, float* replicas, const float* w, int K, int64_t n,
+                            int64_t ld, int broadcast, hipStream_t s);
+
+}  // namespace oscars

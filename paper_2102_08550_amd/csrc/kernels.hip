@@ -1,0 +1,517 @@
+// Device code of the Oscars hot path for gfx950 (CDNA4).
+//
+//  * gemm_kernel   grouped MFMA GEMM, one launch per layer and pass, grid z =
+//                  active replica slot.  Three pass shapes share one body:
+//                  forward (NT), backward-data (NN), backward-weight (TN) with
+//                  the SGD update x <- x - eta g(x) of Eq. 4 fused into the
+//                  epilogue, so weight gradients never reach HBM.
+//  * softmax_ce    logit gradient of the mean softmax cross-entropy.
+//  * cast_bf16     fp32 master -> bf16 working copy (bf16 models).
+//  * aggregate     the parameter server's average of Eq. 4 as a pairwise-tree
+//                  K-way reduction, 128-bit loads, lane groups combined with
+//                  cross-lane shuffles, optional broadcast back to every replica.
+//
+// Tiles: 128 x 128 outputs per 256-thread workgroup, four waves of 64 x 64,
+// each wave 2 x 2 MFMA 32x32 blocks.  LDS holds both operands K-contiguous:
+// 128 rows x 128 bytes (64 bf16 or 32 fp32), 16-byte chunks placed at
+// chunk ^ ((row ^ row >> 3) & 7) so that MFMA operand reads (consecutive rows,
+// one chunk) and transposing writes (rows 8 apart) both spread over the banks.
+// Operands stored M/N-contiguous in memory (weights in backward-data, both
+// operands of backward-weight) are transposed on their way into LDS.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/oscars.h"
+#include "kernels.h"
+
+namespace oscars {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int BM = 128, BN = 128, NTHR = 256;
+constexpr int ROW_U32 = 32;               // one LDS tile row: 128 bytes
+constexpr int TILE_U32 = 128 * ROW_U32;   // one operand tile: 16 KB
+
+__device__ __forceinline__ int lds_word(int row, int chunk) {
+  return row * ROW_U32 + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 2);
+}
+
+// fp32 -> bf16, round to nearest even on the fp32 bits.
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <bool BF16> struct El;
+template <> struct El<true> {
+  typedef uint16_t T;
+  static constexpr int CH = 8;   // elements per 16-byte chunk
+  static constexpr int BK = 64;  // K per LDS tile
+};
+template <> struct El<false> {
+  typedef float T;
+  static constexpr int CH = 4;
+  static constexpr int BK = 32;
+};
+
+// 16 bytes starting at p; elements at and beyond `valid` read as zero.
+template <bool BF16>
+__device__ __forceinline__ u32x4 load_chunk(const typename El<BF16>::T* p, int valid) {
+  if (valid >= El<BF16>::CH) return *reinterpret_cast<const u32x4*>(p);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if constexpr (BF16) {
+    for (int e = 0; e < 8; ++e)
+      if (e < valid) v[e >> 1] |= static_cast<uint32_t>(p[e]) << (16 * (e & 1));
+  } else {
+    for (int e = 0; e < 4; ++e)
+      if (e < valid) v[e] = __float_as_uint(p[e]);
+  }
+  return v;
+}
+
+// Tile of an operand stored K-contiguous: 128 rows (M or N) x BK.
+template <bool BF16>
+struct RowTile {
+  typedef typename El<BF16>::T T;
+  static constexpr int CH = El<BF16>::CH;
+  u32x4 v[4];
+  __device__ __forceinline__ void load(const T* base, int64_t ld, const int32_t* gather, int row0,
+                                       int R, int k0, int K, int tid) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int idx = tid + NTHR * p, r = idx >> 3, c = idx & 7;
+      const int gr = row0 + r, k = k0 + c * CH;
+      const bool ok = gr < R && k < K;
+      const int64_t row = ok ? (gather ? gather[gr] : gr) : 0;
+      v[p] = ok ? load_chunk<BF16>(base + row * ld + k, K - k) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int idx = tid + NTHR * p;
+      *reinterpret_cast<u32x4*>(lds + lds_word(idx >> 3, idx & 7)) = v[p];
+    }
+  }
+};
+
+// Tile of an operand stored M/N-contiguous ([K][MN] in memory), transposed
+// into the K-contiguous LDS layout.  bf16: pairs of k rows are packed into
+// 32-bit words; fp32: single words.
+template <bool BF16> struct TransTile;
+
+template <>
+struct TransTile<true> {
+  u32x4 lo[2], hi[2];
+  __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, const int32_t* gather,
+                                       int mn0, int MN, int k0, int K, int tid) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int idx = tid + NTHR * p, mc = idx & 15, kp = idx >> 4;
+      const int k = k0 + 2 * kp, mn = mn0 + 8 * mc;
+      const bool ok0 = k < K && mn < MN, ok1 = k + 1 < K && mn < MN;
+      const int64_t r0 = ok0 ? (gather ? gather[k] : k) : 0;
+      const int64_t r1 = ok1 ? (gather ? gather[k + 1] : k + 1) : 0;
+      lo[p] = ok0 ? load_chunk<true>(base + r0 * ld + mn, MN - mn) : u32x4{0u, 0u, 0u, 0u};
+      hi[p] = ok1 ? load_chunk<true>(base + r1 * ld + mn, MN - mn) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int idx = tid + NTHR * p, mc = idx & 15, kp = idx >> 4;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t a = lo[p][e >> 1], b = hi[p][e >> 1];
+        const uint32_t w = (e & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
+        lds[lds_word(8 * mc + e, kp >> 2) + (kp & 3)] = w;
+      }
+    }
+  }
+};
+
+template <>
+struct TransTile<false> {
+  u32x4 v[4];
+  __device__ __forceinline__ void load(const float* base, int64_t ld, const int32_t* gather, int mn0,
+                                       int MN, int k0, int K, int tid) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int idx = tid + NTHR * p, mc = idx & 31, kk = idx >> 5;
+      const int k = k0 + kk, mn = mn0 + 4 * mc;
+      const bool ok = k < K && mn < MN;
+      const int64_t r = ok ? (gather ? gather[k] : k) : 0;
+      v[p] = ok ? load_chunk<false>(base + r * ld + mn, MN - mn) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int idx = tid + NTHR * p, mc = idx & 31, kk = idx >> 5;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) lds[lds_word(4 * mc + e, kk >> 2) + (kk & 3)] = v[p][e];
+    }
+  }
+};
+
+// 2 x 2 blocks of 32x32 MFMA over one LDS tile pair.
+template <bool BF16>
+__device__ __forceinline__ void mma_tile(const uint32_t* As, const uint32_t* Bs, int wm, int wn,
+                                         int lane, f32x16 (&acc)[2][2]) {
+  const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int ch = 2 * s + h;
+    u32x4 a[2], b[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a[i] = *reinterpret_cast<const u32x4*>(As + lds_word(wm * 64 + 32 * i + r, ch));
+      b[i] = *reinterpret_cast<const u32x4*>(Bs + lds_word(wn * 64 + 32 * i + r, ch));
+    }
+    if constexpr (BF16) {
+      // lanes 0-31 hold k = 16s..16s+7 of their row, lanes 32-63 k = 16s+8..16s+15
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
+    } else {
+      // lanes 0-31 hold k = 8s..8s+3, lanes 32-63 k = 8s+4..8s+7; MFMA t
+      // contracts element t of every lane, i.e. k = 8s + t and 8s + 4 + t.
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[i][t]),
+                                                             __uint_as_float(b[j][t]), acc[i][j],
+                                                             0, 0, 0);
+    }
+  }
+}
+
+template <bool BF16, int MODE>
+__global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
+  typedef typename El<BF16>::T T;
+  constexpr int BK = El<BF16>::BK;
+  __shared__ __attribute__((aligned(16))) uint32_t lds[2][2][TILE_U32];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int z = blockIdx.z;
+  const int rep = g.order[z];
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int M = g.M, N = g.N, K = g.K;
+
+  const T* A = static_cast<const T*>(g.a) + z * g.a_slot;
+  const T* B = static_cast<const T*>(g.b) + (g.b_by_order ? rep : z) * g.b_slot;
+  const int32_t* gat = g.gather ? g.gather + z * g.gather_slot : nullptr;
+  const int32_t* gatA = (MODE == GEMM_FWD) ? gat : nullptr;
+  const int32_t* gatB = (MODE == GEMM_WGRAD) ? gat : nullptr;
+
+  // Operand A: K-contiguous in FWD/DGRAD, M-contiguous (delta [B][out]) in WGRAD.
+  // Operand B: K-contiguous in FWD, N-contiguous in DGRAD (W) and WGRAD (acts).
+  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16>, RowTile<BF16>>::type ta;
+  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16>, TransTile<BF16>>::type tb;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const bool bias_wg = (MODE == GEMM_WGRAD) && blockIdx.x == 0;
+  float dbias = 0.0f;
+
+  const int nk = (K + BK - 1) / BK;
+  ta.load(A, g.a_ld, gatA, m0, M, 0, K, tid);
+  tb.load(B, g.b_ld, gatB, n0, N, 0, K, tid);
+  ta.store(lds[0][0], tid);
+  tb.store(lds[0][1], tid);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      ta.load(A, g.a_ld, gatA, m0, M, (kt + 1) * BK, K, tid);
+      tb.load(B, g.b_ld, gatB, n0, N, (kt + 1) * BK, K, tid);
+    }
+    mma_tile<BF16>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
+    if (bias_wg && tid < BM) {
+      // db[o] = sum_b delta[b][o]: row tid of the A tile, in k order.
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(&lds[buf][0][lds_word(tid, c)]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if constexpr (BF16) {
+            dbias += __uint_as_float(v[e] << 16);
+            dbias += __uint_as_float(v[e] & 0xFFFF0000u);
+          } else {
+            dbias += __uint_as_float(v[e]);
+          }
+        }
+      }
+    }
+    if (more) {
+      ta.store(lds[buf ^ 1][0], tid);
+      tb.store(lds[buf ^ 1][1], tid);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue.  MFMA 32x32 accumulator: lane l holds column l & 31 and rows
+  // 8 (r >> 2) + 4 (l >> 5) + (r & 3), r = 0..15.
+  float* master = g.master + static_cast<int64_t>(rep) * g.master_slot;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn * 64 + 32 * j + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (m >= M || n >= N) continue;
+        const float v = acc[i][j][r];
+        if constexpr (MODE == GEMM_FWD) {
+          float o = v + master[g.b_off + n];
+          if (g.relu) o = fmaxf(o, 0.0f);
+          const int64_t at = z * g.out_slot + static_cast<int64_t>(m) * g.out_ld + n;
+          if (g.out_bf16)
+            static_cast<uint16_t*>(g.out)[at] = static_cast<uint16_t>(f2bf(o));
+          else
+            static_cast<float*>(g.out)[at] = o;
+        } else if constexpr (MODE == GEMM_DGRAD) {
+          const int64_t am = z * g.mask_slot + static_cast<int64_t>(m) * g.mask_ld + n;
+          const T mk = static_cast<const T*>(g.mask)[am];
+          bool pos;
+          if constexpr (BF16) pos = mk != 0 && (mk & 0x8000u) == 0;
+          else pos = mk > 0.0f;
+          const float o = pos ? v : 0.0f;
+          const int64_t at = z * g.out_slot + static_cast<int64_t>(m) * g.out_ld + n;
+          if (g.out_bf16)
+            static_cast<uint16_t*>(g.out)[at] = static_cast<uint16_t>(f2bf(o));
+          else
+            static_cast<float*>(g.out)[at] = o;
+        } else {
+          const int64_t at = g.w_off + static_cast<int64_t>(m) * N + n;
+          const float w = fmaf(-g.lr, v, master[at]);
+          master[at] = w;
+          if (g.wcopy) g.wcopy[z * g.wcopy_slot + at] = static_cast<uint16_t>(f2bf(w));
+        }
+      }
+    }
+  }
+  if (bias_wg && tid < BM && m0 + tid < M) {
+    float* bp = master + g.b_off + m0 + tid;
+    *bp = fmaf(-g.lr, dbias, *bp);
+  }
+}
+
+template <bool BF16_OUT>
+__global__ __launch_bounds__(64) void softmax_ce_kernel(const float* logits, int64_t ld,
+                                                        int64_t slot_stride, int C, int B,
+                                                        const int32_t* y, const int32_t* gather,
+                                                        int64_t gather_slot, void* delta,
+                                                        float* loss, int64_t loss_slot) {
+  const int b = blockIdx.x, z = blockIdx.y, lane = threadIdx.x;
+  const float* row = logits + z * slot_stride + static_cast<int64_t>(b) * ld;
+  const int label = y[gather[z * gather_slot + b]];
+  const bool label_ok = label >= 0 && label < C;
+  float mx = -INFINITY;
+  for (int c = lane; c < C; c += 64) mx = fmaxf(mx, row[c]);
+  for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
+  float s = 0.0f;
+  for (int c = lane; c < C; c += 64) s += expf(row[c] - mx);
+  for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d);
+  const float invB = 1.0f / static_cast<float>(B);
+  const int64_t base = z * slot_stride + static_cast<int64_t>(b) * ld;
+  for (int c = lane; c < ld; c += 64) {
+    float dv = 0.0f;
+    if (c < C) dv = (expf(row[c] - mx) / s - (c == label ? 1.0f : 0.0f)) * invB;
+    if constexpr (BF16_OUT)
+      static_cast<uint16_t*>(delta)[base + c] = static_cast<uint16_t>(f2bf(dv));
+    else
+      static_cast<float*>(delta)[base + c] = dv;
+  }
+  if (lane == 0)
+    loss[z * loss_slot + b] = label_ok ? logf(s) - (row[label] - mx) : __builtin_nanf("");
+}
+
+__global__ __launch_bounds__(256) void cast_bf16_kernel(const float* master, int64_t master_slot,
+                                                        const int32_t* order, uint16_t* wcopy,
+                                                        int64_t wcopy_slot, int64_t n) {
+  const int z = blockIdx.y;
+  const float* src = master + static_cast<int64_t>(order[z]) * master_slot;
+  uint16_t* dst = wcopy + z * wcopy_slot;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x * 4;
+  for (int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 4; i < n;
+       i += stride) {
+    if (i + 4 <= n) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(src + i);
+      uint2 o;
+      o.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+      o.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+      *reinterpret_cast<uint2*>(dst + i) = o;
+    } else {
+      for (int64_t e = i; e < n; ++e) dst[e] = static_cast<uint16_t>(f2bf(src[e]));
+    }
+  }
+}
+
+struct AggWeights {
+  float w[OSCARS_MAX_K];
+};
+
+// Lane group q of a wave (G groups of 64 / G lanes) owns leaves qL .. qL+L-1,
+// each lane four consecutive elements.  The lane sums its leaves as a
+// pairwise tree; xor-shuffles over the group bits then join neighbouring
+// subtrees, which completes the same balanced tree over P = G L leaves.
+template <int G, int L>
+__global__ __launch_bounds__(256) void aggregate_kernel(float* g, float* reps, AggWeights w,
+                                                        int K, int64_t n, int64_t ld, int bcast) {
+  constexpr int LPG = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane / LPG, e = lane % LPG;
+  const int64_t i0 = ((static_cast<int64_t>(blockIdx.x) * 4 + wave) * LPG + e) * 4;
+  const int valid = (n - i0 >= 4) ? 4 : static_cast<int>(n - i0 > 0 ? n - i0 : 0);
+  f32x4 leaf[L];
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    const int k = q * L + i;
+    f32x4 x = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (k < K) {
+      const float* p = reps + k * ld + i0;
+      if (valid == 4) {
+        x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+      } else {
+        for (int t = 0; t < 4; ++t)
+          if (t < valid) x[t] = p[t];
+      }
+      x = x * w.w[k];
+    }
+    leaf[i] = x;
+  }
+#pragma unroll
+  for (int s = 1; s < L; s *= 2)
+#pragma unroll
+    for (int i = 0; i < L; i += 2 * s) leaf[i] = leaf[i] + leaf[i + s];
+  f32x4 v = leaf[0];
+#pragma unroll
+  for (int d = LPG; d < 64; d *= 2) {
+    f32x4 o;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) o[t] = __shfl_xor(v[t], d);
+    v = v + o;
+  }
+  if (valid == 4) {
+    if (q == 0) __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(g + i0));
+    if (bcast) {
+#pragma unroll
+      for (int i = 0; i < L; ++i) {
+        const int k = q * L + i;
+        if (k < K) __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(reps + k * ld + i0));
+      }
+    }
+  } else if (valid > 0) {
+    for (int t = 0; t < valid; ++t) {
+      if (q == 0) g[i0 + t] = v[t];
+      if (bcast)
+        for (int i = 0; i < L; ++i) {
+          const int k = q * L + i;
+          if (k < K) reps[k * ld + i0 + t] = v[t];
+        }
+    }
+  }
+}
+
+template <int G, int L>
+hipError_t agg_launch(float* g, float* reps, const AggWeights& w, int K, int64_t n, int64_t ld,
+                      int bcast, hipStream_t s) {
+  constexpr int per_block = 4 * (64 / G) * 4;
+  const int64_t blocks = (n + per_block - 1) / per_block;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((aggregate_kernel<G, L>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                     g, reps, w, K, n, ld, bcast);
+  return hipGetLastError();
+}
+
+template <bool BF16, int MODE>
+hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
+  const dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, n_slots);
+  hipLaunchKernelGGL((gemm_kernel<BF16, MODE>), grid, dim3(NTHR), 0, s, g);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s) {
+  if (bf16) {
+    switch (mode) {
+      case GEMM_FWD: return gemm_launch<true, GEMM_FWD>(g, n_slots, s);
+      case GEMM_DGRAD: return gemm_launch<true, GEMM_DGRAD>(g, n_slots, s);
+      case GEMM_WGRAD: return gemm_launch<true, GEMM_WGRAD>(g, n_slots, s);
+    }
+  } else {
+    switch (mode) {
+      case GEMM_FWD: return gemm_launch<false, GEMM_FWD>(g, n_slots, s);
+      case GEMM_DGRAD: return gemm_launch<false, GEMM_DGRAD>(g, n_slots, s);
+      case GEMM_WGRAD: return gemm_launch<false, GEMM_WGRAD>(g, n_slots, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
+                             const int32_t* y, const int32_t* gather, int64_t gather_slot,
+                             void* delta, bool delta_bf16, float* loss, int64_t loss_slot,
+                             int n_slots, hipStream_t s) {
+  const dim3 grid(B, n_slots);
+  if (delta_bf16)
+    hipLaunchKernelGGL((softmax_ce_kernel<true>), grid, dim3(64), 0, s, logits, ld, slot_stride, C,
+                       B, y, gather, gather_slot, delta, loss, loss_slot);
+  else
+    hipLaunchKernelGGL((softmax_ce_kernel<false>), grid, dim3(64), 0, s, logits, ld, slot_stride,
+                       C, B, y, gather, gather_slot, delta, loss, loss_slot);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int32_t* order,
+                            uint16_t* wcopy, int64_t wcopy_slot, int64_t n, int n_slots,
+                            hipStream_t s) {
+  int64_t blocks = (n / 4 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(cast_bf16_kernel, dim3(static_cast<unsigned>(blocks), n_slots), dim3(256), 0,
+                     s, master, master_slot, order, wcopy, wcopy_slot, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_aggregate(float* g, float* replicas, const float* w, int K, int64_t n,
+                            int64_t ld, int broadcast, hipStream_t s) {
+  AggWeights aw;
+  for (int k = 0; k < OSCARS_MAX_K; ++k) aw.w[k] = k < K ? w[k] : 0.0f;
+  int P = 1;
+  while (P < K) P *= 2;
+  switch (P) {
+    case 1: return agg_launch<1, 1>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 2: return agg_launch<2, 1>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 4: return agg_launch<4, 1>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 8: return agg_launch<4, 2>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 16: return agg_launch<4, 4>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 32: return agg_launch<4, 8>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 64: return agg_launch<4, 16>(g, replicas, aw, K, n, ld, broadcast, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace oscars

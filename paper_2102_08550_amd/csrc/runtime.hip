@@ -1,0 +1,519 @@
+// Context, workspace and round scheduler of the Oscars hot path.
+//
+// oscars_local_steps runs Eq. 4's second branch for all K workers at once:
+// workers are sorted by tau (descending, ties by index) into slots, so the
+// workers still running in local step j are the slot prefix
+// {z : tau[order[z]] > j}.  Each step launches, for that prefix only,
+// forward GEMMs, softmax cross-entropy, and per layer (top down) the
+// backward-data GEMM followed by the backward-weight GEMM with the fused SGD
+// update.  Workers whose tau is used up get no work and no writes: the GPU
+// counterpart of the idle time before the barrier (Eq. 1).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/oscars.h"
+#include "host_logic.h"
+#include "kernels.h"
+
+using namespace oscars;
+
+namespace {
+
+thread_local int32_t g_last_hip = 0;
+
+oscars_status hip_fail(hipError_t e) {
+  g_last_hip = static_cast<int32_t>(e);
+  return OSCARS_E_HIP;
+}
+
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kMaxTau = 4096;
+
+}  // namespace
+
+struct oscars_ctx {
+  int L = 0;
+  std::vector<int32_t> dims;
+  bool bf16 = false;
+  int K = 0, max_batch = 0;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  std::vector<int64_t> w_off, b_off, ld;  // per layer l = 1..L (index 0 unused for offsets)
+  int64_t n_pad = 0;
+  size_t esize = 4;  // bytes per activation / delta element
+
+  std::vector<void*> allocs;
+  uint16_t* wcopy = nullptr;       // [K][n_pad] bf16 weight copies (bf16 models)
+  std::vector<void*> act;          // act[l], l = 1..L-1: [K][max_batch][ld[l]]
+  float* logits = nullptr;         // [K][max_batch][ld[L]]
+  std::vector<void*> delta;        // delta[l], l = 1..L: [K][max_batch][ld[l]]
+  int32_t* table_dev = nullptr;    // order [64] then index table [slots][tau_max][B]
+  int64_t table_cap = 0;           // int32 elements
+  float* loss_dev = nullptr;       // [slots][tau_max][B]
+  int64_t loss_cap = 0;
+  int32_t* pinned = nullptr;       // host staging of table_dev
+  int64_t pinned_cap = 0;
+  hipEvent_t upload_done = nullptr;
+  bool upload_pending = false;
+
+  std::vector<int64_t> cursors;
+  std::vector<WorkerSampler> samplers;
+
+  std::vector<int32_t> last_order, last_tau;
+  int last_tau_max = 0, last_B = 0;
+
+  uint32_t prof_mask = 0;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<int, int>> prof_recs;  // (kind, first event index)
+
+  int64_t act_slot(int l) const { return static_cast<int64_t>(max_batch) * ld[l]; }
+};
+
+namespace {
+
+void free_ctx(oscars_ctx* c) {
+  if (!c) return;
+  (void)hipStreamSynchronize(c->stream);
+  for (void* p : c->allocs) (void)hipFree(p);
+  if (c->table_dev) (void)hipFree(c->table_dev);
+  if (c->loss_dev) (void)hipFree(c->loss_dev);
+  if (c->pinned) (void)hipHostFree(c->pinned);
+  if (c->upload_done) (void)hipEventDestroy(c->upload_done);
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  delete c;
+}
+
+hipError_t dev_alloc(oscars_ctx* c, size_t bytes, void** out) {
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, bytes);
+  if (e != hipSuccess) return e;
+  c->allocs.push_back(p);
+  e = hipMemsetAsync(p, 0, bytes, c->stream);
+  *out = p;
+  return e;
+}
+
+// Run `launch` (returns hipError_t), bracketed by profiling events if the
+// kind is selected.
+template <typename F>
+hipError_t timed(oscars_ctx* c, int kind, F&& launch) {
+  if (!(c->prof_mask & (1u << kind))) return launch();
+  const int i = static_cast<int>(c->prof_recs.size()) * 2;
+  while (static_cast<int>(c->ev_pool.size()) < i + 2) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return err;
+    c->ev_pool.push_back(e);
+  }
+  hipError_t err = hipEventRecord(c->ev_pool[i], c->stream);
+  if (err != hipSuccess) return err;
+  err = launch();
+  if (err != hipSuccess) return err;
+  err = hipEventRecord(c->ev_pool[i + 1], c->stream);
+  if (err != hipSuccess) return err;
+  c->prof_recs.emplace_back(kind, i);
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, int32_t max_batch,
+                            void* hip_stream) {
+  if (!out || !m || !m->dims) return OSCARS_E_INVALID;
+  if (m->n_layers < 1 || m->n_layers > OSCARS_MAX_LAYERS) return OSCARS_E_INVALID;
+  if (m->dtype != OSCARS_FP32 && m->dtype != OSCARS_BF16) return OSCARS_E_INVALID;
+  if (K < 1 || K > OSCARS_MAX_K || max_batch < 1 || max_batch > OSCARS_MAX_BATCH)
+    return OSCARS_E_INVALID;
+  for (int l = 0; l <= m->n_layers; ++l) {
+    const int32_t w = m->dims[l];
+    if (w < 1 || w > OSCARS_MAX_WIDTH) return OSCARS_E_INVALID;
+    if (l < m->n_layers && w % 8 != 0) return OSCARS_E_INVALID;
+  }
+  oscars_ctx* c = new (std::nothrow) oscars_ctx();
+  if (!c) return OSCARS_E_NOMEM;
+  c->L = m->n_layers;
+  c->dims.assign(m->dims, m->dims + m->n_layers + 1);
+  c->bf16 = m->dtype == OSCARS_BF16;
+  c->esize = c->bf16 ? 2 : 4;
+  c->K = K;
+  c->max_batch = max_batch;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->w_off.assign(c->L + 1, 0);
+  c->b_off.assign(c->L + 1, 0);
+  c->ld.assign(c->L + 1, 0);
+  int64_t off = 0;
+  for (int l = 1; l <= c->L; ++l) {
+    c->w_off[l] = off;
+    off = round_up(off + static_cast<int64_t>(c->dims[l]) * c->dims[l - 1], 64);
+    c->b_off[l] = off;
+    off = round_up(off + c->dims[l], 64);
+    c->ld[l] = round_up(c->dims[l], 64);
+  }
+  c->ld[0] = c->dims[0];
+  c->n_pad = off;
+  c->cursors.assign(K, 0);
+  c->samplers.resize(K);
+
+  hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess && c->bf16) {
+    void* p = nullptr;
+    e = dev_alloc(c, static_cast<size_t>(K) * c->n_pad * 2, &p);
+    c->wcopy = static_cast<uint16_t*>(p);
+  }
+  c->act.assign(c->L + 1, nullptr);
+  c->delta.assign(c->L + 1, nullptr);
+  for (int l = 1; l <= c->L && e == hipSuccess; ++l) {
+    const size_t n = static_cast<size_t>(K) * c->act_slot(l);
+    if (l < c->L) e = dev_alloc(c, n * c->esize, &c->act[l]);
+    if (e == hipSuccess) e = dev_alloc(c, n * c->esize, &c->delta[l]);
+  }
+  if (e == hipSuccess) {
+    void* p = nullptr;
+    e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(c->L) * 4, &p);
+    c->logits = static_cast<float*>(p);
+  }
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) {
+    free_ctx(c);
+    return e == hipErrorOutOfMemory ? OSCARS_E_NOMEM : hip_fail(e);
+  }
+  *out = c;
+  return OSCARS_OK;
+}
+
+void oscars_destroy(oscars_ctx* ctx) { free_ctx(ctx); }
+
+oscars_status oscars_set_stream(oscars_ctx* ctx, void* hip_stream) {
+  if (!ctx) return OSCARS_E_INVALID;
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  ctx->stream = static_cast<hipStream_t>(hip_stream);
+  return OSCARS_OK;
+}
+
+int64_t oscars_num_params(const oscars_ctx* ctx) { return ctx ? ctx->n_pad : -1; }
+
+oscars_status oscars_layer_offsets(const oscars_ctx* ctx, int32_t l, int64_t* w_off,
+                                   int64_t* b_off) {
+  if (!ctx || !w_off || !b_off || l < 1 || l > ctx->L) return OSCARS_E_INVALID;
+  *w_off = ctx->w_off[l];
+  *b_off = ctx->b_off[l];
+  return OSCARS_OK;
+}
+
+oscars_status oscars_get_cursors(const oscars_ctx* ctx, int64_t* steps_done) {
+  if (!ctx || !steps_done) return OSCARS_E_INVALID;
+  std::copy(ctx->cursors.begin(), ctx->cursors.end(), steps_done);
+  return OSCARS_OK;
+}
+
+oscars_status oscars_set_cursors(oscars_ctx* ctx, const int64_t* steps_done) {
+  if (!ctx || !steps_done) return OSCARS_E_INVALID;
+  for (int k = 0; k < ctx->K; ++k)
+    if (steps_done[k] < 0) return OSCARS_E_INVALID;
+  std::copy(steps_done, steps_done + ctx->K, ctx->cursors.begin());
+  return OSCARS_OK;
+}
+
+oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_shards* s,
+                                 const int32_t* tau, float lr, int32_t batch) {
+  // ---- validation (no side effects on failure) ----
+  if (!c || !replicas || !s || !tau || !s->x || !s->y || !s->offsets) return OSCARS_E_INVALID;
+  if (!aligned16(replicas) || !aligned16(s->x)) return OSCARS_E_INVALID;
+  if (!std::isfinite(lr) || !(lr > 0.0f)) return OSCARS_E_INVALID;
+  if (batch < 1 || batch > c->max_batch) return OSCARS_E_INVALID;
+  if (s->n_rows < 1 || s->n_rows > 0x7FFFFFFF) return OSCARS_E_INVALID;
+  const int K = c->K;
+  if (s->offsets[0] != 0 || s->offsets[K] != s->n_rows) return OSCARS_E_INVALID;
+  for (int k = 0; k < K; ++k) {
+    if (s->offsets[k + 1] <= s->offsets[k]) return OSCARS_E_INVALID;
+    if (tau[k] < 0 || tau[k] > kMaxTau) return OSCARS_E_INVALID;
+  }
+
+  // ---- slots: workers with work, by tau descending, ties by index ----
+  std::vector<int32_t> order;
+  for (int k = 0; k < K; ++k)
+    if (tau[k] > 0) order.push_back(k);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int32_t a, int32_t b) { return tau[a] > tau[b]; });
+  const int n_slots = static_cast<int>(order.size());
+  c->last_order = order;
+  c->last_tau.assign(tau, tau + K);
+  c->last_B = batch;
+  c->last_tau_max = n_slots ? tau[order[0]] : 0;
+  if (n_slots == 0) return OSCARS_OK;
+  const int tau_max = tau[order[0]];
+  const int B = batch;
+
+  // ---- index table: order[64] then rows[slot][j][b] ----
+  const int64_t need = 64 + static_cast<int64_t>(n_slots) * tau_max * B;
+  hipError_t e = hipSuccess;
+  if (c->upload_pending) {
+    e = hipEventSynchronize(c->upload_done);
+    if (e != hipSuccess) return hip_fail(e);
+    c->upload_pending = false;
+  }
+  if (need > c->pinned_cap) {
+    if (c->pinned) (void)hipHostFree(c->pinned);
+    c->pinned = nullptr;
+    c->pinned_cap = 0;
+    e = hipHostMalloc(reinterpret_cast<void**>(&c->pinned), need * sizeof(int32_t));
+    if (e != hipSuccess) return OSCARS_E_NOMEM;
+    c->pinned_cap = need;
+  }
+  const int64_t loss_need = static_cast<int64_t>(n_slots) * tau_max * B;
+  if (need > c->table_cap || loss_need > c->loss_cap) {
+    e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  if (need > c->table_cap) {
+    if (c->table_dev) (void)hipFree(c->table_dev);
+    c->table_dev = nullptr;
+    c->table_cap = 0;
+    e = hipMalloc(reinterpret_cast<void**>(&c->table_dev), need * sizeof(int32_t));
+    if (e != hipSuccess) return OSCARS_E_NOMEM;
+    c->table_cap = need;
+  }
+  if (loss_need > c->loss_cap) {
+    if (c->loss_dev) (void)hipFree(c->loss_dev);
+    c->loss_dev = nullptr;
+    c->loss_cap = 0;
+    e = hipMalloc(reinterpret_cast<void**>(&c->loss_dev), loss_need * sizeof(float));
+    if (e != hipSuccess) return OSCARS_E_NOMEM;
+    c->loss_cap = loss_need;
+  }
+  int32_t* h_order = c->pinned;
+  int32_t* h_rows = c->pinned + 64;
+  for (int z = 0; z < 64; ++z) h_order[z] = z < n_slots ? order[z] : 0;
+  for (int z = 0; z < n_slots; ++z) {
+    const int k = order[z];
+    WorkerSampler& ws = c->samplers[k];
+    ws.reset(s->seed, static_cast<uint32_t>(k), s->offsets[k], s->offsets[k + 1] - s->offsets[k]);
+    for (int j = 0; j < tau[k]; ++j)
+      for (int b = 0; b < B; ++b)
+        h_rows[(static_cast<int64_t>(z) * tau_max + j) * B + b] =
+            static_cast<int32_t>(ws.row((c->cursors[k] + j) * B + b));
+  }
+  e = hipMemcpyAsync(c->table_dev, c->pinned, need * sizeof(int32_t), hipMemcpyHostToDevice,
+                     c->stream);
+  if (e == hipSuccess) e = hipEventRecord(c->upload_done, c->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  c->upload_pending = true;
+  const int32_t* d_order = c->table_dev;
+  const int32_t* d_rows = c->table_dev + 64;
+
+  // ---- bf16 working copies of the active replicas ----
+  if (c->bf16) {
+    e = timed(c, OSCARS_KERNEL_CAST, [&] {
+      return launch_cast_bf16(replicas, c->n_pad, d_order, c->wcopy, c->n_pad, c->n_pad, n_slots,
+                              c->stream);
+    });
+    if (e != hipSuccess) return hip_fail(e);
+  }
+
+  const int L = c->L;
+  const int64_t rows_slot = static_cast<int64_t>(tau_max) * B;
+  for (int j = 0; j < tau_max; ++j) {
+    int ns = 0;
+    while (ns < n_slots && tau[order[ns]] > j) ++ns;
+    const int32_t* rows_j = d_rows + static_cast<int64_t>(j) * B;
+
+    auto weights = [&](GemmArgs& g, int l) {
+      if (c->bf16) {
+        g.b = c->wcopy + c->w_off[l];
+        g.b_by_order = 0;
+      } else {
+        g.b = replicas + c->w_off[l];
+        g.b_by_order = 1;
+      }
+      g.b_slot = c->n_pad;
+      g.b_ld = c->dims[l - 1];
+    };
+    auto common = [&](GemmArgs& g, int l) {
+      g.master = replicas;
+      g.master_slot = c->n_pad;
+      g.w_off = c->w_off[l];
+      g.b_off = c->b_off[l];
+      g.order = d_order;
+      g.lr = lr;
+    };
+
+    // forward
+    for (int l = 1; l <= L; ++l) {
+      GemmArgs g{};
+      g.M = B;
+      g.N = c->dims[l];
+      g.K = c->dims[l - 1];
+      if (l == 1) {
+        g.a = s->x;
+        g.a_ld = c->dims[0];
+        g.a_slot = 0;
+        g.gather = rows_j;
+        g.gather_slot = rows_slot;
+      } else {
+        g.a = c->act[l - 1];
+        g.a_ld = c->ld[l - 1];
+        g.a_slot = c->act_slot(l - 1);
+      }
+      weights(g, l);
+      common(g, l);
+      if (l < L) {
+        g.out = c->act[l];
+        g.relu = 1;
+        g.out_bf16 = c->bf16;
+      } else {
+        g.out = c->logits;
+        g.relu = 0;
+        g.out_bf16 = 0;
+      }
+      g.out_ld = c->ld[l];
+      g.out_slot = c->act_slot(l);
+      e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_gemm(g, GEMM_FWD, c->bf16, ns, c->stream); });
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    // loss gradient
+    e = timed(c, OSCARS_KERNEL_SOFTMAX, [&] {
+      return launch_softmax_ce(c->logits, c->ld[L], c->act_slot(L), c->dims[L], B, s->y, rows_j,
+                               rows_slot, c->delta[L], c->bf16, c->loss_dev + static_cast<int64_t>(j) * B,
+                               rows_slot, ns, c->stream);
+    });
+    if (e != hipSuccess) return hip_fail(e);
+    // backward, top layer first; dgrad(l) reads W_l before wgrad(l) updates it
+    for (int l = L; l >= 1; --l) {
+      if (l > 1) {
+        GemmArgs g{};
+        g.M = B;
+        g.N = c->dims[l - 1];
+        g.K = c->dims[l];
+        g.a = c->delta[l];
+        g.a_ld = c->ld[l];
+        g.a_slot = c->act_slot(l);
+        weights(g, l);
+        common(g, l);
+        g.out = c->delta[l - 1];
+        g.out_ld = c->ld[l - 1];
+        g.out_slot = c->act_slot(l - 1);
+        g.out_bf16 = c->bf16;
+        g.mask = c->act[l - 1];
+        g.mask_ld = c->ld[l - 1];
+        g.mask_slot = c->act_slot(l - 1);
+        e = timed(c, OSCARS_KERNEL_DGRAD,
+                  [&] { return launch_gemm(g, GEMM_DGRAD, c->bf16, ns, c->stream); });
+        if (e != hipSuccess) return hip_fail(e);
+      }
+      GemmArgs g{};
+      g.M = c->dims[l];
+      g.N = c->dims[l - 1];
+      g.K = B;
+      g.a = c->delta[l];
+      g.a_ld = c->ld[l];
+      g.a_slot = c->act_slot(l);
+      if (l == 1) {
+        g.b = s->x;
+        g.b_ld = c->dims[0];
+        g.b_slot = 0;
+        g.gather = rows_j;
+        g.gather_slot = rows_slot;
+      } else {
+        g.b = c->act[l - 1];
+        g.b_ld = c->ld[l - 1];
+        g.b_slot = c->act_slot(l - 1);
+      }
+      g.b_by_order = 0;
+      common(g, l);
+      g.wcopy = c->bf16 ? c->wcopy : nullptr;
+      g.wcopy_slot = c->n_pad;
+      e = timed(c, OSCARS_KERNEL_WGRAD,
+                [&] { return launch_gemm(g, GEMM_WGRAD, c->bf16, ns, c->stream); });
+      if (e != hipSuccess) return hip_fail(e);
+    }
+  }
+  for (int k = 0; k < K; ++k) c->cursors[k] += tau[k];
+  return OSCARS_OK;
+}
+
+oscars_status oscars_round_losses(oscars_ctx* c, float* losses) {
+  if (!c || !losses) return OSCARS_E_INVALID;
+  for (int k = 0; k < c->K; ++k) losses[k] = NAN;
+  const int n_slots = static_cast<int>(c->last_order.size());
+  if (n_slots == 0) return OSCARS_OK;
+  const int64_t cnt = static_cast<int64_t>(n_slots) * c->last_tau_max * c->last_B;
+  std::vector<float> h(cnt);
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e == hipSuccess)
+    e = hipMemcpy(h.data(), c->loss_dev, cnt * sizeof(float), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  for (int z = 0; z < n_slots; ++z) {
+    const int k = c->last_order[z];
+    double acc = 0.0;
+    for (int j = 0; j < c->last_tau[k]; ++j)
+      for (int b = 0; b < c->last_B; ++b)
+        acc += h[(static_cast<int64_t>(z) * c->last_tau_max + j) * c->last_B + b];
+    losses[k] = static_cast<float>(acc / (static_cast<double>(c->last_tau[k]) * c->last_B));
+  }
+  return OSCARS_OK;
+}
+
+oscars_status oscars_aggregate(float* global, float* replicas, const float* weights, int32_t K,
+                               int64_t n, int64_t ld, int32_t broadcast, void* hip_stream) {
+  if (!global || !replicas || !weights) return OSCARS_E_INVALID;
+  if (K < 1 || K > OSCARS_MAX_K || n < 1 || ld < n || ld % 4 != 0) return OSCARS_E_INVALID;
+  if (!aligned16(global) || !aligned16(replicas)) return OSCARS_E_INVALID;
+  for (int k = 0; k < K; ++k)
+    if (!std::isfinite(weights[k])) return OSCARS_E_INVALID;
+  const uintptr_t g0 = reinterpret_cast<uintptr_t>(global), g1 = g0 + n * sizeof(float);
+  const uintptr_t r0 = reinterpret_cast<uintptr_t>(replicas),
+                  r1 = r0 + ((K - 1) * ld + n) * sizeof(float);
+  if (g0 < r1 && r0 < g1) return OSCARS_E_INVALID;
+  hipError_t e = launch_aggregate(global, replicas, weights, K, n, ld, broadcast,
+                                  static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? OSCARS_OK : hip_fail(e);
+}
+
+oscars_status oscars_profile_begin(oscars_ctx* c, uint32_t kind_mask) {
+  if (!c || (kind_mask >> OSCARS_KERNEL_COUNT) != 0) return OSCARS_E_INVALID;
+  c->prof_mask = kind_mask;
+  c->prof_recs.clear();
+  while (c->ev_pool.size() < 512) {
+    hipEvent_t ev;
+    hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) return hip_fail(e);
+    c->ev_pool.push_back(ev);
+  }
+  return OSCARS_OK;
+}
+
+oscars_status oscars_profile_end(oscars_ctx* c, double* ms, int64_t* launches) {
+  if (!c || !ms || !launches) return OSCARS_E_INVALID;
+  for (int i = 0; i < OSCARS_KERNEL_COUNT; ++i) {
+    ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  for (const auto& r : c->prof_recs) {
+    float t = 0.0f;
+    e = hipEventElapsedTime(&t, c->ev_pool[r.second], c->ev_pool[r.second + 1]);
+    if (e != hipSuccess) return hip_fail(e);
+    ms[r.first] += t;
+    launches[r.first] += 1;
+  }
+  c->prof_mask = 0;
+  c->prof_recs.clear();
+  return OSCARS_OK;
+}
+
+int32_t oscars_last_hip_error(void) { return g_last_hip; }
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+"""Shared pieces of the GPU parity tests: run a workload through the C ABI and
+through the oracle on the same seeded inputs, and compare."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+import workload
+
+FP32_TOL = 1e-3   # parameters after min(R, 10) rounds and after R rounds, fp32 workloads
+BF16_TOL = 2e-2   # same, bf16-input workloads
+AGG_TOL = 1e-5    # per aggregation (bitwise is what is asserted where the tree is shared)
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def rel_err(a_layers, b_layers) -> float:
+    num = sum(float(np.sum((np.asarray(a, np.float64) - np.asarray(b, np.float64)) ** 2))
+              for la, lb in zip(a_layers, b_layers) for a, b in zip(la, lb))
+    den = sum(float(np.sum(np.asarray(b, np.float64) ** 2)) for lb in b_layers for b in lb)
+    return (num / den) ** 0.5
+
+
+def oracle_tau(cfg, rounds):
+    if cfg.tau_rule == "given":
+        return np.array([cfg.tau_given] * rounds)
+    if cfg.tau_rule == "speeds":
+        return np.array([oracle.load_balance(workload.speeds_to_t_iter(cfg.speeds), cfg.M)[1]]
+                        * rounds)
+    return workload.gen_tau_uniform(cfg)[:rounds]
+
+
+def gpu_rounds(cfg, ds, init, tau_rounds, check_agg=True):
+    """Run len(tau_rounds) rounds on the GPU.  After every round's local steps
+    the replicas are copied out and the GPU aggregate is compared bit for bit
+    with the oracle's tree over those same replicas.  Returns (list of global
+    layer lists per round, list of per-worker losses per round)."""
+    import torch
+
+    from paper_2102_08550_amd.rounds import OscarsRun
+    run = OscarsRun(cfg, ds, init)
+    globals_, losses = [], []
+    try:
+        for r, tau in enumerate(tau_rounds):
+            run.local_steps([int(t) for t in tau])
+            losses.append(run.ctx.round_losses())
+            reps = run.replicas.view(cfg.K, run.n).cpu().numpy() if check_agg else None
+            run.aggregate(True)
+            torch.cuda.synchronize()
+            g = run.g.cpu().numpy()
+            if check_agg:
+                expect = oracle.tree_aggregate([reps[k] for k in range(cfg.K)],
+                                               oracle.paper_weights(cfg.K))
+                assert np.array_equal(g.view(np.uint32), expect.view(np.uint32)), \
+                    f"round {r}: aggregate differs from the oracle tree"
+                back = run.replicas.view(cfg.K, run.n).cpu().numpy()
+                assert np.array_equal(back, np.broadcast_to(g, back.shape)), "broadcast"
+            globals_.append(run.ctx.unpack(g))
+    finally:
+        run.close()
+    return globals_, losses
+
+
+def oracle_rounds(cfg, ds, init, tau_rounds):
+    X = ds.x_f32().astype(np.float64)
+    out, g, s, losses = [], init, None, []
+    for tau in tau_rounds:
+        res = oracle.run_rounds(g, X, ds.y, cfg.K, np.array([tau]), cfg.lr, cfg.batch,
+                                workload.sampler_seed(cfg), cfg.dtype == workload.BF16,
+                                steps_done=s)
+        g, s = res.params, res.steps_done
+        out.append(g)
+        losses.append(res.losses[0])
+    return out, losses

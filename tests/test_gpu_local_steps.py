@@ -1,0 +1,235 @@
+"""GPU parity of the local SGD steps (Approach, Eq. 4, second branch) and of
+whole rounds against the oracle, on the same seeded inputs.
+
+Element-wise trajectories: the small workloads at full size, and the large
+ones with their layer widths scaled down (tiles still ragged in M, N and K).
+Full-size C3 / C5: the first round in the launch configuration the benchmark
+times; the worker with the fewest steps is recomputed by the oracle in full,
+and the aggregate is compared bit for bit with the oracle's tree."""
+import numpy as np
+import pytest
+
+import oracle
+import workload
+from _parity import (BF16_TOL, FP32_TOL, gpu_rounds, oracle_rounds, oracle_tau, rel_err, say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2102_08550_amd
+    return paper_2102_08550_amd
+
+
+TRAJ = {
+    "c1": workload.C1,
+    "c2": workload.C2,
+    "c3s": workload.scaled(workload.C3, dims=(3072, 264, 136, 10), n_rows=6400, rounds=4),
+    "c5s": workload.scaled(workload.C5, dims=(512, 392, 264, 200, 1000), n_rows=16000, rounds=3,
+                           batch=72),
+    "tiny-fp32": workload.Config("tiny-fp32", (8, 3), workload.FP32, K=3, n_rows=7, batch=1,
+                                 tau_rule="given", tau_given=(0, 2, 5), lr=0.3, rounds=3, seed=9),
+    "tiny-bf16": workload.Config("tiny-bf16", (16, 24, 37), workload.BF16, K=3, n_rows=40,
+                                 batch=5, tau_rule="given", tau_given=(4, 0, 1), lr=0.2, rounds=3,
+                                 seed=10),
+    "k1-sgd": workload.Config("k1-sgd", (40, 136, 10), workload.FP32, K=1, n_rows=300, batch=33,
+                              tau_rule="given", tau_given=(1,), lr=0.1, rounds=12, seed=11),
+}
+
+
+@pytest.mark.parametrize("name", list(TRAJ))
+def test_trajectory_matches_oracle(P, name):
+    cfg = TRAJ[name]
+    say(f"trajectory {name}: dims={cfg.dims} K={cfg.K} B={cfg.batch} R={cfg.rounds}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    from paper_2102_08550_amd.rounds import tau_schedule
+    tau = tau_schedule(cfg)
+    assert np.array_equal(tau, oracle_tau(cfg, cfg.rounds))
+    g_gpu, l_gpu = gpu_rounds(cfg, ds, init, tau)
+    g_ref, l_ref = oracle_rounds(cfg, ds, init, tau)
+    tol = BF16_TOL if cfg.dtype == workload.BF16 else FP32_TOL
+    errs = [rel_err(a, b) for a, b in zip(g_gpu, g_ref)]
+    say(f"  rel err per round: {[f'{e:.2e}' for e in errs]}")
+    checkpoints = sorted({min(cfg.rounds, 10) - 1, cfg.rounds - 1})
+    for r in checkpoints:
+        assert errs[r] <= tol, (r, errs[r])
+    for r in range(cfg.rounds):
+        for k in range(cfg.K):
+            if tau[r][k] == 0:
+                assert np.isnan(l_gpu[r][k])
+            else:
+                assert abs(l_gpu[r][k] - l_ref[r][k]) <= 5 * tol * max(1.0, abs(l_ref[r][k])), \
+                    (r, k, l_gpu[r][k], l_ref[r][k])
+
+
+def _run_once(P, cfg, ds, init, tau_rounds):
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    run = OscarsRun(cfg, ds, init)
+    for tau in tau_rounds:
+        run.local_steps([int(t) for t in tau])
+    torch.cuda.synchronize()
+    reps = run.replicas.view(cfg.K, run.n).cpu().numpy().copy()
+    cur = run.ctx.cursors()
+    run.close()
+    return reps, cur
+
+
+MASK_CFGS = [
+    workload.scaled(workload.C5, dims=(256, 136, 200), n_rows=2000, rounds=1, batch=40, K=5,
+                    tau_rule="given", tau_given=(3, 1, 0, 4, 2)),
+    workload.scaled(workload.C2, dims=(64, 72, 10), n_rows=900, rounds=1, batch=17, K=4,
+                    tau_rule="given", tau_given=(2, 5, 1, 3)),
+]
+
+
+@pytest.mark.parametrize("cfg", MASK_CFGS, ids=["bf16", "fp32"])
+def test_masking_independence_and_determinism(P, cfg):
+    """A replica's result does not depend on which other replicas run beside
+    it (grouped == solo, bit for bit); tau_k = 0 leaves a replica untouched;
+    two identical runs agree bit for bit."""
+    say(f"masking {cfg.dtype} tau={cfg.tau_given}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = np.array([cfg.tau_given])
+    grouped, cur = _run_once(P, cfg, ds, init, tau)
+    again, _ = _run_once(P, cfg, ds, init, tau)
+    assert np.array_equal(grouped.view(np.uint32), again.view(np.uint32))
+    assert cur == list(cfg.tau_given)
+    from paper_2102_08550_amd import Context
+    for k in range(cfg.K):
+        solo_tau = np.zeros((1, cfg.K), np.int32)
+        solo_tau[0, k] = cfg.tau_given[k]
+        solo, _ = _run_once(P, cfg, ds, init, solo_tau)
+        assert np.array_equal(solo[k].view(np.uint32), grouped[k].view(np.uint32)), k
+    # tau = 0 replica equals the initial model
+    ctx = Context(cfg.dims, 1 if cfg.dtype == "bf16" else 0, cfg.K, cfg.batch)
+    flat = ctx.pack(init)
+    ctx.close()
+    for k in range(cfg.K):
+        if cfg.tau_given[k] == 0:
+            assert np.array_equal(grouped[k], flat)
+
+
+def test_cursor_resume(P):
+    """Two rounds in one context equal one round, then a fresh context given
+    the saved cursors and replicas, then the second round (bit for bit)."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    cfg = workload.scaled(workload.C3, dims=(128, 72, 10), n_rows=500, batch=24, K=4, rounds=2,
+                          tau_rule="given")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    taus = [[3, 1, 4, 2], [2, 5, 1, 3]]
+    a = OscarsRun(cfg, ds, init)
+    for t in taus:
+        a.round(t)
+    torch.cuda.synchronize()
+    ref = a.g.cpu().numpy()
+    cur_a = a.ctx.cursors()
+    a.close()
+    b = OscarsRun(cfg, ds, init)
+    b.round(taus[0])
+    saved_g = b.g.clone()
+    saved_cur = b.ctx.cursors()
+    b.close()
+    c = OscarsRun(cfg, ds, init)
+    c.g.copy_(saved_g)
+    c.replicas.copy_(saved_g.repeat(cfg.K))
+    c.ctx.set_cursors(saved_cur)
+    c.round(taus[1])
+    torch.cuda.synchronize()
+    assert np.array_equal(c.g.cpu().numpy(), ref)
+    assert c.ctx.cursors() == cur_a == [5, 6, 5, 5]
+    c.close()
+
+
+def test_local_steps_rejects_bad_arguments(P):
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    cfg = workload.scaled(workload.C2, dims=(64, 72, 10), n_rows=400, batch=16, K=4, rounds=1,
+                          tau_rule="given")
+    ds = workload.gen_dataset(cfg)
+    run = OscarsRun(cfg, ds, workload.gen_init(cfg))
+    before = run.replicas.cpu().numpy().copy()
+    ctx = run.ctx
+    cases = [
+        dict(tau=[1, -1, 1, 1]),
+        dict(tau=[1, 1, 1, 5000]),
+        dict(lr=0.0),
+        dict(lr=float("nan")),
+        dict(batch=17),  # above max_batch
+        dict(batch=0),
+        dict(offsets=[0, 100, 100, 300, 400]),  # empty shard
+        dict(offsets=[0, 100, 200, 300, 399]),  # does not end at n_rows
+    ]
+    for c in cases:
+        args = dict(tau=[1, 1, 1, 1], lr=0.1, batch=16, offsets=run.offsets)
+        args.update(c)
+        with pytest.raises(P.OscarsError) as ei:
+            ctx.local_steps(run.replicas, run.x, run.y, args["offsets"], run.seed, args["tau"],
+                            args["lr"], args["batch"])
+        assert ei.value.status == P.E_INVALID, c
+    torch.cuda.synchronize()
+    assert np.array_equal(run.replicas.cpu().numpy(), before)
+    assert ctx.cursors() == [0, 0, 0, 0]
+    big = torch.zeros(cfg.K * run.n + 4, device="cuda")
+    with pytest.raises(P.OscarsError):  # 4-byte aligned, not 16-byte aligned replicas
+        ctx.local_steps(big[1:1 + cfg.K * run.n], run.x, run.y, run.offsets, run.seed, [1] * 4,
+                        0.1, 16)
+    run.close()
+    with pytest.raises(P.OscarsError):  # width not a multiple of 8
+        P.Context((60, 72, 10), P.FP32, 4, 16)
+    with pytest.raises(P.OscarsError):
+        P.Context((64, 72, 10), P.FP32, 65, 16)
+
+
+@pytest.mark.parametrize("name", ["c3", "c5"])
+def test_full_size_first_round(P, name):
+    """Full-size workload, benchmark launch configuration, first round."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun, tau_schedule
+    cfg = workload.CONFIGS[name]
+    say(f"full-size {cfg.name}: generating data")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = tau_schedule(cfg)[0]
+    run = OscarsRun(cfg, ds, init)
+    say(f"  local steps tau={tau.tolist()}")
+    run.local_steps(tau.tolist())
+    losses = run.ctx.round_losses()
+    reps = run.replicas.view(cfg.K, run.n).cpu().numpy()
+    run.aggregate(True)
+    torch.cuda.synchronize()
+    g = run.g.cpu().numpy()
+    cur = run.ctx.cursors()
+    run.close()
+    assert cur == tau.tolist()
+    say("  aggregate vs oracle tree")
+    expect = oracle.tree_aggregate([reps[k] for k in range(cfg.K)], oracle.paper_weights(cfg.K))
+    assert np.array_equal(g.view(np.uint32), expect.view(np.uint32))
+    k = int(np.argmin(tau))
+    say(f"  oracle recomputes worker {k} ({tau[k]} steps)")
+    X = ds.x_f32()
+    off = oracle.shard_offsets(cfg.n_rows, cfg.K)
+    x_ref, loss_ref = oracle.worker_local_steps(
+        [(W.astype(np.float64), b.astype(np.float64)) for W, b in init], X, ds.y, off,
+        workload.sampler_seed(cfg), k, 0, int(tau[k]), cfg.lr, cfg.batch, True)
+    from paper_2102_08550_amd import Context
+    ctx = Context(cfg.dims, P.BF16, 1, 1)
+    got = ctx.unpack(reps[k])
+    ctx.close()
+    err = rel_err(got, x_ref)
+    # change made by the step, against the oracle's change
+    step_err = rel_err([(a - W0, c - b0) for (a, c), (W0, b0) in zip(got, init)],
+                       [(a - W0, c - b0) for (a, c), (W0, b0) in zip(x_ref, init)])
+    say(f"  worker {k}: rel err {err:.3e}, rel err of the update {step_err:.3e}, "
+        f"loss {losses[k]:.5f} vs {loss_ref:.5f}")
+    assert err <= BF16_TOL
+    assert step_err <= 5e-2
+    assert abs(losses[k] - loss_ref) <= 1e-2 * abs(loss_ref)
+    assert np.all(np.isfinite(losses))
