@@ -1,0 +1,265 @@
+"""Benchmark of the Oscars local-SGD hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload c5]
+
+A step is one Oscars round over the whole hot path: Algorithm 1 (tau from the
+workers' iteration times), the mini-batch index table, tau_k local SGD steps
+of every simulated worker (forward, loss gradient, backward-data,
+backward-weight + SGD update, finished workers masked out), and the
+parameter-server aggregation with broadcast.  Inputs are resident in HBM
+before the timed region.  Prints one JSON line.
+
+Default workload: MLP 4096-4096-4096-4096-1000, bf16 inputs/weights with fp32
+accumulation and fp32 masters, K = 8 workers with speed factors
+1,1,2,2,3,4,6,8, batch 256, 200k-sample 1000-class Gaussian mixture, plus the
+aggregation of the 54.4M-parameter model every round.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
+PMC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+
+
+def gemm_work(cfg, tau):
+    """Algorithmic FLOPs and bytes of every GEMM launch of one round, per kind.
+    Bytes: each operand read once, each result written once (weights bf16 in
+    the products of bf16 workloads; fp32 master read and write in the update)."""
+    import numpy as np
+    es = 2 if cfg.dtype == "bf16" else 4
+    B, dims = cfg.batch, cfg.dims
+    L = len(dims) - 1
+    work = {"gemm_fwd": [0.0, 0.0], "gemm_dgrad": [0.0, 0.0], "gemm_wgrad_update": [0.0, 0.0],
+            "softmax_ce": [0.0, 0.0], "cast_bf16": [0.0, 0.0]}
+    tau = np.asarray(tau)
+    n_params = sum(o * i + o for i, o in zip(dims[:-1], dims[1:]))
+    if cfg.dtype == "bf16":
+        work["cast_bf16"][1] += int((tau > 0).sum()) * n_params * 6.0
+    for j in range(int(tau.max())):
+        ns = int((tau > j).sum())
+        for l in range(1, L + 1):
+            i, o = dims[l - 1], dims[l]
+            out_es = es if l < L else 4
+            work["gemm_fwd"][0] += ns * 2.0 * B * o * i
+            work["gemm_fwd"][1] += ns * (es * o * i + 4 * o + es * B * i + out_es * B * o)
+            if l > 1:
+                work["gemm_dgrad"][0] += ns * 2.0 * B * o * i
+                work["gemm_dgrad"][1] += ns * (es * o * i + es * B * o + 2 * es * B * i)
+            work["gemm_wgrad_update"][0] += ns * 2.0 * B * o * i
+            work["gemm_wgrad_update"][1] += ns * (8.0 * (o * i + o) + (2.0 * o * i if es == 2 else 0)
+                                                  + es * B * o + es * B * i)
+        C = dims[-1]
+        work["softmax_ce"][1] += ns * B * (4 * C + es * C)
+    return work
+
+
+def kernel_source_hash() -> str:
+    p = os.path.join(ROOT, "paper_2102_08550_amd", "csrc", "kernels.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def pmc_traffic(kernel: str, workload_name: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    try:
+        data = json.load(open(PMC_FILE))
+    except (OSError, ValueError):
+        return None
+    ent = data.get(workload_name, {}).get(kernel)
+    if not ent or ent.get("kernels_sha256_16") != kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, ds, init, tau, budget_s: float):
+    """The oracle as it stands, on the host cores: worker steps of the first
+    round (the worker with the most steps) until the time budget is used, and
+    the oracle aggregation on a slice of K replicas."""
+    import numpy as np
+
+    import oracle
+    import workload
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
+    except Exception:
+        threads = os.cpu_count() or 1
+    k = int(np.argmax(tau))
+    off = oracle.shard_offsets(cfg.n_rows, cfg.K)
+    seed = workload.sampler_seed(cfg)
+    x = [(W.astype(np.float64), b.astype(np.float64)) for W, b in init]
+    t0 = time.perf_counter()
+    steps = 0
+    cache = {}
+    while steps < int(tau[k]):
+        rows = oracle.batch_rows(seed, off, k, steps, cfg.batch, cache)
+        xb = workload.bf16_bits_to_f32(ds.x[rows]) if cfg.dtype == "bf16" else ds.x[rows]
+        x, _ = oracle.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr, cfg.dtype == "bf16")
+        steps += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    n_slice = 4_000_000
+    reps = [np.random.default_rng(i).standard_normal(n_slice).astype(np.float32)
+            for i in range(cfg.K)]
+    t1 = time.perf_counter()
+    oracle.tree_aggregate(reps, oracle.paper_weights(cfg.K))
+    dta = time.perf_counter() - t1
+    return {
+        "value": steps * cfg.batch / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
+        "sample": f"worker {k}: {steps} local SGD step(s) of batch {cfg.batch} from the initial "
+                  f"model ({dt:.1f} s, float64 with bf16 rounding points); aggregation of "
+                  f"{cfg.K} x {n_slice} fp32 slices",
+        "aggregate_GBps": (cfg.K + 1) * n_slice * 4 / dta / 1e9,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c5"])
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="seconds of oracle work for the CPU baseline (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workload
+    import paper_2102_08550_amd as P
+    from paper_2102_08550_amd.rounds import OscarsRun
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = workload.CONFIGS[args.workload]
+    print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    stream = torch.cuda.current_stream()
+    run = OscarsRun(cfg, ds, init, stream=stream)
+
+    def tau_for(step):
+        if cfg.tau_rule == "speeds":  # Algorithm 1 from the workers' iteration times
+            return P.load_balance(workload.speeds_to_t_iter(cfg.speeds), cfg.M)[1]
+        if cfg.tau_rule == "given":
+            return list(cfg.tau_given)
+        draws = workload.gen_tau_uniform(cfg)
+        return draws[step % len(draws)].tolist()
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for s in range(args.warmup):
+        run.round(tau_for(s))
+    torch.cuda.synchronize()
+
+    kinds = [P.KERNEL_CAST, P.KERNEL_FWD, P.KERNEL_SOFTMAX, P.KERNEL_DGRAD, P.KERNEL_WGRAD]
+    agg_events = []
+    samples = 0
+    work_tot = {}
+    print(f"[bench] timing {args.steps} rounds", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    run.ctx.profile_begin(kinds)
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        tau = tau_for(args.warmup + s)
+        run.local_steps(tau)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run.aggregate(True)
+        e1.record(stream)
+        agg_events.append((e0, e1))
+        samples += int(np.sum(tau)) * cfg.batch
+        for kname, (fl, by) in gemm_work(cfg, tau).items():
+            a = work_tot.setdefault(kname, [0.0, 0.0])
+            a[0] += fl
+            a[1] += by
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = run.ctx.profile_end()
+    elapsed = t1 - t0
+    ms_per_step = elapsed * 1000.0 / args.steps
+
+    agg_ms = sum(a.elapsed_time(b) for a, b in agg_events)
+    n = run.n
+    agg_bytes = args.steps * (2 * cfg.K + 1) * n * 4.0
+    kernels = {}
+    for name, (ms, cnt) in prof.items():
+        if cnt == 0:
+            continue
+        fl, by = work_tot.get(name, [0.0, 0.0])
+        kernels[name] = {"ms": ms, "launches": cnt, "avg_us": ms * 1000.0 / cnt,
+                         "TFLOPs": fl / (ms / 1e3) / 1e12 if fl else None,
+                         "GBps": by / (ms / 1e3) / 1e9 if by else None,
+                         "flop_per_launch": fl / cnt, "bytes_per_launch": by / cnt}
+    kernels["aggregate"] = {"ms": agg_ms, "launches": args.steps,
+                            "avg_us": agg_ms * 1000.0 / args.steps, "TFLOPs": None,
+                            "GBps": agg_bytes / (agg_ms / 1e3) / 1e9,
+                            "flop_per_launch": 0.0, "bytes_per_launch": agg_bytes / args.steps}
+    dom = max(kernels, key=lambda k: kernels[k]["ms"])
+    d = kernels[dom]
+    ridge = MFMA_PEAK_TFLOPS[cfg.dtype] * 1e12 / (HBM_PEAK_GBPS * 1e9)
+    intensity = d["flop_per_launch"] / d["bytes_per_launch"] if d["bytes_per_launch"] else 0.0
+    if intensity > ridge:
+        roof = {"bound": "mfma", "achieved": d["TFLOPs"], "peak": MFMA_PEAK_TFLOPS[cfg.dtype],
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": d["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = pmc_traffic(dom, args.workload)
+    roof["kernel"] = dom
+    roof["avg_launch_us"] = d["avg_us"]
+    roof["algorithmic_per_launch"] = {"flop": d["flop_per_launch"], "bytes": d["bytes_per_launch"]}
+
+    local_ms = sum(v["ms"] for k, v in kernels.items() if k != "aggregate")
+    flops = sum(v[0] for v in work_tot.values())
+    out = {
+        "metric": "local-SGD samples/sec (K sim workers, 1 GPU); aggregation GB/s vs HBM peak",
+        "value": samples / elapsed,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded Gaussian mixture, random init)",
+        "config": {"workload": cfg.name, "dims": list(cfg.dims), "K": cfg.K, "batch": cfg.batch,
+                   "tau": tau_for(0), "lr": cfg.lr, "n_params": cfg.n_params,
+                   "samples_per_round": samples // args.steps, "parallelism": "1 GPU, K simulated"},
+        "aggregation": {"GBps": agg_bytes / (agg_ms / 1e3) / 1e9,
+                        "frac_hbm_peak": agg_bytes / (agg_ms / 1e3) / 1e9 / HBM_PEAK_GBPS,
+                        "avg_us": agg_ms * 1000.0 / args.steps, "bytes_per_round": agg_bytes / args.steps},
+        "local_steps": {"kernel_ms_per_round": local_ms / args.steps,
+                        "TFLOPs": flops / (local_ms / 1e3) / 1e12 if local_ms else None,
+                        "frac_mfma_peak": flops / (local_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[cfg.dtype]
+                        if local_ms else None,
+                        "samples_per_s_kernels": samples / (local_ms / 1e3) if local_ms else None},
+        "kernels": kernels,
+        "roofline": roof,
+    }
+    losses = run.ctx.round_losses()
+    out["last_round_mean_loss"] = float(np.nanmean(losses))
+    run.close()
+    if args.cpu_budget > 0:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(cfg, ds, init, np.asarray(tau_for(0)), args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -35,12 +35,19 @@ Params = List[Tuple[np.ndarray, np.ndarray]]
 
 
 def bf16_round(a: np.ndarray) -> np.ndarray:
-    """float64 -> float32 -> bf16 (round to nearest, ties to even), returned as float64."""
+    """float64 -> float32 -> bf16 (round to nearest, ties to even), returned as float64.
+
+    On the float32 bit pattern u: add 0x7FFF plus the lowest kept bit, then
+    clear the low 16 bits.  Finite patterns are below 0xFF800000, so the sum
+    cannot wrap; NaN is kept as NaN and +-inf stay infinite."""
     f = np.asarray(a, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = ((u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
-    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+    u = f.view(np.uint32)
+    r = (u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
+    out = r.view(np.float32)
+    nan = np.isnan(f)
+    if nan.any():
+        out[nan] = np.nan
+    return out.astype(np.float64)
 
 
 def _identity(a: np.ndarray) -> np.ndarray:

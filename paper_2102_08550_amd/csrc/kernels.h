@@ -9,31 +9,32 @@ namespace oscars {
 
 enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };
 
-// One grouped GEMM launch over `n_slots` replicas (grid z = slot).  Slot z
-// works on replica order[z].  Every "per-slot" pointer below is the slot-0
-// address; the kernel adds z times the matching stride.
+// One grouped GEMM launch over `n_slots` replicas (grid y = slot).  Slot z
+// works on replica order[z].  Every per-slot pointer is the slot-0 address;
+// the kernel adds z (or order[z] where *_by_order is set) times its stride.
+// C[m][n] = sum_k A(m, k) B(n, k); the M side is always a weight dimension so
+// that each lane's four consecutive accumulator rows are four consecutive
+// elements in memory (weights and activations are both stored with the
+// feature index fastest).
 //
-//   FWD   C[b][o] = A[b][:] . W[o][:] + bias[o]  (ReLU if relu), stored to out
-//         A: activations [M=B][K=in] (row stride a_ld), or dataset rows
-//            x[gather[b]] when gather != nullptr; W: [N=out][K=in].
-//   DGRAD C[b][i] = sum_o D[b][o] W[o][i], zeroed where mask[b][i] <= 0
-//         D: [M=B][K=out] (a_ld), W: [K=out][N=in] (b_ld = in).
-//   WGRAD dW[o][i] = sum_b D[b][o] A[b][i];  W <- W - lr dW (fp32 master),
-//         bias <- bias - lr sum_b D[b][o]; bf16 copy of W refreshed if any.
-//         D: [K=B][M=out] (a_ld), A: [K=B][N=in] (b_ld) or x[gather[b]].
+//   FWD   C[o][b] = sum_i W[o][i] act[b][i];  out[b][o] = C + bias[o]
+//         (ReLU if relu).  A = W [M=out][K=in]; B = act [N=batch][K=in]
+//         (b_ld), or dataset rows x[gather[b]] when gather != nullptr.
+//   DGRAD C[i][b] = sum_o W[o][i] D[b][o];  out[b][i] = C where
+//         mask[b][i] > 0, else 0.  A = W as [K=out][M=in]; B = D [N=batch][K=out].
+//   WGRAD C[i][o] = sum_b act[b][i] D[b][o] = dW[o][i];  W <- W - lr dW
+//         (fp32 master), bias[o] <- bias[o] - lr sum_b D[b][o], bf16 copy of
+//         W refreshed if wcopy.  A = act as [K=batch][M=in] (or x[gather[b]]);
+//         B = D as [K=batch][N=out].
 struct GemmArgs {
   int M, N, K;
-  // operand A (FWD: activations / x; DGRAD: delta; WGRAD: delta)
-  const void* a;
+  const void* a;  // operand A (FWD, DGRAD: weights; WGRAD: activations / x)
   int64_t a_ld, a_slot;
-  // operand B (FWD, DGRAD: weights; WGRAD: activations / x)
-  const void* b;
+  int a_by_order;  // a's slot offset uses order[z] (fp32 masters) instead of z
+  const void* b;  // operand B (FWD: activations / x; DGRAD, WGRAD: delta)
   int64_t b_ld, b_slot;
-  int b_by_order;  // b's slot offset uses order[z] (fp32 masters) instead of z
-  // row gather of the dataset operand (FWD: A rows; WGRAD: B rows)
-  const int32_t* gather;
+  const int32_t* gather;  // dataset rows of the batch (FWD: B rows; WGRAD: A's k rows)
   int64_t gather_slot;
-  // outputs / epilogue inputs
   void* out;  // FWD: activations or logits; DGRAD: delta of the layer below
   int64_t out_ld, out_slot;
   const void* mask;  // DGRAD: activations of the layer below

@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/oscars.h"
 #include "kernels.h"
 
@@ -196,6 +198,12 @@ __device__ __forceinline__ void mma_tile(const uint32_t* As, const uint32_t* Bs,
   }
 }
 
+// Linear tile index -> tile, so that the workgroups the hardware places on
+// one XCD (linear id mod 8) take consecutive tiles, which share an A tile.
+__device__ __forceinline__ int xcd_tile(int L, int T) {
+  return (T % 8 == 0) ? (L % 8) * (T / 8) + L / 8 : L;
+}
+
 template <bool BF16, int MODE>
 __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
   typedef typename El<BF16>::T T;
@@ -203,22 +211,56 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[2][2][TILE_U32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int z = blockIdx.z;
+  const int wm = wave >> 1, wn = wave & 1, h = lane >> 5;
+  const int z = blockIdx.y;
   const int rep = g.order[z];
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int M = g.M, N = g.N, K = g.K;
+  const int gn = (N + BN - 1) / BN;
+  const int t = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (t / gn) * BM, n0 = (t % gn) * BN;
 
-  const T* A = static_cast<const T*>(g.a) + z * g.a_slot;
-  const T* B = static_cast<const T*>(g.b) + (g.b_by_order ? rep : z) * g.b_slot;
+  const T* A = static_cast<const T*>(g.a) + (g.a_by_order ? rep : z) * g.a_slot;
+  const T* B = static_cast<const T*>(g.b) + z * g.b_slot;
   const int32_t* gat = g.gather ? g.gather + z * g.gather_slot : nullptr;
-  const int32_t* gatA = (MODE == GEMM_FWD) ? gat : nullptr;
-  const int32_t* gatB = (MODE == GEMM_WGRAD) ? gat : nullptr;
+  float* master = g.master + static_cast<int64_t>(rep) * g.master_slot;
 
-  // Operand A: K-contiguous in FWD/DGRAD, M-contiguous (delta [B][out]) in WGRAD.
-  // Operand B: K-contiguous in FWD, N-contiguous in DGRAD (W) and WGRAD (acts).
-  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16>, RowTile<BF16>>::type ta;
-  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16>, TransTile<BF16>>::type tb;
+  // A: weights K-contiguous in FWD, weights M-contiguous in DGRAD, activations
+  // M-contiguous in WGRAD.  B: activations / delta K-contiguous in FWD and
+  // DGRAD, delta N-contiguous in WGRAD.
+  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16>, TransTile<BF16>>::type ta;
+  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16>, RowTile<BF16>>::type tb;
+  const int32_t* gatA = (MODE == GEMM_WGRAD) ? gat : nullptr;
+  const int32_t* gatB = (MODE == GEMM_FWD) ? gat : nullptr;
+
+  // Accumulator element (i, j, r) sits at row m = mrow(i, r>>2) + (r & 3),
+  // column n = ncol(j): four consecutive rows per lane and group r>>2.
+  auto mrow = [&](int i, int q) { return m0 + wm * 64 + 32 * i + 8 * q + 4 * h; };
+  auto ncol = [&](int j) { return n0 + wn * 64 + 32 * j + (lane & 31); };
+
+  // WGRAD: the fp32 master tile is fetched before the K loop so that its HBM
+  // latency overlaps the products.
+  f32x4 wpre[2][2][4];
+  if constexpr (MODE == GEMM_WGRAD) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = mrow(i, q), n = ncol(j);
+          f32x4 w = {0.0f, 0.0f, 0.0f, 0.0f};
+          if (n < N) {
+            const float* p = master + g.w_off + static_cast<int64_t>(n) * M + m;
+            if (m + 3 < M) {
+              w = *reinterpret_cast<const f32x4*>(p);
+            } else {
+              for (int e = 0; e < 4; ++e)
+                if (m + e < M) w[e] = p[e];
+            }
+          }
+          wpre[i][j][q] = w;
+        }
+  }
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -228,7 +270,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const bool bias_wg = (MODE == GEMM_WGRAD) && blockIdx.x == 0;
+  const bool bias_wg = (MODE == GEMM_WGRAD) && m0 == 0;
   float dbias = 0.0f;
 
   const int nk = (K + BK - 1) / BK;
@@ -246,11 +288,11 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
       tb.load(B, g.b_ld, gatB, n0, N, (kt + 1) * BK, K, tid);
     }
     mma_tile<BF16>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
-    if (bias_wg && tid < BM) {
-      // db[o] = sum_b delta[b][o]: row tid of the A tile, in k order.
+    if (bias_wg && tid < BN) {
+      // db[o] = sum_b delta[b][o]: row tid of the B tile, in k order.
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(&lds[buf][0][lds_word(tid, c)]);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(&lds[buf][1][lds_word(tid, c)]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if constexpr (BF16) {
@@ -269,50 +311,84 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  // Epilogue.  MFMA 32x32 accumulator: lane l holds column l & 31 and rows
-  // 8 (r >> 2) + 4 (l >> 5) + (r & 3), r = 0..15.
-  float* master = g.master + static_cast<int64_t>(rep) * g.master_slot;
+  // Epilogue, one group of four consecutive rows m..m+3 at column n at a time.
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int n = n0 + wn * 64 + 32 * j + (lane & 31);
+      const int n = ncol(j);
+      if (n >= N) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (m >= M || n >= N) continue;
-        const float v = acc[i][j][r];
+      for (int q = 0; q < 4; ++q) {
+        const int m = mrow(i, q);
+        if (m >= M) continue;
+        const int cnt = (M - m >= 4) ? 4 : M - m;
+        f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                   acc[i][j][4 * q + 3]};
         if constexpr (MODE == GEMM_FWD) {
-          float o = v + master[g.b_off + n];
-          if (g.relu) o = fmaxf(o, 0.0f);
-          const int64_t at = z * g.out_slot + static_cast<int64_t>(m) * g.out_ld + n;
-          if (g.out_bf16)
-            static_cast<uint16_t*>(g.out)[at] = static_cast<uint16_t>(f2bf(o));
-          else
-            static_cast<float*>(g.out)[at] = o;
+          // out[b = n][o = m..m+3]
+          const float* bias = master + g.b_off + m;
+          for (int e = 0; e < 4; ++e) {
+            float o = v[e] + (e < cnt ? bias[e] : 0.0f);
+            v[e] = g.relu ? fmaxf(o, 0.0f) : o;
+          }
         } else if constexpr (MODE == GEMM_DGRAD) {
-          const int64_t am = z * g.mask_slot + static_cast<int64_t>(m) * g.mask_ld + n;
-          const T mk = static_cast<const T*>(g.mask)[am];
-          bool pos;
-          if constexpr (BF16) pos = mk != 0 && (mk & 0x8000u) == 0;
-          else pos = mk > 0.0f;
-          const float o = pos ? v : 0.0f;
-          const int64_t at = z * g.out_slot + static_cast<int64_t>(m) * g.out_ld + n;
-          if (g.out_bf16)
-            static_cast<uint16_t*>(g.out)[at] = static_cast<uint16_t>(f2bf(o));
-          else
-            static_cast<float*>(g.out)[at] = o;
+          const int64_t am = z * g.mask_slot + static_cast<int64_t>(n) * g.mask_ld + m;
+          const T* mk = static_cast<const T*>(g.mask) + am;
+          for (int e = 0; e < 4; ++e) {
+            bool pos = false;
+            if (e < cnt) {
+              if constexpr (BF16) pos = mk[e] != 0 && (mk[e] & 0x8000u) == 0;
+              else pos = mk[e] > 0.0f;
+            }
+            v[e] = pos ? v[e] : 0.0f;
+          }
+        }
+        if constexpr (MODE == GEMM_WGRAD) {
+          // W[o = n][i = m..m+3] <- W - lr dW, from the prefetched tile
+          const int64_t at = g.w_off + static_cast<int64_t>(n) * M + m;
+          f32x4 w = wpre[i][j][q];
+          for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, v[e], w[e]);
+          if (cnt == 4) {
+            *reinterpret_cast<f32x4*>(master + at) = w;
+            if (g.wcopy) {
+              uint2 o;
+              o.x = f2bf(w[0]) | (f2bf(w[1]) << 16);
+              o.y = f2bf(w[2]) | (f2bf(w[3]) << 16);
+              *reinterpret_cast<uint2*>(g.wcopy + z * g.wcopy_slot + at) = o;
+            }
+          } else {
+            for (int e = 0; e < cnt; ++e) {
+              master[at + e] = w[e];
+              if (g.wcopy) g.wcopy[z * g.wcopy_slot + at + e] = static_cast<uint16_t>(f2bf(w[e]));
+            }
+          }
         } else {
-          const int64_t at = g.w_off + static_cast<int64_t>(m) * N + n;
-          const float w = fmaf(-g.lr, v, master[at]);
-          master[at] = w;
-          if (g.wcopy) g.wcopy[z * g.wcopy_slot + at] = static_cast<uint16_t>(f2bf(w));
+          const int64_t at = z * g.out_slot + static_cast<int64_t>(n) * g.out_ld + m;
+          if (g.out_bf16) {
+            uint16_t* o = static_cast<uint16_t*>(g.out) + at;
+            if (cnt == 4) {
+              uint2 pk;
+              pk.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+              pk.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+              *reinterpret_cast<uint2*>(o) = pk;
+            } else {
+              for (int e = 0; e < cnt; ++e) o[e] = static_cast<uint16_t>(f2bf(v[e]));
+            }
+          } else {
+            float* o = static_cast<float*>(g.out) + at;
+            if (cnt == 4) {
+              *reinterpret_cast<f32x4*>(o) = v;
+            } else {
+              for (int e = 0; e < cnt; ++e) o[e] = v[e];
+            }
+          }
         }
       }
     }
   }
-  if (bias_wg && tid < BM && m0 + tid < M) {
-    float* bp = master + g.b_off + m0 + tid;
+  if (bias_wg && tid < BN && n0 + tid < N) {
+    float* bp = master + g.b_off + n0 + tid;
     *bp = fmaf(-g.lr, dbias, *bp);
   }
 }
@@ -447,7 +523,7 @@ hipError_t agg_launch(float* g, float* reps, const AggWeights& w, int K, int64_t
 
 template <bool BF16, int MODE>
 hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
-  const dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, n_slots);
+  const dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM), n_slots);
   hipLaunchKernelGGL((gemm_kernel<BF16, MODE>), grid, dim3(NTHR), 0, s, g);
   return hipGetLastError();
 }

@@ -329,16 +329,18 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
     while (ns < n_slots && tau[order[ns]] > j) ++ns;
     const int32_t* rows_j = d_rows + static_cast<int64_t>(j) * B;
 
+    // Weights as operand A: slot-indexed bf16 copies, or the fp32 masters
+    // themselves (reached through order[]).
     auto weights = [&](GemmArgs& g, int l) {
       if (c->bf16) {
-        g.b = c->wcopy + c->w_off[l];
-        g.b_by_order = 0;
+        g.a = c->wcopy + c->w_off[l];
+        g.a_by_order = 0;
       } else {
-        g.b = replicas + c->w_off[l];
-        g.b_by_order = 1;
+        g.a = replicas + c->w_off[l];
+        g.a_by_order = 1;
       }
-      g.b_slot = c->n_pad;
-      g.b_ld = c->dims[l - 1];
+      g.a_slot = c->n_pad;
+      g.a_ld = c->dims[l - 1];
     };
     auto common = [&](GemmArgs& g, int l) {
       g.master = replicas;
@@ -349,24 +351,24 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
       g.lr = lr;
     };
 
-    // forward
+    // forward: C[o][b] = W_l . act_{l-1}
     for (int l = 1; l <= L; ++l) {
       GemmArgs g{};
-      g.M = B;
-      g.N = c->dims[l];
+      g.M = c->dims[l];
+      g.N = B;
       g.K = c->dims[l - 1];
+      weights(g, l);
       if (l == 1) {
-        g.a = s->x;
-        g.a_ld = c->dims[0];
-        g.a_slot = 0;
+        g.b = s->x;
+        g.b_ld = c->dims[0];
+        g.b_slot = 0;
         g.gather = rows_j;
         g.gather_slot = rows_slot;
       } else {
-        g.a = c->act[l - 1];
-        g.a_ld = c->ld[l - 1];
-        g.a_slot = c->act_slot(l - 1);
+        g.b = c->act[l - 1];
+        g.b_ld = c->ld[l - 1];
+        g.b_slot = c->act_slot(l - 1);
       }
-      weights(g, l);
       common(g, l);
       if (l < L) {
         g.out = c->act[l];
@@ -392,14 +394,15 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
     // backward, top layer first; dgrad(l) reads W_l before wgrad(l) updates it
     for (int l = L; l >= 1; --l) {
       if (l > 1) {
+        // C[i][b] = sum_o W_l[o][i] delta_l[b][o], masked by act_{l-1} > 0
         GemmArgs g{};
-        g.M = B;
-        g.N = c->dims[l - 1];
+        g.M = c->dims[l - 1];
+        g.N = B;
         g.K = c->dims[l];
-        g.a = c->delta[l];
-        g.a_ld = c->ld[l];
-        g.a_slot = c->act_slot(l);
         weights(g, l);
+        g.b = c->delta[l];
+        g.b_ld = c->ld[l];
+        g.b_slot = c->act_slot(l);
         common(g, l);
         g.out = c->delta[l - 1];
         g.out_ld = c->ld[l - 1];
@@ -412,25 +415,26 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
                   [&] { return launch_gemm(g, GEMM_DGRAD, c->bf16, ns, c->stream); });
         if (e != hipSuccess) return hip_fail(e);
       }
+      // C[i][o] = sum_b act_{l-1}[b][i] delta_l[b][o] = dW_l[o][i], fused SGD update
       GemmArgs g{};
-      g.M = c->dims[l];
-      g.N = c->dims[l - 1];
+      g.M = c->dims[l - 1];
+      g.N = c->dims[l];
       g.K = B;
-      g.a = c->delta[l];
-      g.a_ld = c->ld[l];
-      g.a_slot = c->act_slot(l);
       if (l == 1) {
-        g.b = s->x;
-        g.b_ld = c->dims[0];
-        g.b_slot = 0;
+        g.a = s->x;
+        g.a_ld = c->dims[0];
+        g.a_slot = 0;
         g.gather = rows_j;
         g.gather_slot = rows_slot;
       } else {
-        g.b = c->act[l - 1];
-        g.b_ld = c->ld[l - 1];
-        g.b_slot = c->act_slot(l - 1);
+        g.a = c->act[l - 1];
+        g.a_ld = c->ld[l - 1];
+        g.a_slot = c->act_slot(l - 1);
       }
-      g.b_by_order = 0;
+      g.a_by_order = 0;
+      g.b = c->delta[l];
+      g.b_ld = c->ld[l];
+      g.b_slot = c->act_slot(l);
       common(g, l);
       g.wcopy = c->bf16 ? c->wcopy : nullptr;
       g.wcopy_slot = c->n_pad;
@@ -485,7 +489,7 @@ oscars_status oscars_profile_begin(oscars_ctx* c, uint32_t kind_mask) {
   if (!c || (kind_mask >> OSCARS_KERNEL_COUNT) != 0) return OSCARS_E_INVALID;
   c->prof_mask = kind_mask;
   c->prof_recs.clear();
-  while (c->ev_pool.size() < 512) {
+  while (c->ev_pool.size() < 8192) {
     hipEvent_t ev;
     hipError_t e = hipEventCreate(&ev);
     if (e != hipSuccess) return hip_fail(e);

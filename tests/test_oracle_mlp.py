@@ -89,10 +89,13 @@ def test_bf16_round_matches_torch():
     x = rng.standard_normal(20000) * np.exp(rng.uniform(-30, 30, 20000))
     # exact ties: float32 values whose low 16 bits are 0x8000, both parities
     ties = (np.arange(1, 200, dtype=np.uint32) << 16 | 0x8000).view(np.float32).astype(np.float64)
-    x = np.concatenate([x, ties, -ties, [0.0, -0.0, 1.0, 65504.0, 3.0e38]])
+    x = np.concatenate([x, ties, -ties, [0.0, -0.0, 1.0, 65504.0, 3.0e38, -3.3e38, np.inf,
+                                         -np.inf, np.nan]])
     ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
     got = oracle.bf16_round(x)
-    assert np.array_equal(got, ref)
+    assert np.array_equal(got, ref, equal_nan=True)
+    fin = ~np.isnan(ref)
+    assert np.array_equal(np.signbit(got[fin]), np.signbit(ref[fin]))
 
 
 def test_bf16_grads_close_to_exact():

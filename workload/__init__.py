@@ -106,8 +106,11 @@ def bf16_bits(x32: np.ndarray) -> np.ndarray:
     """Round float32 to bfloat16 (round-to-nearest-even) and return the 16-bit
     patterns.  Input storage only: bf16 configurations keep x in this form."""
     u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
-    r = ((u.astype(np.uint64) + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
-    return r
+    if not np.all(np.isfinite(x32)):
+        raise ValueError("inputs must be finite")
+    # finite patterns are at most 0xFF7FFFFF, so the sum stays below 2^32
+    r = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16))
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
