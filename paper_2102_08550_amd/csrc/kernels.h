@@ -19,22 +19,29 @@ enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };
 //
 //   FWD   C[o][b] = sum_i W[o][i] act[b][i];  out[b][o] = C + bias[o]
 //         (ReLU if relu).  A = W [M=out][K=in]; B = act [N=batch][K=in]
-//         (b_ld), or dataset rows x[gather[b]] when gather != nullptr.
+//         (b_ld), or dataset rows x[gather[b]] when gather != nullptr, which
+//         are then also copied to rows_out.
 //   DGRAD C[i][b] = sum_o W[o][i] D[b][o];  out[b][i] = C where
 //         mask[b][i] > 0, else 0.  A = W as [K=out][M=in]; B = D [N=batch][K=out].
 //   WGRAD C[i][o] = sum_b act[b][i] D[b][o] = dW[o][i];  W <- W - lr dW
 //         (fp32 master), bias[o] <- bias[o] - lr sum_b D[b][o], bf16 copy of
-//         W refreshed if wcopy.  A = act as [K=batch][M=in] (or x[gather[b]]);
-//         B = D as [K=batch][N=out].
+//         W refreshed if wcopy.  A = act as [K=batch][M=in] (layer 1: the
+//         rows the forward pass gathered); B = D as [K=batch][N=out].
 struct GemmArgs {
   int M, N, K;
+  // Chunked extent of each operand's contiguous dimension (K for a
+  // K-contiguous operand, M or N otherwise): a multiple of 8 elements, with
+  // readable (zero) padding between the logical size and the extent.
+  int a_ext, b_ext;
   const void* a;  // operand A (FWD, DGRAD: weights; WGRAD: activations / x)
   int64_t a_ld, a_slot;
   int a_by_order;  // a's slot offset uses order[z] (fp32 masters) instead of z
   const void* b;  // operand B (FWD: activations / x; DGRAD, WGRAD: delta)
   int64_t b_ld, b_slot;
-  const int32_t* gather;  // dataset rows of the batch (FWD: B rows; WGRAD: A's k rows)
+  const int32_t* gather;  // FWD layer 1: dataset rows of the batch (B rows)
   int64_t gather_slot;
+  void* rows_out;  // FWD layer 1: the gathered rows, [batch][rows_out_ld] per slot
+  int64_t rows_out_ld, rows_out_slot;
   void* out;  // FWD: activations or logits; DGRAD: delta of the layer below
   int64_t out_ld, out_slot;
   const void* mask;  // DGRAD: activations of the layer below

@@ -11,8 +11,8 @@
 //                  K-way reduction, 128-bit loads, lane groups combined with
 //                  cross-lane shuffles, optional broadcast back to every replica.
 //
-// Tiles: 128 x 128 outputs per 256-thread workgroup, four waves of 64 x 64,
-// each wave 2 x 2 MFMA 32x32 blocks.  LDS holds both operands K-contiguous:
+// Tiles: 128 x 128 outputs per workgroup; the wave layout depends on the pass
+// (see Shape below).  LDS holds both operands K-contiguous:
 // 128 rows x 128 bytes (64 bf16 or 32 fp32), 16-byte chunks placed at
 // chunk ^ ((row ^ row >> 3) & 7) so that MFMA operand reads (consecutive rows,
 // one chunk) and transposing writes (rows 8 apart) both spread over the banks.
@@ -34,7 +34,24 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int BM = 128, BN = 128, NTHR = 256;
+constexpr int BM = 128, BN = 128;
+
+// Workgroup shape per pass (measured on MI355X, MLP 4096x4 -> 1000 bf16):
+//   forward / backward-data (K = layer width, long): 8 waves as 2 x 4, each
+//     64 x 32, two register stages so tiles kt+1 and kt+2 load while tile kt
+//     is multiplied;
+//   backward-weight + update (K = batch, short, fp32 master read and written):
+//     4 waves as 2 x 2, each 64 x 64, one register stage.
+template <int WAVES, int STAGES>
+struct Shape {
+  static constexpr int NT = 64 * WAVES;            // threads
+  static constexpr int WAVES_M = 2, WAVES_N = WAVES / 2;
+  static constexpr int MI = BM / (32 * WAVES_M);   // MFMA blocks per wave along M
+  static constexpr int NJ = BN / (32 * WAVES_N);   // and along N
+  static constexpr int ST = STAGES;
+};
+template <int MODE> struct ModeShape { typedef Shape<8, 2> type; };
+template <> struct ModeShape<GEMM_WGRAD> { typedef Shape<4, 1> type; };
 constexpr int ROW_U32 = 32;               // one LDS tile row: 128 bytes
 constexpr int TILE_U32 = 128 * ROW_U32;   // one operand tile: 16 KB
 
@@ -60,41 +77,72 @@ template <> struct El<false> {
   static constexpr int BK = 32;
 };
 
-// 16 bytes starting at p; elements at and beyond `valid` read as zero.
-template <bool BF16>
-__device__ __forceinline__ u32x4 load_chunk(const typename El<BF16>::T* p, int valid) {
-  if (valid >= El<BF16>::CH) return *reinterpret_cast<const u32x4*>(p);
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if constexpr (BF16) {
-    for (int e = 0; e < 8; ++e)
-      if (e < valid) v[e >> 1] |= static_cast<uint32_t>(p[e]) << (16 * (e & 1));
-  } else {
-    for (int e = 0; e < 4; ++e)
-      if (e < valid) v[e] = __float_as_uint(p[e]);
-  }
-  return v;
+// Loaders never branch and never depend on a load inside the K loop: row
+// pointers (gathered or not) are set up once, before the loop; an
+// out-of-range lane reads the operand's first chunk (always valid memory) and
+// keeps zeros instead.  `ext` is the chunked extent of the contiguous
+// dimension: a multiple of the chunk, with memory up to it readable (zero
+// padding beyond the logical size where needed).
+// Out-of-range lanes read these zeros instead of selecting zeros after the
+// load, so nothing waits on a load before its data is stored to LDS.
+__device__ __attribute__((aligned(16))) uint32_t k_zero16[4];
+
+template <typename T>
+__device__ __forceinline__ u32x4 load16(bool ok, const T* p) {
+  return *reinterpret_cast<const u32x4*>(ok ? static_cast<const void*>(p)
+                                            : static_cast<const void*>(k_zero16));
 }
 
 // Tile of an operand stored K-contiguous: 128 rows (M or N) x BK.
-template <bool BF16>
+//   rows valid: row0 + r < R (row r of memory is gather[row0 + r] if gathered);
+//   chunk valid: k < ext.
+template <bool BF16, int NTHR>
+struct RowSrc {
+  typedef typename El<BF16>::T T;
+  static constexpr int P = 1024 / NTHR;
+  const T* rowp[P];
+  bool rowok[P];
+  __device__ __forceinline__ void init(const T* base, int64_t ld, const int32_t* gather, int row0,
+                                       int R, int tid) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int gr = row0 + ((tid + NTHR * p) >> 3);
+      rowok[p] = gr < R;
+      const int grc = gr < R ? gr : R - 1;
+      const int64_t row = gather ? gather[grc] : grc;
+      rowp[p] = base + row * ld;
+    }
+  }
+};
+
+template <bool BF16, int NTHR>
 struct RowTile {
   typedef typename El<BF16>::T T;
   static constexpr int CH = El<BF16>::CH;
-  u32x4 v[4];
-  __device__ __forceinline__ void load(const T* base, int64_t ld, const int32_t* gather, int row0,
-                                       int R, int k0, int K, int tid) {
+  static constexpr int P = 1024 / NTHR;
+  u32x4 v[P];
+  __device__ __forceinline__ void load(const RowSrc<BF16, NTHR>& src, const T* base, int k0,
+                                       int ext, int tid) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int idx = tid + NTHR * p, r = idx >> 3, c = idx & 7;
-      const int gr = row0 + r, k = k0 + c * CH;
-      const bool ok = gr < R && k < K;
-      const int64_t row = ok ? (gather ? gather[gr] : gr) : 0;
-      v[p] = ok ? load_chunk<BF16>(base + row * ld + k, K - k) : u32x4{0u, 0u, 0u, 0u};
+    for (int p = 0; p < P; ++p) {
+      const int k = k0 + ((tid + NTHR * p) & 7) * CH;
+      const bool ok = src.rowok[p] && k < ext;
+      v[p] = load16(ok, src.rowp[p] + k);
+    }
+  }
+  // Copy of the loaded chunks to dst (same row index, row stride ld_dst).
+  __device__ __forceinline__ void copy_out(T* dst, int64_t ld_dst, int row0, int R, int k0,
+                                           int ext, int tid) const {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int idx = tid + NTHR * p, gr = row0 + (idx >> 3), k = k0 + (idx & 7) * CH;
+      if (gr < R && k < ext)
+        *reinterpret_cast<u32x4*>(dst + static_cast<int64_t>(gr) * ld_dst + k) = v[p];
     }
   }
   __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < P; ++p) {
       const int idx = tid + NTHR * p;
       *reinterpret_cast<u32x4*>(lds + lds_word(idx >> 3, idx & 7)) = v[p];
     }
@@ -104,27 +152,27 @@ struct RowTile {
 // Tile of an operand stored M/N-contiguous ([K][MN] in memory), transposed
 // into the K-contiguous LDS layout.  bf16: pairs of k rows are packed into
 // 32-bit words; fp32: single words.
-template <bool BF16> struct TransTile;
+//   rows valid: k < K;  chunk valid: mn < ext.
+template <bool BF16, int NTHR> struct TransTile;
 
-template <>
-struct TransTile<true> {
-  u32x4 lo[2], hi[2];
-  __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, const int32_t* gather,
-                                       int mn0, int MN, int k0, int K, int tid) {
+template <int NTHR>
+struct TransTile<true, NTHR> {
+  static constexpr int P = 512 / NTHR;
+  u32x4 lo[P], hi[P];
+  __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int mn0, int ext, int k0,
+                                       int K, int tid) {
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
+    for (int p = 0; p < P; ++p) {
       const int idx = tid + NTHR * p, mc = idx & 15, kp = idx >> 4;
       const int k = k0 + 2 * kp, mn = mn0 + 8 * mc;
-      const bool ok0 = k < K && mn < MN, ok1 = k + 1 < K && mn < MN;
-      const int64_t r0 = ok0 ? (gather ? gather[k] : k) : 0;
-      const int64_t r1 = ok1 ? (gather ? gather[k + 1] : k + 1) : 0;
-      lo[p] = ok0 ? load_chunk<true>(base + r0 * ld + mn, MN - mn) : u32x4{0u, 0u, 0u, 0u};
-      hi[p] = ok1 ? load_chunk<true>(base + r1 * ld + mn, MN - mn) : u32x4{0u, 0u, 0u, 0u};
+      const bool ok0 = k < K && mn < ext, ok1 = k + 1 < K && mn < ext;
+      lo[p] = load16(ok0, base + k * ld + mn);
+      hi[p] = load16(ok1, base + (k + 1) * ld + mn);
     }
   }
   __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
+    for (int p = 0; p < P; ++p) {
       const int idx = tid + NTHR * p, mc = idx & 15, kp = idx >> 4;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -136,23 +184,23 @@ struct TransTile<true> {
   }
 };
 
-template <>
-struct TransTile<false> {
-  u32x4 v[4];
-  __device__ __forceinline__ void load(const float* base, int64_t ld, const int32_t* gather, int mn0,
-                                       int MN, int k0, int K, int tid) {
+template <int NTHR>
+struct TransTile<false, NTHR> {
+  static constexpr int P = 1024 / NTHR;
+  u32x4 v[P];
+  __device__ __forceinline__ void load(const float* base, int64_t ld, int mn0, int ext, int k0,
+                                       int K, int tid) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < P; ++p) {
       const int idx = tid + NTHR * p, mc = idx & 31, kk = idx >> 5;
       const int k = k0 + kk, mn = mn0 + 4 * mc;
-      const bool ok = k < K && mn < MN;
-      const int64_t r = ok ? (gather ? gather[k] : k) : 0;
-      v[p] = ok ? load_chunk<false>(base + r * ld + mn, MN - mn) : u32x4{0u, 0u, 0u, 0u};
+      const bool ok = k < K && mn < ext;
+      v[p] = load16(ok, base + k * ld + mn);
     }
   }
   __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < P; ++p) {
       const int idx = tid + NTHR * p, mc = idx & 31, kk = idx >> 5;
 #pragma unroll
       for (int e = 0; e < 4; ++e) lds[lds_word(4 * mc + e, kk >> 2) + (kk & 3)] = v[p][e];
@@ -160,26 +208,28 @@ struct TransTile<false> {
   }
 };
 
-// 2 x 2 blocks of 32x32 MFMA over one LDS tile pair.
-template <bool BF16>
+// MI x NJ blocks of 32x32 MFMA of one wave over one LDS tile pair.  The
+// wave's rows start at wm * 32 MI, its columns at wn * 32 NJ.
+template <bool BF16, int MI, int NJ>
 __device__ __forceinline__ void mma_tile(const uint32_t* As, const uint32_t* Bs, int wm, int wn,
-                                         int lane, f32x16 (&acc)[2][2]) {
+                                         int lane, f32x16 (&acc)[MI][NJ]) {
   const int r = lane & 31, h = lane >> 5;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     const int ch = 2 * s + h;
-    u32x4 a[2], b[2];
+    u32x4 a[MI], b[NJ];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a[i] = *reinterpret_cast<const u32x4*>(As + lds_word(wm * 64 + 32 * i + r, ch));
-      b[i] = *reinterpret_cast<const u32x4*>(Bs + lds_word(wn * 64 + 32 * i + r, ch));
-    }
+    for (int i = 0; i < MI; ++i)
+      a[i] = *reinterpret_cast<const u32x4*>(As + lds_word(wm * 32 * MI + 32 * i + r, ch));
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      b[j] = *reinterpret_cast<const u32x4*>(Bs + lds_word(wn * 32 * NJ + 32 * j + r, ch));
     if constexpr (BF16) {
       // lanes 0-31 hold k = 16s..16s+7 of their row, lanes 32-63 k = 16s+8..16s+15
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
     } else {
@@ -188,9 +238,9 @@ __device__ __forceinline__ void mma_tile(const uint32_t* As, const uint32_t* Bs,
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < NJ; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[i][t]),
                                                              __uint_as_float(b[j][t]), acc[i][j],
                                                              0, 0, 0);
@@ -204,14 +254,16 @@ __device__ __forceinline__ int xcd_tile(int L, int T) {
   return (T % 8 == 0) ? (L % 8) * (T / 8) + L / 8 : L;
 }
 
-template <bool BF16, int MODE>
-__global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
+template <bool BF16, int MODE, bool GATHER>
+__global__ __launch_bounds__(ModeShape<MODE>::type::NT) void gemm_kernel(GemmArgs g) {
   typedef typename El<BF16>::T T;
+  typedef typename ModeShape<MODE>::type S;
+  constexpr int NTHR = S::NT, WAVES_N = S::WAVES_N, MI = S::MI, NJ = S::NJ;
   constexpr int BK = El<BF16>::BK;
   __shared__ __attribute__((aligned(16))) uint32_t lds[2][2][TILE_U32];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, h = lane >> 5;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N, h = lane >> 5;
   const int z = blockIdx.y;
   const int rep = g.order[z];
   const int M = g.M, N = g.N, K = g.K;
@@ -221,30 +273,35 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
 
   const T* A = static_cast<const T*>(g.a) + (g.a_by_order ? rep : z) * g.a_slot;
   const T* B = static_cast<const T*>(g.b) + z * g.b_slot;
-  const int32_t* gat = g.gather ? g.gather + z * g.gather_slot : nullptr;
   float* master = g.master + static_cast<int64_t>(rep) * g.master_slot;
 
   // A: weights K-contiguous in FWD, weights M-contiguous in DGRAD, activations
   // M-contiguous in WGRAD.  B: activations / delta K-contiguous in FWD and
   // DGRAD, delta N-contiguous in WGRAD.
-  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16>, TransTile<BF16>>::type ta;
-  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16>, RowTile<BF16>>::type tb;
-  const int32_t* gatA = (MODE == GEMM_WGRAD) ? gat : nullptr;
-  const int32_t* gatB = (MODE == GEMM_FWD) ? gat : nullptr;
+  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16, NTHR>, TransTile<BF16, NTHR>>::type ta;
+  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16, NTHR>, RowTile<BF16, NTHR>>::type tb;
+  // Row pointers of the K-contiguous operands, fixed for the whole K loop.
+  RowSrc<BF16, NTHR> sa, sb;
+  if constexpr (MODE == GEMM_FWD) sa.init(A, g.a_ld, nullptr, m0, M, tid);
+  if constexpr (MODE != GEMM_WGRAD)
+    sb.init(B, g.b_ld, GATHER ? g.gather + z * g.gather_slot : nullptr, n0, N, tid);
+  // Forward layer 1: the workgroups of the first M tile also keep the gathered
+  // batch rows, contiguous, for the backward-weight pass of that layer.
+  T* rows_out = (GATHER && m0 == 0) ? static_cast<T*>(g.rows_out) + z * g.rows_out_slot : nullptr;
 
   // Accumulator element (i, j, r) sits at row m = mrow(i, r>>2) + (r & 3),
   // column n = ncol(j): four consecutive rows per lane and group r>>2.
-  auto mrow = [&](int i, int q) { return m0 + wm * 64 + 32 * i + 8 * q + 4 * h; };
-  auto ncol = [&](int j) { return n0 + wn * 64 + 32 * j + (lane & 31); };
+  auto mrow = [&](int i, int q) { return m0 + wm * 32 * MI + 32 * i + 8 * q + 4 * h; };
+  auto ncol = [&](int j) { return n0 + wn * 32 * NJ + 32 * j + (lane & 31); };
 
   // WGRAD: the fp32 master tile is fetched before the K loop so that its HBM
   // latency overlaps the products.
-  f32x4 wpre[2][2][4];
+  f32x4 wpre[MI][NJ][4];
   if constexpr (MODE == GEMM_WGRAD) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int m = mrow(i, q), n = ncol(j);
@@ -262,32 +319,35 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
         }
   }
 
-  f32x16 acc[2][2];
+  f32x16 acc[MI][NJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const bool bias_wg = (MODE == GEMM_WGRAD) && m0 == 0;
   float dbias = 0.0f;
 
-  const int nk = (K + BK - 1) / BK;
-  ta.load(A, g.a_ld, gatA, m0, M, 0, K, tid);
-  tb.load(B, g.b_ld, gatB, n0, N, 0, K, tid);
-  ta.store(lds[0][0], tid);
-  tb.store(lds[0][1], tid);
-  __syncthreads();
+  // A: rows m (RowTile, FWD) or k rows with m chunks (TransTile).
+  // B: rows n (RowTile, FWD / DGRAD) or k rows with n chunks (TransTile, WGRAD).
+#define LOAD_A(t, k0)                                                     \
+  do {                                                                    \
+    if constexpr (MODE == GEMM_FWD) t.load(sa, A, k0, g.a_ext, tid);      \
+    else t.load(A, g.a_ld, m0, g.a_ext, k0, K, tid);                      \
+  } while (0)
+#define LOAD_B(t, k0)                                                     \
+  do {                                                                    \
+    if constexpr (MODE == GEMM_WGRAD) t.load(B, g.b_ld, n0, g.b_ext, k0, K, tid); \
+    else {                                                                \
+      t.load(sb, B, k0, g.b_ext, tid);                                    \
+      if (GATHER && rows_out) t.copy_out(rows_out, g.rows_out_ld, n0, N, k0, g.b_ext, tid); \
+    }                                                                     \
+  } while (0)
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      ta.load(A, g.a_ld, gatA, m0, M, (kt + 1) * BK, K, tid);
-      tb.load(B, g.b_ld, gatB, n0, N, (kt + 1) * BK, K, tid);
-    }
-    mma_tile<BF16>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
+  auto compute = [&](int buf) {
+    mma_tile<BF16, MI, NJ>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
     if (bias_wg && tid < BN) {
       // db[o] = sum_b delta[b][o]: row tid of the B tile, in k order.
 #pragma unroll
@@ -304,18 +364,63 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(GemmArgs g) {
         }
       }
     }
-    if (more) {
+  };
+
+  // Loads past the end of K read zeros, so the loop bodies are straight-line.
+  const int nk = (K + BK - 1) / BK;
+  if constexpr (S::ST == 1) {
+    // One register stage, LDS double buffer (always for the short K of the
+    // backward-weight pass, the batch).
+    LOAD_A(ta, 0);
+    LOAD_B(tb, 0);
+    ta.store(lds[0][0], tid);
+    tb.store(lds[0][1], tid);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int buf = kt & 1;
+      LOAD_A(ta, (kt + 1) * BK);
+      LOAD_B(tb, (kt + 1) * BK);
+      compute(buf);
       ta.store(lds[buf ^ 1][0], tid);
       tb.store(lds[buf ^ 1][1], tid);
+      __syncthreads();
     }
+  } else {
+    // Two register stages: tiles kt+1 and kt+2 are in flight while tile kt is
+    // multiplied out of LDS.
+    decltype(ta) ta1;
+    decltype(tb) tb1;
+    LOAD_A(ta, 0);
+    LOAD_B(tb, 0);
+    LOAD_A(ta1, BK);
+    LOAD_B(tb1, BK);
+    ta.store(lds[0][0], tid);
+    tb.store(lds[0][1], tid);
     __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      LOAD_A(ta, (kt + 2) * BK);
+      LOAD_B(tb, (kt + 2) * BK);
+      compute(0);
+      ta1.store(lds[1][0], tid);
+      tb1.store(lds[1][1], tid);
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      LOAD_A(ta1, (kt + 3) * BK);
+      LOAD_B(tb1, (kt + 3) * BK);
+      compute(1);
+      ta.store(lds[0][0], tid);
+      tb.store(lds[0][1], tid);
+      __syncthreads();
+    }
   }
+#undef LOAD_A
+#undef LOAD_B
 
   // Epilogue, one group of four consecutive rows m..m+3 at column n at a time.
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < MI; ++i) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < NJ; ++j) {
       const int n = ncol(j);
       if (n >= N) continue;
 #pragma unroll
@@ -524,7 +629,16 @@ hipError_t agg_launch(float* g, float* reps, const AggWeights& w, int K, int64_t
 template <bool BF16, int MODE>
 hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
   const dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM), n_slots);
-  hipLaunchKernelGGL((gemm_kernel<BF16, MODE>), grid, dim3(NTHR), 0, s, g);
+  if (g.gather) {
+    if constexpr (MODE == GEMM_FWD)
+      hipLaunchKernelGGL((gemm_kernel<BF16, MODE, true>), grid, dim3(ModeShape<MODE>::type::NT),
+                         0, s, g);
+    else
+      return hipErrorInvalidValue;  // only the forward pass gathers dataset rows
+  } else {
+    hipLaunchKernelGGL((gemm_kernel<BF16, MODE, false>), grid, dim3(ModeShape<MODE>::type::NT), 0,
+                       s, g);
+  }
   return hipGetLastError();
 }
 

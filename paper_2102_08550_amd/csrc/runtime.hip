@@ -52,7 +52,7 @@ struct oscars_ctx {
 
   std::vector<void*> allocs;
   uint16_t* wcopy = nullptr;       // [K][n_pad] bf16 weight copies (bf16 models)
-  std::vector<void*> act;          // act[l], l = 1..L-1: [K][max_batch][ld[l]]
+  std::vector<void*> act;          // act[l], l = 0..L-1: [K][max_batch][ld[l]] (act[0]: batch rows)
   float* logits = nullptr;         // [K][max_batch][ld[L]]
   std::vector<void*> delta;        // delta[l], l = 1..L: [K][max_batch][ld[l]]
   int32_t* table_dev = nullptr;    // order [64] then index table [slots][tau_max][B]
@@ -172,6 +172,8 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
   }
   c->act.assign(c->L + 1, nullptr);
   c->delta.assign(c->L + 1, nullptr);
+  if (e == hipSuccess)  // act[0]: the gathered batch rows of the current step
+    e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(0) * c->esize, &c->act[0]);
   for (int l = 1; l <= c->L && e == hipSuccess; ++l) {
     const size_t n = static_cast<size_t>(K) * c->act_slot(l);
     if (l < c->L) e = dev_alloc(c, n * c->esize, &c->act[l]);
@@ -357,6 +359,8 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
       g.M = c->dims[l];
       g.N = B;
       g.K = c->dims[l - 1];
+      g.a_ext = g.K;
+      g.b_ext = g.K;
       weights(g, l);
       if (l == 1) {
         g.b = s->x;
@@ -364,6 +368,9 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
         g.b_slot = 0;
         g.gather = rows_j;
         g.gather_slot = rows_slot;
+        g.rows_out = c->act[0];
+        g.rows_out_ld = c->ld[0];
+        g.rows_out_slot = c->act_slot(0);
       } else {
         g.b = c->act[l - 1];
         g.b_ld = c->ld[l - 1];
@@ -399,6 +406,8 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
         g.M = c->dims[l - 1];
         g.N = B;
         g.K = c->dims[l];
+        g.a_ext = g.M;                          // W rows, m chunks
+        g.b_ext = static_cast<int>(round_up(g.K, 8));  // delta rows are zero-padded
         weights(g, l);
         g.b = c->delta[l];
         g.b_ld = c->ld[l];
@@ -420,17 +429,11 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
       g.M = c->dims[l - 1];
       g.N = c->dims[l];
       g.K = B;
-      if (l == 1) {
-        g.a = s->x;
-        g.a_ld = c->dims[0];
-        g.a_slot = 0;
-        g.gather = rows_j;
-        g.gather_slot = rows_slot;
-      } else {
-        g.a = c->act[l - 1];
-        g.a_ld = c->ld[l - 1];
-        g.a_slot = c->act_slot(l - 1);
-      }
+      g.a_ext = g.M;
+      g.b_ext = static_cast<int>(round_up(g.N, 8));  // delta rows are zero-padded
+      g.a = c->act[l - 1];  // for l = 1: the batch rows the forward pass gathered
+      g.a_ld = c->ld[l - 1];
+      g.a_slot = c->act_slot(l - 1);
       g.a_by_order = 0;
       g.b = c->delta[l];
       g.b_ld = c->ld[l];
