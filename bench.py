@@ -132,6 +132,9 @@ def main():
     ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c5"])
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--probe-copy-mib", type=int, default=0,
+                    help="first run a plain device-to-device copy of this many MiB, three "
+                         "times (calibration of hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -145,6 +148,14 @@ def main():
     from paper_2102_08550_amd.rounds import OscarsRun
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.probe_copy_mib > 0:
+        n = args.probe_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cfg = workload.CONFIGS[args.workload]
     print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
     ds = workload.gen_dataset(cfg)

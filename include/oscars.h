@@ -62,7 +62,8 @@ typedef struct oscars_ctx oscars_ctx;
  * Model: a fully connected ReLU network with a softmax cross-entropy loss.
  *   n_layers  L >= 1 (L = 1 is softmax regression);
  *   dims      host [L + 1]: dims[0] = input width d, dims[L] = classes C,
- *             every entry in [1, OSCARS_MAX_WIDTH]; d must be a multiple of 8;
+ *             every entry in [1, OSCARS_MAX_WIDTH]; all but dims[L] must be
+ *             multiples of 8 (16-byte rows for the kernels' vector loads);
  *   dtype     OSCARS_FP32: inputs, weights and arithmetic in fp32;
  *             OSCARS_BF16: bf16 inputs and weights in the products, fp32
  *             accumulation, fp32 master parameters.
@@ -82,7 +83,8 @@ typedef struct {
  * parameter server holds different training data).
  *   x        device [n_rows][d]: fp32, or bf16 bit patterns for OSCARS_BF16;
  *            16-byte aligned;
- *   y        device [n_rows] int32 labels in [0, C);
+ *   y        device [n_rows] int32 labels in [0, C) (a row with a label
+ *            outside that range gets a NaN loss and no one-hot term);
  *   n_rows   number of rows;
  *   offsets  host [K + 1], non-decreasing, offsets[0] = 0,
  *            offsets[K] = n_rows; worker k owns rows [offsets[k], offsets[k+1]),
