@@ -42,16 +42,17 @@ constexpr int BM = 128, BN = 128;
 //     is multiplied;
 //   backward-weight + update (K = batch, short, fp32 master read and written):
 //     4 waves as 2 x 2, each 64 x 64, one register stage.
-template <int WAVES, int STAGES>
+template <int WAVES, int STAGES, int MINW>
 struct Shape {
+  static constexpr int MIN_WAVES = MINW;           // register budget: waves per SIMD
   static constexpr int NT = 64 * WAVES;            // threads
   static constexpr int WAVES_M = 2, WAVES_N = WAVES / 2;
   static constexpr int MI = BM / (32 * WAVES_M);   // MFMA blocks per wave along M
   static constexpr int NJ = BN / (32 * WAVES_N);   // and along N
   static constexpr int ST = STAGES;
 };
-template <int MODE> struct ModeShape { typedef Shape<8, 2> type; };
-template <> struct ModeShape<GEMM_WGRAD> { typedef Shape<4, 1> type; };
+template <int MODE> struct ModeShape { typedef Shape<8, 2, 1> type; };
+template <> struct ModeShape<GEMM_WGRAD> { typedef Shape<4, 1, 2> type; };
 constexpr int ROW_U32 = 32;               // one LDS tile row: 128 bytes
 constexpr int TILE_U32 = 128 * ROW_U32;   // one operand tile: 16 KB
 
@@ -255,7 +256,8 @@ __device__ __forceinline__ int xcd_tile(int L, int T) {
 }
 
 template <bool BF16, int MODE, bool GATHER>
-__global__ __launch_bounds__(ModeShape<MODE>::type::NT) void gemm_kernel(GemmArgs g) {
+__global__ __launch_bounds__(ModeShape<MODE>::type::NT, ModeShape<MODE>::type::MIN_WAVES) void
+gemm_kernel(GemmArgs g) {
   typedef typename El<BF16>::T T;
   typedef typename ModeShape<MODE>::type S;
   constexpr int NTHR = S::NT, WAVES_N = S::WAVES_N, MI = S::MI, NJ = S::NJ;
@@ -294,29 +296,22 @@ __global__ __launch_bounds__(ModeShape<MODE>::type::NT) void gemm_kernel(GemmArg
   auto mrow = [&](int i, int q) { return m0 + wm * 32 * MI + 32 * i + 8 * q + 4 * h; };
   auto ncol = [&](int j) { return n0 + wn * 32 * NJ + 32 * j + (lane & 31); };
 
-  // WGRAD: the fp32 master tile is fetched before the K loop so that its HBM
-  // latency overlaps the products.
-  f32x4 wpre[MI][NJ][4];
+  // WGRAD: the fp32 master tile W[n0..n0+127][m0..m0+127] is fetched before
+  // the K loop, so its HBM latency overlaps the products.  Layout: chunk
+  // c = tid + NTHR p covers row n0 + (c >> 5), columns m0 + 4 (c & 31) .. +3,
+  // so 32 lanes read one contiguous 512-byte row segment.
+  constexpr int WCH = (MODE == GEMM_WGRAD) ? BM * BN / 4 / NTHR : 1;
+  f32x4 wpre[WCH];
+  // Workgroup-uniform tile base; lanes add a 32-bit offset (row * M + col).
+  float* wtile = master + g.w_off + static_cast<int64_t>(n0) * M + m0;
   if constexpr (MODE == GEMM_WGRAD) {
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int m = mrow(i, q), n = ncol(j);
-          f32x4 w = {0.0f, 0.0f, 0.0f, 0.0f};
-          if (n < N) {
-            const float* p = master + g.w_off + static_cast<int64_t>(n) * M + m;
-            if (m + 3 < M) {
-              w = *reinterpret_cast<const f32x4*>(p);
-            } else {
-              for (int e = 0; e < 4; ++e)
-                if (m + e < M) w[e] = p[e];
-            }
-          }
-          wpre[i][j][q] = w;
-        }
+    for (int p = 0; p < WCH; ++p) {
+      const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);
+      const bool ok = n0 + row < N && m0 + col < M;  // M % 4 == 0: chunks are whole
+      wpre[p] = ok ? *reinterpret_cast<const f32x4*>(wtile + (row * M + col))
+                   : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
   }
 
   f32x16 acc[MI][NJ];
@@ -416,6 +411,50 @@ __global__ __launch_bounds__(ModeShape<MODE>::type::NT) void gemm_kernel(GemmArg
 #undef LOAD_A
 #undef LOAD_B
 
+  if constexpr (MODE == GEMM_WGRAD) {
+    // dW tile -> LDS as [o][i] (row n - n0, 16-byte chunk (m - m0) / 4 placed
+    // at chunk ^ (row & 31)), then every thread updates the chunks it
+    // prefetched: coalesced master read/write and bf16 refresh.
+    float* dws = reinterpret_cast<float*>(&lds[0][0][0]);
+    auto dw_at = [](int row, int ch) { return row * BM + ((ch ^ (row & 31)) << 2); };
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = ncol(j) - n0, ch = (mrow(i, q) - m0) >> 2;
+          *reinterpret_cast<f32x4*>(dws + dw_at(row, ch)) =
+              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                    acc[i][j][4 * q + 3]};
+        }
+    __syncthreads();
+    uint16_t* ctile =
+        g.wcopy ? g.wcopy + z * g.wcopy_slot + g.w_off + static_cast<int64_t>(n0) * M + m0 : nullptr;
+#pragma unroll
+    for (int p = 0; p < WCH; ++p) {
+      const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);
+      if (n0 + row < N && m0 + col < M) {
+        const f32x4 d = *reinterpret_cast<const f32x4*>(dws + dw_at(row, c & 31));
+        f32x4 w = wpre[p];
+        for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, d[e], w[e]);
+        const int at = row * M + col;
+        *reinterpret_cast<f32x4*>(wtile + at) = w;
+        if (ctile) {
+          uint2 o;
+          o.x = f2bf(w[0]) | (f2bf(w[1]) << 16);
+          o.y = f2bf(w[2]) | (f2bf(w[3]) << 16);
+          *reinterpret_cast<uint2*>(ctile + at) = o;
+        }
+      }
+    }
+    if (bias_wg && tid < BN && n0 + tid < N) {
+      float* bp = master + g.b_off + n0 + tid;
+      *bp = fmaf(-g.lr, dbias, *bp);
+    }
+    return;
+  }
+
   // Epilogue, one group of four consecutive rows m..m+3 at column n at a time.
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
@@ -449,26 +488,7 @@ __global__ __launch_bounds__(ModeShape<MODE>::type::NT) void gemm_kernel(GemmArg
             v[e] = pos ? v[e] : 0.0f;
           }
         }
-        if constexpr (MODE == GEMM_WGRAD) {
-          // W[o = n][i = m..m+3] <- W - lr dW, from the prefetched tile
-          const int64_t at = g.w_off + static_cast<int64_t>(n) * M + m;
-          f32x4 w = wpre[i][j][q];
-          for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, v[e], w[e]);
-          if (cnt == 4) {
-            *reinterpret_cast<f32x4*>(master + at) = w;
-            if (g.wcopy) {
-              uint2 o;
-              o.x = f2bf(w[0]) | (f2bf(w[1]) << 16);
-              o.y = f2bf(w[2]) | (f2bf(w[3]) << 16);
-              *reinterpret_cast<uint2*>(g.wcopy + z * g.wcopy_slot + at) = o;
-            }
-          } else {
-            for (int e = 0; e < cnt; ++e) {
-              master[at + e] = w[e];
-              if (g.wcopy) g.wcopy[z * g.wcopy_slot + at + e] = static_cast<uint16_t>(f2bf(w[e]));
-            }
-          }
-        } else {
+        {
           const int64_t at = z * g.out_slot + static_cast<int64_t>(n) * g.out_ld + m;
           if (g.out_bf16) {
             uint16_t* o = static_cast<uint16_t*>(g.out) + at;
@@ -491,10 +511,6 @@ __global__ __launch_bounds__(ModeShape<MODE>::type::NT) void gemm_kernel(GemmArg
         }
       }
     }
-  }
-  if (bias_wg && tid < BN && n0 + tid < N) {
-    float* bp = master + g.b_off + n0 + tid;
-    *bp = fmaf(-g.lr, dbias, *bp);
   }
 }
 
