@@ -30,31 +30,39 @@ namespace oscars {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int BM = 128, BN = 128;
-
-// Workgroup shape per pass (measured on MI355X, MLP 4096x4 -> 1000 bf16):
-//   forward / backward-data (K = layer width, long): 8 waves as 2 x 4, each
-//     64 x 32, two register stages so tiles kt+1 and kt+2 load while tile kt
-//     is multiplied;
-//   backward-weight + update (K = batch, short, fp32 master read and written):
-//     4 waves as 2 x 2, each 64 x 64, one register stage.
-template <int WAVES, int STAGES, int MINW>
+// Workgroup tile shapes.  All shapes use the same K tile (BK) and the same
+// MFMA k-grouping, so an output element is summed in the same order whatever
+// the shape: the shape only decides which workgroup computes it.
+//   BM x BN outputs, WAVES_M x WAVES_N waves (each BM/WAVES_M x BN/WAVES_N),
+//   ST register stages for the long-K passes, MINW minimum waves per SIMD.
+template <int BM_, int BN_, int WM_, int WN_, int STAGES, int MINW>
 struct Shape {
-  static constexpr int MIN_WAVES = MINW;           // register budget: waves per SIMD
-  static constexpr int NT = 64 * WAVES;            // threads
-  static constexpr int WAVES_M = 2, WAVES_N = WAVES / 2;
-  static constexpr int MI = BM / (32 * WAVES_M);   // MFMA blocks per wave along M
-  static constexpr int NJ = BN / (32 * WAVES_N);   // and along N
+  static constexpr int BM = BM_, BN = BN_;
+  static constexpr int WAVES_M = WM_, WAVES_N = WN_;
+  static constexpr int NT = 64 * WM_ * WN_;          // threads
+  static constexpr int MI = BM_ / (32 * WM_);        // MFMA blocks per wave along M
+  static constexpr int NJ = BN_ / (32 * WN_);        // and along N
   static constexpr int ST = STAGES;
+  static constexpr int MIN_WAVES = MINW;
 };
-template <int MODE> struct ModeShape { typedef Shape<8, 2, 1> type; };
-template <> struct ModeShape<GEMM_WGRAD> { typedef Shape<4, 1, 2> type; };
+// Forward / backward-data (K = layer width): 128 x 128 with 8 waves when
+// enough tiles fill the chip, else 64 x 128 or 64 x 64 with 4 waves (more
+// workgroups for the same outputs when few replicas are active).
+// Backward-weight + update (K = batch): 128 x 128, 4 waves, one stage.
+enum { SHAPE_L = 0, SHAPE_M = 1, SHAPE_S = 2 };
+template <int MODE, int SID> struct ShapeOf;
+template <int MODE> struct ShapeOf<MODE, SHAPE_L> { typedef Shape<128, 128, 2, 4, 2, 1> type; };
+template <int MODE> struct ShapeOf<MODE, SHAPE_M> { typedef Shape<64, 128, 1, 4, 2, 1> type; };
+template <int MODE> struct ShapeOf<MODE, SHAPE_S> { typedef Shape<64, 64, 2, 2, 2, 1> type; };
+template <> struct ShapeOf<GEMM_WGRAD, SHAPE_L> { typedef Shape<128, 128, 2, 2, 1, 2> type; };
+
 constexpr int ROW_U32 = 32;               // one LDS tile row: 128 bytes
-constexpr int TILE_U32 = 128 * ROW_U32;   // one operand tile: 16 KB
+constexpr int TILE_U32 = 128 * ROW_U32;   // one operand tile of up to 128 rows: 16 KB
 
 __device__ __forceinline__ int lds_word(int row, int chunk) {
   return row * ROW_U32 + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 2);
@@ -97,10 +105,11 @@ __device__ __forceinline__ u32x4 load16(bool ok, const T* p) {
 // Tile of an operand stored K-contiguous: 128 rows (M or N) x BK.
 //   rows valid: row0 + r < R (row r of memory is gather[row0 + r] if gathered);
 //   chunk valid: k < ext.
-template <bool BF16, int NTHR>
+template <bool BF16, int NTHR, int ROWS>
 struct RowSrc {
   typedef typename El<BF16>::T T;
-  static constexpr int P = 1024 / NTHR;
+  static_assert(ROWS * 8 % NTHR == 0, "whole chunks per thread");
+  static constexpr int P = ROWS * 8 / NTHR;
   const T* rowp[P];
   bool rowok[P];
   __device__ __forceinline__ void init(const T* base, int64_t ld, const int32_t* gather, int row0,
@@ -116,13 +125,13 @@ struct RowSrc {
   }
 };
 
-template <bool BF16, int NTHR>
+template <bool BF16, int NTHR, int ROWS>
 struct RowTile {
   typedef typename El<BF16>::T T;
   static constexpr int CH = El<BF16>::CH;
-  static constexpr int P = 1024 / NTHR;
+  static constexpr int P = ROWS * 8 / NTHR;
   u32x4 v[P];
-  __device__ __forceinline__ void load(const RowSrc<BF16, NTHR>& src, const T* base, int k0,
+  __device__ __forceinline__ void load(const RowSrc<BF16, NTHR, ROWS>& src, const T* base, int k0,
                                        int ext, int tid) {
 #pragma unroll
     for (int p = 0; p < P; ++p) {
@@ -154,17 +163,19 @@ struct RowTile {
 // into the K-contiguous LDS layout.  bf16: pairs of k rows are packed into
 // 32-bit words; fp32: single words.
 //   rows valid: k < K;  chunk valid: mn < ext.
-template <bool BF16, int NTHR> struct TransTile;
+template <bool BF16, int NTHR, int ROWS> struct TransTile;
 
-template <int NTHR>
-struct TransTile<true, NTHR> {
-  static constexpr int P = 512 / NTHR;
+template <int NTHR, int ROWS>
+struct TransTile<true, NTHR, ROWS> {
+  static constexpr int MC = ROWS / 8;  // 16-byte chunks per k row
+  static_assert(32 * MC % NTHR == 0, "whole items per thread");
+  static constexpr int P = 32 * MC / NTHR;
   u32x4 lo[P], hi[P];
   __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int mn0, int ext, int k0,
                                        int K, int tid) {
 #pragma unroll
     for (int p = 0; p < P; ++p) {
-      const int idx = tid + NTHR * p, mc = idx & 15, kp = idx >> 4;
+      const int idx = tid + NTHR * p, mc = idx % MC, kp = idx / MC;
       const int k = k0 + 2 * kp, mn = mn0 + 8 * mc;
       const bool ok0 = k < K && mn < ext, ok1 = k + 1 < K && mn < ext;
       lo[p] = load16(ok0, base + k * ld + mn);
@@ -174,7 +185,7 @@ struct TransTile<true, NTHR> {
   __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
 #pragma unroll
     for (int p = 0; p < P; ++p) {
-      const int idx = tid + NTHR * p, mc = idx & 15, kp = idx >> 4;
+      const int idx = tid + NTHR * p, mc = idx % MC, kp = idx / MC;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const uint32_t a = lo[p][e >> 1], b = hi[p][e >> 1];
@@ -185,15 +196,17 @@ struct TransTile<true, NTHR> {
   }
 };
 
-template <int NTHR>
-struct TransTile<false, NTHR> {
-  static constexpr int P = 1024 / NTHR;
+template <int NTHR, int ROWS>
+struct TransTile<false, NTHR, ROWS> {
+  static constexpr int MC = ROWS / 4;
+  static_assert(32 * MC % NTHR == 0, "whole items per thread");
+  static constexpr int P = 32 * MC / NTHR;
   u32x4 v[P];
   __device__ __forceinline__ void load(const float* base, int64_t ld, int mn0, int ext, int k0,
                                        int K, int tid) {
 #pragma unroll
     for (int p = 0; p < P; ++p) {
-      const int idx = tid + NTHR * p, mc = idx & 31, kk = idx >> 5;
+      const int idx = tid + NTHR * p, mc = idx % MC, kk = idx / MC;
       const int k = k0 + kk, mn = mn0 + 4 * mc;
       const bool ok = k < K && mn < ext;
       v[p] = load16(ok, base + k * ld + mn);
@@ -202,7 +215,7 @@ struct TransTile<false, NTHR> {
   __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
 #pragma unroll
     for (int p = 0; p < P; ++p) {
-      const int idx = tid + NTHR * p, mc = idx & 31, kk = idx >> 5;
+      const int idx = tid + NTHR * p, mc = idx % MC, kk = idx / MC;
 #pragma unroll
       for (int e = 0; e < 4; ++e) lds[lds_word(4 * mc + e, kk >> 2) + (kk & 3)] = v[p][e];
     }
@@ -255,14 +268,18 @@ __device__ __forceinline__ int xcd_tile(int L, int T) {
   return (T % 8 == 0) ? (L % 8) * (T / 8) + L / 8 : L;
 }
 
-template <bool BF16, int MODE, bool GATHER>
-__global__ __launch_bounds__(ModeShape<MODE>::type::NT, ModeShape<MODE>::type::MIN_WAVES) void
+template <bool BF16, int MODE, bool GATHER, int SID>
+__global__ __launch_bounds__((ShapeOf<MODE, SID>::type::NT), (ShapeOf<MODE, SID>::type::MIN_WAVES)) void
 gemm_kernel(GemmArgs g) {
   typedef typename El<BF16>::T T;
-  typedef typename ModeShape<MODE>::type S;
+  typedef typename ShapeOf<MODE, SID>::type S;
   constexpr int NTHR = S::NT, WAVES_N = S::WAVES_N, MI = S::MI, NJ = S::NJ;
+  constexpr int BM = S::BM, BN = S::BN;
   constexpr int BK = El<BF16>::BK;
-  __shared__ __attribute__((aligned(16))) uint32_t lds[2][2][TILE_U32];
+  // LDS: A tiles (BM rows) for buffers 0 and 1, then B tiles (BN rows).
+  __shared__ __attribute__((aligned(16))) uint32_t lds_all[2 * (BM + BN) * ROW_U32];
+  auto lds_a = [&](int buf) { return lds_all + buf * BM * ROW_U32; };
+  auto lds_b = [&](int buf) { return lds_all + 2 * BM * ROW_U32 + buf * BN * ROW_U32; };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N, h = lane >> 5;
@@ -280,10 +297,11 @@ gemm_kernel(GemmArgs g) {
   // A: weights K-contiguous in FWD, weights M-contiguous in DGRAD, activations
   // M-contiguous in WGRAD.  B: activations / delta K-contiguous in FWD and
   // DGRAD, delta N-contiguous in WGRAD.
-  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16, NTHR>, TransTile<BF16, NTHR>>::type ta;
-  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16, NTHR>, RowTile<BF16, NTHR>>::type tb;
+  typename std::conditional<MODE == GEMM_FWD, RowTile<BF16, NTHR, BM>, TransTile<BF16, NTHR, BM>>::type ta;
+  typename std::conditional<MODE == GEMM_WGRAD, TransTile<BF16, NTHR, BN>, RowTile<BF16, NTHR, BN>>::type tb;
   // Row pointers of the K-contiguous operands, fixed for the whole K loop.
-  RowSrc<BF16, NTHR> sa, sb;
+  RowSrc<BF16, NTHR, BM> sa;
+  RowSrc<BF16, NTHR, BN> sb;
   if constexpr (MODE == GEMM_FWD) sa.init(A, g.a_ld, nullptr, m0, M, tid);
   if constexpr (MODE != GEMM_WGRAD)
     sb.init(B, g.b_ld, GATHER ? g.gather + z * g.gather_slot : nullptr, n0, N, tid);
@@ -309,7 +327,7 @@ gemm_kernel(GemmArgs g) {
     for (int p = 0; p < WCH; ++p) {
       const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);
       const bool ok = n0 + row < N && m0 + col < M;  // M % 4 == 0: chunks are whole
-      wpre[p] = ok ? *reinterpret_cast<const f32x4*>(wtile + (row * M + col))
+      wpre[p] = ok ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(wtile + (row * M + col)))
                    : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
   }
@@ -342,12 +360,12 @@ gemm_kernel(GemmArgs g) {
   } while (0)
 
   auto compute = [&](int buf) {
-    mma_tile<BF16, MI, NJ>(lds[buf][0], lds[buf][1], wm, wn, lane, acc);
+    mma_tile<BF16, MI, NJ>(lds_a(buf), lds_b(buf), wm, wn, lane, acc);
     if (bias_wg && tid < BN) {
       // db[o] = sum_b delta[b][o]: row tid of the B tile, in k order.
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(&lds[buf][1][lds_word(tid, c)]);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(lds_b(buf) + lds_word(tid, c));
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if constexpr (BF16) {
@@ -368,54 +386,56 @@ gemm_kernel(GemmArgs g) {
     // backward-weight pass, the batch).
     LOAD_A(ta, 0);
     LOAD_B(tb, 0);
-    ta.store(lds[0][0], tid);
-    tb.store(lds[0][1], tid);
+    ta.store(lds_a(0), tid);
+    tb.store(lds_b(0), tid);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       const int buf = kt & 1;
       LOAD_A(ta, (kt + 1) * BK);
       LOAD_B(tb, (kt + 1) * BK);
       compute(buf);
-      ta.store(lds[buf ^ 1][0], tid);
-      tb.store(lds[buf ^ 1][1], tid);
+      ta.store(lds_a(buf ^ 1), tid);
+      tb.store(lds_b(buf ^ 1), tid);
       __syncthreads();
     }
   } else {
-    // Two register stages: tiles kt+1 and kt+2 are in flight while tile kt is
-    // multiplied out of LDS.
-    decltype(ta) ta1;
-    decltype(tb) tb1;
-    LOAD_A(ta, 0);
-    LOAD_B(tb, 0);
-    LOAD_A(ta1, BK);
-    LOAD_B(tb1, BK);
-    ta.store(lds[0][0], tid);
-    tb.store(lds[0][1], tid);
+    // ST register stages: while tile j is multiplied out of LDS buffer j & 1,
+    // tiles j+1 .. j+ST are loading into the register sets t*[(j+1) % ST] ..
+    // The loop is unrolled by ST so every register set is indexed statically.
+    constexpr int ST = S::ST;
+    decltype(ta) tA[ST];
+    decltype(tb) tB[ST];
+#pragma unroll
+    for (int u = 0; u < ST; ++u) {
+      LOAD_A(tA[u], u * BK);
+      LOAD_B(tB[u], u * BK);
+    }
+    tA[0].store(lds_a(0), tid);
+    tB[0].store(lds_b(0), tid);
     __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-      LOAD_A(ta, (kt + 2) * BK);
-      LOAD_B(tb, (kt + 2) * BK);
-      compute(0);
-      ta1.store(lds[1][0], tid);
-      tb1.store(lds[1][1], tid);
-      __syncthreads();
-      if (kt + 1 >= nk) break;
-      LOAD_A(ta1, (kt + 3) * BK);
-      LOAD_B(tb1, (kt + 3) * BK);
-      compute(1);
-      ta.store(lds[0][0], tid);
-      tb.store(lds[0][1], tid);
-      __syncthreads();
+    for (int kt = 0; kt < nk; kt += ST) {
+#pragma unroll
+      for (int u = 0; u < ST; ++u) {
+        const int j = kt + u;
+        if (j >= nk) break;
+        LOAD_A(tA[u], (j + ST) * BK);
+        LOAD_B(tB[u], (j + ST) * BK);
+        compute(j & 1);
+        tA[(u + 1) % ST].store(lds_a((j + 1) & 1), tid);
+        tB[(u + 1) % ST].store(lds_b((j + 1) & 1), tid);
+        __syncthreads();
+      }
     }
   }
 #undef LOAD_A
 #undef LOAD_B
 
   if constexpr (MODE == GEMM_WGRAD) {
+    static_assert(BM == 128 && BN == 128, "update epilogue layout");
     // dW tile -> LDS as [o][i] (row n - n0, 16-byte chunk (m - m0) / 4 placed
     // at chunk ^ (row & 31)), then every thread updates the chunks it
     // prefetched: coalesced master read/write and bf16 refresh.
-    float* dws = reinterpret_cast<float*>(&lds[0][0][0]);
+    float* dws = reinterpret_cast<float*>(lds_all);  // all 64 KB of LDS
     auto dw_at = [](int row, int ch) { return row * BM + ((ch ^ (row & 31)) << 2); };
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -439,12 +459,12 @@ gemm_kernel(GemmArgs g) {
         f32x4 w = wpre[p];
         for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, d[e], w[e]);
         const int at = row * M + col;
-        *reinterpret_cast<f32x4*>(wtile + at) = w;
+        __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(wtile + at));
         if (ctile) {
-          uint2 o;
-          o.x = f2bf(w[0]) | (f2bf(w[1]) << 16);
-          o.y = f2bf(w[2]) | (f2bf(w[3]) << 16);
-          *reinterpret_cast<uint2*>(ctile + at) = o;
+          u32x2 o;
+          o[0] = f2bf(w[0]) | (f2bf(w[1]) << 16);
+          o[1] = f2bf(w[2]) | (f2bf(w[3]) << 16);
+          __builtin_nontemporal_store(o, reinterpret_cast<u32x2*>(ctile + at));
         }
       }
     }
@@ -642,20 +662,48 @@ hipError_t agg_launch(float* g, float* reps, const AggWeights& w, int K, int64_t
   return hipGetLastError();
 }
 
-template <bool BF16, int MODE>
-hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
-  const dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM), n_slots);
+template <bool BF16, int MODE, int SID>
+hipError_t gemm_launch_shape(const GemmArgs& g, int n_slots, hipStream_t s) {
+  typedef typename ShapeOf<MODE, SID>::type S;
+  const dim3 grid(((g.N + S::BN - 1) / S::BN) * ((g.M + S::BM - 1) / S::BM), n_slots);
   if (g.gather) {
     if constexpr (MODE == GEMM_FWD)
-      hipLaunchKernelGGL((gemm_kernel<BF16, MODE, true>), grid, dim3(ModeShape<MODE>::type::NT),
-                         0, s, g);
+      hipLaunchKernelGGL((gemm_kernel<BF16, MODE, true, SID>), grid, dim3(S::NT), 0, s, g);
     else
       return hipErrorInvalidValue;  // only the forward pass gathers dataset rows
   } else {
-    hipLaunchKernelGGL((gemm_kernel<BF16, MODE, false>), grid, dim3(ModeShape<MODE>::type::NT), 0,
-                       s, g);
+    hipLaunchKernelGGL((gemm_kernel<BF16, MODE, false, SID>), grid, dim3(S::NT), 0, s, g);
   }
   return hipGetLastError();
+}
+
+int device_cu_count() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      cus = v;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
+template <bool BF16, int MODE>
+hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
+  if constexpr (MODE == GEMM_WGRAD) {
+    return gemm_launch_shape<BF16, MODE, SHAPE_L>(g, n_slots, s);
+  } else {
+    // Largest tile that still gives every CU a workgroup.
+    const int64_t cus = device_cu_count();
+    auto tiles = [&](int bm, int bn) {
+      return static_cast<int64_t>((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * n_slots;
+    };
+    if (tiles(128, 128) >= cus) return gemm_launch_shape<BF16, MODE, SHAPE_L>(g, n_slots, s);
+    if (tiles(64, 128) >= cus) return gemm_launch_shape<BF16, MODE, SHAPE_M>(g, n_slots, s);
+    return gemm_launch_shape<BF16, MODE, SHAPE_S>(g, n_slots, s);
+  }
 }
 
 }  // namespace
