@@ -305,9 +305,12 @@ gemm_kernel(GemmArgs g) {
   if constexpr (MODE == GEMM_FWD) sa.init(A, g.a_ld, nullptr, m0, M, tid);
   if constexpr (MODE != GEMM_WGRAD)
     sb.init(B, g.b_ld, GATHER ? g.gather + z * g.gather_slot : nullptr, n0, N, tid);
-  // Forward layer 1: the workgroups of the first M tile also keep the gathered
-  // batch rows, contiguous, for the backward-weight pass of that layer.
-  T* rows_out = (GATHER && m0 == 0) ? static_cast<T*>(g.rows_out) + z * g.rows_out_slot : nullptr;
+  // Forward layer 1 also keeps the gathered batch rows, contiguous, for the
+  // backward-weight pass of that layer: K tile kt of the rows is written by
+  // the workgroup of M tile kt mod (number of M tiles), so the copy is spread
+  // over all workgroups of the launch.
+  T* rows_out = GATHER ? static_cast<T*>(g.rows_out) + z * g.rows_out_slot : nullptr;
+  const int gm = (M + BM - 1) / BM, mt = m0 / BM;
 
   // Accumulator element (i, j, r) sits at row m = mrow(i, r>>2) + (r & 3),
   // column n = ncol(j): four consecutive rows per lane and group r>>2.
@@ -355,7 +358,8 @@ gemm_kernel(GemmArgs g) {
     if constexpr (MODE == GEMM_WGRAD) t.load(B, g.b_ld, n0, g.b_ext, k0, K, tid); \
     else {                                                                \
       t.load(sb, B, k0, g.b_ext, tid);                                    \
-      if (GATHER && rows_out) t.copy_out(rows_out, g.rows_out_ld, n0, N, k0, g.b_ext, tid); \
+      if (GATHER && ((k0) / BK) % gm == mt)                               \
+        t.copy_out(rows_out, g.rows_out_ld, n0, N, k0, g.b_ext, tid);     \
     }                                                                     \
   } while (0)
 
