@@ -32,19 +32,22 @@ PMC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
 
 
 def gemm_work(cfg, tau):
-    """Algorithmic FLOPs and bytes of every GEMM launch of one round, per kind.
-    Bytes: each operand read once, each result written once (weights bf16 in
-    the products of bf16 workloads; fp32 master read and write in the update)."""
+    """Algorithmic FLOPs and bytes of every launch of one round (oscars_round),
+    per kind.  Bytes: each operand read once, each result written once (weights
+    bf16 in the products of bf16 workloads; fp32 master read and write in the
+    update; the start model cast to bf16 once; the average reads K replicas and
+    writes the global model)."""
     import numpy as np
     es = 2 if cfg.dtype == "bf16" else 4
     B, dims = cfg.batch, cfg.dims
     L = len(dims) - 1
     work = {"gemm_fwd": [0.0, 0.0], "gemm_dgrad": [0.0, 0.0], "gemm_wgrad_update": [0.0, 0.0],
-            "softmax_ce": [0.0, 0.0], "cast_bf16": [0.0, 0.0]}
+            "softmax_ce": [0.0, 0.0], "cast_bf16": [0.0, 0.0], "aggregate": [0.0, 0.0]}
     tau = np.asarray(tau)
     n_params = sum(o * i + o for i, o in zip(dims[:-1], dims[1:]))
     if cfg.dtype == "bf16":
-        work["cast_bf16"][1] += int((tau > 0).sum()) * n_params * 6.0
+        work["cast_bf16"][1] += n_params * 6.0
+    work["aggregate"][1] += (cfg.K + 1) * n_params * 4.0
     for j in range(int(tau.max())):
         ns = int((tau > j).sum())
         for l in range(1, L + 1):
@@ -124,12 +127,69 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
     }
 
 
+def bench_aggregation(args, cfg):
+    """Aggregation stress: K = 32 replicas of 25.6M fp32.  Before each round
+    (untimed) the replicas are rebuilt as g + delta_k; the aggregate +
+    broadcast launch of each round is timed with events on the same stream."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import workload
+    import paper_2102_08550_amd as P
+    print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
+    g0, delta = workload.gen_agg_vectors(cfg)
+    stale = workload.gen_staleness(cfg)
+    n, K = cfg.n_flat, cfg.K
+    G = torch.from_numpy(g0).cuda()
+    D = torch.from_numpy(delta).cuda()
+    del delta
+    R = torch.empty_like(D)
+    stream = torch.cuda.current_stream()
+    evs = []
+    for s in range(args.warmup + args.steps):
+        w = P.paper_weights(K, stale[s % cfg.rounds])
+        torch.add(G.unsqueeze(0), D, out=R)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        P.aggregate(G, R, w, K, n, n, True)
+        e1.record(stream)
+        if s >= args.warmup:
+            evs.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in evs)
+    bytes_round = (2 * K + 1) * n * 4.0
+    gbps = bytes_round * args.steps / (ms / 1e3) / 1e9
+    out = {
+        "metric": "local-SGD samples/sec (K sim workers, 1 GPU); aggregation GB/s vs HBM peak",
+        "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded N(0,1) + N(0,0.02^2))",
+        "config": {"workload": cfg.name, "K": K, "n": n, "broadcast": True},
+        "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": gbps / HBM_PEAK_GBPS, "traffic": None, "kernel": "aggregate",
+                     "avg_launch_us": ms * 1000.0 / args.steps,
+                     "algorithmic_per_launch": {"flop": 0.0, "bytes": bytes_round}},
+    }
+    if args.cpu_budget > 0:
+        m = 4_000_000
+        xs = [np.random.default_rng(k).standard_normal(m).astype(np.float32) for k in range(K)]
+        t0 = time.perf_counter()
+        oracle.tree_aggregate(xs, oracle.paper_weights(K))
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": (K + 1) * m * 4 / dt / 1e9, "unit": "GB/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"oracle tree aggregation of {K} x {m} fp32 (no broadcast)"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c5"])
+    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"],
+                    help="c5 (default): the full round; c4: aggregation-only stress")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--probe-copy-mib", type=int, default=0,
@@ -157,6 +217,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     cfg = workload.CONFIGS[args.workload]
+    if args.workload == "c4":
+        return bench_aggregation(args, cfg)
     print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
     ds = workload.gen_dataset(cfg)
     init = workload.gen_init(cfg)
@@ -176,8 +238,8 @@ def main():
         run.round(tau_for(s))
     torch.cuda.synchronize()
 
-    kinds = [P.KERNEL_CAST, P.KERNEL_FWD, P.KERNEL_SOFTMAX, P.KERNEL_DGRAD, P.KERNEL_WGRAD]
-    agg_events = []
+    kinds = [P.KERNEL_CAST, P.KERNEL_FWD, P.KERNEL_SOFTMAX, P.KERNEL_DGRAD, P.KERNEL_WGRAD,
+             P.KERNEL_AGGREGATE]
     samples = 0
     work_tot = {}
     print(f"[bench] timing {args.steps} rounds", file=sys.stderr, flush=True)
@@ -186,12 +248,7 @@ def main():
     t0 = time.perf_counter()
     for s in range(args.steps):
         tau = tau_for(args.warmup + s)
-        run.local_steps(tau)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        run.aggregate(True)
-        e1.record(stream)
-        agg_events.append((e0, e1))
+        run.round(tau)
         samples += int(np.sum(tau)) * cfg.batch
         for kname, (fl, by) in gemm_work(cfg, tau).items():
             a = work_tot.setdefault(kname, [0.0, 0.0])
@@ -203,9 +260,6 @@ def main():
     elapsed = t1 - t0
     ms_per_step = elapsed * 1000.0 / args.steps
 
-    agg_ms = sum(a.elapsed_time(b) for a, b in agg_events)
-    n = run.n
-    agg_bytes = args.steps * (2 * cfg.K + 1) * n * 4.0
     kernels = {}
     for name, (ms, cnt) in prof.items():
         if cnt == 0:
@@ -215,10 +269,6 @@ def main():
                          "TFLOPs": fl / (ms / 1e3) / 1e12 if fl else None,
                          "GBps": by / (ms / 1e3) / 1e9 if by else None,
                          "flop_per_launch": fl / cnt, "bytes_per_launch": by / cnt}
-    kernels["aggregate"] = {"ms": agg_ms, "launches": args.steps,
-                            "avg_us": agg_ms * 1000.0 / args.steps, "TFLOPs": None,
-                            "GBps": agg_bytes / (agg_ms / 1e3) / 1e9,
-                            "flop_per_launch": 0.0, "bytes_per_launch": agg_bytes / args.steps}
     dom = max(kernels, key=lambda k: kernels[k]["ms"])
     d = kernels[dom]
     ridge = MFMA_PEAK_TFLOPS[cfg.dtype] * 1e12 / (HBM_PEAK_GBPS * 1e9)
@@ -235,7 +285,7 @@ def main():
     roof["algorithmic_per_launch"] = {"flop": d["flop_per_launch"], "bytes": d["bytes_per_launch"]}
 
     local_ms = sum(v["ms"] for k, v in kernels.items() if k != "aggregate")
-    flops = sum(v[0] for v in work_tot.values())
+    flops = sum(v[0] for k, v in work_tot.items() if k != "aggregate")
     out = {
         "metric": "local-SGD samples/sec (K sim workers, 1 GPU); aggregation GB/s vs HBM peak",
         "value": samples / elapsed,
@@ -252,9 +302,12 @@ def main():
         "config": {"workload": cfg.name, "dims": list(cfg.dims), "K": cfg.K, "batch": cfg.batch,
                    "tau": tau_for(0), "lr": cfg.lr, "n_params": cfg.n_params,
                    "samples_per_round": samples // args.steps, "parallelism": "1 GPU, K simulated"},
-        "aggregation": {"GBps": agg_bytes / (agg_ms / 1e3) / 1e9,
-                        "frac_hbm_peak": agg_bytes / (agg_ms / 1e3) / 1e9 / HBM_PEAK_GBPS,
-                        "avg_us": agg_ms * 1000.0 / args.steps, "bytes_per_round": agg_bytes / args.steps},
+        "aggregation": {"GBps": kernels["aggregate"]["GBps"],
+                        "frac_hbm_peak": kernels["aggregate"]["GBps"] / HBM_PEAK_GBPS,
+                        "avg_us": kernels["aggregate"]["avg_us"],
+                        "bytes_per_round": kernels["aggregate"]["bytes_per_launch"],
+                        "note": "K-way average into the global model; oscars_round starts the "
+                                "next round's workers from it, so no broadcast copies are written"},
         "local_steps": {"kernel_ms_per_round": local_ms / args.steps,
                         "TFLOPs": flops / (local_ms / 1e3) / 1e12 if local_ms else None,
                         "frac_mfma_peak": flops / (local_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[cfg.dtype]

@@ -157,8 +157,27 @@ oscars_status oscars_sample_indices(const oscars_shards* shards, int32_t K, int3
 oscars_status oscars_local_steps(oscars_ctx* ctx, float* replicas, const oscars_shards* shards,
                                  const int32_t* tau, float lr, int32_t batch);
 
+/* One round of Eq. 4 (Approach): every worker starts from the global model,
+ * runs its tau[k] local SGD steps (as oscars_local_steps), and the parameter
+ * server's average of the K results becomes the new global model (as
+ * oscars_aggregate with broadcast = 0, n = ld = oscars_num_params).
+ *   global    device [oscars_num_params] fp32, in: the model every worker
+ *             starts from (the workers' pull), out: the average; 16-byte
+ *             aligned, not overlapping replicas;
+ *   replicas  device [K][oscars_num_params] fp32, out: the workers' models at
+ *             the barrier, before averaging (their previous contents are not
+ *             read; a worker with tau[k] = 0 gets a copy of the start model);
+ *   weights   host [K] fp32, finite.
+ * Equivalent to copying global into every replica, oscars_local_steps and
+ * oscars_aggregate(global, replicas, weights, K, n, n, 0), bit for bit, but
+ * without writing K copies of the model: the first step reads the global
+ * model directly. */
+oscars_status oscars_round(oscars_ctx* ctx, float* global, float* replicas,
+                           const oscars_shards* shards, const int32_t* tau, float lr,
+                           int32_t batch, const float* weights);
+
 /* Mean training loss of each worker over its steps in the last
- * oscars_local_steps call (NaN for a worker that ran no step).  Waits for the
+ * oscars_local_steps or oscars_round call (NaN for a worker that ran no step).  Waits for the
  * context's stream.  losses: host [K]. */
 oscars_status oscars_round_losses(oscars_ctx* ctx, float* losses);
 
@@ -192,7 +211,8 @@ enum {
   OSCARS_KERNEL_SOFTMAX = 2,
   OSCARS_KERNEL_DGRAD = 3,
   OSCARS_KERNEL_WGRAD = 4,
-  OSCARS_KERNEL_COUNT = 5
+  OSCARS_KERNEL_AGGREGATE = 5, /* the aggregation inside oscars_round */
+  OSCARS_KERNEL_COUNT = 6
 };
 oscars_status oscars_profile_begin(oscars_ctx* ctx, uint32_t kind_mask);
 oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches);

@@ -24,8 +24,9 @@ LIB_PATH = os.path.join(_HERE, "_lib", "liboscars.so")
 OK, E_INVALID, E_NOMEM, E_HIP, E_INFEASIBLE, E_STATE = 0, -1, -2, -3, -4, -5
 FP32, BF16 = 0, 1
 MAX_K = 64
-KERNEL_CAST, KERNEL_FWD, KERNEL_SOFTMAX, KERNEL_DGRAD, KERNEL_WGRAD = range(5)
-KERNEL_NAMES = ("cast_bf16", "gemm_fwd", "softmax_ce", "gemm_dgrad", "gemm_wgrad_update")
+KERNEL_CAST, KERNEL_FWD, KERNEL_SOFTMAX, KERNEL_DGRAD, KERNEL_WGRAD, KERNEL_AGGREGATE = range(6)
+KERNEL_NAMES = ("cast_bf16", "gemm_fwd", "softmax_ce", "gemm_dgrad", "gemm_wgrad_update",
+                "aggregate")
 
 _i32, _i64, _u32, _u64, _f32, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
                                      ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p)
@@ -62,6 +63,7 @@ _SIGS = {
     "oscars_shard_offsets": (_i32, [_i64, _i32, _P(_i64)]),
     "oscars_sample_indices": (_i32, [_P(_Shards), _i32, _i32, _i64, _i32, _i32, _P(_i64)]),
     "oscars_local_steps": (_i32, [_vp, _vp, _P(_Shards), _P(_i32), _f32, _i32]),
+    "oscars_round": (_i32, [_vp, _vp, _vp, _P(_Shards), _P(_i32), _f32, _i32, _P(_f32)]),
     "oscars_round_losses": (_i32, [_vp, _P(_f32)]),
     "oscars_aggregate": (_i32, [_vp, _vp, _P(_f32), _i32, _i64, _i64, _i32, _vp]),
     "oscars_get_cursors": (_i32, [_vp, _P(_i64)]),
@@ -234,8 +236,7 @@ class Context:
             out.append((flat[wo:wo + o * i].reshape(o, i), flat[bo:bo + o]))
         return out
 
-    def local_steps(self, replicas, x, y, offsets: Sequence[int], seed: int, tau: Sequence[int],
-                    lr: float, batch: int):
+    def _step_args(self, replicas, x, y, offsets, seed, tau):
         import torch
         rp = _dev_ptr(replicas, torch.float32, "replicas")
         if replicas.numel() < self.K * self.n_pad:
@@ -251,8 +252,27 @@ class Context:
         t, tp = _arr(tau, np.int32)
         if len(t) != self.K or len(offsets) != self.K + 1:
             raise ValueError("tau needs K entries and offsets K + 1")
+        return rp, sh, (keep, t), tp
+
+    def local_steps(self, replicas, x, y, offsets: Sequence[int], seed: int, tau: Sequence[int],
+                    lr: float, batch: int):
+        rp, sh, keep, tp = self._step_args(replicas, x, y, offsets, seed, tau)
         _check(_lib().oscars_local_steps(self._h, rp, ctypes.byref(sh), tp, float(lr), int(batch)),
                "oscars_local_steps")
+
+    def round(self, global_, replicas, x, y, offsets: Sequence[int], seed: int,
+              tau: Sequence[int], lr: float, batch: int, weights: Sequence[float]):
+        """One round of Eq. 4 from the global model (oscars_round)."""
+        import torch
+        gp = _dev_ptr(global_, torch.float32, "global")
+        if global_.numel() < self.n_pad:
+            raise ValueError("global must hold n_pad floats")
+        rp, sh, keep, tp = self._step_args(replicas, x, y, offsets, seed, tau)
+        w, wp = _arr(weights, np.float32)
+        if len(w) != self.K:
+            raise ValueError("one weight per worker")
+        _check(_lib().oscars_round(self._h, gp, rp, ctypes.byref(sh), tp, float(lr), int(batch),
+                                   wp), "oscars_round")
 
     def round_losses(self) -> np.ndarray:
         out = np.zeros(self.K, np.float32)
@@ -277,7 +297,8 @@ class Context:
         _check(_lib().oscars_profile_begin(self._h, mask), "oscars_profile_begin")
 
     def profile_end(self):
-        ms = (ctypes.c_double * 5)()
-        n = (_i64 * 5)()
+        k = len(KERNEL_NAMES)
+        ms = (ctypes.c_double * k)()
+        n = (_i64 * k)()
         _check(_lib().oscars_profile_end(self._h, ms, n), "oscars_profile_end")
-        return {KERNEL_NAMES[i]: (ms[i], n[i]) for i in range(5)}
+        return {KERNEL_NAMES[i]: (ms[i], n[i]) for i in range(k)}

@@ -46,8 +46,13 @@ struct GemmArgs {
   int64_t out_ld, out_slot;
   const void* mask;  // DGRAD: activations of the layer below
   int64_t mask_ld, mask_slot;
-  float* master;  // fp32 replicas (bias for FWD; W and bias for WGRAD)
+  float* master;  // fp32 replicas written by WGRAD (by order[z])
   int64_t master_slot;  // replica stride
+  // fp32 parameters read: the bias in FWD, W and bias in WGRAD.  Normally the
+  // replicas themselves (master_in = master); in the first local step of a
+  // round that starts from the global model, the global model with stride 0.
+  const float* master_in;
+  int64_t master_in_slot;
   int64_t w_off, b_off;  // W_l and b_l offsets within a replica
   uint16_t* wcopy;  // WGRAD, bf16 models: slot-indexed bf16 weight copies
   int64_t wcopy_slot;

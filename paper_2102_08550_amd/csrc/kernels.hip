@@ -293,6 +293,7 @@ gemm_kernel(GemmArgs g) {
   const T* A = static_cast<const T*>(g.a) + (g.a_by_order ? rep : z) * g.a_slot;
   const T* B = static_cast<const T*>(g.b) + z * g.b_slot;
   float* master = g.master + static_cast<int64_t>(rep) * g.master_slot;
+  const float* master_in = g.master_in + static_cast<int64_t>(rep) * g.master_in_slot;
 
   // A: weights K-contiguous in FWD, weights M-contiguous in DGRAD, activations
   // M-contiguous in WGRAD.  B: activations / delta K-contiguous in FWD and
@@ -323,14 +324,15 @@ gemm_kernel(GemmArgs g) {
   // so 32 lanes read one contiguous 512-byte row segment.
   constexpr int WCH = (MODE == GEMM_WGRAD) ? BM * BN / 4 / NTHR : 1;
   f32x4 wpre[WCH];
-  // Workgroup-uniform tile base; lanes add a 32-bit offset (row * M + col).
+  // Workgroup-uniform tile bases; lanes add a 32-bit offset (row * M + col).
   float* wtile = master + g.w_off + static_cast<int64_t>(n0) * M + m0;
+  const float* wtile_in = master_in + g.w_off + static_cast<int64_t>(n0) * M + m0;
   if constexpr (MODE == GEMM_WGRAD) {
 #pragma unroll
     for (int p = 0; p < WCH; ++p) {
       const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);
       const bool ok = n0 + row < N && m0 + col < M;  // M % 4 == 0: chunks are whole
-      wpre[p] = ok ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(wtile + (row * M + col)))
+      wpre[p] = ok ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(wtile_in + (row * M + col)))
                    : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
   }
@@ -472,10 +474,8 @@ gemm_kernel(GemmArgs g) {
         }
       }
     }
-    if (bias_wg && tid < BN && n0 + tid < N) {
-      float* bp = master + g.b_off + n0 + tid;
-      *bp = fmaf(-g.lr, dbias, *bp);
-    }
+    if (bias_wg && tid < BN && n0 + tid < N)
+      master[g.b_off + n0 + tid] = fmaf(-g.lr, dbias, master_in[g.b_off + n0 + tid]);
     return;
   }
 
@@ -495,7 +495,7 @@ gemm_kernel(GemmArgs g) {
                    acc[i][j][4 * q + 3]};
         if constexpr (MODE == GEMM_FWD) {
           // out[b = n][o = m..m+3]
-          const float* bias = master + g.b_off + m;
+          const float* bias = master_in + g.b_off + m;
           for (int e = 0; e < 4; ++e) {
             float o = v[e] + (e < cnt ? bias[e] : 0.0f);
             v[e] = g.relu ? fmaxf(o, 0.0f) : o;
@@ -593,76 +593,105 @@ struct AggWeights {
   float w[OSCARS_MAX_K];
 };
 
-// Lane group q of a wave (G groups of 64 / G lanes) owns leaves qL .. qL+L-1,
-// each lane four consecutive elements.  The lane sums its leaves as a
-// pairwise tree; xor-shuffles over the group bits then join neighbouring
-// subtrees, which completes the same balanced tree over P = G L leaves.
-template <int G, int L>
+// Lane group q of a wave (G groups of 64 / G lanes) owns leaves qL .. qL+L-1;
+// each lane owns V chunks of four consecutive elements.  The lane sums its
+// leaves as a pairwise tree; xor-shuffles over the group bits then join
+// neighbouring subtrees, which completes the same balanced tree over
+// P = G L leaves.
+// Replicas and the global model are streamed once per round: non-temporal.
+__device__ __forceinline__ void agg_store(f32x4 v, f32x4* p) { __builtin_nontemporal_store(v, p); }
+
+template <int G, int L, int V>
 __global__ __launch_bounds__(256) void aggregate_kernel(float* g, float* reps, AggWeights w,
                                                         int K, int64_t n, int64_t ld, int bcast) {
   constexpr int LPG = 64 / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane / LPG, e = lane % LPG;
-  const int64_t i0 = ((static_cast<int64_t>(blockIdx.x) * 4 + wave) * LPG + e) * 4;
-  const int valid = (n - i0 >= 4) ? 4 : static_cast<int>(n - i0 > 0 ? n - i0 : 0);
-  f32x4 leaf[L];
+  const int64_t base = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (V * LPG * 4);
+  f32x4 leaf[V][L];
 #pragma unroll
-  for (int i = 0; i < L; ++i) {
-    const int k = q * L + i;
-    f32x4 x = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (k < K) {
-      const float* p = reps + k * ld + i0;
-      if (valid == 4) {
-        x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
-      } else {
-        for (int t = 0; t < 4; ++t)
-          if (t < valid) x[t] = p[t];
+  for (int v = 0; v < V; ++v) {
+    const int64_t i0 = base + (v * LPG + e) * 4;
+    const int valid = (n - i0 >= 4) ? 4 : static_cast<int>(n - i0 > 0 ? n - i0 : 0);
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int k = q * L + i;
+      f32x4 x = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (k < K) {
+        const float* p = reps + k * ld + i0;
+        if (valid == 4) {
+          x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+        } else {
+          for (int t = 0; t < 4; ++t)
+            if (t < valid) x[t] = p[t];
+        }
+        x = x * w.w[k];
       }
-      x = x * w.w[k];
+      leaf[v][i] = x;
     }
-    leaf[i] = x;
   }
 #pragma unroll
-  for (int s = 1; s < L; s *= 2)
+  for (int v = 0; v < V; ++v) {
+    const int64_t i0 = base + (v * LPG + e) * 4;
+    const int valid = (n - i0 >= 4) ? 4 : static_cast<int>(n - i0 > 0 ? n - i0 : 0);
 #pragma unroll
-    for (int i = 0; i < L; i += 2 * s) leaf[i] = leaf[i] + leaf[i + s];
-  f32x4 v = leaf[0];
+    for (int s = 1; s < L; s *= 2)
 #pragma unroll
-  for (int d = LPG; d < 64; d *= 2) {
-    f32x4 o;
+      for (int i = 0; i < L; i += 2 * s) leaf[v][i] = leaf[v][i] + leaf[v][i + s];
+    f32x4 r = leaf[v][0];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) o[t] = __shfl_xor(v[t], d);
-    v = v + o;
-  }
-  if (valid == 4) {
-    if (q == 0) __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(g + i0));
-    if (bcast) {
+    for (int d = LPG; d < 64; d *= 2) {
+      f32x4 o;
 #pragma unroll
-      for (int i = 0; i < L; ++i) {
-        const int k = q * L + i;
-        if (k < K) __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(reps + k * ld + i0));
-      }
+      for (int t = 0; t < 4; ++t) o[t] = __shfl_xor(r[t], d);
+      r = r + o;
     }
-  } else if (valid > 0) {
-    for (int t = 0; t < valid; ++t) {
-      if (q == 0) g[i0 + t] = v[t];
-      if (bcast)
+    if (valid == 4) {
+      if (q == 0) agg_store(r, reinterpret_cast<f32x4*>(g + i0));
+      if (bcast) {
+#pragma unroll
         for (int i = 0; i < L; ++i) {
           const int k = q * L + i;
-          if (k < K) reps[k * ld + i0 + t] = v[t];
+          if (k < K) agg_store(r, reinterpret_cast<f32x4*>(reps + k * ld + i0));
         }
+      }
+    } else if (valid > 0) {
+      for (int t = 0; t < valid; ++t) {
+        if (q == 0) g[i0 + t] = r[t];
+        if (bcast)
+          for (int i = 0; i < L; ++i) {
+            const int k = q * L + i;
+            if (k < K) reps[k * ld + i0 + t] = r[t];
+          }
+      }
     }
   }
 }
 
-template <int G, int L>
+// Broadcast of g into every replica, as a write-dominated pass of its own:
+// each lane reads four elements of g once and stores them to all K replicas.
+// Broadcast of g into every replica, as a write-dominated pass of its own:
+// each lane reads four elements of g once and stores them to all K replicas.
+__global__ __launch_bounds__(256) void broadcast_kernel(const float* g, float* reps, int K,
+                                                        int64_t n, int64_t ld) {
+  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (i0 + 4 <= n) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(g + i0);
+    for (int k = 0; k < K; ++k) agg_store(v, reinterpret_cast<f32x4*>(reps + k * ld + i0));
+  } else if (i0 < n) {
+    for (int64_t i = i0; i < n; ++i)
+      for (int k = 0; k < K; ++k) reps[k * ld + i] = g[i];
+  }
+}
+
+template <int G, int L, int V>
 hipError_t agg_launch(float* g, float* reps, const AggWeights& w, int K, int64_t n, int64_t ld,
                       int bcast, hipStream_t s) {
-  constexpr int per_block = 4 * (64 / G) * 4;
+  constexpr int per_block = 4 * V * (64 / G) * 4;
   const int64_t blocks = (n + per_block - 1) / per_block;
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((aggregate_kernel<G, L>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                     g, reps, w, K, n, ld, bcast);
+  hipLaunchKernelGGL((aggregate_kernel<G, L, V>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                     s, g, reps, w, K, n, ld, bcast);
   return hipGetLastError();
 }
 
@@ -754,6 +783,31 @@ hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int3
   return hipGetLastError();
 }
 
+// Leaves per lane and lane groups: P = G L with at most 4 groups of 16 lanes
+// (measured best on MI355X for K = 8, 16, 32 against 1, 2 and 8 groups and
+// two chunks per lane).
+constexpr int AGG_GMAX = 4, AGG_V = 1;
+// From this many replicas on the broadcast is a pass of its own (K = 32:
+// 5.5 -> 5.8 TB/s on MI355X; K = 8 is faster fused).
+constexpr int AGG_SPLIT_K = 16;
+template <int P>
+hipError_t agg_dispatch(float* g, float* reps, const AggWeights& w, int K, int64_t n, int64_t ld,
+                        int bcast, hipStream_t s) {
+  constexpr int G = P < AGG_GMAX ? P : AGG_GMAX;
+  // From AGG_SPLIT_K replicas on, the broadcast runs as its own pass:
+  // HBM then sees a read phase and a write phase instead of K + 1 interleaved
+  // write streams per workgroup.  The values written are the same.
+  if (!bcast || K < AGG_SPLIT_K)
+    return agg_launch<G, P / G, AGG_V>(g, reps, w, K, n, ld, bcast, s);
+  hipError_t e = agg_launch<G, P / G, AGG_V>(g, reps, w, K, n, ld, 0, s);
+  if (e != hipSuccess) return e;
+  const int64_t blocks = (n + 1023) / 1024;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(broadcast_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, g,
+                     reps, K, n, ld);
+  return hipGetLastError();
+}
+
 hipError_t launch_aggregate(float* g, float* replicas, const float* w, int K, int64_t n,
                             int64_t ld, int broadcast, hipStream_t s) {
   AggWeights aw;
@@ -761,13 +815,13 @@ hipError_t launch_aggregate(float* g, float* replicas, const float* w, int K, in
   int P = 1;
   while (P < K) P *= 2;
   switch (P) {
-    case 1: return agg_launch<1, 1>(g, replicas, aw, K, n, ld, broadcast, s);
-    case 2: return agg_launch<2, 1>(g, replicas, aw, K, n, ld, broadcast, s);
-    case 4: return agg_launch<4, 1>(g, replicas, aw, K, n, ld, broadcast, s);
-    case 8: return agg_launch<4, 2>(g, replicas, aw, K, n, ld, broadcast, s);
-    case 16: return agg_launch<4, 4>(g, replicas, aw, K, n, ld, broadcast, s);
-    case 32: return agg_launch<4, 8>(g, replicas, aw, K, n, ld, broadcast, s);
-    case 64: return agg_launch<4, 16>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 1: return agg_dispatch<1>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 2: return agg_dispatch<2>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 4: return agg_dispatch<4>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 8: return agg_dispatch<8>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 16: return agg_dispatch<16>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 32: return agg_dispatch<32>(g, replicas, aw, K, n, ld, broadcast, s);
+    case 64: return agg_dispatch<64>(g, replicas, aw, K, n, ld, broadcast, s);
   }
   return hipErrorInvalidValue;
 }

@@ -52,6 +52,7 @@ struct oscars_ctx {
 
   std::vector<void*> allocs;
   uint16_t* wcopy = nullptr;       // [K][n_pad] bf16 weight copies (bf16 models)
+  uint16_t* gq = nullptr;          // [n_pad] bf16 copy of a round's start model (bf16 models)
   std::vector<void*> act;          // act[l], l = 0..L-1: [K][max_batch][ld[l]] (act[0]: batch rows)
   float* logits = nullptr;         // [K][max_batch][ld[L]]
   std::vector<void*> delta;        // delta[l], l = 1..L: [K][max_batch][ld[l]]
@@ -169,6 +170,8 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
     void* p = nullptr;
     e = dev_alloc(c, static_cast<size_t>(K) * c->n_pad * 2, &p);
     c->wcopy = static_cast<uint16_t*>(p);
+    if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->n_pad) * 2, &p);
+    c->gq = static_cast<uint16_t*>(p);
   }
   c->act.assign(c->L + 1, nullptr);
   c->delta.assign(c->L + 1, nullptr);
@@ -228,8 +231,16 @@ oscars_status oscars_set_cursors(oscars_ctx* ctx, const int64_t* steps_done) {
   return OSCARS_OK;
 }
 
-oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_shards* s,
-                                 const int32_t* tau, float lr, int32_t batch) {
+}  // extern "C"
+
+namespace {
+
+// tau_k local steps of every worker.  start == nullptr: worker k starts from
+// replica k.  Otherwise every worker starts from `start` (the global model of
+// a round): the first step reads `start` and writes replica k; workers with
+// tau_k = 0 get a copy of `start`.
+oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start,
+                              const oscars_shards* s, const int32_t* tau, float lr, int32_t batch) {
   // ---- validation (no side effects on failure) ----
   if (!c || !replicas || !s || !tau || !s->x || !s->y || !s->offsets) return OSCARS_E_INVALID;
   if (!aligned16(replicas) || !aligned16(s->x)) return OSCARS_E_INVALID;
@@ -254,6 +265,14 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
   c->last_tau.assign(tau, tau + K);
   c->last_B = batch;
   c->last_tau_max = n_slots ? tau[order[0]] : 0;
+  if (start) {
+    for (int k = 0; k < K; ++k) {
+      if (tau[k] > 0) continue;
+      hipError_t e = hipMemcpyAsync(replicas + static_cast<int64_t>(k) * c->n_pad, start,
+                                    c->n_pad * sizeof(float), hipMemcpyDeviceToDevice, c->stream);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+  }
   if (n_slots == 0) return OSCARS_OK;
   const int tau_max = tau[order[0]];
   const int B = batch;
@@ -315,11 +334,12 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
   const int32_t* d_order = c->table_dev;
   const int32_t* d_rows = c->table_dev + 64;
 
-  // ---- bf16 working copies of the active replicas ----
+  // ---- bf16 working copies: of the start model once, else of every active replica ----
   if (c->bf16) {
     e = timed(c, OSCARS_KERNEL_CAST, [&] {
-      return launch_cast_bf16(replicas, c->n_pad, d_order, c->wcopy, c->n_pad, c->n_pad, n_slots,
-                              c->stream);
+      return start ? launch_cast_bf16(start, 0, d_order, c->gq, 0, c->n_pad, 1, c->stream)
+                   : launch_cast_bf16(replicas, c->n_pad, d_order, c->wcopy, c->n_pad, c->n_pad,
+                                      n_slots, c->stream);
     });
     if (e != hipSuccess) return hip_fail(e);
   }
@@ -332,21 +352,31 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
     const int32_t* rows_j = d_rows + static_cast<int64_t>(j) * B;
 
     // Weights as operand A: slot-indexed bf16 copies, or the fp32 masters
-    // themselves (reached through order[]).
+    // themselves (reached through order[]); in the first step of a round that
+    // starts from the global model, that model (shared by every slot).
+    const bool from_start = start && j == 0;
     auto weights = [&](GemmArgs& g, int l) {
-      if (c->bf16) {
+      if (from_start) {
+        g.a = c->bf16 ? static_cast<const void*>(c->gq + c->w_off[l])
+                      : static_cast<const void*>(start + c->w_off[l]);
+        g.a_by_order = 0;
+        g.a_slot = 0;
+      } else if (c->bf16) {
         g.a = c->wcopy + c->w_off[l];
         g.a_by_order = 0;
+        g.a_slot = c->n_pad;
       } else {
         g.a = replicas + c->w_off[l];
         g.a_by_order = 1;
+        g.a_slot = c->n_pad;
       }
-      g.a_slot = c->n_pad;
       g.a_ld = c->dims[l - 1];
     };
     auto common = [&](GemmArgs& g, int l) {
       g.master = replicas;
       g.master_slot = c->n_pad;
+      g.master_in = from_start ? start : replicas;
+      g.master_in_slot = from_start ? 0 : c->n_pad;
       g.w_off = c->w_off[l];
       g.b_off = c->b_off[l];
       g.order = d_order;
@@ -448,6 +478,33 @@ oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_sh
   }
   for (int k = 0; k < K; ++k) c->cursors[k] += tau[k];
   return OSCARS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+oscars_status oscars_local_steps(oscars_ctx* c, float* replicas, const oscars_shards* s,
+                                 const int32_t* tau, float lr, int32_t batch) {
+  return run_local_steps(c, replicas, nullptr, s, tau, lr, batch);
+}
+
+oscars_status oscars_round(oscars_ctx* c, float* global, float* replicas, const oscars_shards* s,
+                           const int32_t* tau, float lr, int32_t batch, const float* weights) {
+  if (!c || !global || !replicas || !weights) return OSCARS_E_INVALID;
+  if (!aligned16(global)) return OSCARS_E_INVALID;
+  for (int k = 0; k < c->K; ++k)
+    if (!std::isfinite(weights[k])) return OSCARS_E_INVALID;
+  const uintptr_t g0 = reinterpret_cast<uintptr_t>(global), g1 = g0 + c->n_pad * sizeof(float);
+  const uintptr_t r0 = reinterpret_cast<uintptr_t>(replicas),
+                  r1 = r0 + static_cast<uintptr_t>(c->K) * c->n_pad * sizeof(float);
+  if (g0 < r1 && r0 < g1) return OSCARS_E_INVALID;
+  oscars_status st = run_local_steps(c, replicas, global, s, tau, lr, batch);
+  if (st != OSCARS_OK) return st;
+  hipError_t e = timed(c, OSCARS_KERNEL_AGGREGATE, [&] {
+    return launch_aggregate(global, replicas, weights, c->K, c->n_pad, c->n_pad, 0, c->stream);
+  });
+  return e == hipSuccess ? OSCARS_OK : hip_fail(e);
 }
 
 oscars_status oscars_round_losses(oscars_ctx* c, float* losses) {

@@ -1,8 +1,10 @@
-"""Round driver over the C ABI: one Oscars round (Approach, Eq. 4) is
-``oscars_local_steps`` (every worker's tau_k local SGD steps) followed by
-``oscars_aggregate`` with broadcast (the 1/K average written back to every
-replica).  This module only moves data into device memory and sequences the
-two calls; all arithmetic runs in the HIP library."""
+"""Round driver over the C ABI.  One Oscars round (Approach, Eq. 4) is either
+``oscars_round`` (every worker starts from the global model, runs its tau_k
+local SGD steps, and the 1/K average becomes the new global model), or the
+two separate calls ``oscars_local_steps`` then ``oscars_aggregate`` with
+broadcast (the average written back to every replica).  This module only
+moves data into device memory and sequences calls; all arithmetic runs in
+the HIP library."""
 from __future__ import annotations
 
 from typing import Optional, Sequence
@@ -58,6 +60,13 @@ class OscarsRun:
         aggregate(self.g, self.replicas, self.weights, self.cfg.K, self.n, self.n, broadcast)
 
     def round(self, tau: Sequence[int]):
+        """One round through oscars_round; afterwards ``g`` is the average and
+        ``replicas`` the workers' models before averaging."""
+        self.ctx.round(self.g, self.replicas, self.x, self.y, self.offsets, self.seed, tau,
+                       self.cfg.lr, self.cfg.batch, self.weights)
+
+    def round_broadcast(self, tau: Sequence[int]):
+        """The same round as local steps plus aggregation with broadcast."""
         self.local_steps(tau)
         self.aggregate(True)
 

@@ -35,11 +35,13 @@ def oracle_tau(cfg, rounds):
     return workload.gen_tau_uniform(cfg)[:rounds]
 
 
-def gpu_rounds(cfg, ds, init, tau_rounds, check_agg=True):
-    """Run len(tau_rounds) rounds on the GPU.  After every round's local steps
-    the replicas are copied out and the GPU aggregate is compared bit for bit
-    with the oracle's tree over those same replicas.  Returns (list of global
-    layer lists per round, list of per-worker losses per round)."""
+def gpu_rounds(cfg, ds, init, tau_rounds, check_agg=True, fused=False):
+    """Run len(tau_rounds) rounds on the GPU, either as oscars_local_steps +
+    oscars_aggregate with broadcast, or (fused) as oscars_round.  After every
+    round the workers' pre-average models are copied out and the GPU aggregate
+    is compared bit for bit with the oracle's tree over those same replicas.
+    Returns (list of global layer lists per round, list of per-worker losses
+    per round)."""
     import torch
 
     from paper_2102_08550_amd.rounds import OscarsRun
@@ -47,10 +49,16 @@ def gpu_rounds(cfg, ds, init, tau_rounds, check_agg=True):
     globals_, losses = [], []
     try:
         for r, tau in enumerate(tau_rounds):
-            run.local_steps([int(t) for t in tau])
-            losses.append(run.ctx.round_losses())
-            reps = run.replicas.view(cfg.K, run.n).cpu().numpy() if check_agg else None
-            run.aggregate(True)
+            tau = [int(t) for t in tau]
+            if fused:
+                run.round(tau)
+                losses.append(run.ctx.round_losses())
+                reps = run.replicas.view(cfg.K, run.n).cpu().numpy() if check_agg else None
+            else:
+                run.local_steps(tau)
+                losses.append(run.ctx.round_losses())
+                reps = run.replicas.view(cfg.K, run.n).cpu().numpy() if check_agg else None
+                run.aggregate(True)
             torch.cuda.synchronize()
             g = run.g.cpu().numpy()
             if check_agg:
@@ -58,8 +66,9 @@ def gpu_rounds(cfg, ds, init, tau_rounds, check_agg=True):
                                                oracle.paper_weights(cfg.K))
                 assert np.array_equal(g.view(np.uint32), expect.view(np.uint32)), \
                     f"round {r}: aggregate differs from the oracle tree"
-                back = run.replicas.view(cfg.K, run.n).cpu().numpy()
-                assert np.array_equal(back, np.broadcast_to(g, back.shape)), "broadcast"
+                if not fused:
+                    back = run.replicas.view(cfg.K, run.n).cpu().numpy()
+                    assert np.array_equal(back, np.broadcast_to(g, back.shape)), "broadcast"
             globals_.append(run.ctx.unpack(g))
     finally:
         run.close()

@@ -40,16 +40,20 @@ TRAJ = {
 }
 
 
-@pytest.mark.parametrize("name", list(TRAJ))
-def test_trajectory_matches_oracle(P, name):
+TRAJ_CASES = [(n, False) for n in TRAJ] + [("c2", True), ("c5s", True), ("tiny-bf16", True)]
+
+
+@pytest.mark.parametrize("name,fused", TRAJ_CASES,
+                         ids=[f"{n}-{'round' if f else 'steps+agg'}" for n, f in TRAJ_CASES])
+def test_trajectory_matches_oracle(P, name, fused):
     cfg = TRAJ[name]
-    say(f"trajectory {name}: dims={cfg.dims} K={cfg.K} B={cfg.batch} R={cfg.rounds}")
+    say(f"trajectory {name} fused={fused}: dims={cfg.dims} K={cfg.K} B={cfg.batch} R={cfg.rounds}")
     ds = workload.gen_dataset(cfg)
     init = workload.gen_init(cfg)
     from paper_2102_08550_amd.rounds import tau_schedule
     tau = tau_schedule(cfg)
     assert np.array_equal(tau, oracle_tau(cfg, cfg.rounds))
-    g_gpu, l_gpu = gpu_rounds(cfg, ds, init, tau)
+    g_gpu, l_gpu = gpu_rounds(cfg, ds, init, tau, fused=fused)
     g_ref, l_ref = oracle_rounds(cfg, ds, init, tau)
     tol = BF16_TOL if cfg.dtype == workload.BF16 else FP32_TOL
     errs = [rel_err(a, b) for a, b in zip(g_gpu, g_ref)]
@@ -113,6 +117,33 @@ def test_masking_independence_and_determinism(P, cfg):
     for k in range(cfg.K):
         if cfg.tau_given[k] == 0:
             assert np.array_equal(grouped[k], flat)
+
+
+@pytest.mark.parametrize("dtype", [workload.BF16, workload.FP32])
+def test_round_equals_local_steps_plus_aggregate(P, dtype):
+    """oscars_round == (copy global into every replica, oscars_local_steps,
+    oscars_aggregate without broadcast), bit for bit, over three rounds with a
+    worker idle (tau = 0) in one of them."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    cfg = workload.Config("round-eq", (72, 136, 64, 37), dtype, K=5, n_rows=900, batch=24,
+                          tau_rule="given", lr=0.1, rounds=3, seed=12)
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    taus = [[3, 1, 0, 2, 4], [1, 1, 1, 1, 1], [2, 5, 3, 0, 1]]
+    a = OscarsRun(cfg, ds, init)
+    b = OscarsRun(cfg, ds, init)
+    for t in taus:
+        a.round(t)
+        b.replicas.copy_(b.g.repeat(cfg.K))
+        b.local_steps(t)
+        b.aggregate(False)
+        torch.cuda.synchronize()
+        assert torch.equal(a.replicas, b.replicas)
+        assert torch.equal(a.g, b.g)
+        assert np.allclose(a.ctx.round_losses(), b.ctx.round_losses(), equal_nan=True)
+    a.close()
+    b.close()
 
 
 def test_cursor_resume(P):
