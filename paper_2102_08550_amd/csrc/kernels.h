@@ -56,6 +56,8 @@ struct GemmArgs {
   int64_t w_off, b_off;  // W_l and b_l offsets within a replica
   uint16_t* wcopy;  // WGRAD, bf16 models: slot-indexed bf16 weight copies
   int64_t wcopy_slot;
+  int wcopy_slots;  // WGRAD: only slots z < wcopy_slots refresh their copy (the
+                    // others take their last local step: nothing reads it)
   const int32_t* order;  // [slots] replica id of each slot
   float lr;
   int relu;  // FWD: apply ReLU

@@ -455,8 +455,9 @@ gemm_kernel(GemmArgs g) {
                     acc[i][j][4 * q + 3]};
         }
     __syncthreads();
-    uint16_t* ctile =
-        g.wcopy ? g.wcopy + z * g.wcopy_slot + g.w_off + static_cast<int64_t>(n0) * M + m0 : nullptr;
+    uint16_t* ctile = (g.wcopy && z < g.wcopy_slots)
+                          ? g.wcopy + z * g.wcopy_slot + g.w_off + static_cast<int64_t>(n0) * M + m0
+                          : nullptr;
 #pragma unroll
     for (int p = 0; p < WCH; ++p) {
       const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);

@@ -347,8 +347,9 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
   const int L = c->L;
   const int64_t rows_slot = static_cast<int64_t>(tau_max) * B;
   for (int j = 0; j < tau_max; ++j) {
-    int ns = 0;
+    int ns = 0, ns_next = 0;
     while (ns < n_slots && tau[order[ns]] > j) ++ns;
+    while (ns_next < n_slots && tau[order[ns_next]] > j + 1) ++ns_next;
     const int32_t* rows_j = d_rows + static_cast<int64_t>(j) * B;
 
     // Weights as operand A: slot-indexed bf16 copies, or the fp32 masters
@@ -471,6 +472,7 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
       common(g, l);
       g.wcopy = c->bf16 ? c->wcopy : nullptr;
       g.wcopy_slot = c->n_pad;
+      g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
       e = timed(c, OSCARS_KERNEL_WGRAD,
                 [&] { return launch_gemm(g, GEMM_WGRAD, c->bf16, ns, c->stream); });
       if (e != hipSuccess) return hip_fail(e);
