@@ -85,9 +85,10 @@ def pmc_traffic(kernel: str, workload_name: str):
 
 
 def cpu_baseline(cfg, ds, init, tau, budget_s: float):
-    """The oracle as it stands, on the host cores: worker steps of the first
-    round (the worker with the most steps) until the time budget is used, and
-    the oracle aggregation on a slice of K replicas."""
+    """The oracle as it stands, on the host cores: the workers' local SGD steps
+    of round after round (worker by worker, each from the initial model of the
+    round, as a worker runs them), until the time budget is used; and the
+    oracle aggregation on a slice of K replicas."""
     import numpy as np
 
     import oracle
@@ -97,20 +98,28 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
         threads = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
     except Exception:
         threads = os.cpu_count() or 1
-    k = int(np.argmax(tau))
     off = oracle.shard_offsets(cfg.n_rows, cfg.K)
     seed = workload.sampler_seed(cfg)
-    x = [(W.astype(np.float64), b.astype(np.float64)) for W, b in init]
-    t0 = time.perf_counter()
-    steps = 0
+    x0 = [(W.astype(np.float64), b.astype(np.float64)) for W, b in init]
     cache = {}
-    while steps < int(tau[k]):
-        rows = oracle.batch_rows(seed, off, k, steps, cfg.batch, cache)
-        xb = workload.bf16_bits_to_f32(ds.x[rows]) if cfg.dtype == "bf16" else ds.x[rows]
-        x, _ = oracle.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr, cfg.dtype == "bf16")
-        steps += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
+    steps, rounds = 0, 0
+    done = [0] * cfg.K
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        for k in sorted(range(cfg.K), key=lambda k: -int(tau[k])):
+            x = x0
+            for j in range(int(tau[k])):
+                rows = oracle.batch_rows(seed, off, k, done[k] + j, cfg.batch, cache)
+                xb = workload.bf16_bits_to_f32(ds.x[rows]) if cfg.dtype == "bf16" else ds.x[rows]
+                x, _ = oracle.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr,
+                                       cfg.dtype == "bf16")
+                steps += 1
+                if time.perf_counter() - t0 > budget_s:
+                    break
+            done[k] += int(tau[k])
+            if time.perf_counter() - t0 > budget_s:
+                break
+        rounds += 1
     dt = time.perf_counter() - t0
     n_slice = 4_000_000
     reps = [np.random.default_rng(i).standard_normal(n_slice).astype(np.float32)
@@ -120,9 +129,9 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
     dta = time.perf_counter() - t1
     return {
         "value": steps * cfg.batch / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
-        "sample": f"worker {k}: {steps} local SGD step(s) of batch {cfg.batch} from the initial "
-                  f"model ({dt:.1f} s, float64 with bf16 rounding points); aggregation of "
-                  f"{cfg.K} x {n_slice} fp32 slices",
+        "sample": f"{steps} local SGD steps of batch {cfg.batch} (workers' steps of {rounds} "
+                  f"round(s), each worker from the round's start model; {dt:.1f} s, float64 "
+                  f"with bf16 rounding points); aggregation of {cfg.K} x {n_slice} fp32 slices",
         "aggregate_GBps": (cfg.K + 1) * n_slice * 4 / dta / 1e9,
     }
 
