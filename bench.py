@@ -249,6 +249,8 @@ def main():
     # around the dominant kernel's launches only (events around every launch
     # would add about 10% to a round).
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    # The first round also picks the forward / backward-data GEMM tilings (each
+    # configuration's first launch times the candidates); it is not profiled.
     run.round(tau_for(0))
     torch.cuda.synchronize()
     run.ctx.profile_begin(kinds)

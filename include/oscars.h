@@ -217,6 +217,33 @@ enum {
 oscars_status oscars_profile_begin(oscars_ctx* ctx, uint32_t kind_mask);
 oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches);
 
+/* Tiling of the forward and backward-data GEMMs, process-wide (a tuning and
+ * testing aid).  Every tiling sums each output in the same order (K in
+ * chunks of 1024 summed left to right), so results are bit-identical
+ * whatever the tiling; only the speed differs.
+ *   OSCARS_TILING_AUTO (default): the first launch of each GEMM configuration
+ *     (layer shape, batch, number of active replicas) in the process times
+ *     every feasible tiling on the stream, which waits for that stream once,
+ *     and keeps the fastest; while the stream is being captured into a graph
+ *     a fixed rule chooses instead.
+ *   L, M, S: 128 x 128, 64 x 128, 64 x 64 output tiles;
+ *   W: 128 x 256 (bf16 models, batches above 128); WS, VS: 128 x 256 and
+ *     64 x 256 with the K chunks split over workgroups (bf16, batches above
+ *     128, more than one K chunk) -- where a forced tiling does not apply, W
+ *     or L is used.
+ * Returns OSCARS_E_INVALID for a value outside [0, OSCARS_TILING_COUNT). */
+enum {
+  OSCARS_TILING_AUTO = 0,
+  OSCARS_TILING_L = 1,
+  OSCARS_TILING_M = 2,
+  OSCARS_TILING_S = 3,
+  OSCARS_TILING_W = 4,
+  OSCARS_TILING_WS = 5,
+  OSCARS_TILING_VS = 6,
+  OSCARS_TILING_COUNT = 7
+};
+oscars_status oscars_set_gemm_tiling(int32_t tiling);
+
 const char* oscars_status_str(oscars_status s);
 /* HIP error code of the last OSCARS_E_HIP in this thread (0 if none). */
 int32_t oscars_last_hip_error(void);

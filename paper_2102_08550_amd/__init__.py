@@ -70,6 +70,7 @@ _SIGS = {
     "oscars_set_cursors": (_i32, [_vp, _P(_i64)]),
     "oscars_profile_begin": (_i32, [_vp, _u32]),
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
+    "oscars_set_gemm_tiling": (_i32, [_i32]),
     "oscars_status_str": (ctypes.c_char_p, [_i32]),
     "oscars_last_hip_error": (_i32, []),
 }
@@ -168,6 +169,19 @@ def sample_indices(n_rows: int, offsets: Sequence[int], seed: int, k: int, first
 
 
 # ---------------------------------------------------------------- GPU calls
+
+# Forward / backward-data GEMM tilings (oscars_set_gemm_tiling); results are
+# bit-identical for every tiling.
+TILING_AUTO, TILING_L, TILING_M, TILING_S, TILING_W, TILING_WS, TILING_VS = range(7)
+TILINGS = {"auto": TILING_AUTO, "L": TILING_L, "M": TILING_M, "S": TILING_S, "W": TILING_W,
+           "WS": TILING_WS, "VS": TILING_VS}
+
+
+def set_gemm_tiling(tiling: int):
+    """Process-wide tiling of the forward / backward-data GEMMs (AUTO: timed
+    once per configuration, fastest kept)."""
+    _check(_lib().oscars_set_gemm_tiling(int(tiling)), "oscars_set_gemm_tiling")
+
 
 def aggregate(global_, replicas, weights: Sequence[float], K: int, n: int, ld: int,
               broadcast: bool = False, stream=None):

@@ -9,6 +9,11 @@ namespace oscars {
 
 enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };
 
+// Forward and backward-data sum K in chunks of this many elements (each
+// chunk from zero, chunk sums left to right); a split-K launch has one
+// partial per chunk.
+constexpr int GEMM_KCHUNK = 1024;
+
 // One grouped GEMM launch over `n_slots` replicas (grid y = slot).  Slot z
 // works on replica order[z].  Every per-slot pointer is the slot-0 address;
 // the kernel adds z (or order[z] where *_by_order is set) times its stride.
@@ -58,6 +63,11 @@ struct GemmArgs {
   int64_t wcopy_slot;
   int wcopy_slots;  // WGRAD: only slots z < wcopy_slots refresh their copy (the
                     // others take their last local step: nothing reads it)
+  // FWD / DGRAD split-K partials: fp32 [slot][chunk][N][out_ld], capacity
+  // part_cap floats (nullptr or too small: no split).  part_slot is set by the
+  // launcher.
+  float* part;
+  int64_t part_cap, part_slot;
   const int32_t* order;  // [slots] replica id of each slot
   float lr;
   int relu;  // FWD: apply ReLU
@@ -65,6 +75,25 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s);
+
+// Forward / backward-data tilings (backward-weight always uses one):
+//   L 128 x 128, M 64 x 128, S 64 x 64 (register-staged operands);
+//   W 128 x 256 and, split over K chunks, WS (128 x 256) and VS (64 x 256)
+//   (bf16, batches above 128, operands streamed into LDS).
+// AUTO times the feasible tilings at the first launch of each configuration
+// and keeps the fastest; any other value forces that tiling where it applies
+// (W for an infeasible split, L where no whole-batch tiling applies).
+enum GemmTiling {
+  GEMM_TILING_AUTO = 0,
+  GEMM_TILING_L = 1,
+  GEMM_TILING_M = 2,
+  GEMM_TILING_S = 3,
+  GEMM_TILING_W = 4,
+  GEMM_TILING_WS = 5,
+  GEMM_TILING_VS = 6,
+  GEMM_TILING_COUNT = 7
+};
+void set_gemm_tiling(int tiling);
 
 // Softmax cross-entropy on logits [slot][B][ld]: delta = (softmax - onehot)/B
 // stored as bf16 or fp32 into delta [slot][B][ld] (columns C..ld-1 zeroed),

@@ -21,6 +21,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <map>
+#include <mutex>
+#include <tuple>
 #include <type_traits>
 
 #include "../../include/oscars.h"
@@ -50,19 +54,35 @@ struct Shape {
   static constexpr int ST = STAGES;
   static constexpr int MIN_WAVES = MINW;
 };
-// Forward / backward-data (K = layer width): 128 x 128 with 8 waves when
-// enough tiles fill the chip, else 64 x 128 or 64 x 64 with 4 waves (more
-// workgroups for the same outputs when few replicas are active).
+// Forward / backward-data (K = layer width):
+//   batches above 128: the whole batch in one tile, 128 x 256 with 8 waves
+//   (W) or 64 x 256 with 4 waves (V), every wave 64 x 64, so each weight is
+//   read once per launch and each LDS operand read feeds two MFMAs;
+//   smaller batches: 128 x 128 with 8 waves (L), 64 x 128 (M) or 64 x 64 (S)
+//   with 4 waves.  The largest tile that still gives every CU a workgroup is
+//   taken; below that, the K chunks are split over workgroups (split-K).
 // Backward-weight + update (K = batch): 128 x 128, 4 waves, one stage.
-enum { SHAPE_L = 0, SHAPE_M = 1, SHAPE_S = 2 };
+enum { SHAPE_L = 0, SHAPE_M = 1, SHAPE_S = 2, SHAPE_W = 3, SHAPE_V = 4 };
 template <int MODE, int SID> struct ShapeOf;
 template <int MODE> struct ShapeOf<MODE, SHAPE_L> { typedef Shape<128, 128, 2, 4, 2, 1> type; };
 template <int MODE> struct ShapeOf<MODE, SHAPE_M> { typedef Shape<64, 128, 1, 4, 2, 1> type; };
 template <int MODE> struct ShapeOf<MODE, SHAPE_S> { typedef Shape<64, 64, 2, 2, 2, 1> type; };
+// W and V are bf16-only and stream both K tiles straight into LDS (ST = LDS
+// stages, see gemm_dma_kernel).
+template <int MODE> struct ShapeOf<MODE, SHAPE_W> { typedef Shape<128, 256, 2, 4, 3, 1> type; };
+template <int MODE> struct ShapeOf<MODE, SHAPE_V> { typedef Shape<64, 256, 1, 4, 3, 1> type; };
+
+// Forward and backward-data sum K in chunks of KCHUNK elements: each chunk
+// from zero, in K order, and the chunk sums left to right,
+// ((p0 + p1) + p2) + ...  The order does not depend on the tile shape or on
+// whether the chunks of one output are summed in one workgroup (non-split)
+// or written as partials by one workgroup each and summed by the reduce
+// kernel (split-K), so a replica's result never depends on how many
+// replicas share the launch.
+constexpr int KCHUNK = GEMM_KCHUNK;
 template <> struct ShapeOf<GEMM_WGRAD, SHAPE_L> { typedef Shape<128, 128, 2, 2, 1, 2> type; };
 
 constexpr int ROW_U32 = 32;               // one LDS tile row: 128 bytes
-constexpr int TILE_U32 = 128 * ROW_U32;   // one operand tile of up to 128 rows: 16 KB
 
 __device__ __forceinline__ int lds_word(int row, int chunk) {
   return row * ROW_U32 + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 2);
@@ -268,7 +288,58 @@ __device__ __forceinline__ int xcd_tile(int L, int T) {
   return (T % 8 == 0) ? (L % 8) * (T / 8) + L / 8 : L;
 }
 
-template <bool BF16, int MODE, bool GATHER, int SID>
+// Forward / backward-data output of four consecutive rows m..m+3 (cnt of them
+// inside M) at column n of slot z: bias and ReLU (forward) or the ReLU mask of
+// the layer below (backward-data), then bf16 or fp32 store.
+template <bool BF16, int MODE>
+__device__ __forceinline__ void store_out(const GemmArgs& g, int z, int n, int m, int cnt, f32x4 v,
+                                          const float* master_in) {
+  typedef typename El<BF16>::T T;
+  if constexpr (MODE == GEMM_FWD) {
+    // out[b = n][o = m..m+3]
+    const float* bias = master_in + g.b_off + m;
+    for (int e = 0; e < 4; ++e) {
+      float o = v[e] + (e < cnt ? bias[e] : 0.0f);
+      v[e] = g.relu ? fmaxf(o, 0.0f) : o;
+    }
+  } else {
+    const int64_t am = z * g.mask_slot + static_cast<int64_t>(n) * g.mask_ld + m;
+    const T* mk = static_cast<const T*>(g.mask) + am;
+    for (int e = 0; e < 4; ++e) {
+      bool pos = false;
+      if (e < cnt) {
+        if constexpr (BF16) pos = mk[e] != 0 && (mk[e] & 0x8000u) == 0;
+        else pos = mk[e] > 0.0f;
+      }
+      v[e] = pos ? v[e] : 0.0f;
+    }
+  }
+  const int64_t at = z * g.out_slot + static_cast<int64_t>(n) * g.out_ld + m;
+  if (g.out_bf16) {
+    uint16_t* o = static_cast<uint16_t*>(g.out) + at;
+    if (cnt == 4) {
+      uint2 pk;
+      pk.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+      pk.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+      *reinterpret_cast<uint2*>(o) = pk;
+    } else {
+      for (int e = 0; e < cnt; ++e) o[e] = static_cast<uint16_t>(f2bf(v[e]));
+    }
+  } else {
+    float* o = static_cast<float*>(g.out) + at;
+    if (cnt == 4) {
+      *reinterpret_cast<f32x4*>(o) = v;
+    } else {
+      for (int e = 0; e < cnt; ++e) o[e] = v[e];
+    }
+  }
+}
+
+// SPLIT: grid x = tiles x K chunks; the workgroup of (tile, chunk c) sums
+// chunk c only and stores it as fp32 partial c of its outputs (g.part);
+// splitk_reduce_kernel then sums the partials in chunk order and applies the
+// epilogue.
+template <bool BF16, int MODE, bool GATHER, int SID, bool SPLIT>
 __global__ __launch_bounds__((ShapeOf<MODE, SID>::type::NT), (ShapeOf<MODE, SID>::type::MIN_WAVES)) void
 gemm_kernel(GemmArgs g) {
   typedef typename El<BF16>::T T;
@@ -276,6 +347,10 @@ gemm_kernel(GemmArgs g) {
   constexpr int NTHR = S::NT, WAVES_N = S::WAVES_N, MI = S::MI, NJ = S::NJ;
   constexpr int BM = S::BM, BN = S::BN;
   constexpr int BK = El<BF16>::BK;
+  constexpr bool CHUNKED = MODE != GEMM_WGRAD;  // the batch (K of WGRAD) is one chunk
+  static_assert(!SPLIT || CHUNKED, "split-K is for forward / backward-data");
+  static_assert(KCHUNK % BK == 0, "whole K tiles per chunk");
+  constexpr int TPC = KCHUNK / BK;  // K tiles per chunk
   // LDS: A tiles (BM rows) for buffers 0 and 1, then B tiles (BN rows).
   __shared__ __attribute__((aligned(16))) uint32_t lds_all[2 * (BM + BN) * ROW_U32];
   auto lds_a = [&](int buf) { return lds_all + buf * BM * ROW_U32; };
@@ -288,7 +363,14 @@ gemm_kernel(GemmArgs g) {
   const int M = g.M, N = g.N, K = g.K;
   const int gn = (N + BN - 1) / BN;
   const int t = xcd_tile(blockIdx.x, gridDim.x);
-  const int m0 = (t / gn) * BM, n0 = (t % gn) * BN;
+  // Split: t = chunk * tiles + tile, so the workgroups of one XCD share the
+  // B operand chunk (the batch's activations or deltas of that K range).
+  const int nchunks = (K + KCHUNK - 1) / KCHUNK;
+  const int tiles = SPLIT ? static_cast<int>(gridDim.x) / nchunks : static_cast<int>(gridDim.x);
+  const int chunk = SPLIT ? t / tiles : 0, tile = SPLIT ? t % tiles : t;
+  const int m0 = (tile / gn) * BM, n0 = (tile % gn) * BN;
+  const int kbeg = SPLIT ? chunk * KCHUNK : 0;
+  const int kend = SPLIT ? (K - kbeg < KCHUNK ? K : kbeg + KCHUNK) : K;
 
   const T* A = static_cast<const T*>(g.a) + (g.a_by_order ? rep : z) * g.a_slot;
   const T* B = static_cast<const T*>(g.b) + z * g.b_slot;
@@ -344,6 +426,9 @@ gemm_kernel(GemmArgs g) {
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  // Non-split forward / backward-data: sum of the finished chunks.
+  constexpr bool TOTAL = CHUNKED && !SPLIT;
+  f32x16 tot[TOTAL ? MI : 1][TOTAL ? NJ : 1];
 
   const bool bias_wg = (MODE == GEMM_WGRAD) && m0 == 0;
   float dbias = 0.0f;
@@ -360,7 +445,7 @@ gemm_kernel(GemmArgs g) {
     if constexpr (MODE == GEMM_WGRAD) t.load(B, g.b_ld, n0, g.b_ext, k0, K, tid); \
     else {                                                                \
       t.load(sb, B, k0, g.b_ext, tid);                                    \
-      if (GATHER && ((k0) / BK) % gm == mt)                               \
+      if (GATHER && (k0) < kend && ((k0) / BK) % gm == mt)                \
         t.copy_out(rows_out, g.rows_out_ld, n0, N, k0, g.b_ext, tid);     \
     }                                                                     \
   } while (0)
@@ -385,21 +470,39 @@ gemm_kernel(GemmArgs g) {
     }
   };
 
+  // After K tile j (counted from kbeg): close the chunk it ends.
+  auto fold = [&](int j, int nk) {
+    if constexpr (TOTAL) {
+      if ((j + 1) % TPC == 0 || j + 1 == nk) {
+        const bool first = j < TPC;
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int jj = 0; jj < NJ; ++jj) {
+            tot[i][jj] = first ? acc[i][jj] : tot[i][jj] + acc[i][jj];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][jj][r] = 0.0f;
+          }
+      }
+    }
+  };
+
   // Loads past the end of K read zeros, so the loop bodies are straight-line.
-  const int nk = (K + BK - 1) / BK;
+  const int nk = (kend - kbeg + BK - 1) / BK;
   if constexpr (S::ST == 1) {
     // One register stage, LDS double buffer (always for the short K of the
     // backward-weight pass, the batch).
-    LOAD_A(ta, 0);
-    LOAD_B(tb, 0);
+    LOAD_A(ta, kbeg);
+    LOAD_B(tb, kbeg);
     ta.store(lds_a(0), tid);
     tb.store(lds_b(0), tid);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       const int buf = kt & 1;
-      LOAD_A(ta, (kt + 1) * BK);
-      LOAD_B(tb, (kt + 1) * BK);
+      LOAD_A(ta, kbeg + (kt + 1) * BK);
+      LOAD_B(tb, kbeg + (kt + 1) * BK);
       compute(buf);
+      fold(kt, nk);
       ta.store(lds_a(buf ^ 1), tid);
       tb.store(lds_b(buf ^ 1), tid);
       __syncthreads();
@@ -413,8 +516,8 @@ gemm_kernel(GemmArgs g) {
     decltype(tb) tB[ST];
 #pragma unroll
     for (int u = 0; u < ST; ++u) {
-      LOAD_A(tA[u], u * BK);
-      LOAD_B(tB[u], u * BK);
+      LOAD_A(tA[u], kbeg + u * BK);
+      LOAD_B(tB[u], kbeg + u * BK);
     }
     tA[0].store(lds_a(0), tid);
     tB[0].store(lds_b(0), tid);
@@ -424,9 +527,10 @@ gemm_kernel(GemmArgs g) {
       for (int u = 0; u < ST; ++u) {
         const int j = kt + u;
         if (j >= nk) break;
-        LOAD_A(tA[u], (j + ST) * BK);
-        LOAD_B(tB[u], (j + ST) * BK);
+        LOAD_A(tA[u], kbeg + (j + ST) * BK);
+        LOAD_B(tB[u], kbeg + (j + ST) * BK);
         compute(j & 1);
+        fold(j, nk);
         tA[(u + 1) % ST].store(lds_a((j + 1) & 1), tid);
         tB[(u + 1) % ST].store(lds_b((j + 1) & 1), tid);
         __syncthreads();
@@ -478,65 +582,294 @@ gemm_kernel(GemmArgs g) {
     if (bias_wg && tid < BN && n0 + tid < N)
       master[g.b_off + n0 + tid] = fmaf(-g.lr, dbias, master_in[g.b_off + n0 + tid]);
     return;
+  } else if constexpr (SPLIT) {
+    // Partial `chunk` of outputs (m, n): fp32 at part[slot][chunk][n][m]
+    // (row stride out_ld; columns up to round_up(M, 4) stay inside it).
+    float* part = g.part + z * g.part_slot + static_cast<int64_t>(chunk) * N * g.out_ld;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int n = ncol(j);
+        if (n >= N) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = mrow(i, q);
+          if (m >= M) continue;
+          *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(n) * g.out_ld + m) =
+              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                    acc[i][j][4 * q + 3]};
+        }
+      }
+    return;
+  } else {
+    // Epilogue, one group of four consecutive rows m..m+3 at column n at a time.
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int n = ncol(j);
+        if (n >= N) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = mrow(i, q);
+          if (m >= M) continue;
+          const int cnt = (M - m >= 4) ? 4 : M - m;
+          store_out<BF16, MODE>(g, z, n, m, cnt,
+                                f32x4{tot[i][j][4 * q], tot[i][j][4 * q + 1], tot[i][j][4 * q + 2],
+                                      tot[i][j][4 * q + 3]},
+                                master_in);
+        }
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward / backward-data of bf16 models with whole-batch tiles (W, V): K
+// tiles go from global memory straight into LDS (global_load_lds, 16 bytes
+// per lane), ST stages deep, so no VGPRs hold tiles in flight and ST - 1
+// stages load while one is multiplied.  One wave instruction fills 8 LDS rows
+// (1 KB, lane l at byte 16 l); the swizzle is applied on the source side:
+// the lane at physical chunk p of tile row r reads logical chunk
+// p ^ ((r ^ r >> 3) & 7).  Backward-data's weight operand is stored
+// M-contiguous and is transposed through registers as in gemm_kernel, one
+// stage ahead.  The summation order is that of gemm_kernel.
+
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void dma16(const void* src, uint32_t* lds_row) {
+  __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)lds_row, 16, 0, 0);
+}
+
+// Wait until at most N vector memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// LDS writes of this wave done, then the workgroup barrier.  The barrier is
+// opaque to the compiler (no memory operation moves across it) and, unlike
+// __syncthreads, does not wait for the loads still streaming into LDS.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));  // lgkmcnt(0)
+  asm volatile("s_barrier" ::: "memory");
+}
+
+template <int NTHR, int ROWS>
+struct DmaTile {
+  static constexpr int P = ROWS * 8 / NTHR;
+  static_assert(ROWS * 8 % NTHR == 0 && NTHR % 64 == 0, "whole wave instructions");
+  const uint16_t* src[P];
+  bool ok[P];
+  int kc[P];
+  __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* gather,
+                                       int row0, int R, int tid) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int idx = tid + NTHR * p, r = idx >> 3;
+      const int lc = (idx & 7) ^ ((r ^ (r >> 3)) & 7);
+      const int gr = row0 + r;
+      ok[p] = gr < R;
+      const int grc = gr < R ? gr : R - 1;
+      const int64_t row = gather ? gather[grc] : grc;
+      kc[p] = 8 * lc;
+      src[p] = base + row * ld + 8 * lc;
+    }
+  }
+  // P wave instructions; wave w's instruction p fills tile rows
+  // (64 w + NTHR p) / 8 .. + 7.
+  __device__ __forceinline__ void issue(uint32_t* tile, int k0, int ext, int tid) const {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const bool in = ok[p] && k0 + kc[p] < ext;
+      dma16(in ? static_cast<const void*>(src[p] + k0) : static_cast<const void*>(k_zero16),
+            tile + (((tid & ~63) + NTHR * p) >> 3) * ROW_U32);
+    }
+  }
+};
+
+template <int MODE, bool GATHER, int SID, bool SPLIT>
+__global__ __launch_bounds__((ShapeOf<MODE, SID>::type::NT), (ShapeOf<MODE, SID>::type::MIN_WAVES)) void
+gemm_dma_kernel(GemmArgs g) {
+  typedef uint16_t T;
+  typedef typename ShapeOf<MODE, SID>::type S;
+  static_assert(MODE == GEMM_FWD || MODE == GEMM_DGRAD, "forward / backward-data only");
+  constexpr int NTHR = S::NT, WAVES_N = S::WAVES_N, MI = S::MI, NJ = S::NJ;
+  constexpr int BM = S::BM, BN = S::BN, NS = S::ST;
+  constexpr int BK = El<true>::BK;
+  constexpr int TPC = KCHUNK / BK;
+  static_assert(NS >= 2, "at least one stage loading while one is used");
+  __shared__ __attribute__((aligned(16))) uint32_t lds_all[NS * (BM + BN) * ROW_U32];
+  auto lds_a = [&](int buf) { return lds_all + buf * BM * ROW_U32; };
+  auto lds_b = [&](int buf) { return lds_all + NS * BM * ROW_U32 + buf * BN * ROW_U32; };
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N, h = lane >> 5;
+  const int z = blockIdx.y;
+  const int rep = g.order[z];
+  const int M = g.M, N = g.N, K = g.K;
+  const int gn = (N + BN - 1) / BN;
+  const int t = xcd_tile(blockIdx.x, gridDim.x);
+  const int nchunks = (K + KCHUNK - 1) / KCHUNK;
+  const int tiles = SPLIT ? static_cast<int>(gridDim.x) / nchunks : static_cast<int>(gridDim.x);
+  const int chunk = SPLIT ? t / tiles : 0, tile = SPLIT ? t % tiles : t;
+  const int m0 = (tile / gn) * BM, n0 = (tile % gn) * BN;
+  const int kbeg = SPLIT ? chunk * KCHUNK : 0;
+  const int kend = SPLIT ? (K - kbeg < KCHUNK ? K : kbeg + KCHUNK) : K;
+  const int nk = (kend - kbeg + BK - 1) / BK;
+
+  const T* A = static_cast<const T*>(g.a) + (g.a_by_order ? rep : z) * g.a_slot;
+  const T* B = static_cast<const T*>(g.b) + z * g.b_slot;
+  const float* master_in = g.master_in + static_cast<int64_t>(rep) * g.master_in_slot;
+  T* rows_out = GATHER ? static_cast<T*>(g.rows_out) + z * g.rows_out_slot : nullptr;
+  const int gm = (M + BM - 1) / BM, mt = m0 / BM;
+
+  DmaTile<NTHR, BN> db;
+  db.init(B, g.b_ld, GATHER ? g.gather + z * g.gather_slot : nullptr, n0, N, tid);
+  DmaTile<NTHR, BM> da;             // FWD: weights, K-contiguous
+  TransTile<true, NTHR, BM> ta;     // DGRAD: weights, M-contiguous, via registers
+  if constexpr (MODE == GEMM_FWD) da.init(A, g.a_ld, nullptr, m0, M, tid);
+
+  f32x16 acc[MI][NJ], tot[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  auto k_of = [&](int s) { return kbeg + s * BK; };
+  // FWD issues stage s as A then B (PA + PB instructions per thread);
+  // DGRAD loads A(s) into registers and issues B(s) (2 + PB).
+  constexpr int PA = MODE == GEMM_FWD ? DmaTile<NTHR, BM>::P : 2 * TransTile<true, NTHR, BM>::P;
+  constexpr int PB = DmaTile<NTHR, BN>::P;
+  auto issue_b = [&](int s) { db.issue(lds_b(s % NS), k_of(s), g.b_ext, tid); };
+
+  if constexpr (MODE == GEMM_FWD) {
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) {
+      da.issue(lds_a(s), k_of(s), g.a_ext, tid);
+      issue_b(s);
+    }
+  } else {
+    // A(0) .. A(NS - 2) into LDS, B(0) .. B(NS - 2) streaming, and A(NS - 1)
+    // loading into registers before B(NS - 2) is issued.
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) {
+      ta.load(A, g.a_ld, m0, g.a_ext, k_of(s), K, tid);
+      wait_vm<0>();
+      ta.store(lds_a(s), tid);
+    }
+#pragma unroll
+    for (int s = 0; s < NS - 2; ++s) issue_b(s);
+    ta.load(A, g.a_ld, m0, g.a_ext, k_of(NS - 1), K, tid);
+    issue_b(NS - 2);
   }
 
-  // Epilogue, one group of four consecutive rows m..m+3 at column n at a time.
+  for (int j = 0; j < nk; ++j) {
+    // Stage j landed.  FWD: stages j + 1 .. j + NS - 2 stay in flight.
+    // DGRAD: A(j + NS - 1) in registers too (issued just before B(j + NS - 2),
+    // the only operation allowed in flight; with two stages B(j) is the
+    // newest, so everything is waited for).
+    if constexpr (MODE == GEMM_FWD) wait_vm<(NS - 2) * (PA + PB)>();
+    else wait_vm<(NS >= 3 ? PB : 0)>();
+    lds_barrier();
+    const int k0 = k_of(j);
+    if (GATHER && k0 < kend && (k0 / BK) % gm == mt) {
+      // Layer 1: this workgroup keeps K tile j of the gathered batch rows.
+      constexpr int PC = BN * 8 / NTHR;
 #pragma unroll
-  for (int i = 0; i < MI; ++i) {
+      for (int p = 0; p < PC; ++p) {
+        const int idx = tid + NTHR * p, row = idx >> 3, c = idx & 7, k = k0 + 8 * c;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(lds_b(j % NS) + lds_word(row, c));
+        if (n0 + row < N && k < g.b_ext)
+          *reinterpret_cast<u32x4*>(rows_out + static_cast<int64_t>(n0 + row) * g.rows_out_ld + k) = v;
+      }
+      wait_vm<0>();
+    }
+    if constexpr (MODE == GEMM_DGRAD) {
+      // A(j + NS - 1) from registers into its LDS buffer (last read by the
+      // product of tile j - 1, before the barrier), then load A(j + NS).
+      ta.store(lds_a((j + NS - 1) % NS), tid);
+      ta.load(A, g.a_ld, m0, g.a_ext, k_of(j + NS), K, tid);
+    } else {
+      da.issue(lds_a((j + NS - 1) % NS), k_of(j + NS - 1), g.a_ext, tid);
+    }
+    issue_b(j + NS - 1);
+    mma_tile<true, MI, NJ>(lds_a(j % NS), lds_b(j % NS), wm, wn, lane, acc);
+    if constexpr (!SPLIT) {
+      if ((j + 1) % TPC == 0 || j + 1 == nk) {
+        const bool first = j < TPC;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int n = ncol(j);
-      if (n >= N) continue;
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int m = mrow(i, q);
-        if (m >= M) continue;
-        const int cnt = (M - m >= 4) ? 4 : M - m;
-        f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                   acc[i][j][4 * q + 3]};
-        if constexpr (MODE == GEMM_FWD) {
-          // out[b = n][o = m..m+3]
-          const float* bias = master_in + g.b_off + m;
-          for (int e = 0; e < 4; ++e) {
-            float o = v[e] + (e < cnt ? bias[e] : 0.0f);
-            v[e] = g.relu ? fmaxf(o, 0.0f) : o;
+          for (int jj = 0; jj < NJ; ++jj) {
+            tot[i][jj] = first ? acc[i][jj] : tot[i][jj] + acc[i][jj];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][jj][e] = 0.0f;
           }
-        } else if constexpr (MODE == GEMM_DGRAD) {
-          const int64_t am = z * g.mask_slot + static_cast<int64_t>(n) * g.mask_ld + m;
-          const T* mk = static_cast<const T*>(g.mask) + am;
-          for (int e = 0; e < 4; ++e) {
-            bool pos = false;
-            if (e < cnt) {
-              if constexpr (BF16) pos = mk[e] != 0 && (mk[e] & 0x8000u) == 0;
-              else pos = mk[e] > 0.0f;
-            }
-            v[e] = pos ? v[e] : 0.0f;
-          }
-        }
-        {
-          const int64_t at = z * g.out_slot + static_cast<int64_t>(n) * g.out_ld + m;
-          if (g.out_bf16) {
-            uint16_t* o = static_cast<uint16_t*>(g.out) + at;
-            if (cnt == 4) {
-              uint2 pk;
-              pk.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
-              pk.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
-              *reinterpret_cast<uint2*>(o) = pk;
-            } else {
-              for (int e = 0; e < cnt; ++e) o[e] = static_cast<uint16_t>(f2bf(v[e]));
-            }
-          } else {
-            float* o = static_cast<float*>(g.out) + at;
-            if (cnt == 4) {
-              *reinterpret_cast<f32x4*>(o) = v;
-            } else {
-              for (int e = 0; e < cnt; ++e) o[e] = v[e];
-            }
-          }
-        }
       }
     }
   }
+  wait_vm<0>();  // nothing streams into LDS past the end of the workgroup
+
+  auto mrow = [&](int i, int q) { return m0 + wm * 32 * MI + 32 * i + 8 * q + 4 * h; };
+  auto ncol = [&](int j) { return n0 + wn * 32 * NJ + 32 * j + (lane & 31); };
+  if constexpr (SPLIT) {
+    float* part = g.part + z * g.part_slot + static_cast<int64_t>(chunk) * N * g.out_ld;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int n = ncol(j);
+        if (n >= N) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = mrow(i, q);
+          if (m >= M) continue;
+          *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(n) * g.out_ld + m) =
+              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                    acc[i][j][4 * q + 3]};
+        }
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int n = ncol(j);
+        if (n >= N) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = mrow(i, q);
+          if (m >= M) continue;
+          const int cnt = (M - m >= 4) ? 4 : M - m;
+          store_out<true, MODE>(g, z, n, m, cnt,
+                                f32x4{tot[i][j][4 * q], tot[i][j][4 * q + 1], tot[i][j][4 * q + 2],
+                                      tot[i][j][4 * q + 3]},
+                                master_in);
+        }
+      }
+  }
+}
+
+// Sum of the split-K partials of slot z in chunk order, then the epilogue.
+// One thread per four consecutive rows m..m+3 of column n.
+template <bool BF16, int MODE>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, int nchunks) {
+  const int z = blockIdx.y;
+  const int mq = (g.M + 3) / 4;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= static_cast<int64_t>(g.N) * mq) return;
+  const int n = static_cast<int>(idx / mq), m = static_cast<int>(idx % mq) * 4;
+  const int cnt = (g.M - m >= 4) ? 4 : g.M - m;
+  const float* p = g.part + z * g.part_slot + static_cast<int64_t>(n) * g.out_ld + m;
+  const int64_t cs = static_cast<int64_t>(g.N) * g.out_ld;
+  f32x4 v = *reinterpret_cast<const f32x4*>(p);
+  for (int c = 1; c < nchunks; ++c) v = v + *reinterpret_cast<const f32x4*>(p + c * cs);
+  const float* master_in = g.master_in + static_cast<int64_t>(g.order[z]) * g.master_in_slot;
+  store_out<BF16, MODE>(g, z, n, m, cnt, v, master_in);
 }
 
 template <bool BF16_OUT>
@@ -696,19 +1029,41 @@ hipError_t agg_launch(float* g, float* reps, const AggWeights& w, int K, int64_t
   return hipGetLastError();
 }
 
-template <bool BF16, int MODE, int SID>
+template <bool BF16, int MODE, int SID, bool SPLIT>
 hipError_t gemm_launch_shape(const GemmArgs& g, int n_slots, hipStream_t s) {
   typedef typename ShapeOf<MODE, SID>::type S;
-  const dim3 grid(((g.N + S::BN - 1) / S::BN) * ((g.M + S::BM - 1) / S::BM), n_slots);
+  const int nchunks = SPLIT ? (g.K + KCHUNK - 1) / KCHUNK : 1;
+  const int64_t gx =
+      static_cast<int64_t>((g.N + S::BN - 1) / S::BN) * ((g.M + S::BM - 1) / S::BM) * nchunks;
+  if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(gx), n_slots);
+  constexpr bool DMA = SID == SHAPE_W || SID == SHAPE_V;
+  static_assert(!DMA || (BF16 && MODE != GEMM_WGRAD), "whole-batch tiles: bf16 forward / backward-data");
   if (g.gather) {
-    if constexpr (MODE == GEMM_FWD)
-      hipLaunchKernelGGL((gemm_kernel<BF16, MODE, true, SID>), grid, dim3(S::NT), 0, s, g);
-    else
+    if constexpr (MODE == GEMM_FWD) {
+      if constexpr (DMA)
+        hipLaunchKernelGGL((gemm_dma_kernel<MODE, true, SID, SPLIT>), grid, dim3(S::NT), 0, s, g);
+      else
+        hipLaunchKernelGGL((gemm_kernel<BF16, MODE, true, SID, SPLIT>), grid, dim3(S::NT), 0, s, g);
+    } else {
       return hipErrorInvalidValue;  // only the forward pass gathers dataset rows
+    }
   } else {
-    hipLaunchKernelGGL((gemm_kernel<BF16, MODE, false, SID>), grid, dim3(S::NT), 0, s, g);
+    if constexpr (DMA)
+      hipLaunchKernelGGL((gemm_dma_kernel<MODE, false, SID, SPLIT>), grid, dim3(S::NT), 0, s, g);
+    else
+      hipLaunchKernelGGL((gemm_kernel<BF16, MODE, false, SID, SPLIT>), grid, dim3(S::NT), 0, s, g);
   }
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !SPLIT) return e;
+  if constexpr (SPLIT) {
+    const int64_t work = static_cast<int64_t>(g.N) * ((g.M + 3) / 4);
+    hipLaunchKernelGGL((splitk_reduce_kernel<BF16, MODE>),
+                       dim3(static_cast<unsigned>((work + 255) / 256), n_slots), dim3(256), 0, s, g,
+                       nchunks);
+    e = hipGetLastError();
+  }
+  return e;
 }
 
 int device_cu_count() {
@@ -724,23 +1079,128 @@ int device_cu_count() {
   return cus;
 }
 
+// Forward / backward-data tilings.  Every tiling sums in the same order, so
+// the choice changes only the speed: the first launch of each configuration
+// times the feasible tilings and keeps the fastest (see select_tiling).
+bool split_fits(const GemmArgs& g, int n_slots) {
+  const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
+  const int64_t slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
+  return nchunks > 1 && g.part && slot * n_slots <= g.part_cap;
+}
+
+bool tiling_fits(int t, bool bf16, const GemmArgs& g, int n_slots) {
+  switch (t) {
+    case GEMM_TILING_L: case GEMM_TILING_M: case GEMM_TILING_S: return true;
+    case GEMM_TILING_W: return bf16 && g.N > 128;
+    case GEMM_TILING_WS: case GEMM_TILING_VS: return bf16 && g.N > 128 && split_fits(g, n_slots);
+  }
+  return false;
+}
+
+template <bool BF16, int MODE>
+hipError_t launch_tiling(const GemmArgs& g_in, int n_slots, hipStream_t s, int t) {
+  if constexpr (BF16) {
+    if (t == GEMM_TILING_W) return gemm_launch_shape<true, MODE, SHAPE_W, false>(g_in, n_slots, s);
+    if (t == GEMM_TILING_WS || t == GEMM_TILING_VS) {
+      GemmArgs g = g_in;
+      g.part_slot = static_cast<int64_t>((g.K + KCHUNK - 1) / KCHUNK) * g.N * g.out_ld;
+      if (t == GEMM_TILING_WS) return gemm_launch_shape<true, MODE, SHAPE_W, true>(g, n_slots, s);
+      return gemm_launch_shape<true, MODE, SHAPE_V, true>(g, n_slots, s);
+    }
+  }
+  if (t == GEMM_TILING_M) return gemm_launch_shape<BF16, MODE, SHAPE_M, false>(g_in, n_slots, s);
+  if (t == GEMM_TILING_S) return gemm_launch_shape<BF16, MODE, SHAPE_S, false>(g_in, n_slots, s);
+  return gemm_launch_shape<BF16, MODE, SHAPE_L, false>(g_in, n_slots, s);
+}
+
+// Without timings (stream being captured into a graph): the largest tile
+// that still gives every CU a workgroup, split-K when even the smallest
+// whole-batch tiles leave CUs idle.
+int static_tiling(bool bf16, const GemmArgs& g, int n_slots) {
+  const int64_t cus = device_cu_count();
+  auto tiles = [&](int bm, int bn) {
+    return static_cast<int64_t>((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * n_slots;
+  };
+  if (bf16 && g.N > 128) {
+    if (tiles(128, 256) >= 3 * cus / 4) return GEMM_TILING_W;
+    if (tiles(128, 128) >= cus / 2 || !split_fits(g, n_slots)) return GEMM_TILING_L;
+    return tiles(64, 256) >= cus / 2 ? GEMM_TILING_WS : GEMM_TILING_VS;
+  }
+  if (tiles(128, 128) >= cus) return GEMM_TILING_L;
+  if (tiles(64, 128) >= cus) return GEMM_TILING_M;
+  return GEMM_TILING_S;
+}
+
+std::atomic<int> g_forced_tiling{GEMM_TILING_AUTO};
+
+struct TuneKey {
+  int dev, bf16, mode, M, N, K, slots, gather, split;
+  bool operator<(const TuneKey& o) const {
+    return std::tie(dev, bf16, mode, M, N, K, slots, gather, split) <
+           std::tie(o.dev, o.bf16, o.mode, o.M, o.N, o.K, o.slots, o.gather, o.split);
+  }
+};
+
 template <bool BF16, int MODE>
 hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
   if constexpr (MODE == GEMM_WGRAD) {
-    return gemm_launch_shape<BF16, MODE, SHAPE_L>(g, n_slots, s);
+    return gemm_launch_shape<BF16, MODE, SHAPE_L, false>(g, n_slots, s);
   } else {
-    // Largest tile that still gives every CU a workgroup.
-    const int64_t cus = device_cu_count();
-    auto tiles = [&](int bm, int bn) {
-      return static_cast<int64_t>((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * n_slots;
-    };
-    if (tiles(128, 128) >= cus) return gemm_launch_shape<BF16, MODE, SHAPE_L>(g, n_slots, s);
-    if (tiles(64, 128) >= cus) return gemm_launch_shape<BF16, MODE, SHAPE_M>(g, n_slots, s);
-    return gemm_launch_shape<BF16, MODE, SHAPE_S>(g, n_slots, s);
+    const int forced = g_forced_tiling.load();
+    if (forced != GEMM_TILING_AUTO) {
+      int t = forced;
+      if (!tiling_fits(t, BF16, g, n_slots)) t = (t == GEMM_TILING_W || !BF16 || g.N <= 128)
+                                                      ? GEMM_TILING_L : GEMM_TILING_W;
+      return launch_tiling<BF16, MODE>(g, n_slots, s, t);
+    }
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone)
+      return launch_tiling<BF16, MODE>(g, n_slots, s, static_tiling(BF16, g, n_slots));
+
+    static std::mutex mu;
+    static std::map<TuneKey, int> best;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    const TuneKey key{dev, BF16, MODE, g.M, g.N, g.K, n_slots, g.gather != nullptr,
+                      split_fits(g, n_slots)};
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = best.find(key);
+    if (it != best.end()) return launch_tiling<BF16, MODE>(g, n_slots, s, it->second);
+
+    // First launch of this configuration: every feasible tiling computes the
+    // (identical) result twice, timed; the fastest second run is kept.
+    static hipEvent_t ev[2] = {nullptr, nullptr};
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < 2 && e == hipSuccess; ++i)
+      if (!ev[i]) e = hipEventCreate(&ev[i]);
+    int choice = static_tiling(BF16, g, n_slots);
+    float best_ms = 0.0f;
+    bool have = false;
+    for (int t = GEMM_TILING_L; t < GEMM_TILING_COUNT && e == hipSuccess; ++t) {
+      if (!tiling_fits(t, BF16, g, n_slots)) continue;
+      float ms = 0.0f;
+      for (int rep = 0; rep < 2 && e == hipSuccess; ++rep) {
+        e = hipEventRecord(ev[0], s);
+        if (e == hipSuccess) e = launch_tiling<BF16, MODE>(g, n_slots, s, t);
+        if (e == hipSuccess) e = hipEventRecord(ev[1], s);
+        if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev[0], ev[1]);
+      }
+      if (e == hipSuccess && (!have || ms < best_ms)) {
+        best_ms = ms;
+        choice = t;
+        have = true;
+      }
+    }
+    if (e != hipSuccess) return e;
+    best[key] = choice;
+    return hipSuccess;  // the result is in place (every timed run computed it)
   }
 }
 
 }  // namespace
+
+void set_gemm_tiling(int tiling) { g_forced_tiling.store(tiling); }
 
 hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s) {
   if (bf16) {

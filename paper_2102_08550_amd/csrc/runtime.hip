@@ -55,6 +55,8 @@ struct oscars_ctx {
   uint16_t* gq = nullptr;          // [n_pad] bf16 copy of a round's start model (bf16 models)
   std::vector<void*> act;          // act[l], l = 0..L-1: [K][max_batch][ld[l]] (act[0]: batch rows)
   float* logits = nullptr;         // [K][max_batch][ld[L]]
+  float* part = nullptr;           // split-K partials of forward / backward-data GEMMs
+  int64_t part_cap = 0;            // floats
   std::vector<void*> delta;        // delta[l], l = 1..L: [K][max_batch][ld[l]]
   int32_t* table_dev = nullptr;    // order [64] then index table [slots][tau_max][B]
   int64_t table_cap = 0;           // int32 elements
@@ -186,6 +188,25 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
     void* p = nullptr;
     e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(c->L) * 4, &p);
     c->logits = static_cast<float*>(p);
+  }
+  // Split-K partials ([slot][chunk][batch][ld] fp32) for launches with up to
+  // kSplitSlots active replicas; the kernels split only whole-batch tiles
+  // (batches above 128) whose K has more than one chunk.
+  if (e == hipSuccess && max_batch > 128) {
+    constexpr int64_t kChunk = GEMM_KCHUNK, kSplitSlots = 4;
+    int64_t need = 0;
+    for (int l = 1; l <= c->L; ++l) {
+      const int64_t fwd = (c->dims[l - 1] + kChunk - 1) / kChunk;
+      if (fwd > 1) need = std::max(need, fwd * max_batch * c->ld[l]);
+      const int64_t bwd = (c->dims[l] + kChunk - 1) / kChunk;
+      if (l > 1 && bwd > 1) need = std::max(need, bwd * max_batch * c->ld[l - 1]);
+    }
+    if (need > 0) {
+      c->part_cap = need * std::min<int64_t>(K, kSplitSlots);
+      void* p = nullptr;
+      e = dev_alloc(c, static_cast<size_t>(c->part_cap) * 4, &p);
+      c->part = static_cast<float*>(p);
+    }
   }
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
@@ -382,6 +403,8 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
       g.b_off = c->b_off[l];
       g.order = d_order;
       g.lr = lr;
+      g.part = c->part;
+      g.part_cap = c->part_cap;
     };
 
     // forward: C[o][b] = W_l . act_{l-1}
@@ -545,6 +568,14 @@ oscars_status oscars_aggregate(float* global, float* replicas, const float* weig
   hipError_t e = launch_aggregate(global, replicas, weights, K, n, ld, broadcast,
                                   static_cast<hipStream_t>(hip_stream));
   return e == hipSuccess ? OSCARS_OK : hip_fail(e);
+}
+
+oscars_status oscars_set_gemm_tiling(int32_t tiling) {
+  static_assert(OSCARS_TILING_COUNT == GEMM_TILING_COUNT && OSCARS_TILING_VS == GEMM_TILING_VS,
+                "tiling codes of the C ABI and of the launchers agree");
+  if (tiling < 0 || tiling >= OSCARS_TILING_COUNT) return OSCARS_E_INVALID;
+  set_gemm_tiling(tiling);
+  return OSCARS_OK;
 }
 
 oscars_status oscars_profile_begin(oscars_ctx* c, uint32_t kind_mask) {

@@ -37,6 +37,15 @@ TRAJ = {
                                  seed=10),
     "k1-sgd": workload.Config("k1-sgd", (40, 136, 10), workload.FP32, K=1, n_rows=300, batch=33,
                               tau_rule="given", tau_given=(1,), lr=0.1, rounds=12, seed=11),
+    # Batches above 128 take the whole-batch tiles; K of 2056 and 1040 is
+    # three and two K chunks (the last one ragged), split over workgroups at
+    # these replica counts.
+    "wide-bf16": workload.Config("wide-bf16", (2056, 1032, 264, 100), workload.BF16, K=4,
+                                 n_rows=3000, batch=256, tau_rule="given", tau_given=(3, 1, 2, 4),
+                                 lr=0.05, rounds=2, seed=13),
+    "wide-fp32": workload.Config("wide-fp32", (1040, 2056, 136, 10), workload.FP32, K=3,
+                                 n_rows=1500, batch=160, tau_rule="given", tau_given=(2, 3, 1),
+                                 lr=0.05, rounds=2, seed=14),
 }
 
 
@@ -88,10 +97,15 @@ MASK_CFGS = [
                     tau_rule="given", tau_given=(3, 1, 0, 4, 2)),
     workload.scaled(workload.C2, dims=(64, 72, 10), n_rows=900, rounds=1, batch=17, K=4,
                     tau_rule="given", tau_given=(2, 5, 1, 3)),
+    # 4096-wide layers at batch 256: 8, 4, 2 and 1 active replicas take the
+    # 128 x 256 tile, the 64 x 256 tile, and split-K over either, while every
+    # solo run takes the 1-replica launches; all must agree bit for bit.
+    workload.scaled(workload.C5, dims=(4096, 4096, 1000), n_rows=4000, rounds=1, batch=256, K=8,
+                    tau_rule="given", tau_given=(2, 1, 3, 1, 2, 1, 1, 4)),
 ]
 
 
-@pytest.mark.parametrize("cfg", MASK_CFGS, ids=["bf16", "fp32"])
+@pytest.mark.parametrize("cfg", MASK_CFGS, ids=["bf16", "fp32", "bf16-wide"])
 def test_masking_independence_and_determinism(P, cfg):
     """A replica's result does not depend on which other replicas run beside
     it (grouped == solo, bit for bit); tau_k = 0 leaves a replica untouched;
@@ -117,6 +131,37 @@ def test_masking_independence_and_determinism(P, cfg):
     for k in range(cfg.K):
         if cfg.tau_given[k] == 0:
             assert np.array_equal(grouped[k], flat)
+
+
+TILING_CFGS = [
+    MASK_CFGS[2],
+    workload.Config("tiling-fp32", (1040, 2056, 136, 10), workload.FP32, K=3, n_rows=1500,
+                    batch=160, tau_rule="given", tau_given=(2, 3, 1), lr=0.05, rounds=1,
+                    seed=15),
+]
+
+
+@pytest.mark.parametrize("cfg", TILING_CFGS, ids=["bf16-wide", "fp32-wide"])
+def test_every_tiling_gives_identical_results(P, cfg):
+    """Every forward / backward-data tiling, split-K included, sums in the
+    same order: the replicas after the local steps agree bit for bit with the
+    automatically chosen tilings."""
+    say(f"tilings {cfg.dtype} dims={cfg.dims} tau={cfg.tau_given}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = np.array([cfg.tau_given])
+    results = {}
+    try:
+        for name, t in P.TILINGS.items():
+            P.set_gemm_tiling(t)
+            results[name], _ = _run_once(P, cfg, ds, init, tau)
+            say(f"  tiling {name} done")
+    finally:
+        P.set_gemm_tiling(P.TILING_AUTO)
+    for name, reps in results.items():
+        assert np.array_equal(reps.view(np.uint32), results["auto"].view(np.uint32)), name
+    with pytest.raises(P.OscarsError):
+        P.set_gemm_tiling(len(P.TILINGS))
 
 
 @pytest.mark.parametrize("dtype", [workload.BF16, workload.FP32])
