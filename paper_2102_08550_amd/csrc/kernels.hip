@@ -80,6 +80,12 @@ template <int MODE> struct ShapeOf<MODE, SHAPE_V> { typedef Shape<64, 256, 1, 4,
 // kernel (split-K), so a replica's result never depends on how many
 // replicas share the launch.
 constexpr int KCHUNK = GEMM_KCHUNK;
+#ifndef WGRAD_MIN_WAVES
+#define WGRAD_MIN_WAVES 3
+#endif
+#ifndef WGRAD_PRE
+#define WGRAD_PRE 8
+#endif
 template <> struct ShapeOf<GEMM_WGRAD, SHAPE_L> { typedef Shape<128, 128, 2, 2, 1, 2> type; };
 
 constexpr int ROW_U32 = 32;               // one LDS tile row: 128 bytes
@@ -854,6 +860,234 @@ gemm_dma_kernel(GemmArgs g) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Backward-weight + SGD update of bf16 models.  Both operands are stored
+// with the batch (K) slowest, act[b][i] and delta[b][o]; their K tiles go
+// into LDS unchanged (global_load_lds, 16 bytes per lane, 4 rows of 256
+// bytes per wave instruction) and are transposed on the way out by
+// ds_read_b64_tr_b16.  Within each 16-lane group that read returns to lane
+// 4a + b element e the element b of the 4 that lane a + 4e addressed; when
+// lane a + 4e addresses row k0 + e, columns c0 + 4a .. + 3, lane j receives
+// rows k0 .. k0 + 3 of column c0 + j, i.e. four consecutive K of one MFMA
+// row.  Two such reads give the 8 K of a 32x32x16 operand lane, in the
+// order of gemm_kernel, so the sums are the same.  Tile rows are 256 bytes;
+// the 16-byte chunk c of row k sits at c ^ 4 (k & 3), which spreads the
+// transposing reads of 4 consecutive rows over all chunk positions.
+// Tile 128 (in) x 128 (out), 4 waves of 64 x 64, K tiles of 32 rows,
+// 3 stages (48 KB of LDS); the update epilogue stages dW through LDS in two
+// halves of 64 output rows (32 KB), so that three workgroups fit a CU.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ int trow_chunk(int k, int c) { return c ^ ((k & 3) << 2); }
+
+template <int ROWS_PER_STAGE, int COLS>
+struct DmaRowsTile {  // K rows x COLS bf16 (COLS * 2 = 256 bytes per row)
+  static_assert(COLS == 128, "256-byte rows");
+  static constexpr int P = ROWS_PER_STAGE / 16;  // wave instructions per thread, 4 waves
+  const uint16_t* src[P];
+  int row[P];
+  bool colok[P];
+  __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, int col0, int ext,
+                                       int tid) {
+    const int w = tid >> 6, l = tid & 63;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int r = 4 * (w + 4 * p) + (l >> 4);
+      const int c = trow_chunk(r, l & 15);
+      row[p] = r;
+      colok[p] = col0 + 8 * c < ext;
+      src[p] = base + r * ld + col0 + 8 * c;
+    }
+  }
+  __device__ __forceinline__ void issue(uint32_t* tile, int k0, int K, int64_t ld, int tid) const {
+    const int w = tid >> 6;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const bool in = colok[p] && k0 + row[p] < K;
+      dma16(in ? static_cast<const void*>(src[p] + static_cast<int64_t>(k0) * ld)
+               : static_cast<const void*>(k_zero16),
+            tile + 4 * (w + 4 * p) * 64);
+    }
+  }
+};
+
+// MFMA operand (8 consecutive K of column col0 + (lane & 31)) from a tile of
+// 256-byte rows, K rows k0 + 8 h .. + 7.
+__device__ __forceinline__ bf16x8 tr_operand(const uint32_t* tile, int k0, int col0, int lane) {
+  const int g = lane >> 4, il = lane & 15, a = il & 3, e = il >> 2, h = lane >> 5;
+  const int col = col0 + 16 * (g & 1) + 4 * a;
+  s16x4 v[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int k = k0 + 8 * h + 4 * q + e;
+    const int byte = k * 256 + trow_chunk(k, col >> 3) * 16 + (col & 4) * 2;
+    v[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_s16x4*)(reinterpret_cast<const char*>(tile) + byte));
+  }
+  const s16x4 lo = v[0], hi = v[1];
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 all = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, all);
+}
+
+// PRE: master chunks per thread fetched before the products (the tile has
+// 16); the others are fetched when the epilogue starts, which keeps
+// registers for a third workgroup per CU.
+template <int MINW, int PRE>
+__global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
+  constexpr int BM = 128, BN = 128, BK = 32, NS = 3, NTHR = 256, MI = 2, NJ = 2;
+  constexpr int STAGE_U32 = BK * 256 / 4;  // one operand stage: 32 rows x 256 bytes
+  __shared__ __attribute__((aligned(16))) uint32_t lds_all[2 * NS * STAGE_U32];
+  auto lds_a = [&](int buf) { return lds_all + buf * STAGE_U32; };
+  auto lds_b = [&](int buf) { return lds_all + (NS + buf) * STAGE_U32; };
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, h = lane >> 5;
+  const int z = blockIdx.y;
+  const int rep = g.order[z];
+  const int M = g.M, N = g.N, K = g.K;
+  const int gn = (N + BN - 1) / BN;
+  const int t = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (t / gn) * BM, n0 = (t % gn) * BN;
+
+  const uint16_t* A = static_cast<const uint16_t*>(g.a) + z * g.a_slot;
+  const uint16_t* B = static_cast<const uint16_t*>(g.b) + z * g.b_slot;
+  float* master = g.master + static_cast<int64_t>(rep) * g.master_slot;
+  const float* master_in = g.master_in + static_cast<int64_t>(rep) * g.master_in_slot;
+
+  DmaRowsTile<BK, BM> da;
+  DmaRowsTile<BK, BN> db;
+  da.init(A, g.a_ld, m0, g.a_ext, tid);
+  db.init(B, g.b_ld, n0, g.b_ext, tid);
+  constexpr int PS = DmaRowsTile<BK, BM>::P + DmaRowsTile<BK, BN>::P;  // per stage and thread
+  auto issue = [&](int s) {
+    da.issue(lds_a(s % NS), s * BK, K, g.a_ld, tid);
+    db.issue(lds_b(s % NS), s * BK, K, g.b_ld, tid);
+  };
+  issue(0);
+  issue(1);
+
+  // fp32 master tile W[n0 .. n0 + 127][m0 .. m0 + 127], issued after the
+  // first two operand stages: chunk c = tid + 256 p is row n0 + (c >> 5),
+  // columns m0 + 4 (c & 31) .. + 3 (32 lanes read one 512-byte row segment).
+  constexpr int WCH = BM * BN / 4 / NTHR;  // chunks per thread, both halves
+  static_assert(PRE >= 0 && PRE <= WCH, "prefetch depth");
+  f32x4 wpre[PRE > 0 ? PRE : 1];
+  float* wtile = master + g.w_off + static_cast<int64_t>(n0) * M + m0;
+  const float* wtile_in = master_in + g.w_off + static_cast<int64_t>(n0) * M + m0;
+  auto master_chunk = [&](int p) {
+    const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);
+    const bool ok = n0 + row < N && m0 + col < M;  // M % 4 == 0: chunks are whole
+    return __builtin_nontemporal_load(
+        reinterpret_cast<const f32x4*>(ok ? wtile_in + (row * M + col)
+                                          : reinterpret_cast<const float*>(k_zero16)));
+  };
+#pragma unroll
+  for (int p = 0; p < PRE; ++p) wpre[p] = master_chunk(p);
+
+  f32x16 acc[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  const bool bias_wg = m0 == 0;
+  float dbias = 0.0f;
+
+  const int nk = (K + BK - 1) / BK;
+  for (int j = 0; j < nk; ++j) {
+    // Stage j landed; in flight after it: stage j + 1 and, until stage 2 is
+    // waited for, the master tile (issued between stages 1 and 2).
+    if (j < 2) wait_vm<PS + PRE>();
+    else wait_vm<PS>();
+    lds_barrier();
+    issue(j + 2);
+    const uint32_t* As = lds_a(j % NS);
+    const uint32_t* Bs = lds_b(j % NS);
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      bf16x8 a[MI], b[NJ];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) a[i] = tr_operand(As, 16 * s, wm * 64 + 32 * i, lane);
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) b[jj] = tr_operand(Bs, 16 * s, wn * 64 + 32 * jj, lane);
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj)
+          acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0);
+    }
+    if (bias_wg && tid < BN) {
+      // db[o] = sum_b delta[b][o], column tid of this stage, in K order.
+      const char* bs = reinterpret_cast<const char*>(Bs);
+#pragma unroll 8
+      for (int r = 0; r < BK; ++r) {
+        const uint16_t v = *reinterpret_cast<const uint16_t*>(
+            bs + r * 256 + trow_chunk(r, tid >> 3) * 16 + (tid & 7) * 2);
+        dbias += __uint_as_float(static_cast<uint32_t>(v) << 16);
+      }
+    }
+  }
+  wait_vm<0>();  // trailing stages and the master tile
+  lds_barrier();  // every wave done with the operand stages
+
+  // Epilogue in two halves of 64 output rows: the waves holding those rows
+  // store dW^T to LDS as [o][i] (row n - n0 - 64 half, 16-byte chunk
+  // (m - m0) / 4 placed at chunk ^ (row & 31)), then every thread updates
+  // the master chunks of that half it prefetched.
+  float* dws = reinterpret_cast<float*>(lds_all);  // 64 rows x 512 bytes
+  auto dw_at = [](int row, int ch) { return row * BM + ((ch ^ (row & 31)) << 2); };
+  uint16_t* ctile = (g.wcopy && z < g.wcopy_slots)
+                        ? g.wcopy + z * g.wcopy_slot + g.w_off + static_cast<int64_t>(n0) * M + m0
+                        : nullptr;
+  f32x4 wlate[WCH - PRE > 0 ? WCH - PRE : 1];
+  if constexpr (PRE < WCH) {
+#pragma unroll
+    for (int p = PRE; p < WCH; ++p) wlate[p - PRE] = master_chunk(p);
+  }
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    if (wn == half) {
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = 32 * jj + (lane & 31);  // n - n0 - 64 half
+            const int ch = (wm * 64 + 32 * i + 8 * q + 4 * h) >> 2;
+            *reinterpret_cast<f32x4*>(dws + dw_at(row, ch)) =
+                f32x4{acc[i][jj][4 * q], acc[i][jj][4 * q + 1], acc[i][jj][4 * q + 2],
+                      acc[i][jj][4 * q + 3]};
+          }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = half * WCH / 2; p < (half + 1) * WCH / 2; ++p) {
+      const int c = tid + NTHR * p, row = c >> 5, col = 4 * (c & 31);
+      if (n0 + row < N && m0 + col < M) {
+        const f32x4 d = *reinterpret_cast<const f32x4*>(dws + dw_at(row - 64 * half, c & 31));
+        f32x4 w = p < PRE ? wpre[p < PRE ? p : 0] : wlate[p >= PRE ? p - PRE : 0];
+        (void)wpre;
+        for (int e = 0; e < 4; ++e) w[e] = fmaf(-g.lr, d[e], w[e]);
+        const int at = row * M + col;
+        __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(wtile + at));
+        if (ctile) {
+          u32x2 o;
+          o[0] = f2bf(w[0]) | (f2bf(w[1]) << 16);
+          o[1] = f2bf(w[2]) | (f2bf(w[3]) << 16);
+          __builtin_nontemporal_store(o, reinterpret_cast<u32x2*>(ctile + at));
+        }
+      }
+    }
+    if (half == 0) __syncthreads();
+  }
+  if (bias_wg && tid < BN && n0 + tid < N)
+    master[g.b_off + n0 + tid] = fmaf(-g.lr, dbias, master_in[g.b_off + n0 + tid]);
+}
+
 // Sum of the split-K partials of slot z in chunk order, then the epilogue.
 // One thread per four consecutive rows m..m+3 of column n.
 template <bool BF16, int MODE>
@@ -1144,6 +1378,13 @@ struct TuneKey {
 template <bool BF16, int MODE>
 hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
   if constexpr (MODE == GEMM_WGRAD) {
+    if constexpr (BF16) {
+      const int64_t gx = static_cast<int64_t>((g.M + 127) / 128) * ((g.N + 127) / 128);
+      if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((wgrad_dma_kernel<WGRAD_MIN_WAVES, WGRAD_PRE>), dim3(static_cast<unsigned>(gx), n_slots),
+                         dim3(256), 0, s, g);
+      return hipGetLastError();
+    }
     return gemm_launch_shape<BF16, MODE, SHAPE_L, false>(g, n_slots, s);
   } else {
     const int forced = g_forced_tiling.load();
