@@ -16,9 +16,10 @@ so that float32 replicas can be compared bit for bit.
 Parity status of each function is given in its module docstring.
 """
 from .load_balance import (InfeasibleBarrier, barrier_constraint, load_balance,  # noqa: F401
-                           local_steps_from_barrier, max_wait, wait_times)
+                           local_steps_from_barrier, max_wait, plan_from_measured,
+                           quantize_iteration_times, wait_times)
 from .sampler import (SplitMix64, batch_rows, epoch_permutation,  # noqa: F401
                       shard_offsets)
 from .aggregate import paper_weights, tree_aggregate  # noqa: F401
-from .mlp import bf16_round, loss_and_grads, sgd_step  # noqa: F401
+from .mlp import bf16_round, evaluate, loss_and_grads, sgd_step  # noqa: F401
 from .local_sgd import OracleRun, run_rounds, worker_local_steps  # noqa: F401

@@ -15,9 +15,19 @@ Readings where the paper is silent or inconsistent:
   better and the first-index tie-break would keep it anyway; this is also what
   makes the scan end when all t_i are equal (the constraint then never fails);
 * if the constraint already fails at T = max t the problem is infeasible.
+
+Measured iteration times (the controller's input, Problem Formulation: each
+worker's iteration time is steady and observed by the global view) are turned
+into integer ticks before Algorithm 1: the tick is the fastest worker's time
+divided by a resolution R, and each time becomes the nearest whole number of
+ticks (halves rounded up), at least one.  The fastest worker is then exactly
+R ticks.  Pinned by tests: times that are exact multiples of the tick map to
+those multiples, scaling every time by a constant changes nothing, R = 1
+gives the fastest worker one tick, and a hand-worked case.
 """
 from __future__ import annotations
 
+import math
 from typing import List, Sequence, Tuple
 
 
@@ -69,3 +79,19 @@ def load_balance(t_iter: Sequence[int], M: int) -> Tuple[int, List[int]]:
     best = min(max_wait_time)
     T_star = T_set[max_wait_time.index(best)]
     return T_star, local_steps_from_barrier(T_star, t)
+
+
+def quantize_iteration_times(t_measured: Sequence[float], resolution: int) -> List[int]:
+    """Measured iteration times (any unit) -> integer ticks, tick = min(t) / R."""
+    t = [float(v) for v in t_measured]
+    if not t or resolution < 1 or not all(math.isfinite(v) and v > 0.0 for v in t):
+        raise ValueError("need positive finite times and a resolution >= 1")
+    tick = min(t) / resolution
+    return [max(1, int(math.floor(v / tick + 0.5))) for v in t]
+
+
+def plan_from_measured(t_measured: Sequence[float], resolution: int, M: int):
+    """The controller's plan: ticks, then Algorithm 1.  Returns (ticks, T*, tau)."""
+    ticks = quantize_iteration_times(t_measured, resolution)
+    T_star, tau = load_balance(ticks, M)
+    return ticks, T_star, tau

@@ -94,3 +94,30 @@ def sgd_step(params: Params, Xb: np.ndarray, yb: Sequence[int], lr: float,
     loss, grads = loss_and_grads(params, Xb, yb, bf16)
     new = [(W - lr * dW, b - lr * db) for (W, b), (dW, db) in zip(params, grads)]
     return new, loss
+
+
+def evaluate(params: Params, X: np.ndarray, y: Sequence[int], bf16: bool = False):
+    """Held-out evaluation of a model: the forward pass of ``loss_and_grads``
+    (same rounding points) over all rows.  Returns (summed softmax
+    cross-entropy, number of rows whose label has the largest logit, and per
+    row the gap between the largest and second largest logit, which says
+    where float rounding can decide that count)."""
+    q = bf16_round if bf16 else _identity
+    y = np.asarray(y, dtype=np.int64)
+    A = np.asarray(X, dtype=np.float64)
+    L = len(params)
+    for l, (W, b) in enumerate(params):
+        Z = A @ q(W).T + b
+        A = q(np.maximum(Z, 0.0)) if l < L - 1 else Z
+    logits = A
+    n = logits.shape[0]
+    top = logits.max(axis=1)
+    shift = logits - top[:, None]
+    loss_sum = float(np.sum(np.log(np.exp(shift).sum(axis=1)) - shift[np.arange(n), y]))
+    correct = int(np.sum(logits[np.arange(n), y] >= top))
+    if logits.shape[1] > 1:
+        part = np.partition(logits, -2, axis=1)
+        gap = part[:, -1] - part[:, -2]
+    else:
+        gap = np.full(n, np.inf)
+    return loss_sum, correct, gap

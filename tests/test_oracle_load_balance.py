@@ -114,3 +114,40 @@ def test_infeasible_and_bad_args():
             oracle.load_balance(bad, 3)
     with pytest.raises(ValueError):
         oracle.load_balance([1, 2], 0)
+
+
+def test_quantize_exact_multiples_and_scale():
+    """Times that are whole multiples of the tick give those multiples, at
+    any common scale; R = 1 makes the fastest worker one tick."""
+    mult = [24, 24, 12, 12, 8, 6, 4, 3]
+    for scale in (1.0, 0.37, 1e-3, 2.5e4):
+        t = [m * scale for m in mult]
+        assert oracle.quantize_iteration_times(t, 3) == mult
+        assert oracle.quantize_iteration_times(t, 6) == [2 * m for m in mult]
+    assert oracle.quantize_iteration_times([5.0, 10.0, 7.4, 7.6], 1) == [1, 2, 1, 2]
+
+
+def test_quantize_hand_worked():
+    # fastest 2.0 ms, R = 4 -> tick 0.5 ms: 2.0 -> 4, 3.1 -> 6.2 -> 6, 3.25 -> 6.5 -> 7,
+    # 9.0 -> 18, 0.26 is never below the fastest; halves round up.
+    assert oracle.quantize_iteration_times([2.0, 3.1, 3.25, 9.0], 4) == [4, 6, 7, 18]
+    ticks, T, tau = oracle.plan_from_measured([1.0, 2.0, 4.0], 1, 8)
+    assert ticks == [1, 2, 4] and T == 4 and tau == [4, 2, 1]
+
+
+def test_plan_from_measured_noise_robust():
+    """Jitter well below half a tick leaves the plan of the speed workload unchanged."""
+    rng = __import__("numpy").random.default_rng(3)
+    base = [24, 24, 12, 12, 8, 6, 4, 3]
+    for _ in range(50):
+        t = [b * 1.7 * (1.0 + rng.uniform(-0.01, 0.01)) for b in base]
+        ticks, T, tau = oracle.plan_from_measured(t, 3, 8)
+        assert ticks == base and T == 24 and tau == [1, 1, 2, 2, 3, 4, 6, 8]
+
+
+def test_quantize_bad_args():
+    for bad in ([], [1.0, 0.0], [1.0, float("nan")], [-1.0]):
+        with pytest.raises(ValueError):
+            oracle.quantize_iteration_times(bad, 2)
+    with pytest.raises(ValueError):
+        oracle.quantize_iteration_times([1.0], 0)

@@ -106,3 +106,31 @@ def test_bf16_grads_close_to_exact():
     for (a, b), (c, d) in zip(g64, g16):
         assert np.linalg.norm(a - c) / np.linalg.norm(a) < 3e-2
         assert np.linalg.norm(b - d) / np.linalg.norm(b) < 3e-2
+
+
+def test_evaluate_matches_torch():
+    """Held-out loss and accuracy: summed CrossEntropyLoss and argmax of an
+    nn.Linear / ReLU stack in float64."""
+    params, X, y = _tiny((12, 9, 7, 5), seed=8, B=40)
+    model = _torch_model(params)
+    with torch.no_grad():
+        logits = model(torch.from_numpy(X))
+        loss_t = torch.nn.CrossEntropyLoss(reduction="sum")(logits, torch.from_numpy(y)).item()
+        correct_t = int((logits.argmax(dim=1) == torch.from_numpy(y)).sum())
+    loss, correct, gap = oracle.evaluate(params, X, y)
+    assert np.isclose(loss, loss_t, rtol=1e-13)
+    assert correct == correct_t
+    assert gap.shape == (40,) and np.all(gap >= 0.0)
+
+
+def test_evaluate_counts_ties_and_single_class():
+    """A label tied with another class at the top counts as correct; with
+    one class every row is correct and the loss is zero."""
+    W = np.zeros((3, 2))
+    b = np.array([1.0, 1.0, 0.0])
+    X = np.ones((4, 2))
+    loss, correct, gap = oracle.evaluate([(W, b)], X, [0, 1, 2, 0])
+    assert correct == 3 and np.all(gap == 0.0)
+    assert np.isclose(loss, 4 * np.log(2 * np.e + 1) - 3 * 1.0)
+    loss1, correct1, _ = oracle.evaluate([(np.ones((1, 2)), np.zeros(1))], X, [0, 0, 0, 0])
+    assert correct1 == 4 and loss1 == 0.0
