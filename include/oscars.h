@@ -125,6 +125,23 @@ oscars_status oscars_layer_offsets(const oscars_ctx* ctx, int32_t l, int64_t* w_
 oscars_status oscars_load_balance(const int64_t* t_iter, int32_t N, int64_t M, int64_t* T_star,
                                   int32_t* tau);
 
+/* The load-balancing controller's plan from measured iteration times
+ * (Problem Formulation: each worker's iteration time is steady; Approach: the
+ * global view measures them and runs Algorithm 1), host only.
+ *   t_measured  host [N] per-worker iteration times, finite and > 0, any one
+ *               unit (e.g. milliseconds);
+ *   resolution  1 <= R <= OSCARS_MAX_RESOLUTION: the tick is min(t) / R, so
+ *               the fastest worker takes R ticks;
+ *   ticks       out host [N] or NULL: t_i in ticks, max(1, floor(t_i / tick + 0.5));
+ *   M, T_star, tau as oscars_load_balance, which then runs on the ticks.
+ * OSCARS_E_INVALID for a bad time, resolution, or a time above
+ * OSCARS_MAX_TICKS ticks; OSCARS_E_INFEASIBLE as oscars_load_balance.
+ * The scan of Algorithm 1 grows with R: it ends within about M * R ticks. */
+#define OSCARS_MAX_RESOLUTION 4096
+#define OSCARS_MAX_TICKS 1073741824
+oscars_status oscars_plan_tau(const double* t_measured, int32_t N, int32_t resolution, int64_t M,
+                              int64_t* ticks, int64_t* T_star, int32_t* tau);
+
 /* Eq. 4 weights, host only: w[k] = 1/K as fp32 for every k.  `staleness`
  * (host [K], may be NULL) is accepted and has no effect: the update rule
  * averages uniformly. */
@@ -180,6 +197,22 @@ oscars_status oscars_round(oscars_ctx* ctx, float* global, float* replicas,
  * oscars_local_steps or oscars_round call (NaN for a worker that ran no step).  Waits for the
  * context's stream.  losses: host [K]. */
 oscars_status oscars_round_losses(oscars_ctx* ctx, float* losses);
+
+/* Held-out evaluation of one model (the convergence measure of Evaluation:
+ * loss and accuracy of the trained classifier).  The forward pass of the
+ * local steps (same GEMMs, same rounding points) over rows 0 .. n_rows-1 of
+ * x, max_batch rows at a time, on the context's stream:
+ *   params    device [n_pad] fp32, flat layout (e.g. the global model);
+ *   x, y      device, as in oscars_shards (dtype of the model);
+ *   loss_sum  out: summed softmax cross-entropy (fp32 per row, summed in
+ *             double in row order);
+ *   correct   out: rows whose label's logit is the largest (ties count).
+ * Uses the context's activation workspace (not the losses of the last
+ * local steps), allocates and frees temporary device buffers, and waits for
+ * the stream.  Not for a stream being captured into a graph. */
+oscars_status oscars_evaluate(oscars_ctx* ctx, const float* params, const void* x,
+                              const int32_t* y, int64_t n_rows, double* loss_sum,
+                              int64_t* correct);
 
 /* Parameter-server aggregation (Approach, Eq. 4, first branch).
  *   global    device [n] fp32 out: g[i] = sum_k w_k * replicas[k * ld + i],

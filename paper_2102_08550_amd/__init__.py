@@ -71,6 +71,8 @@ _SIGS = {
     "oscars_profile_begin": (_i32, [_vp, _u32]),
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
     "oscars_set_gemm_tiling": (_i32, [_i32]),
+    "oscars_plan_tau": (_i32, [_P(ctypes.c_double), _i32, _i32, _i64, _P(_i64), _P(_i64), _P(_i32)]),
+    "oscars_evaluate": (_i32, [_vp, _vp, _vp, _vp, _i64, _P(ctypes.c_double), _P(_i64)]),
     "oscars_status_str": (ctypes.c_char_p, [_i32]),
     "oscars_last_hip_error": (_i32, []),
 }
@@ -82,6 +84,9 @@ def _lib():
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"HIP library not built: {LIB_PATH} is missing "
                               "(run python paper_2102_08550_amd/build.py)")
+        # torch first: the library then binds to the HIP runtime torch has
+        # loaded, so that both share one runtime (and one view of the GPU).
+        import torch  # noqa: F401
         lib = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGS.items():
             fn = getattr(lib, name)
@@ -131,6 +136,19 @@ def load_balance(t_iter: Sequence[int], M: int) -> Tuple[int, List[int]]:
     _check(_lib().oscars_load_balance(tp, len(t), int(M), ctypes.byref(T),
                                       tau.ctypes.data_as(_P(_i32))), "oscars_load_balance")
     return int(T.value), tau.tolist()
+
+
+def plan_tau(t_measured: Sequence[float], resolution: int, M: int):
+    """The controller's plan from measured iteration times: (ticks, T*, tau).
+    The tick is min(t) / resolution; Algorithm 1 then runs on the ticks."""
+    t = np.ascontiguousarray(t_measured, dtype=np.float64)
+    ticks = np.zeros(len(t), np.int64)
+    tau = np.zeros(len(t), np.int32)
+    T = _i64(0)
+    _check(_lib().oscars_plan_tau(t.ctypes.data_as(_P(ctypes.c_double)), len(t), int(resolution),
+                                  int(M), ticks.ctypes.data_as(_P(_i64)), ctypes.byref(T),
+                                  tau.ctypes.data_as(_P(_i32))), "oscars_plan_tau")
+    return ticks.tolist(), int(T.value), tau.tolist()
 
 
 def paper_weights(K: int, staleness: Optional[Sequence[int]] = None) -> np.ndarray:
@@ -293,6 +311,20 @@ class Context:
         _check(_lib().oscars_round_losses(self._h, out.ctypes.data_as(_P(_f32))),
                "oscars_round_losses")
         return out
+
+    def evaluate(self, params, x, y, n_rows: Optional[int] = None):
+        """Held-out (summed loss, correct count) of the flat model ``params``
+        (device tensor [n_pad] fp32) on rows 0..n_rows-1 of x / y."""
+        import torch
+        n = int(x.shape[0] if n_rows is None else n_rows)
+        if n > x.shape[0] or n > y.shape[0]:
+            raise ValueError("n_rows exceeds the rows of x or y")
+        loss = ctypes.c_double(0.0)
+        hits = _i64(0)
+        _check(_lib().oscars_evaluate(self._h, _dev_ptr(params, torch.float32, "params"),
+                                      _dev_ptr(x, None, "x"), _dev_ptr(y, torch.int32, "y"), n,
+                                      ctypes.byref(loss), ctypes.byref(hits)), "oscars_evaluate")
+        return float(loss.value), int(hits.value)
 
     def cursors(self) -> List[int]:
         out = np.zeros(self.K, np.int64)

@@ -80,6 +80,30 @@ oscars_status oscars_load_balance(const int64_t* t_iter, int32_t N, int64_t M, i
   return OSCARS_OK;
 }
 
+oscars_status oscars_plan_tau(const double* t_measured, int32_t N, int32_t resolution, int64_t M,
+                              int64_t* ticks, int64_t* T_star, int32_t* tau) {
+  if (!t_measured || !T_star || !tau || N < 1 || M < 1) return OSCARS_E_INVALID;
+  if (resolution < 1 || resolution > OSCARS_MAX_RESOLUTION) return OSCARS_E_INVALID;
+  double tmin = t_measured[0];
+  for (int32_t i = 0; i < N; ++i) {
+    const double v = t_measured[i];
+    if (!std::isfinite(v) || !(v > 0.0)) return OSCARS_E_INVALID;
+    if (v < tmin) tmin = v;
+  }
+  // The fastest worker is `resolution` ticks; every time becomes the nearest
+  // whole number of ticks (halves up), at least one.
+  const double tick = tmin / resolution;
+  std::vector<int64_t> q(N);
+  for (int32_t i = 0; i < N; ++i) {
+    const double x = std::floor(t_measured[i] / tick + 0.5);
+    if (!(x <= static_cast<double>(OSCARS_MAX_TICKS))) return OSCARS_E_INVALID;
+    q[i] = x < 1.0 ? 1 : static_cast<int64_t>(x);
+  }
+  const oscars_status st = oscars_load_balance(q.data(), N, M, T_star, tau);
+  if (st == OSCARS_OK && ticks) std::copy(q.begin(), q.end(), ticks);
+  return st;
+}
+
 oscars_status oscars_paper_weights(const int32_t* staleness, int32_t K, float* w) {
   (void)staleness;  // Eq. 4 averages uniformly; staleness does not enter.
   if (!w || K < 1) return OSCARS_E_INVALID;

@@ -97,11 +97,12 @@ void set_gemm_tiling(int tiling);
 
 // Softmax cross-entropy on logits [slot][B][ld]: delta = (softmax - onehot)/B
 // stored as bf16 or fp32 into delta [slot][B][ld] (columns C..ld-1 zeroed),
-// per-row loss into loss[slot][B].
+// per-row loss into loss[slot][B]; if correct != nullptr, correct[slot][B] =
+// 1 where the label's logit is the largest (ties count), else 0.
 hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
                              const int32_t* y, const int32_t* gather, int64_t gather_slot,
                              void* delta, bool delta_bf16, float* loss, int64_t loss_slot,
-                             int n_slots, hipStream_t s);
+                             int n_slots, hipStream_t s, int32_t* correct = nullptr);
 
 // wcopy[z][i] = bf16(master[order[z]][i]) for i < n, z < n_slots.
 hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int32_t* order,

@@ -1111,7 +1111,8 @@ __global__ __launch_bounds__(64) void softmax_ce_kernel(const float* logits, int
                                                         int64_t slot_stride, int C, int B,
                                                         const int32_t* y, const int32_t* gather,
                                                         int64_t gather_slot, void* delta,
-                                                        float* loss, int64_t loss_slot) {
+                                                        float* loss, int64_t loss_slot,
+                                                        int32_t* correct) {
   const int b = blockIdx.x, z = blockIdx.y, lane = threadIdx.x;
   const float* row = logits + z * slot_stride + static_cast<int64_t>(b) * ld;
   const int label = y[gather[z * gather_slot + b]];
@@ -1132,8 +1133,11 @@ __global__ __launch_bounds__(64) void softmax_ce_kernel(const float* logits, int
     else
       static_cast<float*>(delta)[base + c] = dv;
   }
-  if (lane == 0)
+  if (lane == 0) {
     loss[z * loss_slot + b] = label_ok ? logf(s) - (row[label] - mx) : __builtin_nanf("");
+    // the label's logit is the largest (ties with another class count)
+    if (correct) correct[z * loss_slot + b] = label_ok && row[label] >= mx ? 1 : 0;
+  }
 }
 
 __global__ __launch_bounds__(256) void cast_bf16_kernel(const float* master, int64_t master_slot,
@@ -1463,14 +1467,14 @@ hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots,
 hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
                              const int32_t* y, const int32_t* gather, int64_t gather_slot,
                              void* delta, bool delta_bf16, float* loss, int64_t loss_slot,
-                             int n_slots, hipStream_t s) {
+                             int n_slots, hipStream_t s, int32_t* correct) {
   const dim3 grid(B, n_slots);
   if (delta_bf16)
     hipLaunchKernelGGL((softmax_ce_kernel<true>), grid, dim3(64), 0, s, logits, ld, slot_stride, C,
-                       B, y, gather, gather_slot, delta, loss, loss_slot);
+                       B, y, gather, gather_slot, delta, loss, loss_slot, correct);
   else
     hipLaunchKernelGGL((softmax_ce_kernel<false>), grid, dim3(64), 0, s, logits, ld, slot_stride,
-                       C, B, y, gather, gather_slot, delta, loss, loss_slot);
+                       C, B, y, gather, gather_slot, delta, loss, loss_slot, correct);
   return hipGetLastError();
 }
 

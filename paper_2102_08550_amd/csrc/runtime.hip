@@ -554,6 +554,95 @@ oscars_status oscars_round_losses(oscars_ctx* c, float* losses) {
   return OSCARS_OK;
 }
 
+oscars_status oscars_evaluate(oscars_ctx* c, const float* params, const void* x, const int32_t* y,
+                              int64_t n_rows, double* loss_sum, int64_t* correct) {
+  if (!c || !params || !x || !y || !loss_sum || !correct) return OSCARS_E_INVALID;
+  if (!aligned16(params) || !aligned16(x)) return OSCARS_E_INVALID;
+  if (n_rows < 1 || n_rows > 0x7FFFFFFF) return OSCARS_E_INVALID;
+  const int L = c->L, Bmax = c->max_batch;
+  // Temporary buffers: [64 slot ids = 0][n_rows row ids], per-row loss and hit.
+  std::vector<int32_t> h_tab(64 + n_rows, 0);
+  for (int64_t i = 0; i < n_rows; ++i) h_tab[64 + i] = static_cast<int32_t>(i);
+  int32_t* d_tab = nullptr;
+  float* d_loss = nullptr;
+  int32_t* d_hit = nullptr;
+  auto release = [&]() {
+    if (d_tab) (void)hipFree(d_tab);
+    if (d_loss) (void)hipFree(d_loss);
+    if (d_hit) (void)hipFree(d_hit);
+  };
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&d_tab), h_tab.size() * sizeof(int32_t));
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&d_loss), n_rows * sizeof(float));
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&d_hit), n_rows * sizeof(int32_t));
+  if (e == hipSuccess)
+    e = hipMemcpy(d_tab, h_tab.data(), h_tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    release();
+    return e == hipErrorOutOfMemory ? OSCARS_E_NOMEM : hip_fail(e);
+  }
+  // Weights as the forward pass reads them: the bf16 copy of params (one
+  // cast into the start-model buffer) or params themselves.
+  if (c->bf16)
+    e = launch_cast_bf16(params, 0, d_tab, c->gq, 0, c->n_pad, 1, c->stream);
+  for (int64_t i0 = 0; i0 < n_rows && e == hipSuccess; i0 += Bmax) {
+    const int N = static_cast<int>(std::min<int64_t>(Bmax, n_rows - i0));
+    const int32_t* rows = d_tab + 64 + i0;
+    for (int l = 1; l <= L && e == hipSuccess; ++l) {
+      GemmArgs g{};
+      g.M = c->dims[l];
+      g.N = N;
+      g.K = c->dims[l - 1];
+      g.a_ext = g.K;
+      g.b_ext = g.K;
+      g.a = c->bf16 ? static_cast<const void*>(c->gq + c->w_off[l])
+                    : static_cast<const void*>(params + c->w_off[l]);
+      g.a_ld = c->dims[l - 1];
+      if (l == 1) {
+        g.b = x;
+        g.b_ld = c->dims[0];
+        g.gather = rows;
+        g.rows_out = c->act[0];
+        g.rows_out_ld = c->ld[0];
+      } else {
+        g.b = c->act[l - 1];
+        g.b_ld = c->ld[l - 1];
+      }
+      g.master = const_cast<float*>(params);  // not written by the forward pass
+      g.master_in = params;
+      g.b_off = c->b_off[l];
+      g.w_off = c->w_off[l];
+      g.order = d_tab;
+      g.part = c->part;
+      g.part_cap = c->part_cap;
+      g.out = l < L ? c->act[l] : static_cast<void*>(c->logits);
+      g.relu = l < L;
+      g.out_bf16 = l < L && c->bf16;
+      g.out_ld = c->ld[l];
+      e = launch_gemm(g, GEMM_FWD, c->bf16, 1, c->stream);
+    }
+    if (e == hipSuccess)
+      e = launch_softmax_ce(c->logits, c->ld[L], c->act_slot(L), c->dims[L], N, y, rows, 0,
+                            c->delta[L], c->bf16, d_loss + i0, 0, 1, c->stream, d_hit + i0);
+  }
+  std::vector<float> h_loss(e == hipSuccess ? n_rows : 0);
+  std::vector<int32_t> h_hit(e == hipSuccess ? n_rows : 0);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e == hipSuccess) e = hipMemcpy(h_loss.data(), d_loss, n_rows * sizeof(float), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(h_hit.data(), d_hit, n_rows * sizeof(int32_t), hipMemcpyDeviceToHost);
+  release();
+  if (e != hipSuccess) return hip_fail(e);
+  double acc = 0.0;
+  int64_t hits = 0;
+  for (int64_t i = 0; i < n_rows; ++i) {
+    acc += h_loss[i];
+    hits += h_hit[i];
+  }
+  *loss_sum = acc;
+  *correct = hits;
+  return OSCARS_OK;
+}
+
 oscars_status oscars_aggregate(float* global, float* replicas, const float* weights, int32_t K,
                                int64_t n, int64_t ld, int32_t broadcast, void* hip_stream) {
   if (!global || !replicas || !weights) return OSCARS_E_INVALID;

@@ -1,0 +1,125 @@
+"""GPU parity of the held-out evaluation and of the paradigm comparison
+(Motivation: BSP, local SGD without and with load balancing; Approach:
+Algorithm 1 on measured times; Eq. 1 for the barrier).
+
+* ``oscars_evaluate`` against the oracle's forward pass on the same model and
+  rows: summed loss within the trajectory tolerance; the correct count may
+  differ from the oracle's only on rows whose two largest logits are closer
+  than the rounding of the products can decide.
+* Each paradigm run through ``run_paradigm`` (real rounds on the GPU,
+  emulated cluster clock): the load balancer's tau sequence equals the
+  oracle's plans replayed on the same clock, and the final global model and
+  its held-out loss match the oracle's run with that tau sequence."""
+import numpy as np
+import pytest
+
+import oracle
+import workload
+from _parity import BF16_TOL, FP32_TOL, oracle_rounds, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2102_08550_amd
+    return paper_2102_08550_amd
+
+
+def _dev(ds):
+    import torch
+    x = np.ascontiguousarray(ds.x)
+    xt = torch.from_numpy(x.view(np.int16) if x.dtype == np.uint16 else x).cuda()
+    yt = torch.from_numpy(np.ascontiguousarray(ds.y, dtype=np.int32)).cuda()
+    return xt, yt
+
+
+EVAL_CFGS = [
+    workload.Config("eval-fp32", (64, 72, 10), workload.FP32, K=2, n_rows=64, batch=48,
+                    tau_rule="given", tau_given=(1, 1), seed=21, mean_scale=0.3),
+    workload.Config("eval-bf16", (264, 136, 200, 37), workload.BF16, K=2, n_rows=64, batch=160,
+                    tau_rule="given", tau_given=(1, 1), seed=22, mean_scale=0.3),
+]
+
+
+@pytest.mark.parametrize("cfg", EVAL_CFGS, ids=["fp32", "bf16"])
+def test_evaluate_matches_oracle(P, cfg):
+    import torch
+    say(f"evaluate {cfg.name}")
+    init = workload.gen_init(cfg)
+    ctx = P.Context(cfg.dims, P.BF16 if cfg.dtype == workload.BF16 else P.FP32, cfg.K, cfg.batch)
+    try:
+        params = torch.from_numpy(ctx.pack(init)).cuda()
+        for n in (1, cfg.batch - 5, 3 * cfg.batch + 17):
+            ev = workload.gen_eval_set(cfg, n)
+            x, y = _dev(ev)
+            loss, hits = ctx.evaluate(params, x, y)
+            ref_loss, ref_hits, gap = oracle.evaluate(
+                [(W.astype(np.float64), b.astype(np.float64)) for W, b in init],
+                ev.x_f32().astype(np.float64), ev.y, cfg.dtype == workload.BF16)
+            tol = BF16_TOL if cfg.dtype == workload.BF16 else FP32_TOL
+            assert abs(loss - ref_loss) <= tol * max(1.0, abs(ref_loss)), (n, loss, ref_loss)
+            near = int(np.sum(gap <= 1e-3 * (1.0 + np.abs(gap).max())))
+            assert abs(hits - ref_hits) <= near, (n, hits, ref_hits, near)
+        with pytest.raises(P.OscarsError):
+            ctx.evaluate(params, x, y, 0)
+        with pytest.raises(P.OscarsError):
+            ctx.evaluate(params[1:], x, y)  # not 16-byte aligned
+    finally:
+        ctx.close()
+
+
+PARA_CFG = workload.Config("para", (64, 72, 10), workload.FP32, K=4, n_rows=2000, batch=16,
+                           tau_rule="speeds", speeds=(1, 2, 2, 4), lr=0.05, seed=23,
+                           mean_scale=0.3)
+
+
+def _oracle_taus(C, schedule, paradigm, base, budget, local_steps, resolution, M, K):
+    """The tau sequence a paradigm takes, replayed on the host: plans from the
+    oracle's Algorithm 1 on the times of the previous round, clock by Eq. 1."""
+    taus, clock = [], 0.0
+    observed = schedule.iteration_times(-1, 0.0, base)
+    r = 0
+    while clock < budget:
+        if paradigm == "bsp":
+            tau = [1] * K
+        elif paradigm == "local":
+            tau = [local_steps] * K
+        else:
+            tau = oracle.plan_from_measured(list(observed), resolution, M)[2]
+        t = schedule.iteration_times(r, clock, base)
+        clock += max(a * b for a, b in zip(tau, t))
+        observed = t
+        taus.append(tau)
+        r += 1
+    return taus
+
+
+@pytest.mark.parametrize("paradigm", ["bsp", "local", "oscars"])
+def test_paradigm_matches_oracle(P, paradigm):
+    from paper_2102_08550_amd import controller as C
+    cfg = PARA_CFG
+    say(f"paradigm {paradigm}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    ev = workload.gen_eval_set(cfg, 500)
+    sched = C.SpeedSchedule(cfg.speeds, {6.0: (4, 2, 2, 1)}, jitter=0.02, seed=5)
+    base, budget = 1.0, 12.0
+    res = C.run_paradigm(cfg, ds, init, ev, paradigm, sched, base, budget, local_steps=2,
+                         resolution=4, return_model=True)
+    taus = [rec["tau"] for rec in res["records"] if "tau" in rec]
+    expect = _oracle_taus(C, sched, paradigm, base, budget, 2, 4, cfg.M, cfg.K)
+    assert taus == expect
+    if paradigm == "oscars":
+        assert taus[0] == [1, 2, 2, 4] and taus[-1] == [4, 2, 2, 1]
+    g_ref = oracle_rounds(cfg, ds, init, np.array(taus))[0][-1]
+    err = rel_err(res["model"], g_ref)
+    say(f"  {len(taus)} rounds, final rel err {err:.2e}")
+    assert err <= FP32_TOL
+    ref_loss, _, _ = oracle.evaluate(g_ref, ev.x_f32().astype(np.float64), ev.y, False)
+    last = res["records"][-1]
+    assert abs(last["eval_loss"] - ref_loss / 500) <= FP32_TOL * max(1.0, ref_loss / 500)
+    # the emulated clock is the sum of the barriers
+    assert last["clock"] >= budget and last["samples"] == sum(map(sum, taus)) * cfg.batch

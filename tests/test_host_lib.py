@@ -70,6 +70,41 @@ def test_load_balance_bad_args(P):
         assert ei.value.status == P.E_INVALID
 
 
+def test_plan_tau_matches_oracle(P):
+    """Quantized measured times and the resulting plan: bit-exact with the oracle."""
+    rnd = random.Random(5)
+    for _ in range(400):
+        N = rnd.randint(1, 9)
+        t = [rnd.uniform(0.05, 9.0) * 10 ** rnd.randint(-3, 3) for _ in range(N)]
+        R = rnd.randint(1, 40)
+        M = rnd.randint(1, 12)
+        ticks = oracle.quantize_iteration_times(t, R)
+        if max(ticks) > 2**30:  # above the library's tick limit: rejected, not scanned
+            with pytest.raises(P.OscarsError) as ei:
+                P.plan_tau(t, R, M)
+            assert ei.value.status == P.E_INVALID
+            continue
+        try:
+            expect = oracle.plan_from_measured(t, R, M)
+        except oracle.InfeasibleBarrier:
+            with pytest.raises(P.OscarsError) as ei:
+                P.plan_tau(t, R, M)
+            assert ei.value.status == P.E_INFEASIBLE
+            continue
+        assert P.plan_tau(t, R, M) == (expect[0], expect[1], expect[2])
+    # halves round up on both sides
+    assert P.plan_tau([2.0, 3.25, 3.1, 9.0], 4, 8)[0] == [4, 7, 6, 18]
+
+
+def test_plan_tau_bad_args(P):
+    for t, R, M in (([], 2, 3), ([1.0, 0.0], 2, 3), ([1.0, float("nan")], 2, 3),
+                    ([1.0, float("inf")], 2, 3), ([1.0], 0, 3), ([1.0], 4097, 3),
+                    ([1.0], 2, 0), ([1.0, 1e12], 4096, 3)):
+        with pytest.raises(P.OscarsError) as ei:
+            P.plan_tau(t, R, M)
+        assert ei.value.status == P.E_INVALID, (t, R, M)
+
+
 def test_shard_offsets_match_oracle(P):
     for N, K in [(8192, 4), (60000, 8), (50000, 16), (200000, 8), (23, 4), (5, 7), (0, 3),
                  (2**40 + 3, 64)]:
@@ -127,6 +162,11 @@ T = ctypes.c_int64(0)
 assert lib.oscars_load_balance(t.ctypes.data_as(P(ctypes.c_int64)), 8, ctypes.c_int64(8),
                                ctypes.byref(T), tau.ctypes.data_as(P(ctypes.c_int32))) == 0
 assert T.value == 24 and tau.tolist() == [1, 1, 2, 2, 3, 4, 6, 8]
+tm = np.array([2.4, 2.4, 1.2, 1.2, 0.8, 0.6, 0.4, 0.3]); ticks = np.zeros(8, np.int64)
+assert lib.oscars_plan_tau(tm.ctypes.data_as(P(ctypes.c_double)), 8, 3, ctypes.c_int64(8),
+                           ticks.ctypes.data_as(P(ctypes.c_int64)), ctypes.byref(T),
+                           tau.ctypes.data_as(P(ctypes.c_int32))) == 0
+assert ticks.tolist() == [24, 24, 12, 12, 8, 6, 4, 3] and tau.tolist() == [1, 1, 2, 2, 3, 4, 6, 8]
 class S(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("y", ctypes.c_void_p), ("n_rows", ctypes.c_int64),
                 ("offsets", P(ctypes.c_int64)), ("seed", ctypes.c_uint64)]

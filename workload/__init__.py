@@ -11,9 +11,12 @@ Setup, which is not available here):
 
 * config ``c`` seeds ``numpy.random.SeedSequence(seed)`` and spawns seven
   streams: class means, labels + noise, initial weights, tau draws,
-  staleness, aggregation vectors, sampler seed.
-* data: C-class Gaussian mixture, mu_c ~ N(0, I_d) (float32), y ~ U{0..C-1},
-  x = mu_y + N(0, I_d); bf16 configurations store x rounded to bf16 (RNE).
+  staleness, aggregation vectors, sampler seed; an eighth stream draws the
+  labels and noise of a held-out evaluation set.
+* data: C-class Gaussian mixture, mu_c ~ N(0, s^2 I_d) (float32, s =
+  ``mean_scale``, 1 unless a workload asks for overlapping classes),
+  y ~ U{0..C-1}, x = mu_y + N(0, I_d); bf16 configurations store x rounded
+  to bf16 (RNE).
   Rows are drawn in fixed chunks of ``_CHUNK`` rows so that the stream does not
   depend on available memory.
 * init: for each layer, W[out][in] then b[out] ~ U(-1/sqrt(in), +1/sqrt(in)),
@@ -54,6 +57,7 @@ class Config:
     n_flat: int = 0  # aggregation-only: vector length
     sigma: float = 0.02  # aggregation-only: spread of the replicas around g
     staleness_max: int = 4
+    mean_scale: float = 1.0  # class means ~ N(0, mean_scale^2 I): smaller overlaps the classes more
 
     @property
     def n_layers(self) -> int:
@@ -96,9 +100,11 @@ def scaled(cfg: Config, **changes) -> Config:
     return dataclasses.replace(cfg, **changes)
 
 
-def _streams(cfg: Config):
+def _streams(cfg: Config, count: int = 7):
+    # spawn(n)[i] does not depend on n, so the held-out stream (index 7) leaves
+    # the first seven unchanged
     ss = np.random.SeedSequence(cfg.seed)
-    kids = ss.spawn(7)
+    kids = ss.spawn(count)
     return [np.random.Generator(np.random.PCG64(k)) for k in kids]
 
 
@@ -127,19 +133,35 @@ class Dataset:
         return bf16_bits_to_f32(self.x) if self.dtype == BF16 else self.x
 
 
-def gen_dataset(cfg: Config) -> Dataset:
-    """Gaussian mixture: x = mu_y + noise.  bf16 configs store bf16 bit patterns."""
-    g_means, g_data = _streams(cfg)[0:2]
-    d, C, n = cfg.d, cfg.n_classes, cfg.n_rows
-    mu = g_means.standard_normal((C, d), dtype=np.float32)
-    y = g_data.integers(0, C, size=n, dtype=np.int64).astype(np.int32)
-    out = np.empty((n, d), dtype=np.uint16 if cfg.dtype == BF16 else np.float32)
+def _class_means(cfg: Config, g_means) -> np.ndarray:
+    mu = g_means.standard_normal((cfg.n_classes, cfg.d), dtype=np.float32)
+    if cfg.mean_scale != 1.0:
+        mu *= np.float32(cfg.mean_scale)
+    return mu
+
+
+def _mixture_rows(cfg: Config, mu, g_data, n: int) -> Dataset:
+    y = g_data.integers(0, cfg.n_classes, size=n, dtype=np.int64).astype(np.int32)
+    out = np.empty((n, cfg.d), dtype=np.uint16 if cfg.dtype == BF16 else np.float32)
     for r0 in range(0, n, _CHUNK):
         r1 = min(n, r0 + _CHUNK)
-        blk = g_data.standard_normal((r1 - r0, d), dtype=np.float32)
+        blk = g_data.standard_normal((r1 - r0, cfg.d), dtype=np.float32)
         blk += mu[y[r0:r1]]
         out[r0:r1] = bf16_bits(blk) if cfg.dtype == BF16 else blk
     return Dataset(out, y, cfg.dtype)
+
+
+def gen_eval_set(cfg: Config, n: int) -> Dataset:
+    """Held-out rows of the same mixture (same class means, labels and noise
+    from a stream of their own), the stand-in for a test set."""
+    streams = _streams(cfg, 8)
+    return _mixture_rows(cfg, _class_means(cfg, streams[0]), streams[7], n)
+
+
+def gen_dataset(cfg: Config) -> Dataset:
+    """Gaussian mixture: x = mu_y + noise.  bf16 configs store bf16 bit patterns."""
+    g_means, g_data = _streams(cfg)[0:2]
+    return _mixture_rows(cfg, _class_means(cfg, g_means), g_data, cfg.n_rows)
 
 
 def gen_init(cfg: Config) -> List[Tuple[np.ndarray, np.ndarray]]:
