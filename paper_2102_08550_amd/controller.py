@@ -236,7 +236,8 @@ def time_to_loss(result: Dict, target: float) -> Optional[float]:
 
 
 def compare(cfg, schedule: SpeedSchedule, time_budget_steps: float, local_steps: int = 4,
-            resolution: int = 8, n_eval: int = 10000, base: Optional[float] = None) -> Dict:
+            resolution: int = 8, n_eval: int = 10000, base: Optional[float] = None,
+            eval_every: int = 1) -> Dict:
     """The three paradigms on one workload and one emulated cluster.  The
     budget is in units of the speed-1 step time."""
     import workload
@@ -253,7 +254,8 @@ def compare(cfg, schedule: SpeedSchedule, time_budget_steps: float, local_steps:
     for p in PARADIGMS:
         t0 = time.perf_counter()
         res = run_paradigm(cfg, dataset, init, eval_set, p, schedule, base_ms, budget,
-                           local_steps=local_steps, resolution=resolution)
+                           local_steps=local_steps, resolution=resolution,
+                           eval_every=eval_every)
         res["wall_s"] = time.perf_counter() - t0
         results[p] = res
     # target: the best loss BSP reached within the budget
@@ -261,11 +263,13 @@ def compare(cfg, schedule: SpeedSchedule, time_budget_steps: float, local_steps:
     for p, res in results.items():
         recs = res["records"]
         last = recs[-1]
+        last_eval = [rec for rec in recs if "eval_loss" in rec][-1]
         idle = [rec["idle"] for rec in recs if "idle" in rec]
         out["paradigms"][p] = {
             "rounds": len(recs) - 1, "clock_ms": last["clock"], "samples": res["samples"],
             "samples_per_clock_s": res["samples"] / (last["clock"] / 1e3) if last["clock"] else None,
-            "final_eval_loss": last.get("eval_loss"), "final_eval_acc": last.get("eval_acc"),
+            "final_eval_loss": last_eval["eval_loss"], "final_eval_acc": last_eval["eval_acc"],
+            "final_eval_clock_ms": last_eval["clock"],
             "mean_idle": float(np.mean(idle)) if idle else None,
             "clock_to_bsp_best_loss_ms": time_to_loss(res, target),
             "tau_changes": res["tau_changes"], "gpu_ms": res["gpu_ms"],
@@ -293,7 +297,7 @@ def main(argv=None):
     schedule = SpeedSchedule(cfg.speeds, changes={args.budget / 2: tuple(reversed(cfg.speeds))},
                              jitter=args.jitter, seed=cfg.seed)
     res = compare(cfg, schedule, args.budget, local_steps=args.local_steps,
-                  resolution=args.resolution)
+                  resolution=args.resolution, eval_every=args.eval_every)
     line = json.dumps(res)
     print(line)
     if args.out:
