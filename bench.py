@@ -84,6 +84,24 @@ def pmc_traffic(kernel: str, workload_name: str):
     return ent.get("bytes_per_launch")
 
 
+def host_info():
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        aff = None
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "affinity": aff,
+            "note": "numpy matmul uses its BLAS threads ('cores'); elementwise numpy is one thread"}
+
+
 def cpu_baseline(cfg, ds, init, tau, budget_s: float):
     """The oracle as it stands, on the host cores: the workers' local SGD steps
     of round after round (worker by worker, each from the initial model of the
@@ -129,6 +147,7 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
     dta = time.perf_counter() - t1
     return {
         "value": steps * cfg.batch / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
+        "host": host_info(),
         "sample": f"{steps} local SGD steps of batch {cfg.batch} (workers' steps of {rounds} "
                   f"round(s), each worker from the round's start model; {dt:.1f} s, float64 "
                   f"with bf16 rounding points); aggregation of {cfg.K} x {n_slice} fp32 slices",
@@ -136,7 +155,7 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
     }
 
 
-def bench_aggregation(args, cfg):
+def bench_aggregation(args, cfg, copy):
     """Aggregation stress: K = 32 replicas of 25.6M fp32.  Before each round
     (untimed) the replicas are rebuilt as g + delta_k; the aggregate +
     broadcast launch of each round is timed with events on the same stream."""
@@ -178,7 +197,9 @@ def bench_aggregation(args, cfg):
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gbps / HBM_PEAK_GBPS, "traffic": None, "kernel": "aggregate",
                      "avg_launch_us": ms * 1000.0 / args.steps,
-                     "algorithmic_per_launch": {"flop": 0.0, "bytes": bytes_round}},
+                     "algorithmic_per_launch": {"flop": 0.0, "bytes": bytes_round},
+                     "achieved_vs_copy": gbps / copy["GBps"]},
+        "hbm_copy": copy,
     }
     if args.cpu_budget > 0:
         m = 4_000_000
@@ -190,6 +211,41 @@ def bench_aggregation(args, cfg):
                                "kind": "oracle",
                                "sample": f"oracle tree aggregation of {K} x {m} fp32 (no broadcast)"}
     print(json.dumps(out), flush=True)
+
+
+def hbm_copy_probe(mib: int = 1024, reps: int = 5):
+    """Practical HBM ceiling of a plain fp32 copy of ``mib`` MiB (read + write
+    bytes over the mean time of ``reps`` copies after one warm copy), with
+    torch's device-to-device copy and with the library's broadcast at K = 1
+    (non-temporal stores); the faster one is the ceiling."""
+    import torch
+
+    import paper_2102_08550_amd as P
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return 2 * n * 4 / (a.elapsed_time(b) / reps / 1e3) / 1e9
+
+    torch_gbps = timed(lambda: dst.copy_(src))
+    nt_gbps = timed(lambda: P.broadcast(src, dst, 1, n, n))
+    assert torch.equal(dst, src)
+    del src, dst
+    gbps = max(torch_gbps, nt_gbps)
+    return {"GBps": gbps, "frac_spec_peak": gbps / HBM_PEAK_GBPS, "bytes": 2 * n * 4,
+            "torch_copy_GBps": torch_gbps, "broadcast_K1_GBps": nt_gbps,
+            "what": f"fp32 copy of {mib} MiB (read + write), mean of {reps}: torch's "
+                    "device-to-device copy and oscars_broadcast with K = 1; the faster"}
 
 
 def main():
@@ -225,9 +281,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    copy = hbm_copy_probe()
     cfg = workload.CONFIGS[args.workload]
     if args.workload == "c4":
-        return bench_aggregation(args, cfg)
+        return bench_aggregation(args, cfg, copy)
     print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
     ds = workload.gen_dataset(cfg)
     init = workload.gen_init(cfg)
@@ -351,7 +408,9 @@ def main():
                         "samples_per_s_kernels": samples_w / (local_ms / 1e3) if local_ms else None},
         "kernels": kernels,
         "roofline": roof,
+        "hbm_copy": copy,
     }
+    roof["achieved_vs_copy"] = roof["achieved"] / copy["GBps"] if roof["unit"] == "GB/s" else None
     losses = run.ctx.round_losses()
     out["last_round_mean_loss"] = float(np.nanmean(losses))
     run.close()

@@ -229,6 +229,16 @@ oscars_status oscars_evaluate(oscars_ctx* ctx, const float* params, const void* 
 oscars_status oscars_aggregate(float* global, float* replicas, const float* weights, int32_t K,
                                int64_t n, int64_t ld, int32_t broadcast, void* hip_stream);
 
+/* Broadcast of the global model to every worker (Approach, Eq. 4: after the
+ * average every worker continues from it):
+ *   replicas[k * ld + i] = global[i] for k < K, i < n, non-temporal stores;
+ *   the same K, n, ld rules, alignment and no-overlap requirement as
+ *   oscars_aggregate.  oscars_round needs no broadcast (its workers start
+ *   from the global model itself); this is the separate step for callers
+ *   that keep K materialised replicas.  With K = 1 it is a plain copy. */
+oscars_status oscars_broadcast(const float* global, float* replicas, int32_t K, int64_t n,
+                               int64_t ld, void* hip_stream);
+
 /* Resume support: per-worker count of local steps done so far. host [K]. */
 oscars_status oscars_get_cursors(const oscars_ctx* ctx, int64_t* steps_done);
 oscars_status oscars_set_cursors(oscars_ctx* ctx, const int64_t* steps_done);

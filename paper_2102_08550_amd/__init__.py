@@ -71,6 +71,7 @@ _SIGS = {
     "oscars_profile_begin": (_i32, [_vp, _u32]),
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
     "oscars_set_gemm_tiling": (_i32, [_i32]),
+    "oscars_broadcast": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp]),
     "oscars_plan_tau": (_i32, [_P(ctypes.c_double), _i32, _i32, _i64, _P(_i64), _P(_i64), _P(_i32)]),
     "oscars_evaluate": (_i32, [_vp, _vp, _vp, _vp, _i64, _P(ctypes.c_double), _P(_i64)]),
     "oscars_status_str": (ctypes.c_char_p, [_i32]),
@@ -214,6 +215,17 @@ def aggregate(global_, replicas, weights: Sequence[float], K: int, n: int, ld: i
         raise ValueError("one weight per replica")
     _check(_lib().oscars_aggregate(gp, rp, wp, int(K), int(n), int(ld), int(bool(broadcast)),
                                    _stream_handle(stream)), "oscars_aggregate")
+
+
+def broadcast(global_, replicas, K: int, n: int, ld: int, stream=None):
+    """replicas[k*ld + i] = global_[i] for k < K, i < n (the step after Eq. 4's average)."""
+    import torch
+    gp = _dev_ptr(global_, torch.float32, "global")
+    rp = _dev_ptr(replicas, torch.float32, "replicas")
+    if global_.numel() < n or replicas.numel() < (K - 1) * ld + n:
+        raise ValueError("buffers smaller than K, n, ld imply")
+    _check(_lib().oscars_broadcast(gp, rp, int(K), int(n), int(ld), _stream_handle(stream)),
+           "oscars_broadcast")
 
 
 class Context:

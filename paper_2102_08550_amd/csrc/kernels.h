@@ -109,6 +109,10 @@ hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int3
                             uint16_t* wcopy, int64_t wcopy_slot, int64_t n, int n_slots,
                             hipStream_t s);
 
+// replicas[k * ld + i] = g[i] for k < K, i < n (non-temporal stores).
+hipError_t launch_broadcast(const float* g, float* replicas, int K, int64_t n, int64_t ld,
+                            hipStream_t s);
+
 // Pairwise-tree weighted K-way reduction with optional broadcast.
 hipError_t launch_aggregate(float* g, float* replicas, const float* w, int K, int64_t n,
                             int64_t ld, int broadcast, hipStream_t s);

@@ -1507,10 +1507,15 @@ hipError_t agg_dispatch(float* g, float* reps, const AggWeights& w, int K, int64
     return agg_launch<G, P / G, AGG_V>(g, reps, w, K, n, ld, bcast, s);
   hipError_t e = agg_launch<G, P / G, AGG_V>(g, reps, w, K, n, ld, 0, s);
   if (e != hipSuccess) return e;
+  return launch_broadcast(g, reps, K, n, ld, s);
+}
+
+hipError_t launch_broadcast(const float* g, float* replicas, int K, int64_t n, int64_t ld,
+                            hipStream_t s) {
   const int64_t blocks = (n + 1023) / 1024;
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
   hipLaunchKernelGGL(broadcast_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, g,
-                     reps, K, n, ld);
+                     replicas, K, n, ld);
   return hipGetLastError();
 }
 

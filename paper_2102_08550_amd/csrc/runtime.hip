@@ -659,6 +659,19 @@ oscars_status oscars_aggregate(float* global, float* replicas, const float* weig
   return e == hipSuccess ? OSCARS_OK : hip_fail(e);
 }
 
+oscars_status oscars_broadcast(const float* global, float* replicas, int32_t K, int64_t n,
+                               int64_t ld, void* hip_stream) {
+  if (!global || !replicas) return OSCARS_E_INVALID;
+  if (K < 1 || K > OSCARS_MAX_K || n < 1 || ld < n || ld % 4 != 0) return OSCARS_E_INVALID;
+  if (!aligned16(global) || !aligned16(replicas)) return OSCARS_E_INVALID;
+  const uintptr_t g0 = reinterpret_cast<uintptr_t>(global), g1 = g0 + n * sizeof(float);
+  const uintptr_t r0 = reinterpret_cast<uintptr_t>(replicas),
+                  r1 = r0 + ((K - 1) * ld + n) * sizeof(float);
+  if (g0 < r1 && r0 < g1) return OSCARS_E_INVALID;
+  hipError_t e = launch_broadcast(global, replicas, K, n, ld, static_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? OSCARS_OK : hip_fail(e);
+}
+
 oscars_status oscars_set_gemm_tiling(int32_t tiling) {
   static_assert(OSCARS_TILING_COUNT == GEMM_TILING_COUNT && OSCARS_TILING_VS == GEMM_TILING_VS,
                 "tiling codes of the C ABI and of the launchers agree");

@@ -92,6 +92,38 @@ def test_aggregate_rejects_bad_arguments(P):
         P.aggregate(dg, dr, np.array([0.25, np.nan, 0.25, 0.25], np.float32), 4, 1024, 1024)
 
 
+@pytest.mark.parametrize("K,n,ld", [(1, 1, 4), (1, 1 << 20, 1 << 20), (3, 100003, 100004),
+                                    (8, 54_440_960, 54_440_960), (64, 4097, 4100)])
+def test_broadcast_copies_bit_for_bit(P, K, n, ld):
+    """Every replica's first n elements become the global model; the padding
+    between n and ld is left as it was."""
+    import torch
+    g = torch.from_numpy(np.random.default_rng(K).standard_normal(n).astype(np.float32)).cuda()
+    reps = torch.full(((K - 1) * ld + n + (ld - n),), -7.0, device="cuda")
+    P.broadcast(g, reps, K, n, ld)
+    torch.cuda.synchronize()
+    view = reps[: K * ld].view(K, ld)
+    assert torch.equal(view[:, :n], g.unsqueeze(0).expand(K, n))
+    if ld > n:
+        assert torch.all(view[:, n:] == -7.0)
+
+
+def test_broadcast_rejects_bad_arguments(P):
+    import torch
+    dr = torch.zeros(4 * 1024, device="cuda")
+    dg = torch.zeros(1024, device="cuda")
+    for K, n, ld in ((0, 1024, 1024), (65, 1024, 1024), (4, 0, 1024), (4, 1024, 1022),
+                     (4, 1024, 1025)):
+        with pytest.raises((P.OscarsError, ValueError)):
+            P.broadcast(dg, dr, K, n, ld)
+    with pytest.raises(P.OscarsError):
+        P.broadcast(dg[1:], dr, 4, 512, 1024)  # not 16-byte aligned
+    with pytest.raises(P.OscarsError):
+        P.broadcast(dr, dr, 4, 1024, 1024)  # global overlaps the replicas
+    torch.cuda.synchronize()
+    assert torch.all(dr == 0.0)
+
+
 def test_c4_full_size_sampled_100_rounds(P):
     """Aggregation stress workload at its full size: K = 32 replicas of 25.6M
     fp32, replicas = g + delta_k before each round, aggregate + broadcast, 100
