@@ -255,7 +255,8 @@ enum {
   OSCARS_KERNEL_DGRAD = 3,
   OSCARS_KERNEL_WGRAD = 4,
   OSCARS_KERNEL_AGGREGATE = 5, /* the aggregation inside oscars_round */
-  OSCARS_KERNEL_COUNT = 6
+  OSCARS_KERNEL_BWD_FUSED = 6, /* backward-data + backward-weight + update, one launch */
+  OSCARS_KERNEL_COUNT = 7
 };
 oscars_status oscars_profile_begin(oscars_ctx* ctx, uint32_t kind_mask);
 oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches);
@@ -286,6 +287,34 @@ enum {
   OSCARS_TILING_COUNT = 7
 };
 oscars_status oscars_set_gemm_tiling(int32_t tiling);
+
+/* Backward pass of the hidden layers (l >= 2) of bf16 models, process-wide
+ * (a tuning and testing aid).  By default one launch per layer does
+ * backward-data, backward-weight and the SGD update of Eq. 4 (Approach): it
+ * rounds the fp32 master it streams for the update to the bf16 weights the
+ * forward pass used, so backward-data reads no weights of its own.  Its
+ * results are bit-identical to the separate backward-data and update
+ * launches, whichever mode runs (a weight that is exactly -0 may come out
+ * as +0 in one and -0 in the other).  The bias gradient of every update
+ * sums the batch in blocks of 64 rows, block sums left to right.
+ *   OSCARS_BACKWARD_AUTO (default): fused; the output features are split
+ *     into their chunks of 1024 over workgroups when the 64-wide input strips
+ *     of the active replicas leave CUs idle;
+ *   OSCARS_BACKWARD_SEPARATE: backward-data and update launches;
+ *   OSCARS_BACKWARD_FUSED: fused, never split;
+ *   OSCARS_BACKWARD_FUSED_SPLIT: fused, split wherever there is more than one
+ *     chunk of output features and the context's partial buffer holds them.
+ * Fusion applies to batches of at most 256 rows; larger batches always use
+ * the separate launches.  Returns OSCARS_E_INVALID for a value outside
+ * [0, OSCARS_BACKWARD_COUNT). */
+enum {
+  OSCARS_BACKWARD_AUTO = 0,
+  OSCARS_BACKWARD_SEPARATE = 1,
+  OSCARS_BACKWARD_FUSED = 2,
+  OSCARS_BACKWARD_FUSED_SPLIT = 3,
+  OSCARS_BACKWARD_COUNT = 4
+};
+oscars_status oscars_set_backward(int32_t mode);
 
 const char* oscars_status_str(oscars_status s);
 /* HIP error code of the last OSCARS_E_HIP in this thread (0 if none). */

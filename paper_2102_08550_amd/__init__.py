@@ -24,9 +24,10 @@ LIB_PATH = os.path.join(_HERE, "_lib", "liboscars.so")
 OK, E_INVALID, E_NOMEM, E_HIP, E_INFEASIBLE, E_STATE = 0, -1, -2, -3, -4, -5
 FP32, BF16 = 0, 1
 MAX_K = 64
-KERNEL_CAST, KERNEL_FWD, KERNEL_SOFTMAX, KERNEL_DGRAD, KERNEL_WGRAD, KERNEL_AGGREGATE = range(6)
+(KERNEL_CAST, KERNEL_FWD, KERNEL_SOFTMAX, KERNEL_DGRAD, KERNEL_WGRAD, KERNEL_AGGREGATE,
+ KERNEL_BWD_FUSED) = range(7)
 KERNEL_NAMES = ("cast_bf16", "gemm_fwd", "softmax_ce", "gemm_dgrad", "gemm_wgrad_update",
-                "aggregate")
+                "aggregate", "gemm_bwd_fused")
 
 _i32, _i64, _u32, _u64, _f32, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
                                      ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p)
@@ -71,6 +72,7 @@ _SIGS = {
     "oscars_profile_begin": (_i32, [_vp, _u32]),
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
     "oscars_set_gemm_tiling": (_i32, [_i32]),
+    "oscars_set_backward": (_i32, [_i32]),
     "oscars_broadcast": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp]),
     "oscars_plan_tau": (_i32, [_P(ctypes.c_double), _i32, _i32, _i64, _P(_i64), _P(_i64), _P(_i32)]),
     "oscars_evaluate": (_i32, [_vp, _vp, _vp, _vp, _i64, _P(ctypes.c_double), _P(_i64)]),
@@ -200,6 +202,20 @@ def set_gemm_tiling(tiling: int):
     """Process-wide tiling of the forward / backward-data GEMMs (AUTO: timed
     once per configuration, fastest kept)."""
     _check(_lib().oscars_set_gemm_tiling(int(tiling)), "oscars_set_gemm_tiling")
+
+
+# Backward pass of hidden bf16 layers (oscars_set_backward); results are
+# bit-identical in every mode.
+BACKWARD_AUTO, BACKWARD_SEPARATE, BACKWARD_FUSED, BACKWARD_FUSED_SPLIT = range(4)
+BACKWARDS = {"auto": BACKWARD_AUTO, "separate": BACKWARD_SEPARATE, "fused": BACKWARD_FUSED,
+             "fused_split": BACKWARD_FUSED_SPLIT}
+
+
+def set_backward(mode: int):
+    """Process-wide backward of hidden bf16 layers: AUTO (fused backward-data
+    + update, split over output chunks when CUs would idle), SEPARATE, FUSED,
+    FUSED_SPLIT."""
+    _check(_lib().oscars_set_backward(int(mode)), "oscars_set_backward")
 
 
 def aggregate(global_, replicas, weights: Sequence[float], K: int, n: int, ld: int,

@@ -95,6 +95,26 @@ enum GemmTiling {
 };
 void set_gemm_tiling(int tiling);
 
+// Backward pass of a hidden layer (l >= 2) of a bf16 model in one launch:
+// backward-data, backward-weight and the SGD update, with the arguments of
+// the backward-data launch plus those of the update (master, master_in,
+// w_off, b_off, wcopy, lr):  M = inputs, N = batch, K = outputs; a = the
+// activations of the layer below [N][a_ld] (also the ReLU mask), b = delta
+// [N][b_ld], out = the delta of the layer below.  Same results, bit for
+// bit, as GEMM_DGRAD followed by GEMM_WGRAD (but for the sign of a weight
+// that is exactly -0).  Batches of at most 256 rows, inputs a multiple of 8,
+// W_l within 32-bit buffer offsets (backward_fusable).
+bool backward_fusable(const GemmArgs& g);
+bool backward_fused_enabled();
+hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s);
+// Backward of hidden bf16 layers: AUTO (fused, split over o chunks when the
+// input strips leave CUs idle), SEPARATE (backward-data and update kernels),
+// FUSED (never split), FUSED_SPLIT (split wherever there is more than one
+// chunk and the partial buffer holds it).
+enum BackwardMode { BACKWARD_AUTO = 0, BACKWARD_SEPARATE = 1, BACKWARD_FUSED = 2,
+                    BACKWARD_FUSED_SPLIT = 3, BACKWARD_MODE_COUNT = 4 };
+void set_backward_mode(int mode);
+
 // Softmax cross-entropy on logits [slot][B][ld]: delta = (softmax - onehot)/B
 // stored as bf16 or fp32 into delta [slot][B][ld] (columns C..ld-1 zeroed),
 // per-row loss into loss[slot][B]; if correct != nullptr, correct[slot][B] =

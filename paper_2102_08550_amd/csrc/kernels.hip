@@ -436,8 +436,10 @@ gemm_kernel(GemmArgs g) {
   constexpr bool TOTAL = CHUNKED && !SPLIT;
   f32x16 tot[TOTAL ? MI : 1][TOTAL ? NJ : 1];
 
+  // Backward-weight bias: db[o] = sum_b delta[b][o] in blocks of 64 batch
+  // rows, each block row by row (dcur), block sums left to right (dbias).
   const bool bias_wg = (MODE == GEMM_WGRAD) && m0 == 0;
-  float dbias = 0.0f;
+  float dbias = 0.0f, dcur = 0.0f;
 
   // A: rows m (RowTile, FWD) or k rows with m chunks (TransTile).
   // B: rows n (RowTile, FWD / DGRAD) or k rows with n chunks (TransTile, WGRAD).
@@ -466,10 +468,10 @@ gemm_kernel(GemmArgs g) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if constexpr (BF16) {
-            dbias += __uint_as_float(v[e] << 16);
-            dbias += __uint_as_float(v[e] & 0xFFFF0000u);
+            dcur += __uint_as_float(v[e] << 16);
+            dcur += __uint_as_float(v[e] & 0xFFFF0000u);
           } else {
-            dbias += __uint_as_float(v[e]);
+            dcur += __uint_as_float(v[e]);
           }
         }
       }
@@ -478,6 +480,13 @@ gemm_kernel(GemmArgs g) {
 
   // After K tile j (counted from kbeg): close the chunk it ends.
   auto fold = [&](int j, int nk) {
+    if constexpr (MODE == GEMM_WGRAD) {
+      static_assert(64 % BK == 0, "64-row bias blocks of whole K tiles");
+      if (((j + 1) * BK) % 64 == 0 || j + 1 == nk) {
+        dbias = j * BK < 64 ? dcur : dbias + dcur;
+        dcur = 0.0f;
+      }
+    }
     if constexpr (TOTAL) {
       if ((j + 1) % TPC == 0 || j + 1 == nk) {
         const bool first = j < TPC;
@@ -993,8 +1002,9 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  // bias: 64-row blocks (two stages) row by row, block sums left to right
   const bool bias_wg = m0 == 0;
-  float dbias = 0.0f;
+  float dbias = 0.0f, dcur = 0.0f;
 
   const int nk = (K + BK - 1) / BK;
   for (int j = 0; j < nk; ++j) {
@@ -1026,7 +1036,12 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
       for (int r = 0; r < BK; ++r) {
         const uint16_t v = *reinterpret_cast<const uint16_t*>(
             bs + r * 256 + trow_chunk(r, tid >> 3) * 16 + (tid & 7) * 2);
-        dbias += __uint_as_float(static_cast<uint32_t>(v) << 16);
+        dcur += __uint_as_float(static_cast<uint32_t>(v) << 16);
+      }
+      static_assert(64 % BK == 0, "64-row bias blocks of whole stages");
+      if (((j + 1) * BK) % 64 == 0 || j + 1 == nk) {
+        dbias = j * BK < 64 ? dcur : dbias + dcur;
+        dcur = 0.0f;
       }
     }
   }
@@ -1086,6 +1101,363 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
   }
   if (bias_wg && tid < BN && n0 + tid < N)
     master[g.b_off + n0 + tid] = fmaf(-g.lr, dbias, master_in[g.b_off + n0 + tid]);
+}
+
+// ---------------------------------------------------------------------------
+// Backward pass of a hidden layer (l >= 2) of a bf16 model in one kernel:
+// backward-data, backward-weight and the SGD update of Eq. 4.  A workgroup
+// owns a strip of 64 input features i (columns of W_l) and walks the output
+// features o in chunks of 64.  For each chunk it streams the fp32 master rows
+// of its strip, rounds them to the bf16 working weights Wq = bf16(W) the
+// forward pass used, and computes
+//   backward-data    C[i][b] += sum_{o in chunk} Wq[o][i] delta[b][o]
+//   backward-weight  dW[o][i] = sum_b act[b][i] delta[b][o]
+//   update           W <- W - eta dW (fp32 master, bf16 copy refreshed);
+//                    the strip t % strips also updates the chunk's bias,
+//                    b <- b - eta sum_b delta.
+// Backward-data thus reads no weights of its own: its products ride on the
+// master stream of the update.  Its result is masked by act > 0 and stored
+// as the bf16 delta of the layer below.
+//
+// Two roles of four waves each, one barrier per chunk step:
+//   stream waves (0-3) at step t stage chunk t + 1 into LDS (delta, and Wq
+//     rounded from the master rows), issue the loads of chunk t + 2 (delta)
+//     and t + 3 (master), and apply dW of chunk t - 1 to its master rows;
+//   math waves (4-7) at step t run the MFMA products of chunk t and leave dW
+//     in LDS.
+// Every SIMD holds one wave of each role, so the update's vector work and
+// memory traffic overlap the products.  The stream waves' loads and stores
+// go through buffer resources (out-of-range offsets read zeros and write
+// nothing), so their loop has no branches around memory operations.
+//
+// The summation orders are those of the separate kernels: backward-data sums
+// o in chunks of KCHUNK (each from zero, 16 at a time, chunk sums left to
+// right); backward-weight sums the batch 16 rows at a time from zero; the
+// bias sums blocks of 64 batch rows row by row and the block sums left to
+// right.  The operand roles of every MFMA are those of the separate kernels
+// too.  Backward-weight runs over 128 or 256 batch rows (zero past B) where
+// the separate kernel stops at the batch rounded up to 32; the extra zero
+// products can only turn a dW of -0 into +0, which changes the updated
+// weight only when that weight is -0 itself.
+// SPLIT: a workgroup covers one KCHUNK range of o and stores its
+// backward-data sum as that chunk's partial; splitk_reduce_kernel finishes.
+//
+// LDS (144 KB): two delta chunks [256 b][64 o] bf16, two Wq chunks
+// [64 o][64 i] bf16 and the activation strip [256 b][64 i] bf16 (128-byte
+// rows), two dW chunks [64 o][64 i] fp32 (256-byte rows).  Batches of at
+// most 256 rows (FB_BMAX); backward-weight sums 128 or 256 rows (NKS K16
+// steps), zero from row B on.
+constexpr int FB_TI = 64, FB_TO = 64, FB_NT = 512, FB_BMAX = 256;
+constexpr int FB_NB = 5;  // master chunks a stream thread holds: t - 1 .. t + 3
+static_assert(KCHUNK % FB_TO == 0, "chunks of whole o tiles");
+
+// 128-byte-row tiles read both plainly (one 16-byte chunk of 16 consecutive
+// rows per 16 lanes) and transposed (ds_read_b64_tr_b16: 4 consecutive rows,
+// 4 aligned chunks per 32 lanes).  Chunk c of row r sits at c ^ sw128(r):
+// the same-parity rows of 16 consecutive rows take 8 distinct positions, and
+// rows 2 apart take opposite halves, so neither read has bank conflicts.
+__device__ __forceinline__ int sw128(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int t128(int r, int c) { return r * 128 + ((c ^ sw128(r)) << 4); }
+
+// MFMA operand from a 128-byte-row tile: 8 consecutive rows (K) of column
+// col0 + (lane & 31), rows k0 + 8 (lane >> 5) .. + 7 (see tr_operand).
+__device__ __forceinline__ bf16x8 tr128(const char* tile, int k0, int col0, int lane) {
+  const int g = lane >> 4, il = lane & 15, a = il & 3, e = il >> 2, h = lane >> 5;
+  const int col = col0 + 16 * (g & 1) + 4 * a;
+  s16x4 v[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int k = k0 + 8 * h + 4 * q + e;
+    v[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_s16x4*)(tile + t128(k, col >> 3) + (col & 4) * 2));
+  }
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 all = {v[0][0], v[0][1], v[0][2], v[0][3], v[1][0], v[1][1], v[1][2], v[1][3]};
+  return __builtin_bit_cast(bf16x8, all);
+}
+// MFMA operand read plainly: row `row`, 16-byte chunk `c` (8 consecutive K).
+__device__ __forceinline__ bf16x8 row128(const char* tile, int row, int c) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(tile + t128(row, c)));
+}
+
+template <int U> struct Ic { static constexpr int value = U; };
+
+// Raw buffer resources (gfx9 descriptor word 3): an access whose byte offset
+// is at or beyond `bytes` reads zeros and writes nothing.  Every offset used
+// here is a whole 16 / 8 / 4 byte unit inside or outside the range.
+constexpr uint32_t kBufWord3 = 0x00020000u;
+constexpr uint32_t kOob = 0xFFFFFFF0u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, kBufWord3);
+}
+
+template <bool SPLIT, int NKS>
+__global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int strips, int nsplit) {
+  __shared__ __attribute__((aligned(16))) char smem[144 * 1024 + 2048];
+  float* const bpart = reinterpret_cast<float*>(smem + 147456);  // bias block sums [2][4][64]
+  auto dbuf = [&](int t) { return smem + (t & 1) * 32768; };                    // delta chunk
+  auto wbuf = [&](int t) { return smem + 65536 + (t & 1) * 8192; };             // Wq chunk
+  auto wdbuf = [&](int t) { return reinterpret_cast<float*>(smem + 81920 + (t & 1) * 16384); };
+  char* const astrip = smem + 114688;  // activation strip [16 NKS][64] bf16
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5;
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int per_slot = strips * nsplit;
+  const int z = lin / per_slot, rs = lin % per_slot;
+  const int split = rs / strips, strip = rs % strips;
+  const int I = g.M, B = g.N, O = g.K;
+  const int i0 = strip * FB_TI;
+  const int nt_all = (O + FB_TO - 1) / FB_TO;
+  constexpr int TPC = KCHUNK / FB_TO;
+  const int tbeg = SPLIT ? split * TPC : 0;
+  const int tend = SPLIT ? (nt_all < tbeg + TPC ? nt_all : tbeg + TPC) : nt_all;
+  // steps t = tbeg - 1 .. tend (stream: stage t + 1, update t - 1), padded
+  // to whole groups of FB_NB for the stream waves' register rotation
+  const int nsteps = (tend - tbeg + 2 + FB_NB - 1) / FB_NB * FB_NB;
+  const int Bp = (B + 31) & ~31;  // batch rows of the bias sum; rows B .. Bp - 1 are zero
+  const int nblk = (Bp + 63) / 64;  // 64-row blocks of the bias sum
+  static_assert(NKS == 8 || NKS == 16, "batch rows 128 or 256");
+
+  // Activation strip [16 NKS][64] into LDS (all waves), zero from row B on.
+  {
+    const uint16_t* act = static_cast<const uint16_t*>(g.a) + z * g.a_slot;
+#pragma unroll
+    for (int p = 0; p < FB_BMAX / 64; ++p) {
+      const int row = (tid >> 3) + 64 * p, c = tid & 7;
+      if (64 * p < 16 * NKS)
+        *reinterpret_cast<u32x4*>(astrip + t128(row, c)) =
+            load16(row < B, act + static_cast<int64_t>(row < B ? row : 0) * g.a_ld + i0 + 8 * c);
+    }
+  }
+  __syncthreads();
+
+  if (w < 4) {
+    // ---------------- stream waves ----------------
+    const int rep = g.order[z];
+    const int ts = tid;  // 0 .. 255
+    const bool refresh = g.wcopy && z < g.wcopy_slots;
+    // W_l rows [tbeg * 64, obound) of this workgroup; offsets relative to row
+    // tbeg * 64, so rows before it are negative (out of range as unsigned).
+    const int row0 = tbeg * FB_TO;
+    const int obound = tend * FB_TO < O ? tend * FB_TO : O;
+    const uint32_t wbytes = static_cast<uint32_t>(obound - row0) * I * 4;
+    const int64_t wbase = g.w_off + static_cast<int64_t>(row0) * I;
+    const float* mw_in = g.master_in + static_cast<int64_t>(rep) * g.master_in_slot;
+    float* mw = g.master + static_cast<int64_t>(rep) * g.master_slot;
+    const __amdgpu_buffer_rsrc_t r_win = buf_rsrc(mw_in + wbase, wbytes);
+    const __amdgpu_buffer_rsrc_t r_wout = buf_rsrc(mw + wbase, wbytes);
+    const __amdgpu_buffer_rsrc_t r_copy =
+        buf_rsrc(refresh ? static_cast<const void*>(g.wcopy + z * g.wcopy_slot + wbase) : mw,
+                 refresh ? wbytes / 2 : 0u);
+    // The bias of chunk t belongs to the strip t % strips (spread evenly).
+    auto bias_own = [&](int t) { return t % strips == strip; };
+    const uint32_t bbytes = static_cast<uint32_t>(obound - row0) * 4;
+    const __amdgpu_buffer_rsrc_t r_bin = buf_rsrc(mw_in + g.b_off + row0, bbytes);
+    const __amdgpu_buffer_rsrc_t r_bout = buf_rsrc(mw + g.b_off + row0, bbytes);
+    const uint16_t* dl = static_cast<const uint16_t*>(g.b) + z * g.b_slot;
+    const __amdgpu_buffer_rsrc_t r_delta = buf_rsrc(dl, static_cast<uint32_t>(B) * g.b_ld * 2);
+
+    // Master chunk t: thread rows (ts >> 4) + 16 p of the chunk, columns
+    // i0 + 4 (ts & 15) .. + 3 (16 lanes read one 256-byte row segment).
+    const int mrow = ts >> 4, mc = ts & 15;
+    const bool col_ok = i0 + 4 * mc < I;
+    auto woff = [&](int t, int p, int es) -> uint32_t {
+      return col_ok ? static_cast<uint32_t>(((t - tbeg) * FB_TO + mrow + 16 * p) * I + i0 + 4 * mc) * es
+                    : kOob;
+    };
+    auto master_chunk = [&](int t, int p) {
+      return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r_win, woff(t, p, 4), 0, 2));
+    };
+    // Delta chunk t: rows (ts >> 3) + 32 p < 16 NKS, 16-byte chunk ts & 7;
+    // zeros beyond the batch and past the workgroup's chunks.
+    u32x4 dreg[NKS / 2];
+    auto load_delta = [&](int t) {
+#pragma unroll
+      for (int p = 0; p < NKS / 2; ++p) {
+        const int row = (ts >> 3) + 32 * p;
+        const uint32_t off =
+            t < tend ? static_cast<uint32_t>(row * g.b_ld + t * FB_TO + 8 * (ts & 7)) * 2 : kOob;
+        dreg[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r_delta, off, 0, 0));
+      }
+    };
+
+    f32x4 mreg[FB_NB][4];
+    load_delta(tbeg);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) mreg[1][p] = master_chunk(tbeg, p);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) mreg[2][p] = master_chunk(tbeg + 1, p);
+
+    // step t = tbeg - 1 + u; master chunk x sits in mreg[(x - tbeg + 1) % FB_NB]
+    auto step = [&](int t, auto uc) {
+      constexpr int u = decltype(uc)::value;
+      constexpr int b_next = (u + 1) % FB_NB, b_ahead = (u + 3) % FB_NB, b_prev = (u + FB_NB - 1) % FB_NB;
+      // bias of chunk t - 1 (its owner's wave 0; out of range elsewhere)
+      const uint32_t boff = ts < FB_TO && t > tbeg && bias_own(t - 1)
+                                ? static_cast<uint32_t>((t - 1 - tbeg) * FB_TO + ts) * 4
+                                : kOob;
+      const float bias_in = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r_bin, boff, 0, 0));
+      // stage chunk t + 1: delta, and Wq rounded from the master rows
+      char* const dt = dbuf(t + 1);
+#pragma unroll
+      for (int p = 0; p < NKS / 2; ++p)
+        *reinterpret_cast<u32x4*>(dt + t128((ts >> 3) + 32 * p, ts & 7)) = dreg[p];
+      char* const wq = wbuf(t + 1);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const f32x4 m = mreg[b_next][p];
+        u32x2 q;
+        q[0] = f2bf(m[0]) | (f2bf(m[1]) << 16);
+        q[1] = f2bf(m[2]) | (f2bf(m[3]) << 16);
+        *reinterpret_cast<u32x2*>(wq + t128(mrow + 16 * p, mc >> 1) + 8 * (mc & 1)) = q;
+      }
+      // loads: delta of chunk t + 2, master of chunk t + 3
+      load_delta(t + 2);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) mreg[b_ahead][p] = master_chunk(t + 3, p);
+      // update of chunk t - 1 with its dW (rows outside [tbeg, tend) are out
+      // of range)
+      const float* dws = wdbuf(t - 1);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int r = mrow + 16 * p;
+        const f32x4 d = *reinterpret_cast<const f32x4*>(dws + r * 64 + ((mc ^ (r & 15)) << 2));
+        f32x4 wv = mreg[b_prev][p];
+        for (int e = 0; e < 4; ++e) wv[e] = fmaf(-g.lr, d[e], wv[e]);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, wv), r_wout, woff(t - 1, p, 4), 0, 2);
+        u32x2 q;
+        q[0] = f2bf(wv[0]) | (f2bf(wv[1]) << 16);
+        q[1] = f2bf(wv[2]) | (f2bf(wv[3]) << 16);
+        __builtin_amdgcn_raw_buffer_store_b64(q, r_copy, woff(t - 1, p, 2), 0, 2);
+      }
+      // bias: db[o] = sum_b delta[b][o] in blocks of 64 batch rows, each row
+      // by row, block sums left to right.  Stream wave w sums block w of
+      // chunk t (column = lane, four rows per transposing read; lane 16 g + j
+      // receives column 16 g + j); wave 0 adds the blocks of chunk t - 1.
+      if (t >= tbeg && t < tend && bias_own(t)) {
+        const char* dtt = dbuf(t);
+        const int gq = lane >> 4, a = lane & 3, e = (lane >> 2) & 3;
+        const int col = 16 * gq + 4 * a;
+        const int r1 = 64 * w + 64 < Bp ? 64 * w + 64 : Bp;
+        float part = 0.0f;
+        for (int k0 = 64 * w; k0 < r1; k0 += 4) {
+          const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4*)(dtt + t128(k0 + e, col >> 3) + (col & 4) * 2));
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            part += __uint_as_float(static_cast<uint32_t>(static_cast<uint16_t>(v[q])) << 16);
+        }
+        bpart[(t & 1) * 256 + 64 * w + lane] = part;
+      }
+      float dbias = 0.0f;
+      if (w == 0 && t > tbeg && t <= tend && bias_own(t - 1)) {
+        const float* bp = bpart + ((t - 1) & 1) * 256;
+        dbias = bp[lane];
+        for (int blk = 1; blk < nblk; ++blk) dbias += bp[64 * blk + lane];
+      }
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, fmaf(-g.lr, dbias, bias_in)),
+                                            r_bout, boff, 0, 0);
+      __syncthreads();
+    };
+    for (int u0 = 0; u0 < nsteps; u0 += FB_NB) {
+      const int t = tbeg - 1 + u0;
+      step(t, Ic<0>());
+      step(t + 1, Ic<1>());
+      step(t + 2, Ic<2>());
+      step(t + 3, Ic<3>());
+      step(t + 4, Ic<4>());
+    }
+    return;
+  }
+
+  // ---------------- math waves ----------------
+  const int wb = w - 4;  // 0 .. 3
+  f32x16 accd[2][2], tot[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) accd[a][b][r] = tot[a][b][r] = 0.0f;
+  const bool dgrad_wave = 64 * wb < B;
+  for (int u = 0; u < nsteps; ++u) {
+    const int t = tbeg - 1 + u;
+    if (t >= tbeg && t < tend) {
+      const char* dt = dbuf(t);
+      const char* wq = wbuf(t);
+      // Backward-weight (dW rows o = 32 (wb & 1) .. + 31 of the chunk, input
+      // features 32 (wb >> 1) .. + 31): one accumulation chain over the batch,
+      // with the four backward-data steps of the chunk (batch rows 64 wb ..
+      // + 63, all 64 inputs; waves past the batch compute rows never stored)
+      // placed between its links.
+      f32x16 accw;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) accw[r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) {
+        accw = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr128(astrip, 16 * s, 32 * (wb >> 1), lane),
+                                                       tr128(dt, 16 * s, 32 * (wb & 1), lane),
+                                                       accw, 0, 0, 0);
+        if (s % (NKS / 4) == 0) {
+          const int k = s / (NKS / 4);
+          const bf16x8 a0 = tr128(wq, 16 * k, 0, lane), a1 = tr128(wq, 16 * k, 32, lane);
+          const bf16x8 b0 = row128(dt, 64 * wb + (lane & 31), 2 * k + h);
+          const bf16x8 b1 = row128(dt, 64 * wb + 32 + (lane & 31), 2 * k + h);
+          accd[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, accd[0][0], 0, 0, 0);
+          accd[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, accd[0][1], 0, 0, 0);
+          accd[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, accd[1][0], 0, 0, 0);
+          accd[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, accd[1][1], 0, 0, 0);
+        }
+      }
+      // dW chunk into LDS as [o][i], 16-byte chunk c of row o at c ^ (o & 15)
+      float* dws = wdbuf(t);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int o = 32 * (wb & 1) + (lane & 31), c = 8 * (wb >> 1) + 2 * q + h;
+        *reinterpret_cast<f32x4*>(dws + o * 64 + ((c ^ (o & 15)) << 2)) =
+            f32x4{accw[4 * q], accw[4 * q + 1], accw[4 * q + 2], accw[4 * q + 3]};
+      }
+      // end of a KCHUNK range of o: chunk sums left to right
+      if (!SPLIT && ((t + 1) % TPC == 0 || t + 1 == tend)) {
+        const bool first = t < TPC;
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            tot[a][j] = first ? accd[a][j] : tot[a][j] + accd[a][j];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) accd[a][j][r] = 0.0f;
+          }
+      }
+    }
+    __syncthreads();
+  }
+
+  if (!dgrad_wave) return;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int b = 64 * wb + 32 * j + (lane & 31);
+      if (b >= B) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + 32 * a + 8 * q + 4 * h;
+        if (i >= I) continue;  // I is a multiple of 8: whole groups of four
+        if constexpr (SPLIT) {
+          // the workgroup's one chunk, as that chunk's partial
+          float* part = g.part + z * g.part_slot + static_cast<int64_t>(split) * B * g.out_ld;
+          *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(b) * g.out_ld + i) =
+              f32x4{accd[a][j][4 * q], accd[a][j][4 * q + 1], accd[a][j][4 * q + 2],
+                    accd[a][j][4 * q + 3]};
+        } else {
+          store_out<true, GEMM_DGRAD>(g, z, b, i, 4,
+                                      f32x4{tot[a][j][4 * q], tot[a][j][4 * q + 1],
+                                            tot[a][j][4 * q + 2], tot[a][j][4 * q + 3]},
+                                      nullptr);
+        }
+      }
+    }
 }
 
 // Sum of the split-K partials of slot z in chunk order, then the epilogue.
@@ -1462,6 +1834,57 @@ hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots,
     }
   }
   return hipErrorInvalidValue;
+}
+
+namespace {
+std::atomic<int> g_backward_mode{BACKWARD_AUTO};
+}  // namespace
+
+void set_backward_mode(int mode) { g_backward_mode.store(mode); }
+
+// Batches of at most FB_BMAX rows, whole 16-byte input chunks, and W_l small
+// enough for 32-bit buffer offsets (with the three chunks read ahead).
+bool backward_fusable(const GemmArgs& g) {
+  return g.N >= 1 && g.N <= FB_BMAX && g.M % 8 == 0 &&
+         static_cast<int64_t>(g.K) * g.M * 4 <= (static_cast<int64_t>(1) << 31);
+}
+
+bool backward_fused_enabled() { return g_backward_mode.load() != BACKWARD_SEPARATE; }
+
+// Grid x = slots x strips x splits, slot slowest, strip fastest: with the
+// XCD-aware order the strips of one slot (which read the same delta) share
+// an XCD and its L2.  Without a forced mode the o range is split into its
+// KCHUNK ranges when the strips alone leave CUs idle.
+hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s) {
+  if (!backward_fusable(g_in) || n_slots < 1) return hipErrorInvalidValue;
+  GemmArgs g = g_in;
+  const int strips = (g.M + FB_TI - 1) / FB_TI;
+  const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
+  g.part_slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
+  const bool can_split = nchunks > 1 && g.part && g.part_slot * n_slots <= g.part_cap;
+  const int mode = g_backward_mode.load();
+  const bool split = can_split && (mode == BACKWARD_FUSED_SPLIT ||
+                                   (mode == BACKWARD_AUTO &&
+                                    static_cast<int64_t>(n_slots) * strips < device_cu_count()));
+  const int nsplit = split ? nchunks : 1;
+  const int64_t gx = static_cast<int64_t>(n_slots) * strips * nsplit;
+  if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(gx)), block(FB_NT);
+  const bool b256 = g.N > 128;  // batch rows summed by backward-weight: 256 or 128
+  if (!split) {
+    if (b256) hipLaunchKernelGGL((bwd_fused_kernel<false, 16>), grid, block, 0, s, g, strips, 1);
+    else hipLaunchKernelGGL((bwd_fused_kernel<false, 8>), grid, block, 0, s, g, strips, 1);
+    return hipGetLastError();
+  }
+  if (b256) hipLaunchKernelGGL((bwd_fused_kernel<true, 16>), grid, block, 0, s, g, strips, nsplit);
+  else hipLaunchKernelGGL((bwd_fused_kernel<true, 8>), grid, block, 0, s, g, strips, nsplit);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t work = static_cast<int64_t>(g.N) * ((g.M + 3) / 4);
+  hipLaunchKernelGGL((splitk_reduce_kernel<true, GEMM_DGRAD>),
+                     dim3(static_cast<unsigned>((work + 255) / 256), n_slots), dim3(256), 0, s, g,
+                     nchunks);
+  return hipGetLastError();
 }
 
 hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,

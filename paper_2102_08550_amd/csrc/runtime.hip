@@ -454,6 +454,36 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
     if (e != hipSuccess) return hip_fail(e);
     // backward, top layer first; dgrad(l) reads W_l before wgrad(l) updates it
     for (int l = L; l >= 1; --l) {
+      if (l > 1 && c->bf16 && backward_fused_enabled()) {
+        // hidden layer of a bf16 model: backward-data, backward-weight and the
+        // update in one launch (bit-identical to the two launches below)
+        GemmArgs g{};
+        g.M = c->dims[l - 1];
+        g.N = B;
+        g.K = c->dims[l];
+        g.a = c->act[l - 1];
+        g.a_ld = c->ld[l - 1];
+        g.a_slot = c->act_slot(l - 1);
+        g.b = c->delta[l];
+        g.b_ld = c->ld[l];
+        g.b_slot = c->act_slot(l);
+        common(g, l);
+        g.out = c->delta[l - 1];
+        g.out_ld = c->ld[l - 1];
+        g.out_slot = c->act_slot(l - 1);
+        g.out_bf16 = 1;
+        g.mask = c->act[l - 1];
+        g.mask_ld = c->ld[l - 1];
+        g.mask_slot = c->act_slot(l - 1);
+        g.wcopy = c->wcopy;
+        g.wcopy_slot = c->n_pad;
+        g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
+        if (backward_fusable(g)) {
+          e = timed(c, OSCARS_KERNEL_BWD_FUSED, [&] { return launch_bwd_fused(g, ns, c->stream); });
+          if (e != hipSuccess) return hip_fail(e);
+          continue;
+        }
+      }
       if (l > 1) {
         // C[i][b] = sum_o W_l[o][i] delta_l[b][o], masked by act_{l-1} > 0
         GemmArgs g{};
@@ -677,6 +707,15 @@ oscars_status oscars_set_gemm_tiling(int32_t tiling) {
                 "tiling codes of the C ABI and of the launchers agree");
   if (tiling < 0 || tiling >= OSCARS_TILING_COUNT) return OSCARS_E_INVALID;
   set_gemm_tiling(tiling);
+  return OSCARS_OK;
+}
+
+oscars_status oscars_set_backward(int32_t mode) {
+  static_assert(OSCARS_BACKWARD_COUNT == BACKWARD_MODE_COUNT &&
+                    OSCARS_BACKWARD_FUSED_SPLIT == BACKWARD_FUSED_SPLIT,
+                "backward modes of the C ABI and of the launchers agree");
+  if (mode < 0 || mode >= OSCARS_BACKWARD_COUNT) return OSCARS_E_INVALID;
+  set_backward_mode(mode);
   return OSCARS_OK;
 }
 

@@ -164,6 +164,58 @@ def test_every_tiling_gives_identical_results(P, cfg):
         P.set_gemm_tiling(len(P.TILINGS))
 
 
+BACKWARD_CFGS = [
+    # output features of 2056 and 1032: three and two chunks of 1024 (the last
+    # ragged), input strips ragged (1032 = 16 x 64 + 8, 200), 37 classes;
+    # batch 256 (split partials available for up to 4 replicas)
+    workload.Config("bwd-wide", (136, 1032, 2056, 200, 37), workload.BF16, K=4, n_rows=2000,
+                    batch=256, tau_rule="given", tau_given=(3, 1, 2, 4), lr=0.05, rounds=1,
+                    seed=16),
+    # batch 40 (not a multiple of 32), one worker idle
+    workload.Config("bwd-b40", (72, 1040, 1032, 10), workload.BF16, K=3, n_rows=600, batch=40,
+                    tau_rule="given", tau_given=(2, 0, 3), lr=0.1, rounds=1, seed=17),
+    # batch 128 (two dgrad waves idle) and batch 1
+    workload.Config("bwd-b128", (256, 2056, 136, 10), workload.BF16, K=2, n_rows=700, batch=128,
+                    tau_rule="given", tau_given=(2, 1), lr=0.05, rounds=1, seed=18),
+    workload.Config("bwd-b1", (64, 264, 72, 5), workload.BF16, K=2, n_rows=50, batch=1,
+                    tau_rule="given", tau_given=(1, 3), lr=0.2, rounds=1, seed=19),
+]
+
+
+@pytest.mark.parametrize("cfg", BACKWARD_CFGS, ids=[c.name for c in BACKWARD_CFGS])
+def test_backward_modes_identical(P, cfg):
+    """The fused backward of hidden bf16 layers (backward-data, backward-weight
+    and update in one launch; unsplit or split over chunks of output
+    features) gives the replicas of the separate launches bit for bit, over
+    local steps that start from the replicas and from a global model."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    say(f"backward modes {cfg.name} dims={cfg.dims} B={cfg.batch} tau={cfg.tau_given}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = [int(t) for t in cfg.tau_given]
+    results = {}
+    try:
+        for name, mode in P.BACKWARDS.items():
+            P.set_backward(mode)
+            run = OscarsRun(cfg, ds, init)
+            run.round(tau)           # first step from the global model
+            run.local_steps(tau)     # then from the replicas
+            torch.cuda.synchronize()
+            results[name] = (run.replicas.cpu().numpy().copy(), run.g.cpu().numpy().copy())
+            run.close()
+            say(f"  backward {name} done")
+    finally:
+        P.set_backward(P.BACKWARD_AUTO)
+    ref_r, ref_g = results["separate"]
+    assert np.isfinite(ref_r).all()
+    for name, (r, g) in results.items():
+        assert np.array_equal(r.view(np.uint32), ref_r.view(np.uint32)), name
+        assert np.array_equal(g.view(np.uint32), ref_g.view(np.uint32)), name
+    with pytest.raises(P.OscarsError):
+        P.set_backward(len(P.BACKWARDS))
+
+
 @pytest.mark.parametrize("dtype", [workload.BF16, workload.FP32])
 def test_round_equals_local_steps_plus_aggregate(P, dtype):
     """oscars_round == (copy global into every replica, oscars_local_steps,
