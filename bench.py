@@ -35,14 +35,20 @@ def gemm_work(cfg, tau):
     """Algorithmic FLOPs and bytes of every launch of one round (oscars_round),
     per kind.  Bytes: each operand read once, each result written once (weights
     bf16 in the products of bf16 workloads; fp32 master read and write in the
-    update; the start model cast to bf16 once; the average reads K replicas and
-    writes the global model)."""
+    update, and the bf16 copy for workers that take another step; the start
+    model cast to bf16 once; the average reads K replicas and writes the
+    global model).  Hidden layers of bf16 models take the fused backward
+    (backward-data + backward-weight + update in one launch, batches up to
+    256): its products are both passes, its bytes the update's plus the
+    delta written for the layer below."""
     import numpy as np
     es = 2 if cfg.dtype == "bf16" else 4
     B, dims = cfg.batch, cfg.dims
     L = len(dims) - 1
+    fused = cfg.dtype == "bf16" and B <= 256
     work = {"gemm_fwd": [0.0, 0.0], "gemm_dgrad": [0.0, 0.0], "gemm_wgrad_update": [0.0, 0.0],
-            "softmax_ce": [0.0, 0.0], "cast_bf16": [0.0, 0.0], "aggregate": [0.0, 0.0]}
+            "gemm_bwd_fused": [0.0, 0.0], "softmax_ce": [0.0, 0.0], "cast_bf16": [0.0, 0.0],
+            "aggregate": [0.0, 0.0]}
     tau = np.asarray(tau)
     n_params = sum(o * i + o for i, o in zip(dims[:-1], dims[1:]))
     if cfg.dtype == "bf16":
@@ -50,17 +56,23 @@ def gemm_work(cfg, tau):
     work["aggregate"][1] += (cfg.K + 1) * n_params * 4.0
     for j in range(int(tau.max())):
         ns = int((tau > j).sum())
+        ns_next = int((tau > j + 1).sum())  # workers whose bf16 copy is refreshed
         for l in range(1, L + 1):
             i, o = dims[l - 1], dims[l]
             out_es = es if l < L else 4
             work["gemm_fwd"][0] += ns * 2.0 * B * o * i
             work["gemm_fwd"][1] += ns * (es * o * i + 4 * o + es * B * i + out_es * B * o)
+            update = (ns * (8.0 * (o * i + o) + es * B * o + es * B * i)
+                      + (ns_next * 2.0 * o * i if es == 2 else 0.0))
+            if l > 1 and fused:
+                work["gemm_bwd_fused"][0] += ns * 4.0 * B * o * i
+                work["gemm_bwd_fused"][1] += update + ns * es * B * i
+                continue
             if l > 1:
                 work["gemm_dgrad"][0] += ns * 2.0 * B * o * i
                 work["gemm_dgrad"][1] += ns * (es * o * i + es * B * o + 2 * es * B * i)
             work["gemm_wgrad_update"][0] += ns * 2.0 * B * o * i
-            work["gemm_wgrad_update"][1] += ns * (8.0 * (o * i + o) + (2.0 * o * i if es == 2 else 0)
-                                                  + es * B * o + es * B * i)
+            work["gemm_wgrad_update"][1] += update
         C = dims[-1]
         work["softmax_ce"][1] += ns * B * (4 * C + es * C)
     return work
@@ -300,7 +312,7 @@ def main():
         return draws[step % len(draws)].tolist()
 
     kinds = [P.KERNEL_CAST, P.KERNEL_FWD, P.KERNEL_SOFTMAX, P.KERNEL_DGRAD, P.KERNEL_WGRAD,
-             P.KERNEL_AGGREGATE]
+             P.KERNEL_AGGREGATE, P.KERNEL_BWD_FUSED]
     # Warmup rounds carry HIP events around every launch: the per-kernel
     # breakdown, and which kernel dominates.  The timed rounds carry events
     # around the dominant kernel's launches only (events around every launch

@@ -1121,8 +1121,8 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
 //
 // Two roles of four waves each, one barrier per chunk step:
 //   stream waves (0-3) at step t stage chunk t + 1 into LDS (delta, and Wq
-//     rounded from the master rows), issue the loads of chunk t + 2 (delta)
-//     and t + 3 (master), and apply dW of chunk t - 1 to its master rows;
+//     rounded from the master rows), issue the loads of chunk t + 3 (delta)
+//     and t + 4 (master), and apply dW of chunk t - 1 to its master rows;
 //   math waves (4-7) at step t run the MFMA products of chunk t and leave dW
 //     in LDS.
 // Every SIMD holds one wave of each role, so the update's vector work and
@@ -1139,8 +1139,9 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
 // the separate kernel stops at the batch rounded up to 32; the extra zero
 // products can only turn a dW of -0 into +0, which changes the updated
 // weight only when that weight is -0 itself.
-// SPLIT: a workgroup covers one KCHUNK range of o and stores its
-// backward-data sum as that chunk's partial; splitk_reduce_kernel finishes.
+// SPLIT: a workgroup covers `cps` KCHUNK ranges of o and stores the
+// backward-data sum of each as that chunk's partial; splitk_reduce_kernel
+// finishes.
 //
 // LDS (144 KB): two delta chunks [256 b][64 o] bf16, two Wq chunks
 // [64 o][64 i] bf16 and the activation strip [256 b][64 i] bf16 (128-byte
@@ -1148,7 +1149,7 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
 // most 256 rows (FB_BMAX); backward-weight sums 128 or 256 rows (NKS K16
 // steps), zero from row B on.
 constexpr int FB_TI = 64, FB_TO = 64, FB_NT = 512, FB_BMAX = 256;
-constexpr int FB_NB = 5;  // master chunks a stream thread holds: t - 1 .. t + 3
+constexpr int FB_NB = 6;  // master chunks a stream thread holds: t - 1 .. t + 4
 static_assert(KCHUNK % FB_TO == 0, "chunks of whole o tiles");
 
 // 128-byte-row tiles read both plainly (one 16-byte chunk of 16 consecutive
@@ -1192,7 +1193,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32
 }
 
 template <bool SPLIT, int NKS>
-__global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int strips, int nsplit) {
+__global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int strips, int nsplit,
+                                                             int cps) {
   __shared__ __attribute__((aligned(16))) char smem[144 * 1024 + 2048];
   float* const bpart = reinterpret_cast<float*>(smem + 147456);  // bias block sums [2][4][64]
   auto dbuf = [&](int t) { return smem + (t & 1) * 32768; };                    // delta chunk
@@ -1209,8 +1211,8 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
   const int i0 = strip * FB_TI;
   const int nt_all = (O + FB_TO - 1) / FB_TO;
   constexpr int TPC = KCHUNK / FB_TO;
-  const int tbeg = SPLIT ? split * TPC : 0;
-  const int tend = SPLIT ? (nt_all < tbeg + TPC ? nt_all : tbeg + TPC) : nt_all;
+  const int tbeg = SPLIT ? split * cps * TPC : 0;
+  const int tend = SPLIT ? (nt_all < tbeg + cps * TPC ? nt_all : tbeg + cps * TPC) : nt_all;
   // steps t = tbeg - 1 .. tend (stream: stage t + 1, update t - 1), padded
   // to whole groups of FB_NB for the stream waves' register rotation
   const int nsteps = (tend - tbeg + 2 + FB_NB - 1) / FB_NB * FB_NB;
@@ -1270,28 +1272,35 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     };
     // Delta chunk t: rows (ts >> 3) + 32 p < 16 NKS, 16-byte chunk ts & 7;
     // zeros beyond the batch and past the workgroup's chunks.
-    u32x4 dreg[NKS / 2];
-    auto load_delta = [&](int t) {
+    // Delta chunk x sits in dreg[(x - tbeg + 1) & 1], master chunk x in
+    // mreg[(x - tbeg + 1) % FB_NB].  A load is waited for only by the step
+    // that needs it, and memory operations complete in order, so each wait
+    // for delta also covers the master rows issued before it: delta three
+    // chunks ahead keeps the master loads (four ahead) three steps in flight.
+    u32x4 dreg[2][NKS / 2];
+    auto load_delta = [&](int t, u32x4 (&dr)[NKS / 2]) {
 #pragma unroll
       for (int p = 0; p < NKS / 2; ++p) {
         const int row = (ts >> 3) + 32 * p;
         const uint32_t off =
             t < tend ? static_cast<uint32_t>(row * g.b_ld + t * FB_TO + 8 * (ts & 7)) * 2 : kOob;
-        dreg[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r_delta, off, 0, 0));
+        dr[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r_delta, off, 0, 0));
       }
     };
 
     f32x4 mreg[FB_NB][4];
-    load_delta(tbeg);
+    load_delta(tbeg, dreg[1]);
+    load_delta(tbeg + 1, dreg[0]);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) mreg[1][p] = master_chunk(tbeg, p);
+    for (int d = 0; d < 3; ++d)
 #pragma unroll
-    for (int p = 0; p < 4; ++p) mreg[2][p] = master_chunk(tbeg + 1, p);
+      for (int p = 0; p < 4; ++p) mreg[1 + d][p] = master_chunk(tbeg + d, p);
 
-    // step t = tbeg - 1 + u; master chunk x sits in mreg[(x - tbeg + 1) % FB_NB]
+    // step t = tbeg - 1 + u
     auto step = [&](int t, auto uc) {
       constexpr int u = decltype(uc)::value;
-      constexpr int b_next = (u + 1) % FB_NB, b_ahead = (u + 3) % FB_NB, b_prev = (u + FB_NB - 1) % FB_NB;
+      constexpr int b_next = (u + 1) % FB_NB, b_ahead = (u + 4) % FB_NB, b_prev = (u + FB_NB - 1) % FB_NB;
+      constexpr int d_next = (u + 1) & 1;  // delta of chunks t + 1 and t + 3
       // bias of chunk t - 1 (its owner's wave 0; out of range elsewhere)
       const uint32_t boff = ts < FB_TO && t > tbeg && bias_own(t - 1)
                                 ? static_cast<uint32_t>((t - 1 - tbeg) * FB_TO + ts) * 4
@@ -1301,7 +1310,7 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
       char* const dt = dbuf(t + 1);
 #pragma unroll
       for (int p = 0; p < NKS / 2; ++p)
-        *reinterpret_cast<u32x4*>(dt + t128((ts >> 3) + 32 * p, ts & 7)) = dreg[p];
+        *reinterpret_cast<u32x4*>(dt + t128((ts >> 3) + 32 * p, ts & 7)) = dreg[d_next][p];
       char* const wq = wbuf(t + 1);
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
@@ -1311,10 +1320,10 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
         q[1] = f2bf(m[2]) | (f2bf(m[3]) << 16);
         *reinterpret_cast<u32x2*>(wq + t128(mrow + 16 * p, mc >> 1) + 8 * (mc & 1)) = q;
       }
-      // loads: delta of chunk t + 2, master of chunk t + 3
-      load_delta(t + 2);
+      // loads: delta of chunk t + 3, master of chunk t + 4
+      load_delta(t + 3, dreg[d_next]);
 #pragma unroll
-      for (int p = 0; p < 4; ++p) mreg[b_ahead][p] = master_chunk(t + 3, p);
+      for (int p = 0; p < 4; ++p) mreg[b_ahead][p] = master_chunk(t + 4, p);
       // update of chunk t - 1 with its dW (rows outside [tbeg, tend) are out
       // of range)
       const float* dws = wdbuf(t - 1);
@@ -1366,6 +1375,7 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
       step(t + 2, Ic<2>());
       step(t + 3, Ic<3>());
       step(t + 4, Ic<4>());
+      step(t + 5, Ic<5>());
     }
     return;
   }
@@ -1417,23 +1427,46 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
         *reinterpret_cast<f32x4*>(dws + o * 64 + ((c ^ (o & 15)) << 2)) =
             f32x4{accw[4 * q], accw[4 * q + 1], accw[4 * q + 2], accw[4 * q + 3]};
       }
-      // end of a KCHUNK range of o: chunk sums left to right
-      if (!SPLIT && ((t + 1) % TPC == 0 || t + 1 == tend)) {
-        const bool first = t < TPC;
+      // end of a KCHUNK range of o: chunk sums left to right, or (SPLIT) the
+      // chunk's partial
+      if ((t + 1) % TPC == 0 || t + 1 == tend) {
+        if constexpr (SPLIT) {
+          if (dgrad_wave) {
+            float* part = g.part + z * g.part_slot + static_cast<int64_t>(t / TPC) * B * g.out_ld;
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+              for (int j = 0; j < 2; ++j) {
+                const int b = 64 * wb + 32 * j + (lane & 31);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                  const int i = i0 + 32 * a + 8 * q + 4 * h;
+                  if (b < B && i < I)
+                    *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(b) * g.out_ld + i) =
+                        f32x4{accd[a][j][4 * q], accd[a][j][4 * q + 1], accd[a][j][4 * q + 2],
+                              accd[a][j][4 * q + 3]};
+                }
+              }
+          }
+        } else {
+          const bool first = t < TPC;
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) tot[a][j] = first ? accd[a][j] : tot[a][j] + accd[a][j];
+        }
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            tot[a][j] = first ? accd[a][j] : tot[a][j] + accd[a][j];
+          for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) accd[a][j][r] = 0.0f;
-          }
       }
     }
     __syncthreads();
   }
 
-  if (!dgrad_wave) return;
+  if (SPLIT || !dgrad_wave) return;
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -1444,18 +1477,10 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
       for (int q = 0; q < 4; ++q) {
         const int i = i0 + 32 * a + 8 * q + 4 * h;
         if (i >= I) continue;  // I is a multiple of 8: whole groups of four
-        if constexpr (SPLIT) {
-          // the workgroup's one chunk, as that chunk's partial
-          float* part = g.part + z * g.part_slot + static_cast<int64_t>(split) * B * g.out_ld;
-          *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(b) * g.out_ld + i) =
-              f32x4{accd[a][j][4 * q], accd[a][j][4 * q + 1], accd[a][j][4 * q + 2],
-                    accd[a][j][4 * q + 3]};
-        } else {
-          store_out<true, GEMM_DGRAD>(g, z, b, i, 4,
-                                      f32x4{tot[a][j][4 * q], tot[a][j][4 * q + 1],
-                                            tot[a][j][4 * q + 2], tot[a][j][4 * q + 3]},
-                                      nullptr);
-        }
+        store_out<true, GEMM_DGRAD>(g, z, b, i, 4,
+                                    f32x4{tot[a][j][4 * q], tot[a][j][4 * q + 1],
+                                          tot[a][j][4 * q + 2], tot[a][j][4 * q + 3]},
+                                    nullptr);
       }
     }
 }
@@ -1853,8 +1878,12 @@ bool backward_fused_enabled() { return g_backward_mode.load() != BACKWARD_SEPARA
 
 // Grid x = slots x strips x splits, slot slowest, strip fastest: with the
 // XCD-aware order the strips of one slot (which read the same delta) share
-// an XCD and its L2.  Without a forced mode the o range is split into its
-// KCHUNK ranges when the strips alone leave CUs idle.
+// an XCD and its L2.  A workgroup covers `cps` chunks of KCHUNK output
+// features (all of them: no split).  Without a forced mode cps (all chunks,
+// or ..., 4, 2, 1) is the one whose workgroups fill their last pass over the
+// CUs best, the largest on ties (a split costs partial traffic and a
+// reduce); measured on MI355X against the other choices at 1 to 8 replicas
+// of 4096 x 4096 layers.
 hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s) {
   if (!backward_fusable(g_in) || n_slots < 1) return hipErrorInvalidValue;
   GemmArgs g = g_in;
@@ -1863,21 +1892,35 @@ hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s) {
   g.part_slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
   const bool can_split = nchunks > 1 && g.part && g.part_slot * n_slots <= g.part_cap;
   const int mode = g_backward_mode.load();
-  const bool split = can_split && (mode == BACKWARD_FUSED_SPLIT ||
-                                   (mode == BACKWARD_AUTO &&
-                                    static_cast<int64_t>(n_slots) * strips < device_cu_count()));
-  const int nsplit = split ? nchunks : 1;
+  int cps = nchunks;
+  if (can_split && mode == BACKWARD_FUSED_SPLIT) {
+    cps = 1;
+  } else if (can_split && mode == BACKWARD_AUTO) {
+    const int64_t cus = device_cu_count();
+    double best = -1.0;
+    for (int c = nchunks;; c = (c + 1) / 2) {
+      const int64_t wgs = static_cast<int64_t>(n_slots) * strips * ((nchunks + c - 1) / c);
+      const double fill = static_cast<double>(wgs) / static_cast<double>((wgs + cus - 1) / cus * cus);
+      if (fill > best + 1e-9) {
+        best = fill;
+        cps = c;
+      }
+      if (c == 1) break;
+    }
+  }
+  const bool split = cps < nchunks;
+  const int nsplit = (nchunks + cps - 1) / cps;
   const int64_t gx = static_cast<int64_t>(n_slots) * strips * nsplit;
   if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(gx)), block(FB_NT);
   const bool b256 = g.N > 128;  // batch rows summed by backward-weight: 256 or 128
   if (!split) {
-    if (b256) hipLaunchKernelGGL((bwd_fused_kernel<false, 16>), grid, block, 0, s, g, strips, 1);
-    else hipLaunchKernelGGL((bwd_fused_kernel<false, 8>), grid, block, 0, s, g, strips, 1);
+    if (b256) hipLaunchKernelGGL((bwd_fused_kernel<false, 16>), grid, block, 0, s, g, strips, 1, cps);
+    else hipLaunchKernelGGL((bwd_fused_kernel<false, 8>), grid, block, 0, s, g, strips, 1, cps);
     return hipGetLastError();
   }
-  if (b256) hipLaunchKernelGGL((bwd_fused_kernel<true, 16>), grid, block, 0, s, g, strips, nsplit);
-  else hipLaunchKernelGGL((bwd_fused_kernel<true, 8>), grid, block, 0, s, g, strips, nsplit);
+  if (b256) hipLaunchKernelGGL((bwd_fused_kernel<true, 16>), grid, block, 0, s, g, strips, nsplit, cps);
+  else hipLaunchKernelGGL((bwd_fused_kernel<true, 8>), grid, block, 0, s, g, strips, nsplit, cps);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t work = static_cast<int64_t>(g.N) * ((g.M + 3) / 4);

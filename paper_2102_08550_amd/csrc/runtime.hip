@@ -189,11 +189,12 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
     e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(c->L) * 4, &p);
     c->logits = static_cast<float*>(p);
   }
-  // Split-K partials ([slot][chunk][batch][ld] fp32) for launches with up to
-  // kSplitSlots active replicas; the kernels split only whole-batch tiles
-  // (batches above 128) whose K has more than one chunk.
+  // Split-K partials ([slot][chunk][batch][ld] fp32) for launches of every
+  // active replica; the kernels split only whole-batch tiles (batches above
+  // 128) whose K has more than one chunk.
   if (e == hipSuccess && max_batch > 128) {
-    constexpr int64_t kChunk = GEMM_KCHUNK, kSplitSlots = 4;
+    constexpr int64_t kChunk = GEMM_KCHUNK;
+    const int64_t kSplitSlots = K;
     int64_t need = 0;
     for (int l = 1; l <= c->L; ++l) {
       const int64_t fwd = (c->dims[l - 1] + kChunk - 1) / kChunk;

@@ -179,6 +179,11 @@ BACKWARD_CFGS = [
                     tau_rule="given", tau_given=(2, 1), lr=0.05, rounds=1, seed=18),
     workload.Config("bwd-b1", (64, 264, 72, 5), workload.BF16, K=2, n_rows=50, batch=1,
                     tau_rule="given", tau_given=(1, 3), lr=0.2, rounds=1, seed=19),
+    # a 4096 x 4096 hidden layer at 6 and 2 active replicas: the automatic
+    # choice gives each workgroup two of the four chunks of output features
+    workload.Config("bwd-4096", (256, 4096, 4096, 10), workload.BF16, K=6, n_rows=1600,
+                    batch=256, tau_rule="given", tau_given=(2, 1, 1, 2, 1, 1), lr=0.05, rounds=1,
+                    seed=20),
 ]
 
 
