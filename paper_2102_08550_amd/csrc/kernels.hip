@@ -1217,6 +1217,8 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
   // to whole groups of FB_NB for the stream waves' register rotation
   const int nsteps = (tend - tbeg + 2 + FB_NB - 1) / FB_NB * FB_NB;
   const int Bp = (B + 31) & ~31;  // batch rows of the bias sum; rows B .. Bp - 1 are zero
+  // The bias of chunk t belongs to the strip t % strips (spread evenly).
+  auto bias_own = [&](int t) { return t % strips == strip; };
   const int nblk = (Bp + 63) / 64;  // 64-row blocks of the bias sum
   static_assert(NKS == 8 || NKS == 16, "batch rows 128 or 256");
 
@@ -1251,27 +1253,46 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     const __amdgpu_buffer_rsrc_t r_copy =
         buf_rsrc(refresh ? static_cast<const void*>(g.wcopy + z * g.wcopy_slot + wbase) : mw,
                  refresh ? wbytes / 2 : 0u);
-    // The bias of chunk t belongs to the strip t % strips (spread evenly).
-    auto bias_own = [&](int t) { return t % strips == strip; };
-    const uint32_t bbytes = static_cast<uint32_t>(obound - row0) * 4;
-    const __amdgpu_buffer_rsrc_t r_bin = buf_rsrc(mw_in + g.b_off + row0, bbytes);
-    const __amdgpu_buffer_rsrc_t r_bout = buf_rsrc(mw + g.b_off + row0, bbytes);
     const uint16_t* dl = static_cast<const uint16_t*>(g.b) + z * g.b_slot;
     const __amdgpu_buffer_rsrc_t r_delta = buf_rsrc(dl, static_cast<uint32_t>(B) * g.b_ld * 2);
 
-    // Master chunk t: thread rows (ts >> 4) + 16 p of the chunk, columns
-    // i0 + 4 (ts & 15) .. + 3 (16 lanes read one 256-byte row segment).
-    const int mrow = ts >> 4, mc = ts & 15;
-    const bool col_ok = i0 + 4 * mc < I;
-    auto woff = [&](int t, int p, int es) -> uint32_t {
-      return col_ok ? static_cast<uint32_t>(((t - tbeg) * FB_TO + mrow + 16 * p) * I + i0 + 4 * mc) * es
-                    : kOob;
+    // Byte offsets are a per-thread base (set once) plus a uniform per-chunk
+    // term.  A thread outside the strip's columns gets the base 0xC0000000,
+    // which no chunk term (|term| < 2^30, W_l under 1 GiB) brings into range;
+    // a chunk before tbeg gives a negative term, out of range as unsigned.
+    // No memory operation of the loop sits under a branch, so the compiler's
+    // counter waits follow the issue order exactly; the bias, which only one
+    // strip per chunk updates, is left to a math wave.
+    // Master chunk t: thread rows (ts >> 3) + 32 p of the chunk, columns
+    // i0 + 8 (ts & 7) .. + 7 (two 16-byte pieces h; 8 lanes cover one
+    // 256-byte row segment), so the bf16 copy is written 16 bytes at a time.
+    const int mrow = ts >> 3, m8 = ts & 7;
+    const bool col_ok = i0 + 8 * m8 < I;  // I is a multiple of 8: whole octets
+    constexpr uint32_t kFar = 0xC0000000u;
+    uint32_t wbase4[2], wbase2[2];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const uint32_t e = static_cast<uint32_t>((mrow + 32 * p) * I + i0 + 8 * m8);
+      wbase4[p] = col_ok ? 4 * e : kFar;
+      wbase2[p] = col_ok ? 2 * e : kFar;
+    }
+    const uint32_t chunk4 = static_cast<uint32_t>(FB_TO * I * 4);  // bytes of 64 fp32 rows
+    auto wterm = [&](int t, uint32_t chunk_bytes) {
+      return static_cast<uint32_t>(t - tbeg) * chunk_bytes;
     };
-    auto master_chunk = [&](int t, int p) {
-      return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r_win, woff(t, p, 4), 0, 2));
+    // piece q = 2 p + h: row mrow + 32 p, columns 8 m8 + 4 h .. + 3
+    auto master_chunk = [&](int t, int q) {
+      return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           r_win, wbase4[q >> 1] + 16 * (q & 1) + wterm(t, chunk4),
+                                           0, 2));
     };
     // Delta chunk t: rows (ts >> 3) + 32 p < 16 NKS, 16-byte chunk ts & 7;
-    // zeros beyond the batch and past the workgroup's chunks.
+    // zeros beyond the batch (rows out of range) and past the workgroup's
+    // chunks (term out of range).
+    uint32_t dbase[NKS / 2];
+#pragma unroll
+    for (int p = 0; p < NKS / 2; ++p)
+      dbase[p] = static_cast<uint32_t>(((ts >> 3) + 32 * p) * g.b_ld + 8 * (ts & 7)) * 2;
     // Delta chunk x sits in dreg[(x - tbeg + 1) & 1], master chunk x in
     // mreg[(x - tbeg + 1) % FB_NB].  A load is waited for only by the step
     // that needs it, and memory operations complete in order, so each wait
@@ -1279,13 +1300,11 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     // chunks ahead keeps the master loads (four ahead) three steps in flight.
     u32x4 dreg[2][NKS / 2];
     auto load_delta = [&](int t, u32x4 (&dr)[NKS / 2]) {
+      const uint32_t term = t < tend ? static_cast<uint32_t>(t) * (FB_TO * 2) : 0x80000000u;
 #pragma unroll
-      for (int p = 0; p < NKS / 2; ++p) {
-        const int row = (ts >> 3) + 32 * p;
-        const uint32_t off =
-            t < tend ? static_cast<uint32_t>(row * g.b_ld + t * FB_TO + 8 * (ts & 7)) * 2 : kOob;
-        dr[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r_delta, off, 0, 0));
-      }
+      for (int p = 0; p < NKS / 2; ++p)
+        dr[p] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(r_delta, dbase[p] + term, 0, 0));
     };
 
     f32x4 mreg[FB_NB][4];
@@ -1294,18 +1313,13 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
 #pragma unroll
     for (int d = 0; d < 3; ++d)
 #pragma unroll
-      for (int p = 0; p < 4; ++p) mreg[1 + d][p] = master_chunk(tbeg + d, p);
+      for (int q = 0; q < 4; ++q) mreg[1 + d][q] = master_chunk(tbeg + d, q);
 
     // step t = tbeg - 1 + u
     auto step = [&](int t, auto uc) {
       constexpr int u = decltype(uc)::value;
       constexpr int b_next = (u + 1) % FB_NB, b_ahead = (u + 4) % FB_NB, b_prev = (u + FB_NB - 1) % FB_NB;
       constexpr int d_next = (u + 1) & 1;  // delta of chunks t + 1 and t + 3
-      // bias of chunk t - 1 (its owner's wave 0; out of range elsewhere)
-      const uint32_t boff = ts < FB_TO && t > tbeg && bias_own(t - 1)
-                                ? static_cast<uint32_t>((t - 1 - tbeg) * FB_TO + ts) * 4
-                                : kOob;
-      const float bias_in = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r_bin, boff, 0, 0));
       // stage chunk t + 1: delta, and Wq rounded from the master rows
       char* const dt = dbuf(t + 1);
 #pragma unroll
@@ -1313,36 +1327,43 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
         *reinterpret_cast<u32x4*>(dt + t128((ts >> 3) + 32 * p, ts & 7)) = dreg[d_next][p];
       char* const wq = wbuf(t + 1);
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const f32x4 m = mreg[b_next][p];
-        u32x2 q;
-        q[0] = f2bf(m[0]) | (f2bf(m[1]) << 16);
-        q[1] = f2bf(m[2]) | (f2bf(m[3]) << 16);
-        *reinterpret_cast<u32x2*>(wq + t128(mrow + 16 * p, mc >> 1) + 8 * (mc & 1)) = q;
+      for (int p = 0; p < 2; ++p) {
+        const f32x4 lo = mreg[b_next][2 * p], hi = mreg[b_next][2 * p + 1];
+        u32x4 q;
+        q[0] = f2bf(lo[0]) | (f2bf(lo[1]) << 16);
+        q[1] = f2bf(lo[2]) | (f2bf(lo[3]) << 16);
+        q[2] = f2bf(hi[0]) | (f2bf(hi[1]) << 16);
+        q[3] = f2bf(hi[2]) | (f2bf(hi[3]) << 16);
+        *reinterpret_cast<u32x4*>(wq + t128(mrow + 32 * p, m8)) = q;
       }
       // loads: delta of chunk t + 3, master of chunk t + 4
       load_delta(t + 3, dreg[d_next]);
 #pragma unroll
-      for (int p = 0; p < 4; ++p) mreg[b_ahead][p] = master_chunk(t + 4, p);
+      for (int q = 0; q < 4; ++q) mreg[b_ahead][q] = master_chunk(t + 4, q);
       // update of chunk t - 1 with its dW (rows outside [tbeg, tend) are out
       // of range)
       const float* dws = wdbuf(t - 1);
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int r = mrow + 16 * p;
-        const f32x4 d = *reinterpret_cast<const f32x4*>(dws + r * 64 + ((mc ^ (r & 15)) << 2));
-        f32x4 wv = mreg[b_prev][p];
-        for (int e = 0; e < 4; ++e) wv[e] = fmaf(-g.lr, d[e], wv[e]);
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, wv), r_wout, woff(t - 1, p, 4), 0, 2);
-        u32x2 q;
-        q[0] = f2bf(wv[0]) | (f2bf(wv[1]) << 16);
-        q[1] = f2bf(wv[2]) | (f2bf(wv[3]) << 16);
-        __builtin_amdgcn_raw_buffer_store_b64(q, r_copy, woff(t - 1, p, 2), 0, 2);
+      for (int p = 0; p < 2; ++p) {
+        const int r = mrow + 32 * p;
+        u32x4 cq;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c = 2 * m8 + h;
+          const f32x4 d = *reinterpret_cast<const f32x4*>(dws + r * 64 + ((c ^ (r & 15)) << 2));
+          f32x4 wv = mreg[b_prev][2 * p + h];
+          for (int e = 0; e < 4; ++e) wv[e] = fmaf(-g.lr, d[e], wv[e]);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, wv), r_wout,
+                                                 wbase4[p] + 16 * h + wterm(t - 1, chunk4), 0, 2);
+          cq[2 * h] = f2bf(wv[0]) | (f2bf(wv[1]) << 16);
+          cq[2 * h + 1] = f2bf(wv[2]) | (f2bf(wv[3]) << 16);
+        }
+        __builtin_amdgcn_raw_buffer_store_b128(cq, r_copy, wbase2[p] + wterm(t - 1, chunk4 / 2), 0, 2);
       }
       // bias: db[o] = sum_b delta[b][o] in blocks of 64 batch rows, each row
       // by row, block sums left to right.  Stream wave w sums block w of
       // chunk t (column = lane, four rows per transposing read; lane 16 g + j
-      // receives column 16 g + j); wave 0 adds the blocks of chunk t - 1.
+      // receives column 16 g + j); a math wave adds the blocks one step later.
       if (t >= tbeg && t < tend && bias_own(t)) {
         const char* dtt = dbuf(t);
         const int gq = lane >> 4, a = lane & 3, e = (lane >> 2) & 3;
@@ -1358,14 +1379,6 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
         }
         bpart[(t & 1) * 256 + 64 * w + lane] = part;
       }
-      float dbias = 0.0f;
-      if (w == 0 && t > tbeg && t <= tend && bias_own(t - 1)) {
-        const float* bp = bpart + ((t - 1) & 1) * 256;
-        dbias = bp[lane];
-        for (int blk = 1; blk < nblk; ++blk) dbias += bp[64 * blk + lane];
-      }
-      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, fmaf(-g.lr, dbias, bias_in)),
-                                            r_bout, boff, 0, 0);
       __syncthreads();
     };
     for (int u0 = 0; u0 < nsteps; u0 += FB_NB) {
@@ -1390,8 +1403,24 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
 #pragma unroll
       for (int r = 0; r < 16; ++r) accd[a][b][r] = tot[a][b][r] = 0.0f;
   const bool dgrad_wave = 64 * wb < B;
+  // Bias update by math wave 4 (lane = row of the chunk): the input of chunk
+  // t is loaded at step t, the block sums of chunk t - 1 are added at step t.
+  const float* b_in = g.master_in + static_cast<int64_t>(g.order[z]) * g.master_in_slot + g.b_off;
+  float* b_out = g.master + static_cast<int64_t>(g.order[z]) * g.master_slot + g.b_off;
+  float bias_next = 0.0f;
   for (int u = 0; u < nsteps; ++u) {
     const int t = tbeg - 1 + u;
+    if (wb == 0) {
+      const float bias_cur = bias_next;
+      if (t >= tbeg && t < tend && bias_own(t) && t * FB_TO + lane < O)
+        bias_next = b_in[t * FB_TO + lane];
+      if (t > tbeg && t <= tend && bias_own(t - 1) && (t - 1) * FB_TO + lane < O) {
+        const float* bp = bpart + ((t - 1) & 1) * 256;
+        float dbias = bp[lane];
+        for (int blk = 1; blk < nblk; ++blk) dbias += bp[64 * blk + lane];
+        b_out[(t - 1) * FB_TO + lane] = fmaf(-g.lr, dbias, bias_cur);
+      }
+    }
     if (t >= tbeg && t < tend) {
       const char* dt = dbuf(t);
       const char* wq = wbuf(t);
@@ -1867,11 +1896,12 @@ std::atomic<int> g_backward_mode{BACKWARD_AUTO};
 
 void set_backward_mode(int mode) { g_backward_mode.store(mode); }
 
-// Batches of at most FB_BMAX rows, whole 16-byte input chunks, and W_l small
-// enough for 32-bit buffer offsets (with the three chunks read ahead).
+// Batches of at most FB_BMAX rows, whole 16-byte input chunks, and W_l (with
+// the chunks read ahead) under 1 GiB, so that 32-bit buffer offsets with an
+// out-of-range base never wrap into range.
 bool backward_fusable(const GemmArgs& g) {
   return g.N >= 1 && g.N <= FB_BMAX && g.M % 8 == 0 &&
-         static_cast<int64_t>(g.K) * g.M * 4 <= (static_cast<int64_t>(1) << 31);
+         static_cast<int64_t>(g.K + 6 * FB_TO) * g.M * 4 < (static_cast<int64_t>(1) << 30);
 }
 
 bool backward_fused_enabled() { return g_backward_mode.load() != BACKWARD_SEPARATE; }
