@@ -1532,32 +1532,65 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, int nchu
   store_out<BF16, MODE>(g, z, n, m, cnt, v, master_in);
 }
 
-template <bool BF16_OUT>
-__global__ __launch_bounds__(64) void softmax_ce_kernel(const float* logits, int64_t ld,
-                                                        int64_t slot_stride, int C, int B,
-                                                        const int32_t* y, const int32_t* gather,
-                                                        int64_t gather_slot, void* delta,
-                                                        float* loss, int64_t loss_slot,
-                                                        int32_t* correct) {
-  const int b = blockIdx.x, z = blockIdx.y, lane = threadIdx.x;
+// One wave per batch row.  NV > 0: the row's C <= 64 NV logits are loaded
+// into registers at once (lane l holds columns l, l + 64, ...); NV = 0: any
+// C, column loop.  Both sum the exponentials in the same order: each lane
+// over its columns left to right, then a butterfly over the lanes.
+template <bool BF16_OUT, int NV>
+__global__ __launch_bounds__(256) void softmax_ce_kernel(const float* logits, int64_t ld,
+                                                         int64_t slot_stride, int C, int B,
+                                                         const int32_t* y, const int32_t* gather,
+                                                         int64_t gather_slot, void* delta,
+                                                         float* loss, int64_t loss_slot,
+                                                         int32_t* correct) {
+  const int lane = threadIdx.x & 63, z = blockIdx.y;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= B) return;
   const float* row = logits + z * slot_stride + static_cast<int64_t>(b) * ld;
   const int label = y[gather[z * gather_slot + b]];
   const bool label_ok = label >= 0 && label < C;
-  float mx = -INFINITY;
-  for (int c = lane; c < C; c += 64) mx = fmaxf(mx, row[c]);
-  for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
-  float s = 0.0f;
-  for (int c = lane; c < C; c += 64) s += expf(row[c] - mx);
-  for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d);
   const float invB = 1.0f / static_cast<float>(B);
   const int64_t base = z * slot_stride + static_cast<int64_t>(b) * ld;
-  for (int c = lane; c < ld; c += 64) {
-    float dv = 0.0f;
-    if (c < C) dv = (expf(row[c] - mx) / s - (c == label ? 1.0f : 0.0f)) * invB;
+  auto put = [&](int c, float dv) {
     if constexpr (BF16_OUT)
       static_cast<uint16_t*>(delta)[base + c] = static_cast<uint16_t>(f2bf(dv));
     else
       static_cast<float*>(delta)[base + c] = dv;
+  };
+  float mx = -INFINITY, s = 0.0f;
+  if constexpr (NV > 0) {
+    float v[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] = lane + 64 * k < C ? row[lane + 64 * k] : -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) mx = fmaxf(mx, v[k]);
+    for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      v[k] = lane + 64 * k < C ? expf(v[k] - mx) : 0.0f;
+      s += v[k];
+    }
+    for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int c = lane + 64 * k;
+      if (c < C) put(c, (v[k] / s - (c == label ? 1.0f : 0.0f)) * invB);
+    }
+    for (int c = 64 * NV + lane; c < ld; c += 64) put(c, 0.0f);
+    for (int k = 0; k < NV; ++k) {
+      const int c = lane + 64 * k;
+      if (c >= C && c < ld) put(c, 0.0f);
+    }
+  } else {
+    for (int c = lane; c < C; c += 64) mx = fmaxf(mx, row[c]);
+    for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
+    for (int c = lane; c < C; c += 64) s += expf(row[c] - mx);
+    for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d);
+    for (int c = lane; c < ld; c += 64) {
+      float dv = 0.0f;
+      if (c < C) dv = (expf(row[c] - mx) / s - (c == label ? 1.0f : 0.0f)) * invB;
+      put(c, dv);
+    }
   }
   if (lane == 0) {
     loss[z * loss_slot + b] = label_ok ? logf(s) - (row[label] - mx) : __builtin_nanf("");
@@ -1960,17 +1993,45 @@ hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <bool BF16_OUT, int NV>
+void softmax_launch(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
+                    const int32_t* y, const int32_t* gather, int64_t gather_slot, void* delta,
+                    float* loss, int64_t loss_slot, int n_slots, hipStream_t s, int32_t* correct) {
+  hipLaunchKernelGGL((softmax_ce_kernel<BF16_OUT, NV>), dim3((B + 3) / 4, n_slots), dim3(256), 0, s,
+                     logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss, loss_slot,
+                     correct);
+}
+
+template <bool BF16_OUT>
+void softmax_dispatch(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
+                      const int32_t* y, const int32_t* gather, int64_t gather_slot, void* delta,
+                      float* loss, int64_t loss_slot, int n_slots, hipStream_t s, int32_t* correct) {
+  const int nv = (C + 63) / 64;
+  if (nv <= 1)
+    softmax_launch<BF16_OUT, 1>(logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss,
+                                loss_slot, n_slots, s, correct);
+  else if (nv <= 4)
+    softmax_launch<BF16_OUT, 4>(logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss,
+                                loss_slot, n_slots, s, correct);
+  else if (nv <= 16)
+    softmax_launch<BF16_OUT, 16>(logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss,
+                                 loss_slot, n_slots, s, correct);
+  else
+    softmax_launch<BF16_OUT, 0>(logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss,
+                                loss_slot, n_slots, s, correct);
+}
+
 hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_stride, int C, int B,
                              const int32_t* y, const int32_t* gather, int64_t gather_slot,
                              void* delta, bool delta_bf16, float* loss, int64_t loss_slot,
                              int n_slots, hipStream_t s, int32_t* correct) {
-  const dim3 grid(B, n_slots);
+  if (B < 1 || n_slots < 1) return hipSuccess;
   if (delta_bf16)
-    hipLaunchKernelGGL((softmax_ce_kernel<true>), grid, dim3(64), 0, s, logits, ld, slot_stride, C,
-                       B, y, gather, gather_slot, delta, loss, loss_slot, correct);
+    softmax_dispatch<true>(logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss,
+                           loss_slot, n_slots, s, correct);
   else
-    hipLaunchKernelGGL((softmax_ce_kernel<false>), grid, dim3(64), 0, s, logits, ld, slot_stride,
-                       C, B, y, gather, gather_slot, delta, loss, loss_slot, correct);
+    softmax_dispatch<false>(logits, ld, slot_stride, C, B, y, gather, gather_slot, delta, loss,
+                            loss_slot, n_slots, s, correct);
   return hipGetLastError();
 }
 
