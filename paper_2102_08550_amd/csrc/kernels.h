@@ -107,14 +107,16 @@ void set_gemm_tiling(int tiling);
 bool backward_fusable(const GemmArgs& g);
 bool backward_fused_enabled();
 hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s);
-// Backward of hidden bf16 layers: AUTO (fused; the o chunks split over the
-// workgroup count that best fills the last CU pass), SEPARATE (backward-data
-// and update kernels), FUSED (never split), FUSED_SPLIT (one chunk per
-// workgroup wherever there is more than one chunk and the partial buffer
-// holds them).
+// Backward of hidden bf16 layers: AUTO (fused, the o chunks split over the
+// workgroup count that best fills the last CU pass, or the separate
+// launches, whichever the caller timed faster for the configuration),
+// SEPARATE (backward-data and update kernels), FUSED (never split),
+// FUSED_SPLIT (one chunk per workgroup wherever there is more than one chunk
+// and the partial buffer holds them).
 enum BackwardMode { BACKWARD_AUTO = 0, BACKWARD_SEPARATE = 1, BACKWARD_FUSED = 2,
                     BACKWARD_FUSED_SPLIT = 3, BACKWARD_MODE_COUNT = 4 };
 void set_backward_mode(int mode);
+int backward_mode();
 
 // Softmax cross-entropy on logits [slot][B][ld]: delta = (softmax - onehot)/B
 // stored as bf16 or fp32 into delta [slot][B][ld] (columns C..ld-1 zeroed),

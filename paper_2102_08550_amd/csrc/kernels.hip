@@ -1928,6 +1928,7 @@ std::atomic<int> g_backward_mode{BACKWARD_AUTO};
 }  // namespace
 
 void set_backward_mode(int mode) { g_backward_mode.store(mode); }
+int backward_mode() { return g_backward_mode.load(); }
 
 // Batches of at most FB_BMAX rows, whole 16-byte input chunks, and W_l (with
 // the chunks read ahead) under 1 GiB, so that 32-bit buffer offsets with an

@@ -11,8 +11,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstring>
+#include <map>
 #include <new>
 #include <vector>
 
@@ -73,6 +75,16 @@ struct oscars_ctx {
   std::vector<int32_t> last_order, last_tau;
   int last_tau_max = 0, last_B = 0;
 
+  // Backward of hidden bf16 layers without a forced mode: fused (true) or
+  // the separate launches, per (inputs, outputs, batch, replicas), timed at
+  // the first launch on scratch replicas (cal_*, allocated then).
+  std::map<std::array<int, 4>, bool> bwd_fused_choice;
+  float* cal_master = nullptr;   // [K][cal_layer] fp32: W_l then b_l
+  uint16_t* cal_copy = nullptr;  // [K][cal_w] bf16 copies of W_l
+  int32_t* cal_order = nullptr;  // [K] = 0 .. K-1
+  int64_t cal_layer = 0, cal_w = 0;
+  hipEvent_t cal_ev[2] = {nullptr, nullptr};
+
   uint32_t prof_mask = 0;
   std::vector<hipEvent_t> ev_pool;
   std::vector<std::pair<int, int>> prof_recs;  // (kind, first event index)
@@ -90,6 +102,8 @@ void free_ctx(oscars_ctx* c) {
   if (c->loss_dev) (void)hipFree(c->loss_dev);
   if (c->pinned) (void)hipHostFree(c->pinned);
   if (c->upload_done) (void)hipEventDestroy(c->upload_done);
+  for (hipEvent_t e : c->cal_ev)
+    if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   delete c;
 }
@@ -261,6 +275,89 @@ namespace {
 // replica k.  Otherwise every worker starts from `start` (the global model of
 // a round): the first step reads `start` and writes replica k; workers with
 // tau_k = 0 get a copy of `start`.
+// Backward of hidden layer l of a bf16 model without a forced mode: at the
+// first launch of each (inputs, outputs, batch, replicas) the fused launch
+// (gf) and the separate backward-data + update launches (gd, gw) each run
+// twice on scratch replicas, timed; the faster second run decides (fused on
+// ties).  The real replicas and weight copies are untouched; both write the
+// delta of the layer below, which the real launch that follows recomputes.
+// On a stream being captured into a graph nothing is timed: fused.
+hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const GemmArgs& gd,
+                           const GemmArgs& gw, bool* fused) {
+  *fused = true;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(c->stream, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone)
+    return hipSuccess;
+  const std::array<int, 4> key{gf.M, gf.K, gf.N, ns};
+  auto it = c->bwd_fused_choice.find(key);
+  if (it != c->bwd_fused_choice.end()) {
+    *fused = it->second;
+    return hipSuccess;
+  }
+  hipError_t e = hipSuccess;
+  if (!c->cal_master) {
+    // scratch for the widest hidden layer, every replica
+    for (int l = 2; l <= c->L; ++l) {
+      const int64_t w = static_cast<int64_t>(c->dims[l]) * c->dims[l - 1];
+      c->cal_w = std::max(c->cal_w, round_up(w, 8));
+      c->cal_layer = std::max(c->cal_layer, round_up(w + c->dims[l], 8));
+    }
+    void* p = nullptr;
+    e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_layer * 4, &p);
+    c->cal_master = static_cast<float*>(p);
+    if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_w * 2, &p);
+    c->cal_copy = static_cast<uint16_t*>(p);
+    if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->K) * 4, &p);
+    c->cal_order = static_cast<int32_t*>(p);
+    std::vector<int32_t> ident(c->K);
+    for (int k = 0; k < c->K; ++k) ident[k] = k;
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(c->cal_order, ident.data(), ident.size() * 4, hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipEventCreate(&c->cal_ev[i]);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t wsize = static_cast<int64_t>(gf.M) * gf.K;  // W_l: outputs x inputs
+  auto to_scratch = [&](GemmArgs& a) {
+    a.master = c->cal_master;
+    a.master_slot = c->cal_layer;
+    a.master_in = c->cal_master;
+    a.master_in_slot = c->cal_layer;
+    a.w_off = 0;
+    a.b_off = wsize;
+    a.order = c->cal_order;
+    if (a.wcopy) {
+      a.wcopy = c->cal_copy;
+      a.wcopy_slot = c->cal_w;
+    }
+  };
+  GemmArgs f = gf, d = gd, w = gw;
+  to_scratch(f);
+  to_scratch(d);
+  to_scratch(w);
+  d.a = c->cal_copy;  // backward-data reads the slots' bf16 weights
+  d.a_slot = c->cal_w;
+  d.a_by_order = 0;
+  float ms_f = 0.0f, ms_s = 0.0f;
+  for (int rep = 0; rep < 2 && e == hipSuccess; ++rep) {
+    e = hipEventRecord(c->cal_ev[0], c->stream);
+    if (e == hipSuccess) e = launch_bwd_fused(f, ns, c->stream);
+    if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
+    if (e == hipSuccess) e = hipEventSynchronize(c->cal_ev[1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms_f, c->cal_ev[0], c->cal_ev[1]);
+    if (e == hipSuccess) e = hipEventRecord(c->cal_ev[0], c->stream);
+    if (e == hipSuccess) e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream);
+    if (e == hipSuccess) e = launch_gemm(w, GEMM_WGRAD, true, ns, c->stream);
+    if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
+    if (e == hipSuccess) e = hipEventSynchronize(c->cal_ev[1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms_s, c->cal_ev[0], c->cal_ev[1]);
+  }
+  if (e != hipSuccess) return e;
+  *fused = ms_f <= ms_s;
+  c->bwd_fused_choice[key] = *fused;
+  return hipSuccess;
+}
+
 oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start,
                               const oscars_shards* s, const int32_t* tau, float lr, int32_t batch) {
   // ---- validation (no side effects on failure) ----
@@ -453,6 +550,51 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
                                rows_slot, ns, c->stream);
     });
     if (e != hipSuccess) return hip_fail(e);
+    // backward-data of layer l > 1: C[i][b] = sum_o W_l[o][i] delta_l[b][o],
+    // masked by act_{l-1} > 0
+    auto dgrad_args = [&](int l) {
+      GemmArgs g{};
+      g.M = c->dims[l - 1];
+      g.N = B;
+      g.K = c->dims[l];
+      g.a_ext = g.M;                                 // W rows, m chunks
+      g.b_ext = static_cast<int>(round_up(g.K, 8));  // delta rows are zero-padded
+      weights(g, l);
+      g.b = c->delta[l];
+      g.b_ld = c->ld[l];
+      g.b_slot = c->act_slot(l);
+      common(g, l);
+      g.out = c->delta[l - 1];
+      g.out_ld = c->ld[l - 1];
+      g.out_slot = c->act_slot(l - 1);
+      g.out_bf16 = c->bf16;
+      g.mask = c->act[l - 1];
+      g.mask_ld = c->ld[l - 1];
+      g.mask_slot = c->act_slot(l - 1);
+      return g;
+    };
+    // backward-weight + SGD update of layer l:
+    // C[i][o] = sum_b act_{l-1}[b][i] delta_l[b][o] = dW_l[o][i]
+    auto wgrad_args = [&](int l) {
+      GemmArgs g{};
+      g.M = c->dims[l - 1];
+      g.N = c->dims[l];
+      g.K = B;
+      g.a_ext = g.M;
+      g.b_ext = static_cast<int>(round_up(g.N, 8));  // delta rows are zero-padded
+      g.a = c->act[l - 1];  // for l = 1: the batch rows the forward pass gathered
+      g.a_ld = c->ld[l - 1];
+      g.a_slot = c->act_slot(l - 1);
+      g.a_by_order = 0;
+      g.b = c->delta[l];
+      g.b_ld = c->ld[l];
+      g.b_slot = c->act_slot(l);
+      common(g, l);
+      g.wcopy = c->bf16 ? c->wcopy : nullptr;
+      g.wcopy_slot = c->n_pad;
+      g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
+      return g;
+    };
     // backward, top layer first; dgrad(l) reads W_l before wgrad(l) updates it
     for (int l = L; l >= 1; --l) {
       if (l > 1 && c->bf16 && backward_fused_enabled()) {
@@ -480,53 +622,25 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
         g.wcopy_slot = c->n_pad;
         g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
         if (backward_fusable(g)) {
-          e = timed(c, OSCARS_KERNEL_BWD_FUSED, [&] { return launch_bwd_fused(g, ns, c->stream); });
-          if (e != hipSuccess) return hip_fail(e);
-          continue;
+          bool fused = true;
+          if (backward_mode() == BACKWARD_AUTO) {
+            e = choose_backward(c, ns, g, dgrad_args(l), wgrad_args(l), &fused);
+            if (e != hipSuccess) return hip_fail(e);
+          }
+          if (fused) {
+            e = timed(c, OSCARS_KERNEL_BWD_FUSED, [&] { return launch_bwd_fused(g, ns, c->stream); });
+            if (e != hipSuccess) return hip_fail(e);
+            continue;
+          }
         }
       }
       if (l > 1) {
-        // C[i][b] = sum_o W_l[o][i] delta_l[b][o], masked by act_{l-1} > 0
-        GemmArgs g{};
-        g.M = c->dims[l - 1];
-        g.N = B;
-        g.K = c->dims[l];
-        g.a_ext = g.M;                          // W rows, m chunks
-        g.b_ext = static_cast<int>(round_up(g.K, 8));  // delta rows are zero-padded
-        weights(g, l);
-        g.b = c->delta[l];
-        g.b_ld = c->ld[l];
-        g.b_slot = c->act_slot(l);
-        common(g, l);
-        g.out = c->delta[l - 1];
-        g.out_ld = c->ld[l - 1];
-        g.out_slot = c->act_slot(l - 1);
-        g.out_bf16 = c->bf16;
-        g.mask = c->act[l - 1];
-        g.mask_ld = c->ld[l - 1];
-        g.mask_slot = c->act_slot(l - 1);
+        const GemmArgs g = dgrad_args(l);
         e = timed(c, OSCARS_KERNEL_DGRAD,
                   [&] { return launch_gemm(g, GEMM_DGRAD, c->bf16, ns, c->stream); });
         if (e != hipSuccess) return hip_fail(e);
       }
-      // C[i][o] = sum_b act_{l-1}[b][i] delta_l[b][o] = dW_l[o][i], fused SGD update
-      GemmArgs g{};
-      g.M = c->dims[l - 1];
-      g.N = c->dims[l];
-      g.K = B;
-      g.a_ext = g.M;
-      g.b_ext = static_cast<int>(round_up(g.N, 8));  // delta rows are zero-padded
-      g.a = c->act[l - 1];  // for l = 1: the batch rows the forward pass gathered
-      g.a_ld = c->ld[l - 1];
-      g.a_slot = c->act_slot(l - 1);
-      g.a_by_order = 0;
-      g.b = c->delta[l];
-      g.b_ld = c->ld[l];
-      g.b_slot = c->act_slot(l);
-      common(g, l);
-      g.wcopy = c->bf16 ? c->wcopy : nullptr;
-      g.wcopy_slot = c->n_pad;
-      g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
+      const GemmArgs g = wgrad_args(l);
       e = timed(c, OSCARS_KERNEL_WGRAD,
                 [&] { return launch_gemm(g, GEMM_WGRAD, c->bf16, ns, c->stream); });
       if (e != hipSuccess) return hip_fail(e);
