@@ -31,21 +31,22 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 PMC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
 
 
-def gemm_work(cfg, tau):
+def gemm_work(cfg, tau, fused_path=None):
     """Algorithmic FLOPs and bytes of every launch of one round (oscars_round),
     per kind.  Bytes: each operand read once, each result written once (weights
     bf16 in the products of bf16 workloads; fp32 master read and write in the
     update, and the bf16 copy for workers that take another step; the start
     model cast to bf16 once; the average reads K replicas and writes the
-    global model).  Hidden layers of bf16 models take the fused backward
-    (backward-data + backward-weight + update in one launch, batches up to
-    256): its products are both passes, its bytes the update's plus the
-    delta written for the layer below."""
+    global model).  A hidden layer whose backward is fused (backward-data +
+    backward-weight + update in one launch; fused_path(l, ns), else every
+    hidden layer of a bf16 model with batches up to 256) counts both products
+    and the update's bytes plus the delta written for the layer below."""
     import numpy as np
     es = 2 if cfg.dtype == "bf16" else 4
     B, dims = cfg.batch, cfg.dims
     L = len(dims) - 1
-    fused = cfg.dtype == "bf16" and B <= 256
+    if fused_path is None:
+        fused_path = lambda l, ns: cfg.dtype == "bf16" and B <= 256
     work = {"gemm_fwd": [0.0, 0.0], "gemm_dgrad": [0.0, 0.0], "gemm_wgrad_update": [0.0, 0.0],
             "gemm_bwd_fused": [0.0, 0.0], "softmax_ce": [0.0, 0.0], "cast_bf16": [0.0, 0.0],
             "aggregate": [0.0, 0.0]}
@@ -64,7 +65,7 @@ def gemm_work(cfg, tau):
             work["gemm_fwd"][1] += ns * (es * o * i + 4 * o + es * B * i + out_es * B * o)
             update = (ns * (8.0 * (o * i + o) + es * B * o + es * B * i)
                       + (ns_next * 2.0 * o * i if es == 2 else 0.0))
-            if l > 1 and fused:
+            if l > 1 and fused_path(l, ns):
                 work["gemm_bwd_fused"][0] += ns * 4.0 * B * o * i
                 work["gemm_bwd_fused"][1] += update + ns * es * B * i
                 continue
@@ -322,6 +323,10 @@ def main():
     # configuration's first launch times the candidates); it is not profiled.
     run.round(tau_for(0))
     torch.cuda.synchronize()
+
+    def fused_path(l, ns):  # the backward path the library took (timed in the first round)
+        return run.ctx.backward_path(l, cfg.batch, ns) == 1
+
     run.ctx.profile_begin(kinds)
     work_w = {}
     n_warm = max(args.warmup, 2) - 1
@@ -330,7 +335,7 @@ def main():
         tau = tau_for(s)
         run.round(tau)
         samples_w += int(np.sum(tau)) * cfg.batch
-        for kname, (fl, by) in gemm_work(cfg, tau).items():
+        for kname, (fl, by) in gemm_work(cfg, tau, fused_path).items():
             a = work_w.setdefault(kname, [0.0, 0.0])
             a[0] += fl
             a[1] += by
@@ -350,8 +355,9 @@ def main():
         tau = tau_for(args.warmup + s)
         if s == args.steps - 1:
             run.ctx.profile_begin([dom_kind])
-            work_tot = gemm_work(cfg, tau)
         run.round(tau)
+        if s == args.steps - 1:
+            work_tot = gemm_work(cfg, tau, fused_path)
         samples += int(np.sum(tau)) * cfg.batch
     torch.cuda.synchronize()
     t1 = time.perf_counter()

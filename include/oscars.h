@@ -321,6 +321,17 @@ enum {
 };
 oscars_status oscars_set_backward(int32_t mode);
 
+/* The backward path of layer `layer` (1..L) in oscars_local_steps and
+ * oscars_round of this context with `replicas` active replicas (1..K) and
+ * batch `batch` (1..max_batch): *fused = 1 for the fused launch of
+ * backward-data, backward-weight and update, 0 for the separate launches
+ * (always for layer 1, fp32 models, OSCARS_BACKWARD_SEPARATE and batches
+ * above 256), -1 where OSCARS_BACKWARD_AUTO has not timed that
+ * configuration in this context yet.  Returns OSCARS_E_INVALID for an
+ * argument out of range. */
+oscars_status oscars_backward_path(const oscars_ctx* ctx, int32_t layer, int32_t batch,
+                                   int32_t replicas, int32_t* fused);
+
 const char* oscars_status_str(oscars_status s);
 /* HIP error code of the last OSCARS_E_HIP in this thread (0 if none). */
 int32_t oscars_last_hip_error(void);

@@ -73,6 +73,7 @@ _SIGS = {
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
     "oscars_set_gemm_tiling": (_i32, [_i32]),
     "oscars_set_backward": (_i32, [_i32]),
+    "oscars_backward_path": (_i32, [_vp, _i32, _i32, _i32, _P(_i32)]),
     "oscars_broadcast": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp]),
     "oscars_plan_tau": (_i32, [_P(ctypes.c_double), _i32, _i32, _i64, _P(_i64), _P(_i64), _P(_i32)]),
     "oscars_evaluate": (_i32, [_vp, _vp, _vp, _vp, _i64, _P(ctypes.c_double), _P(_i64)]),
@@ -363,6 +364,14 @@ class Context:
     def set_cursors(self, steps_done: Sequence[int]):
         a, ap = _arr(steps_done, np.int64)
         _check(_lib().oscars_set_cursors(self._h, ap), "oscars_set_cursors")
+
+    def backward_path(self, layer: int, batch: int, replicas: int) -> int:
+        """Backward of `layer` (1..L) with `replicas` active replicas: 1 fused,
+        0 separate launches, -1 not timed yet (AUTO)."""
+        out = _i32(0)
+        _check(_lib().oscars_backward_path(self._h, int(layer), int(batch), int(replicas),
+                                           ctypes.byref(out)), "oscars_backward_path")
+        return int(out.value)
 
     def profile_begin(self, kinds: Sequence[int]):
         mask = 0

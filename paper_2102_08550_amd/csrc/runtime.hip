@@ -825,6 +825,27 @@ oscars_status oscars_set_gemm_tiling(int32_t tiling) {
   return OSCARS_OK;
 }
 
+oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t batch,
+                                   int32_t replicas, int32_t* fused) {
+  if (!c || !fused || layer < 1 || layer > c->L || batch < 1 || batch > c->max_batch ||
+      replicas < 1 || replicas > c->K)
+    return OSCARS_E_INVALID;
+  *fused = 0;
+  if (layer == 1 || !c->bf16 || !backward_fused_enabled()) return OSCARS_OK;
+  GemmArgs g{};
+  g.M = c->dims[layer - 1];
+  g.N = batch;
+  g.K = c->dims[layer];
+  if (!backward_fusable(g)) return OSCARS_OK;
+  if (backward_mode() != BACKWARD_AUTO) {
+    *fused = 1;
+    return OSCARS_OK;
+  }
+  const auto it = c->bwd_fused_choice.find(std::array<int, 4>{g.M, g.K, g.N, replicas});
+  *fused = it == c->bwd_fused_choice.end() ? -1 : (it->second ? 1 : 0);
+  return OSCARS_OK;
+}
+
 oscars_status oscars_set_backward(int32_t mode) {
   static_assert(OSCARS_BACKWARD_COUNT == BACKWARD_MODE_COUNT &&
                     OSCARS_BACKWARD_FUSED_SPLIT == BACKWARD_FUSED_SPLIT,

@@ -221,6 +221,43 @@ def test_backward_modes_identical(P, cfg):
         P.set_backward(len(P.BACKWARDS))
 
 
+def test_backward_path_reports_the_launches(P):
+    """oscars_backward_path: AUTO has decided every (layer, active replicas)
+    that a round ran; forced modes report their path; layer 1 always takes
+    the separate update; bad arguments are refused."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    cfg = BACKWARD_CFGS[0]
+    say(f"backward path {cfg.name} tau={cfg.tau_given}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = [int(t) for t in cfg.tau_given]
+    L = len(cfg.dims) - 1
+    actives = sorted({sum(t > j for t in tau) for j in range(max(tau))})
+    try:
+        for name, mode in P.BACKWARDS.items():
+            P.set_backward(mode)
+            run = OscarsRun(cfg, ds, init)
+            if mode == P.BACKWARD_AUTO:
+                assert run.ctx.backward_path(2, cfg.batch, actives[0]) == -1  # not timed yet
+            run.round(tau)
+            torch.cuda.synchronize()
+            for ns in actives:
+                assert run.ctx.backward_path(1, cfg.batch, ns) == 0
+                for l in range(2, L + 1):
+                    got = run.ctx.backward_path(l, cfg.batch, ns)
+                    want = {P.BACKWARD_SEPARATE: 0, P.BACKWARD_FUSED: 1,
+                            P.BACKWARD_FUSED_SPLIT: 1}.get(mode, got)
+                    assert got in (0, 1) and got == want, (name, l, ns, got)
+            for bad in ((0, cfg.batch, 1), (L + 1, cfg.batch, 1), (2, 0, 1),
+                        (2, cfg.batch + 1, 1), (2, cfg.batch, 0), (2, cfg.batch, cfg.K + 1)):
+                with pytest.raises(P.OscarsError):
+                    run.ctx.backward_path(*bad)
+            run.close()
+    finally:
+        P.set_backward(P.BACKWARD_AUTO)
+
+
 @pytest.mark.parametrize("dtype", [workload.BF16, workload.FP32])
 def test_round_equals_local_steps_plus_aggregate(P, dtype):
     """oscars_round == (copy global into every replica, oscars_local_steps,
