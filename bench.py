@@ -84,17 +84,23 @@ def kernel_source_hash() -> str:
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
 
-def pmc_traffic(kernel: str, workload_name: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
+def pmc_traffic(kernel: str, workload_name: str, algorithmic_bytes: float):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None.  The
+    summary holds measured / algorithmic bytes per launch (FETCH_SIZE over
+    the fetch pass's algorithmic bytes plus WRITE_SIZE over the write
+    pass's): the backward path of each configuration is timed per process,
+    so a counter pass may run a different mix of launches than this one;
+    the ratio times this run's algorithmic bytes per launch follows the
+    launches timed here."""
     try:
         data = json.load(open(PMC_FILE))
     except (OSError, ValueError):
         return None
     ent = data.get(workload_name, {}).get(kernel)
-    if not ent or ent.get("kernels_sha256_16") != kernel_source_hash():
+    if not ent or ent.get("kernels_sha256_16") != kernel_source_hash() or not ent.get("ratio"):
         return None
-    return ent.get("bytes_per_launch")
+    return ent["ratio"] * algorithmic_bytes
 
 
 def host_info():
@@ -387,7 +393,10 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": d["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = pmc_traffic(dom, args.workload)
+    roof["traffic"] = pmc_traffic(dom, args.workload, d["bytes_per_launch"])
+    if roof["traffic"] is not None:
+        roof["traffic_basis"] = ("committed counter passes' measured/algorithmic bytes per launch "
+                                 "x this run's algorithmic bytes per launch")
     roof["kernel"] = dom
     roof["avg_launch_us"] = d["avg_us"]
     roof["algorithmic_per_launch"] = {"flop": d["flop_per_launch"], "bytes": d["bytes_per_launch"]}

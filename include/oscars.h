@@ -101,7 +101,9 @@ typedef struct {
 
 /* Create a context for K replicas of `model`, mini-batches up to max_batch.
  * Allocates the device workspace (activations, bf16 weight copies, index
- * tables) on the current HIP device.  `hip_stream` (a hipStream_t, NULL =
+ * tables) on the current HIP device (and, under OSCARS_BACKWARD_AUTO, the
+ * first local steps of a bf16 model add scratch replicas for timing the
+ * backward paths; see oscars_set_backward).  `hip_stream` (a hipStream_t, NULL =
  * null stream) is the stream oscars_local_steps enqueues on. */
 oscars_status oscars_create(oscars_ctx** out, const oscars_model* model, int32_t K,
                             int32_t max_batch, void* hip_stream);
