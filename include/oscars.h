@@ -304,8 +304,9 @@ oscars_status oscars_set_gemm_tiling(int32_t tiling);
  *     fills the last pass over the CUs best, the fewest on ties) or the
  *     separate launches, whichever ran faster at the first launch of the
  *     configuration (inputs, outputs, batch, active replicas) in this
- *     context: both run twice there on scratch replicas (allocated then:
- *     K x the widest hidden layer, fp32 and bf16), the second runs timed.
+ *     context: both run three times there on scratch replicas (allocated
+ *     then: K x the widest hidden layer, fp32 and bf16), the faster of each
+ *     one's last two runs counting.
  *     Fused, untimed, on a stream being captured into a graph;
  *   OSCARS_BACKWARD_SEPARATE: backward-data and update launches;
  *   OSCARS_BACKWARD_FUSED: fused, never split;

@@ -94,6 +94,9 @@ __device__ __forceinline__ int lds_word(int row, int chunk) {
   return row * ROW_U32 + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 2);
 }
 
+// A compile-time integer passed as an argument (static register indices).
+template <int U> struct Ic { static constexpr int value = U; };
+
 // fp32 -> bf16, round to nearest even on the fp32 bits.
 __device__ __forceinline__ uint32_t f2bf(float f) {
   const uint32_t u = __float_as_uint(f);
@@ -207,6 +210,12 @@ struct TransTile<true, NTHR, ROWS> {
       lo[p] = load16(ok0, base + k * ld + mn);
       hi[p] = load16(ok1, base + (k + 1) * ld + mn);
     }
+  }
+  // The loaded registers count as written here (an empty asm, ordered after
+  // the preceding volatile asm): their uses stay below this point.
+  __device__ __forceinline__ void pin() {
+#pragma unroll
+    for (int p = 0; p < P; ++p) asm volatile("" : "+v"(lo[p]), "+v"(hi[p]));
   }
   __device__ __forceinline__ void store(uint32_t* lds, int tid) const {
 #pragma unroll
@@ -743,7 +752,7 @@ gemm_dma_kernel(GemmArgs g) {
   DmaTile<NTHR, BN> db;
   db.init(B, g.b_ld, GATHER ? g.gather + z * g.gather_slot : nullptr, n0, N, tid);
   DmaTile<NTHR, BM> da;             // FWD: weights, K-contiguous
-  TransTile<true, NTHR, BM> ta;     // DGRAD: weights, M-contiguous, via registers
+  TransTile<true, NTHR, BM> ta[2];  // DGRAD: weights, M-contiguous, via registers, two ahead
   if constexpr (MODE == GEMM_FWD) da.init(A, g.a_ld, nullptr, m0, M, tid);
 
   f32x16 acc[MI][NJ], tot[MI][NJ];
@@ -768,28 +777,35 @@ gemm_dma_kernel(GemmArgs g) {
       issue_b(s);
     }
   } else {
-    // A(0) .. A(NS - 2) into LDS, B(0) .. B(NS - 2) streaming, and A(NS - 1)
-    // loading into registers before B(NS - 2) is issued.
+    // A(0) .. A(NS - 2) into LDS, B(0) .. B(NS - 2) streaming, A(NS - 1) and
+    // A(NS) loading into the two register tiles; A(NS) and B(NS - 2) are the
+    // operations of "step -1".
+    static_assert(NS >= 3, "B(j) is older than the last step's operations");
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s) {
-      ta.load(A, g.a_ld, m0, g.a_ext, k_of(s), K, tid);
+      ta[0].load(A, g.a_ld, m0, g.a_ext, k_of(s), K, tid);
       wait_vm<0>();
-      ta.store(lds_a(s), tid);
+      ta[0].store(lds_a(s), tid);
     }
 #pragma unroll
     for (int s = 0; s < NS - 2; ++s) issue_b(s);
-    ta.load(A, g.a_ld, m0, g.a_ext, k_of(NS - 1), K, tid);
+    ta[(NS - 1) & 1].load(A, g.a_ld, m0, g.a_ext, k_of(NS - 1), K, tid);
+    ta[NS & 1].load(A, g.a_ld, m0, g.a_ext, k_of(NS), K, tid);
     issue_b(NS - 2);
   }
 
-  for (int j = 0; j < nk; ++j) {
+  // Step j.  The register tile of A(j + NS - 1) is ta[(j + NS - 1) & 1]:
+  // the loop runs pairs of steps so that the index is static.
+  auto step = [&](int j, auto par) {
     // Stage j landed.  FWD: stages j + 1 .. j + NS - 2 stay in flight.
-    // DGRAD: A(j + NS - 1) in registers too (issued just before B(j + NS - 2),
-    // the only operation allowed in flight; with two stages B(j) is the
-    // newest, so everything is waited for).
+    // DGRAD: A(j + NS - 1) in registers too (issued two steps ago); the
+    // last step's A(j + NS) and B(j + NS - 2) stay in flight.
     if constexpr (MODE == GEMM_FWD) wait_vm<(NS - 2) * (PA + PB)>();
-    else wait_vm<(NS >= 3 ? PB : 0)>();
+    else wait_vm<PA + PB>();
     lds_barrier();
+    // DGRAD: nothing that reads the register tile moves above the wait (the
+    // compiler would then wait for every load at the top of the loop)
+    if constexpr (MODE == GEMM_DGRAD) ta[decltype(par)::value].pin();
     const int k0 = k_of(j);
     if (GATHER && k0 < kend && (k0 / BK) % gm == mt) {
       // Layer 1: this workgroup keeps K tile j of the gathered batch rows.
@@ -805,9 +821,11 @@ gemm_dma_kernel(GemmArgs g) {
     }
     if constexpr (MODE == GEMM_DGRAD) {
       // A(j + NS - 1) from registers into its LDS buffer (last read by the
-      // product of tile j - 1, before the barrier), then load A(j + NS).
-      ta.store(lds_a((j + NS - 1) % NS), tid);
-      ta.load(A, g.a_ld, m0, g.a_ext, k_of(j + NS), K, tid);
+      // product of tile j - 1, before the barrier), then load A(j + NS + 1)
+      // into the same registers.
+      constexpr int R = decltype(par)::value;
+      ta[R].store(lds_a((j + NS - 1) % NS), tid);
+      ta[R].load(A, g.a_ld, m0, g.a_ext, k_of(j + NS + 1), K, tid);
     } else {
       da.issue(lds_a((j + NS - 1) % NS), k_of(j + NS - 1), g.a_ext, tid);
     }
@@ -826,7 +844,13 @@ gemm_dma_kernel(GemmArgs g) {
           }
       }
     }
+  };
+  int j = 0;
+  for (; j + 1 < nk; j += 2) {
+    step(j, Ic<(NS - 1) & 1>());
+    step(j + 1, Ic<NS & 1>());
   }
+  if (j < nk) step(j, Ic<(NS - 1) & 1>());
   wait_vm<0>();  // nothing streams into LDS past the end of the workgroup
 
   auto mrow = [&](int i, int q) { return m0 + wm * 32 * MI + 32 * i + 8 * q + 4 * h; };
@@ -1181,7 +1205,6 @@ __device__ __forceinline__ bf16x8 row128(const char* tile, int row, int c) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(tile + t128(row, c)));
 }
 
-template <int U> struct Ic { static constexpr int value = U; };
 
 // Raw buffer resources (gfx9 descriptor word 3): an access whose byte offset
 // is at or beyond `bytes` reads zeros and writes nothing.  Every offset used
