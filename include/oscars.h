@@ -299,15 +299,16 @@ oscars_status oscars_set_gemm_tiling(int32_t tiling);
  * launches, whichever mode runs (a weight that is exactly -0 may come out
  * as +0 in one and -0 in the other).  The bias gradient of every update
  * sums the batch in blocks of 64 rows, block sums left to right.
- *   OSCARS_BACKWARD_AUTO (default): fused (the output features' chunks of
- *     1024 split over the number of workgroups per 64-wide input strip that
- *     fills the last pass over the CUs best, the fewest on ties) or the
- *     separate launches, whichever ran faster at the first launch of the
+ *   OSCARS_BACKWARD_AUTO (default): the fastest at the first launch of the
  *     configuration (inputs, outputs, batch, active replicas) in this
- *     context: both run three times there on scratch replicas (allocated
- *     then: K x the widest hidden layer, fp32 and bf16), the faster of each
- *     one's last two runs counting.
- *     Fused, untimed, on a stream being captured into a graph;
+ *     context of: the fused launch with each feasible number of 1024-output
+ *     chunks per workgroup (all; then half, a quarter, ... down to one,
+ *     where the context's partial buffer holds the split), and the separate
+ *     launches.  Each runs three times there on scratch replicas (allocated
+ *     then: K x the widest hidden layer, fp32 and bf16), the faster of its
+ *     last two runs counting.  On a stream being captured into a graph,
+ *     untimed: fused, split over the number of workgroups per 64-wide input
+ *     strip that fills the last pass over the CUs best (the fewest on ties);
  *   OSCARS_BACKWARD_SEPARATE: backward-data and update launches;
  *   OSCARS_BACKWARD_FUSED: fused, never split;
  *   OSCARS_BACKWARD_FUSED_SPLIT: fused, split wherever there is more than one

@@ -106,7 +106,12 @@ void set_gemm_tiling(int tiling);
 // W_l within 32-bit buffer offsets (backward_fusable).
 bool backward_fusable(const GemmArgs& g);
 bool backward_fused_enabled();
-hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s);
+// cps_forced > 0: each workgroup covers that many KCHUNK ranges of outputs
+// (all of them where the partial buffer cannot hold the split); 0: by mode.
+hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s, int cps_forced = 0);
+// The feasible ranges per workgroup (all chunks first, then halving down to
+// one), at most `max` of them written to cps; returns their number.
+int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max);
 // Backward of hidden bf16 layers: AUTO (fused, the o chunks split over the
 // workgroup count that best fills the last CU pass, or the separate
 // launches, whichever the caller timed faster for the configuration),

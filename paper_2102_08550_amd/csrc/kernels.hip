@@ -1303,11 +1303,13 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     auto wterm = [&](int t, uint32_t chunk_bytes) {
       return static_cast<uint32_t>(t - tbeg) * chunk_bytes;
     };
-    // piece q = 2 p + h: row mrow + 32 p, columns 8 m8 + 4 h .. + 3
+    // piece q = 2 p + h: row mrow + 32 p, columns 8 m8 + 4 h .. + 3.  Default
+    // cache policy: with the non-temporal one these loads made the launch
+    // about 35% slower on some MI355X boxes (the stores stay non-temporal).
     auto master_chunk = [&](int t, int q) {
       return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                            r_win, wbase4[q >> 1] + 16 * (q & 1) + wterm(t, chunk4),
-                                           0, 2));
+                                           0, 0));
     };
     // Delta chunk t: rows (ts >> 3) + 32 p < 16 NKS, 16-byte chunk ts & 7;
     // zeros beyond the batch (rows out of range) and past the workgroup's
@@ -1971,7 +1973,20 @@ bool backward_fused_enabled() { return g_backward_mode.load() != BACKWARD_SEPARA
 // CUs best, the largest on ties (a split costs partial traffic and a
 // reduce); measured on MI355X against the other choices at 1 to 8 replicas
 // of 4096 x 4096 layers.
-hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s) {
+int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max) {
+  if (!backward_fusable(g) || n_slots < 1 || max < 1) return 0;
+  const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
+  const int64_t part_slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
+  const bool can_split = nchunks > 1 && g.part && part_slot * n_slots <= g.part_cap;
+  int n = 0;
+  for (int c = nchunks; n < max; c = (c + 1) / 2) {
+    cps[n++] = c;
+    if (c == 1 || !can_split) break;
+  }
+  return n;
+}
+
+hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s, int cps_forced) {
   if (!backward_fusable(g_in) || n_slots < 1) return hipErrorInvalidValue;
   GemmArgs g = g_in;
   const int strips = (g.M + FB_TI - 1) / FB_TI;
@@ -1980,7 +1995,9 @@ hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s) {
   const bool can_split = nchunks > 1 && g.part && g.part_slot * n_slots <= g.part_cap;
   const int mode = g_backward_mode.load();
   int cps = nchunks;
-  if (can_split && mode == BACKWARD_FUSED_SPLIT) {
+  if (cps_forced > 0) {
+    cps = can_split && cps_forced < nchunks ? cps_forced : nchunks;
+  } else if (can_split && mode == BACKWARD_FUSED_SPLIT) {
     cps = 1;
   } else if (can_split && mode == BACKWARD_AUTO) {
     const int64_t cus = device_cu_count();

@@ -75,10 +75,11 @@ struct oscars_ctx {
   std::vector<int32_t> last_order, last_tau;
   int last_tau_max = 0, last_B = 0;
 
-  // Backward of hidden bf16 layers without a forced mode: fused (true) or
-  // the separate launches, per (inputs, outputs, batch, replicas), timed at
-  // the first launch on scratch replicas (cal_*, allocated then).
-  std::map<std::array<int, 4>, bool> bwd_fused_choice;
+  // Backward of hidden bf16 layers without a forced mode, per (inputs,
+  // outputs, batch, replicas): fused with this many 1024-output chunks per
+  // workgroup (> 0), or the separate launches (0); timed at the first launch
+  // on scratch replicas (cal_*, allocated then).
+  std::map<std::array<int, 4>, int> bwd_fused_choice;
   float* cal_master = nullptr;   // [K][cal_layer] fp32: W_l then b_l
   uint16_t* cal_copy = nullptr;  // [K][cal_w] bf16 copies of W_l
   int32_t* cal_order = nullptr;  // [K] = 0 .. K-1
@@ -277,21 +278,25 @@ namespace {
 // tau_k = 0 get a copy of `start`.
 // Backward of hidden layer l of a bf16 model without a forced mode: at the
 // first launch of each (inputs, outputs, batch, replicas) the fused launch
-// (gf) and the separate backward-data + update launches (gd, gw) each run
-// three times on scratch replicas, timed; the faster of each one's last two
-// runs decides (fused on ties).  The real replicas and weight copies are untouched; both write the
+// (gf) with every feasible number of output chunks per workgroup (all, then
+// halving down to one), and the separate backward-data + update launches
+// (gd, gw), each run three times on scratch replicas, timed; the fastest of
+// the last two runs of each decides (the earlier candidate on ties).  The
+// real replicas and weight copies are untouched; every candidate writes the
 // delta of the layer below, which the real launch that follows recomputes.
-// On a stream being captured into a graph nothing is timed: fused.
+// *cps: the chunks per workgroup of the fused launch, or 0 for the separate
+// launches.  On a stream being captured into a graph nothing is timed: the
+// fused launch with the split its launcher picks (*cps = -1).
 hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const GemmArgs& gd,
-                           const GemmArgs& gw, bool* fused) {
-  *fused = true;
+                           const GemmArgs& gw, int* cps) {
+  *cps = -1;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(c->stream, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone)
     return hipSuccess;
   const std::array<int, 4> key{gf.M, gf.K, gf.N, ns};
   auto it = c->bwd_fused_choice.find(key);
   if (it != c->bwd_fused_choice.end()) {
-    *fused = it->second;
+    *cps = it->second;
     return hipSuccess;
   }
   hipError_t e = hipSuccess;
@@ -338,28 +343,35 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
   d.a = c->cal_copy;  // backward-data reads the slots' bf16 weights
   d.a_slot = c->cal_w;
   d.a_by_order = 0;
-  // three runs of each, alternating; the first (which also picks the
+  // candidates: fused with each feasible split, then separate (0); three
+  // runs of each, round robin; the first (which also picks the
   // backward-data tiling) is not counted, the faster of the other two is
-  float best_f = 0.0f, best_s = 0.0f;
+  int cand[8];
+  int nc = bwd_fused_splits(f, ns, cand, 7);
+  cand[nc++] = 0;
+  float best[8] = {};
   for (int rep = 0; rep < 3 && e == hipSuccess; ++rep) {
-    float ms_f = 0.0f, ms_s = 0.0f;
-    e = hipEventRecord(c->cal_ev[0], c->stream);
-    if (e == hipSuccess) e = launch_bwd_fused(f, ns, c->stream);
-    if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
-    if (e == hipSuccess) e = hipEventSynchronize(c->cal_ev[1]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms_f, c->cal_ev[0], c->cal_ev[1]);
-    if (e == hipSuccess) e = hipEventRecord(c->cal_ev[0], c->stream);
-    if (e == hipSuccess) e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream);
-    if (e == hipSuccess) e = launch_gemm(w, GEMM_WGRAD, true, ns, c->stream);
-    if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
-    if (e == hipSuccess) e = hipEventSynchronize(c->cal_ev[1]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms_s, c->cal_ev[0], c->cal_ev[1]);
-    if (rep == 1 || (rep > 1 && ms_f < best_f)) best_f = ms_f;
-    if (rep == 1 || (rep > 1 && ms_s < best_s)) best_s = ms_s;
+    for (int i = 0; i < nc && e == hipSuccess; ++i) {
+      float ms = 0.0f;
+      e = hipEventRecord(c->cal_ev[0], c->stream);
+      if (cand[i] > 0) {
+        if (e == hipSuccess) e = launch_bwd_fused(f, ns, c->stream, cand[i]);
+      } else {
+        if (e == hipSuccess) e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream);
+        if (e == hipSuccess) e = launch_gemm(w, GEMM_WGRAD, true, ns, c->stream);
+      }
+      if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
+      if (e == hipSuccess) e = hipEventSynchronize(c->cal_ev[1]);
+      if (e == hipSuccess) e = hipEventElapsedTime(&ms, c->cal_ev[0], c->cal_ev[1]);
+      if (rep == 1 || (rep > 1 && ms < best[i])) best[i] = ms;
+    }
   }
   if (e != hipSuccess) return e;
-  *fused = best_f <= best_s;
-  c->bwd_fused_choice[key] = *fused;
+  int pick = 0;
+  for (int i = 1; i < nc; ++i)
+    if (best[i] < best[pick]) pick = i;
+  *cps = cand[pick];
+  c->bwd_fused_choice[key] = *cps;
   return hipSuccess;
 }
 
@@ -627,13 +639,14 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
         g.wcopy_slot = c->n_pad;
         g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
         if (backward_fusable(g)) {
-          bool fused = true;
+          int cps = -1;  // fused, split by the launcher's rule
           if (backward_mode() == BACKWARD_AUTO) {
-            e = choose_backward(c, ns, g, dgrad_args(l), wgrad_args(l), &fused);
+            e = choose_backward(c, ns, g, dgrad_args(l), wgrad_args(l), &cps);
             if (e != hipSuccess) return hip_fail(e);
           }
-          if (fused) {
-            e = timed(c, OSCARS_KERNEL_BWD_FUSED, [&] { return launch_bwd_fused(g, ns, c->stream); });
+          if (cps != 0) {
+            e = timed(c, OSCARS_KERNEL_BWD_FUSED,
+                      [&] { return launch_bwd_fused(g, ns, c->stream, cps > 0 ? cps : 0); });
             if (e != hipSuccess) return hip_fail(e);
             continue;
           }
@@ -847,7 +860,7 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
     return OSCARS_OK;
   }
   const auto it = c->bwd_fused_choice.find(std::array<int, 4>{g.M, g.K, g.N, replicas});
-  *fused = it == c->bwd_fused_choice.end() ? -1 : (it->second ? 1 : 0);
+  *fused = it == c->bwd_fused_choice.end() ? -1 : (it->second > 0 ? 1 : 0);
   return OSCARS_OK;
 }
 
