@@ -44,6 +44,18 @@ def P():
     return paper_2102_08550_amd
 
 
+def test_process_wide_knobs_reject_bad_values(P):
+    """Tiling and backward mode: values outside their range are refused with
+    E_INVALID, valid ones accepted (host-side stores only, no GPU work)."""
+    lib = P._lib()
+    assert lib.oscars_set_gemm_tiling(len(P.TILINGS)) == P.E_INVALID
+    assert lib.oscars_set_gemm_tiling(-1) == P.E_INVALID
+    assert lib.oscars_set_backward(len(P.BACKWARDS)) == P.E_INVALID
+    assert lib.oscars_set_backward(-1) == P.E_INVALID
+    assert lib.oscars_set_backward(P.BACKWARD_AUTO) == P.OK
+    assert lib.oscars_set_gemm_tiling(P.TILING_AUTO) == P.OK
+
+
 def test_load_balance_matches_oracle(P):
     rnd = random.Random(3)
     for _ in range(400):
