@@ -305,29 +305,48 @@ __device__ __forceinline__ int xcd_tile(int L, int T) {
 
 // Forward / backward-data output of four consecutive rows m..m+3 (cnt of them
 // inside M) at column n of slot z: bias and ReLU (forward) or the ReLU mask of
-// the layer below (backward-data), then bf16 or fp32 store.
+// the layer below (backward-data), then bf16 or fp32 store.  epi_load reads
+// what the epilogue needs (forward: the bias, 0 past cnt; backward-data: 1
+// where the mask is positive, else 0), store_out_with applies it and stores.
 template <bool BF16, int MODE>
-__device__ __forceinline__ void store_out(const GemmArgs& g, int z, int n, int m, int cnt, f32x4 v,
+__device__ __forceinline__ f32x4 epi_load(const GemmArgs& g, int z, int n, int m, int cnt,
                                           const float* master_in) {
-  typedef typename El<BF16>::T T;
+  // One vector load, no branch (a branch around it would make the compiler
+  // wait for it on the spot): the bias segment and the mask rows (the
+  // activations of a layer l >= 1) are padded to 64 elements, so the four
+  // elements from m (a multiple of 4 below M) are in range and aligned;
+  // those past cnt are dropped.
+  f32x4 a;
+  if constexpr (MODE == GEMM_FWD) {
+    const f32x4 b = *reinterpret_cast<const f32x4*>(master_in + g.b_off + m);
+    for (int e = 0; e < 4; ++e) a[e] = e < cnt ? b[e] : 0.0f;
+  } else {
+    const int64_t am = z * g.mask_slot + static_cast<int64_t>(n) * g.mask_ld + m;
+    bool pos[4];
+    if constexpr (BF16) {
+      const uint2 q = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(g.mask) + am);
+      const uint32_t w[4] = {q.x & 0xFFFFu, q.x >> 16, q.y & 0xFFFFu, q.y >> 16};
+      for (int e = 0; e < 4; ++e) pos[e] = w[e] != 0 && (w[e] & 0x8000u) == 0;
+    } else {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(static_cast<const float*>(g.mask) + am);
+      for (int e = 0; e < 4; ++e) pos[e] = q[e] > 0.0f;
+    }
+    for (int e = 0; e < 4; ++e) a[e] = e < cnt && pos[e] ? 1.0f : 0.0f;
+  }
+  return a;
+}
+
+template <bool BF16, int MODE>
+__device__ __forceinline__ void store_out_with(const GemmArgs& g, int z, int n, int m, int cnt,
+                                               f32x4 v, f32x4 a) {
   if constexpr (MODE == GEMM_FWD) {
     // out[b = n][o = m..m+3]
-    const float* bias = master_in + g.b_off + m;
     for (int e = 0; e < 4; ++e) {
-      float o = v[e] + (e < cnt ? bias[e] : 0.0f);
+      float o = v[e] + a[e];
       v[e] = g.relu ? fmaxf(o, 0.0f) : o;
     }
   } else {
-    const int64_t am = z * g.mask_slot + static_cast<int64_t>(n) * g.mask_ld + m;
-    const T* mk = static_cast<const T*>(g.mask) + am;
-    for (int e = 0; e < 4; ++e) {
-      bool pos = false;
-      if (e < cnt) {
-        if constexpr (BF16) pos = mk[e] != 0 && (mk[e] & 0x8000u) == 0;
-        else pos = mk[e] > 0.0f;
-      }
-      v[e] = pos ? v[e] : 0.0f;
-    }
+    for (int e = 0; e < 4; ++e) v[e] = a[e] != 0.0f ? v[e] : 0.0f;
   }
   const int64_t at = z * g.out_slot + static_cast<int64_t>(n) * g.out_ld + m;
   if (g.out_bf16) {
@@ -349,6 +368,7 @@ __device__ __forceinline__ void store_out(const GemmArgs& g, int z, int n, int m
     }
   }
 }
+
 
 // SPLIT: grid x = tiles x K chunks; the workgroup of (tile, chunk c) sums
 // chunk c only and stores it as fp32 partial c of its outputs (g.part);
@@ -627,7 +647,24 @@ gemm_kernel(GemmArgs g) {
       }
     return;
   } else {
-    // Epilogue, one group of four consecutive rows m..m+3 at column n at a time.
+    // Epilogue over groups of four consecutive rows m..m+3 at column n: the
+    // inputs (bias / mask) of every group first, loads in flight together
+    // (outside the outputs row 0, column 0 is read and not used), then the
+    // stores.
+    f32x4 ea[MI][NJ][4];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int n = ncol(j);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = mrow(i, q);
+          const bool in = n < N && m < M;
+          ea[i][j][q] = epi_load<BF16, MODE>(g, z, in ? n : 0, in ? m : 0,
+                                             in ? ((M - m >= 4) ? 4 : M - m) : 4, master_in);
+        }
+      }
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -639,10 +676,10 @@ gemm_kernel(GemmArgs g) {
           const int m = mrow(i, q);
           if (m >= M) continue;
           const int cnt = (M - m >= 4) ? 4 : M - m;
-          store_out<BF16, MODE>(g, z, n, m, cnt,
-                                f32x4{tot[i][j][4 * q], tot[i][j][4 * q + 1], tot[i][j][4 * q + 2],
-                                      tot[i][j][4 * q + 3]},
-                                master_in);
+          store_out_with<BF16, MODE>(g, z, n, m, cnt,
+                                     f32x4{tot[i][j][4 * q], tot[i][j][4 * q + 1],
+                                           tot[i][j][4 * q + 2], tot[i][j][4 * q + 3]},
+                                     ea[i][j][q]);
         }
       }
   }
@@ -873,6 +910,24 @@ gemm_dma_kernel(GemmArgs g) {
         }
       }
   } else {
+    // the epilogue's inputs (bias / mask) of every group first, so that their
+    // loads are in flight together, then the stores
+    f32x4 ea[MI][NJ][4];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int n = ncol(j);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // outside the outputs: row 0, column 0 is read instead (no branch
+          // around the load) and not used
+          const int m = mrow(i, q);
+          const bool in = n < N && m < M;
+          ea[i][j][q] = epi_load<true, MODE>(g, z, in ? n : 0, in ? m : 0,
+                                             in ? ((M - m >= 4) ? 4 : M - m) : 4, master_in);
+        }
+      }
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -884,10 +939,10 @@ gemm_dma_kernel(GemmArgs g) {
           const int m = mrow(i, q);
           if (m >= M) continue;
           const int cnt = (M - m >= 4) ? 4 : M - m;
-          store_out<true, MODE>(g, z, n, m, cnt,
-                                f32x4{tot[i][j][4 * q], tot[i][j][4 * q + 1], tot[i][j][4 * q + 2],
-                                      tot[i][j][4 * q + 3]},
-                                master_in);
+          store_out_with<true, MODE>(g, z, n, m, cnt,
+                                     f32x4{tot[i][j][4 * q], tot[i][j][4 * q + 1],
+                                           tot[i][j][4 * q + 2], tot[i][j][4 * q + 3]},
+                                     ea[i][j][q]);
         }
       }
   }
@@ -1521,6 +1576,21 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
   }
 
   if (SPLIT || !dgrad_wave) return;
+  // the masks of every group first (loads in flight together; outside the
+  // outputs row 0, column 0 is read and not used), then the stores
+  f32x4 ea[2][2][4];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int b = 64 * wb + 32 * j + (lane & 31);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + 32 * a + 8 * q + 4 * h;
+        const bool in = b < B && i < I;
+        ea[a][j][q] = epi_load<true, GEMM_DGRAD>(g, z, in ? b : 0, in ? i : 0, 4, nullptr);
+      }
+    }
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -1531,10 +1601,10 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
       for (int q = 0; q < 4; ++q) {
         const int i = i0 + 32 * a + 8 * q + 4 * h;
         if (i >= I) continue;  // I is a multiple of 8: whole groups of four
-        store_out<true, GEMM_DGRAD>(g, z, b, i, 4,
-                                    f32x4{tot[a][j][4 * q], tot[a][j][4 * q + 1],
-                                          tot[a][j][4 * q + 2], tot[a][j][4 * q + 3]},
-                                    nullptr);
+        store_out_with<true, GEMM_DGRAD>(g, z, b, i, 4,
+                                         f32x4{tot[a][j][4 * q], tot[a][j][4 * q + 1],
+                                               tot[a][j][4 * q + 2], tot[a][j][4 * q + 3]},
+                                         ea[a][j][q]);
       }
     }
 }
@@ -1549,12 +1619,26 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, int nchu
   if (idx >= static_cast<int64_t>(g.N) * mq) return;
   const int n = static_cast<int>(idx / mq), m = static_cast<int>(idx % mq) * 4;
   const int cnt = (g.M - m >= 4) ? 4 : g.M - m;
+  const float* master_in = g.master_in + static_cast<int64_t>(g.order[z]) * g.master_in_slot;
+  const f32x4 a = epi_load<BF16, MODE>(g, z, n, m, cnt, master_in);  // issued with the partials
   const float* p = g.part + z * g.part_slot + static_cast<int64_t>(n) * g.out_ld + m;
   const int64_t cs = static_cast<int64_t>(g.N) * g.out_ld;
-  f32x4 v = *reinterpret_cast<const f32x4*>(p);
-  for (int c = 1; c < nchunks; ++c) v = v + *reinterpret_cast<const f32x4*>(p + c * cs);
-  const float* master_in = g.master_in + static_cast<int64_t>(g.order[z]) * g.master_in_slot;
-  store_out<BF16, MODE>(g, z, n, m, cnt, v, master_in);
+  f32x4 v;
+  if (nchunks <= 4) {
+    // all loads first (a chunk past the last reads the last again, unused)
+    f32x4 c[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      c[i] = *reinterpret_cast<const f32x4*>(p + static_cast<int64_t>(min(i, nchunks - 1)) * cs);
+    v = c[0];
+#pragma unroll
+    for (int i = 1; i < 4; ++i)
+      if (i < nchunks) v = v + c[i];
+  } else {
+    v = *reinterpret_cast<const f32x4*>(p);
+    for (int c = 1; c < nchunks; ++c) v = v + *reinterpret_cast<const f32x4*>(p + c * cs);
+  }
+  store_out_with<BF16, MODE>(g, z, n, m, cnt, v, a);
 }
 
 // One wave per batch row.  NV > 0: the row's C <= 64 NV logits are loaded
