@@ -1667,10 +1667,17 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* logits, in
       static_cast<float*>(delta)[base + c] = dv;
   };
   float mx = -INFINITY, s = 0.0f;
+  float zl = 0.0f;  // the label's logit
   if constexpr (NV > 0) {
     float v[NV];
 #pragma unroll
     for (int k = 0; k < NV; ++k) v[k] = lane + 64 * k < C ? row[lane + 64 * k] : -INFINITY;
+    // lane label % 64 holds it in v[label / 64]
+    float sel = v[0];
+#pragma unroll
+    for (int k = 1; k < NV; ++k)
+      if (k == (label >> 6)) sel = v[k];
+    zl = __shfl(sel, label & 63);
 #pragma unroll
     for (int k = 0; k < NV; ++k) mx = fmaxf(mx, v[k]);
     for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
@@ -1691,6 +1698,7 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* logits, in
       if (c >= C && c < ld) put(c, 0.0f);
     }
   } else {
+    if (label_ok) zl = row[label];
     for (int c = lane; c < C; c += 64) mx = fmaxf(mx, row[c]);
     for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
     for (int c = lane; c < C; c += 64) s += expf(row[c] - mx);
@@ -1702,9 +1710,9 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* logits, in
     }
   }
   if (lane == 0) {
-    loss[z * loss_slot + b] = label_ok ? logf(s) - (row[label] - mx) : __builtin_nanf("");
+    loss[z * loss_slot + b] = label_ok ? logf(s) - (zl - mx) : __builtin_nanf("");
     // the label's logit is the largest (ties with another class count)
-    if (correct) correct[z * loss_slot + b] = label_ok && row[label] >= mx ? 1 : 0;
+    if (correct) correct[z * loss_slot + b] = label_ok && zl >= mx ? 1 : 0;
   }
 }
 
