@@ -214,7 +214,9 @@ def bench_aggregation(args, cfg, copy):
         "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded N(0,1) + N(0,0.02^2))",
         "config": {"workload": cfg.name, "K": K, "n": n, "broadcast": True},
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": gbps / HBM_PEAK_GBPS, "traffic": None, "kernel": "aggregate",
+                     "frac": gbps / HBM_PEAK_GBPS,
+                     "traffic": pmc_traffic("aggregate", args.workload, bytes_round),
+                     "kernel": "aggregate",
                      "avg_launch_us": ms * 1000.0 / args.steps,
                      "algorithmic_per_launch": {"flop": 0.0, "bytes": bytes_round},
                      "achieved_vs_copy": gbps / copy["GBps"]},
