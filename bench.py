@@ -283,7 +283,7 @@ def main():
                          "times (calibration of hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the hot path runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
 
     import numpy as np
