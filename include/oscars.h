@@ -306,9 +306,11 @@ oscars_status oscars_set_gemm_tiling(int32_t tiling);
  *     where the context's partial buffer holds the split), and the separate
  *     launches.  Each runs three times there on scratch replicas (allocated
  *     then: K x the widest hidden layer, fp32 and bf16), the faster of its
- *     last two runs counting.  On a stream being captured into a graph,
- *     untimed: fused, split over the number of workgroups per 64-wide input
- *     strip that fills the last pass over the CUs best (the fewest on ties);
+ *     last two runs counting.  Untimed -- on a stream being captured into a
+ *     graph, or where the scratch would take more than a quarter of the
+ *     free device memory --: fused, split over the number of workgroups per
+ *     64-wide input strip that fills the last pass over the CUs best (the
+ *     fewest on ties);
  *   OSCARS_BACKWARD_SEPARATE: backward-data and update launches;
  *   OSCARS_BACKWARD_FUSED: fused, never split;
  *   OSCARS_BACKWARD_FUSED_SPLIT: fused, split wherever there is more than one
@@ -330,8 +332,8 @@ oscars_status oscars_set_backward(int32_t mode);
  * batch `batch` (1..max_batch): *fused = 1 for the fused launch of
  * backward-data, backward-weight and update, 0 for the separate launches
  * (always for layer 1, fp32 models, OSCARS_BACKWARD_SEPARATE and batches
- * above 256), -1 where OSCARS_BACKWARD_AUTO has not timed that
- * configuration in this context yet.  Returns OSCARS_E_INVALID for an
+ * above 256), -1 where OSCARS_BACKWARD_AUTO times configurations and has
+ * not timed that one in this context yet.  Returns OSCARS_E_INVALID for an
  * argument out of range. */
 oscars_status oscars_backward_path(const oscars_ctx* ctx, int32_t layer, int32_t batch,
                                    int32_t replicas, int32_t* fused);

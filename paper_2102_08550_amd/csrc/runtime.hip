@@ -84,6 +84,7 @@ struct oscars_ctx {
   uint16_t* cal_copy = nullptr;  // [K][cal_w] bf16 copies of W_l
   int32_t* cal_order = nullptr;  // [K] = 0 .. K-1
   int64_t cal_layer = 0, cal_w = 0;
+  bool cal_off = false;  // scratch too large for the free device memory: no timing
   hipEvent_t cal_ev[2] = {nullptr, nullptr};
 
   uint32_t prof_mask = 0;
@@ -300,12 +301,22 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
     return hipSuccess;
   }
   hipError_t e = hipSuccess;
+  if (c->cal_off) return hipSuccess;
   if (!c->cal_master) {
-    // scratch for the widest hidden layer, every replica
+    // scratch for the widest hidden layer, every replica; skipped (no timing,
+    // fused) where it would take more than a quarter of the free memory
     for (int l = 2; l <= c->L; ++l) {
       const int64_t w = static_cast<int64_t>(c->dims[l]) * c->dims[l - 1];
       c->cal_w = std::max(c->cal_w, round_up(w, 8));
       c->cal_layer = std::max(c->cal_layer, round_up(w + c->dims[l], 8));
+    }
+    size_t free_b = 0, total_b = 0;
+    e = hipMemGetInfo(&free_b, &total_b);
+    if (e != hipSuccess) return e;
+    const double need = static_cast<double>(c->K) * (c->cal_layer * 4.0 + c->cal_w * 2.0);
+    if (need > static_cast<double>(free_b) / 4.0) {
+      c->cal_off = true;
+      return hipSuccess;
     }
     void* p = nullptr;
     e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_layer * 4, &p);
@@ -856,6 +867,10 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
   g.K = c->dims[layer];
   if (!backward_fusable(g)) return OSCARS_OK;
   if (backward_mode() != BACKWARD_AUTO) {
+    *fused = 1;
+    return OSCARS_OK;
+  }
+  if (c->cal_off) {  // no timing: fused
     *fused = 1;
     return OSCARS_OK;
   }
