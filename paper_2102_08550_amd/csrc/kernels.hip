@@ -1341,29 +1341,48 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     // No memory operation of the loop sits under a branch, so the compiler's
     // counter waits follow the issue order exactly; the bias, which only one
     // strip per chunk updates, is left to a math wave.
-    // Master chunk t: thread rows (ts >> 3) + 32 p of the chunk, columns
-    // i0 + 8 (ts & 7) .. + 7 (two 16-byte pieces h; 8 lanes cover one
-    // 256-byte row segment), so the bf16 copy is written 16 bytes at a time.
-    const int mrow = ts >> 3, m8 = ts & 7;
-    const bool col_ok = i0 + 8 * m8 < I;  // I is a multiple of 8: whole octets
+    // Master chunk t: thread rows (ts >> 3) + 32 p of the chunk, two pieces
+    // h of four columns, i0 + 4 m8 + 32 h .. + 3, so that the 8 lanes of a
+    // row load and store whole 128-byte lines of fp32 per instruction.  For
+    // the bf16 values (the Wq stage and the copy) each lane pair swaps one
+    // piece: lane 2 j + s then holds columns i0 + 8 j + 32 s .. + 7, 16 bytes.
+    const int mrow = ts >> 3, m8 = ts & 7, jx = m8 >> 1, sx = m8 & 1;
     constexpr uint32_t kFar = 0xC0000000u;
-    uint32_t wbase4[2], wbase2[2];
+    uint32_t wbase4[2][2], wbase2[2];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
-      const uint32_t e = static_cast<uint32_t>((mrow + 32 * p) * I + i0 + 8 * m8);
-      wbase4[p] = col_ok ? 4 * e : kFar;
-      wbase2[p] = col_ok ? 2 * e : kFar;
+      // I is a multiple of 8: a piece starting inside the row is whole
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int col = i0 + 4 * m8 + 32 * hh;
+        wbase4[p][hh] = col < I ? 4 * static_cast<uint32_t>((mrow + 32 * p) * I + col) : kFar;
+      }
+      const int col = i0 + 8 * jx + 32 * sx;
+      wbase2[p] = col < I ? 2 * static_cast<uint32_t>((mrow + 32 * p) * I + col) : kFar;
     }
+    // bf16 of pieces 0 and 1 (two words each) -> the lane's 8 columns
+    auto pair_swap = [&](const u32x2& x0, const u32x2& x1) {
+      const u32x2 send = sx ? x0 : x1;
+      u32x2 recv;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)  // quad_perm [1, 0, 3, 2]: lane ^ 1
+        recv[e] = static_cast<uint32_t>(
+            __builtin_amdgcn_mov_dpp(static_cast<int>(send[e]), 0xB1, 0xF, 0xF, true));
+      return sx ? u32x4{recv[0], recv[1], x1[0], x1[1]} : u32x4{x0[0], x0[1], recv[0], recv[1]};
+    };
+    auto pack4 = [](const f32x4& v) {
+      return u32x2{f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16)};
+    };
     const uint32_t chunk4 = static_cast<uint32_t>(FB_TO * I * 4);  // bytes of 64 fp32 rows
     auto wterm = [&](int t, uint32_t chunk_bytes) {
       return static_cast<uint32_t>(t - tbeg) * chunk_bytes;
     };
-    // piece q = 2 p + h: row mrow + 32 p, columns 8 m8 + 4 h .. + 3.  Default
+    // piece q = 2 p + h: row mrow + 32 p, columns 4 m8 + 32 h .. + 3.  Default
     // cache policy: with the non-temporal one these loads made the launch
     // about 35% slower on some MI355X boxes (the stores stay non-temporal).
     auto master_chunk = [&](int t, int q) {
       return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                           r_win, wbase4[q >> 1] + 16 * (q & 1) + wterm(t, chunk4),
+                                           r_win, wbase4[q >> 1][q & 1] + wterm(t, chunk4),
                                            0, 0));
     };
     // Delta chunk t: rows (ts >> 3) + 32 p < 16 NKS, 16-byte chunk ts & 7;
@@ -1407,15 +1426,9 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
         *reinterpret_cast<u32x4*>(dt + t128((ts >> 3) + 32 * p, ts & 7)) = dreg[d_next][p];
       char* const wq = wbuf(t + 1);
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const f32x4 lo = mreg[b_next][2 * p], hi = mreg[b_next][2 * p + 1];
-        u32x4 q;
-        q[0] = f2bf(lo[0]) | (f2bf(lo[1]) << 16);
-        q[1] = f2bf(lo[2]) | (f2bf(lo[3]) << 16);
-        q[2] = f2bf(hi[0]) | (f2bf(hi[1]) << 16);
-        q[3] = f2bf(hi[2]) | (f2bf(hi[3]) << 16);
-        *reinterpret_cast<u32x4*>(wq + t128(mrow + 32 * p, m8)) = q;
-      }
+      for (int p = 0; p < 2; ++p)
+        *reinterpret_cast<u32x4*>(wq + t128(mrow + 32 * p, jx + 4 * sx)) =
+            pair_swap(pack4(mreg[b_next][2 * p]), pack4(mreg[b_next][2 * p + 1]));
       // loads: delta of chunk t + 3, master of chunk t + 4
       load_delta(t + 3, dreg[d_next]);
 #pragma unroll
@@ -1426,19 +1439,19 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
 #pragma unroll
       for (int p = 0; p < 2; ++p) {
         const int r = mrow + 32 * p;
-        u32x4 cq;
+        u32x2 cq[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int c = 2 * m8 + h;
+          const int c = m8 + 8 * h;
           const f32x4 d = *reinterpret_cast<const f32x4*>(dws + r * 64 + ((c ^ (r & 15)) << 2));
           f32x4 wv = mreg[b_prev][2 * p + h];
           for (int e = 0; e < 4; ++e) wv[e] = fmaf(-g.lr, d[e], wv[e]);
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, wv), r_wout,
-                                                 wbase4[p] + 16 * h + wterm(t - 1, chunk4), 0, 2);
-          cq[2 * h] = f2bf(wv[0]) | (f2bf(wv[1]) << 16);
-          cq[2 * h + 1] = f2bf(wv[2]) | (f2bf(wv[3]) << 16);
+                                                 wbase4[p][h] + wterm(t - 1, chunk4), 0, 2);
+          cq[h] = pack4(wv);
         }
-        __builtin_amdgcn_raw_buffer_store_b128(cq, r_copy, wbase2[p] + wterm(t - 1, chunk4 / 2), 0, 2);
+        __builtin_amdgcn_raw_buffer_store_b128(pair_swap(cq[0], cq[1]), r_copy,
+                                               wbase2[p] + wterm(t - 1, chunk4 / 2), 0, 2);
       }
       // bias: db[o] = sum_b delta[b][o] in blocks of 64 batch rows, each row
       // by row, block sums left to right.  Stream wave w sums block w of
