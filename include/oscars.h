@@ -269,8 +269,9 @@ oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches)
  * whatever the tiling; only the speed differs.
  *   OSCARS_TILING_AUTO (default): the first launch of each GEMM configuration
  *     (layer shape, batch, number of active replicas) in the process times
- *     every feasible tiling on the stream, which waits for that stream once,
- *     and keeps the fastest; while the stream is being captured into a graph
+ *     every feasible tiling on the stream (three runs each, the faster of the
+ *     last two counting), which waits for that stream once, and keeps the
+ *     fastest; while the stream is being captured into a graph
  *     a fixed rule chooses instead.
  *   L, M, S: 128 x 128, 64 x 128, 64 x 64 output tiles;
  *   W: 128 x 256 (bf16 models, batches above 128); WS, VS: 128 x 256 and

@@ -81,7 +81,8 @@ hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots,
 //   W 128 x 256 and, split over K chunks, WS (128 x 256) and VS (64 x 256)
 //   (bf16, batches above 128, operands streamed into LDS).
 // AUTO times the feasible tilings at the first launch of each configuration
-// and keeps the fastest; any other value forces that tiling where it applies
+// (three runs each, the faster of the last two counting) and keeps the
+// fastest; any other value forces that tiling where it applies
 // (W for an infeasible split, L where no whole-batch tiling applies).
 enum GemmTiling {
   GEMM_TILING_AUTO = 0,

@@ -258,10 +258,15 @@ struct TransTile<false, NTHR, ROWS> {
 };
 
 // MI x NJ blocks of 32x32 MFMA of one wave over one LDS tile pair.  The
-// wave's rows start at wm * 32 MI, its columns at wn * 32 NJ.
-template <bool BF16, int MI, int NJ>
+// wave's rows start at wm * 32 MI, its columns at wn * 32 NJ.  `after_reads(s)`
+// runs once the operand reads of k group s are issued, before its MFMAs.
+struct NoHook {
+  __device__ __forceinline__ void operator()(int) const {}
+};
+template <bool BF16, int MI, int NJ, typename Hook = NoHook>
 __device__ __forceinline__ void mma_tile(const uint32_t* As, const uint32_t* Bs, int wm, int wn,
-                                         int lane, f32x16 (&acc)[MI][NJ]) {
+                                         int lane, f32x16 (&acc)[MI][NJ],
+                                         const Hook& after_reads = Hook()) {
   const int r = lane & 31, h = lane >> 5;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
@@ -273,6 +278,7 @@ __device__ __forceinline__ void mma_tile(const uint32_t* As, const uint32_t* Bs,
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
       b[j] = *reinterpret_cast<const u32x4*>(Bs + lds_word(wn * 32 * NJ + 32 * j + r, ch));
+    after_reads(s);
     if constexpr (BF16) {
       // lanes 0-31 hold k = 16s..16s+7 of their row, lanes 32-63 k = 16s+8..16s+15
 #pragma unroll
@@ -740,13 +746,14 @@ struct DmaTile {
   }
   // P wave instructions; wave w's instruction p fills tile rows
   // (64 w + NTHR p) / 8 .. + 7.
+  __device__ __forceinline__ void issue_one(int p, uint32_t* tile, int k0, int ext, int tid) const {
+    const bool in = ok[p] && k0 + kc[p] < ext;
+    dma16(in ? static_cast<const void*>(src[p] + k0) : static_cast<const void*>(k_zero16),
+          tile + (((tid & ~63) + NTHR * p) >> 3) * ROW_U32);
+  }
   __device__ __forceinline__ void issue(uint32_t* tile, int k0, int ext, int tid) const {
 #pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const bool in = ok[p] && k0 + kc[p] < ext;
-      dma16(in ? static_cast<const void*>(src[p] + k0) : static_cast<const void*>(k_zero16),
-            tile + (((tid & ~63) + NTHR * p) >> 3) * ROW_U32);
-    }
+    for (int p = 0; p < P; ++p) issue_one(p, tile, k0, ext, tid);
   }
 };
 
@@ -863,11 +870,29 @@ gemm_dma_kernel(GemmArgs g) {
       constexpr int R = decltype(par)::value;
       ta[R].store(lds_a((j + NS - 1) % NS), tid);
       ta[R].load(A, g.a_ld, m0, g.a_ext, k_of(j + NS + 1), K, tid);
-    } else {
+      issue_b(j + NS - 1);
+      mma_tile<true, MI, NJ>(lds_a(j % NS), lds_b(j % NS), wm, wn, lane, acc);
+    } else if constexpr (SPLIT) {
+      // split-K tiles (few workgroups, latency-bound): the whole stage first
       da.issue(lds_a((j + NS - 1) % NS), k_of(j + NS - 1), g.a_ext, tid);
+      issue_b(j + NS - 1);
+      mma_tile<true, MI, NJ>(lds_a(j % NS), lds_b(j % NS), wm, wn, lane, acc);
+    } else {
+      // stage j + NS - 1: its PA + PB instructions spread over the four k
+      // groups of this step, each issued behind the group's operand reads so
+      // that the products start without waiting for the whole stage's issue
+      uint32_t* const na = lds_a((j + NS - 1) % NS);
+      uint32_t* const nb = lds_b((j + NS - 1) % NS);
+      const int kn = k_of(j + NS - 1);
+      mma_tile<true, MI, NJ>(lds_a(j % NS), lds_b(j % NS), wm, wn, lane, acc, [&](int s) {
+#pragma unroll
+        for (int q = 0; q < PA + PB; ++q) {
+          if (q * 4 / (PA + PB) != s) continue;
+          if (q < PA) da.issue_one(q, na, kn, g.a_ext, tid);
+          else db.issue_one(q - PA, nb, kn, g.b_ext, tid);
+        }
+      });
     }
-    issue_b(j + NS - 1);
-    mma_tile<true, MI, NJ>(lds_a(j % NS), lds_b(j % NS), wm, wn, lane, acc);
     if constexpr (!SPLIT) {
       if ((j + 1) % TPC == 0 || j + 1 == nk) {
         const bool first = j < TPC;
@@ -2002,7 +2027,9 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
     if (it != best.end()) return launch_tiling<BF16, MODE>(g, n_slots, s, it->second);
 
     // First launch of this configuration: every feasible tiling computes the
-    // (identical) result twice, timed; the fastest second run is kept.
+    // (identical) result three times, timed; a tiling's time is the faster of
+    // its second and third runs (the first warms caches and code), and the
+    // fastest tiling is kept.
     static hipEvent_t ev[2] = {nullptr, nullptr};
     hipError_t e = hipSuccess;
     for (int i = 0; i < 2 && e == hipSuccess; ++i)
@@ -2012,16 +2039,18 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
     bool have = false;
     for (int t = GEMM_TILING_L; t < GEMM_TILING_COUNT && e == hipSuccess; ++t) {
       if (!tiling_fits(t, BF16, g, n_slots)) continue;
-      float ms = 0.0f;
-      for (int rep = 0; rep < 2 && e == hipSuccess; ++rep) {
+      float t_best = 0.0f;
+      for (int rep = 0; rep < 3 && e == hipSuccess; ++rep) {
+        float ms = 0.0f;
         e = hipEventRecord(ev[0], s);
         if (e == hipSuccess) e = launch_tiling<BF16, MODE>(g, n_slots, s, t);
         if (e == hipSuccess) e = hipEventRecord(ev[1], s);
         if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
         if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev[0], ev[1]);
+        if (rep == 1 || (rep == 2 && ms < t_best)) t_best = ms;
       }
-      if (e == hipSuccess && (!have || ms < best_ms)) {
-        best_ms = ms;
+      if (e == hipSuccess && (!have || t_best < best_ms)) {
+        best_ms = t_best;
         choice = t;
         have = true;
       }
