@@ -327,10 +327,18 @@ def main():
     # around the dominant kernel's launches only (events around every launch
     # would add about 10% to a round).
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    # The first round also picks the forward / backward-data GEMM tilings (each
-    # configuration's first launch times the candidates); it is not profiled.
-    run.round(tau_for(0))
+    # The first rounds pick the forward / backward-data GEMM tilings (the
+    # launches of each configuration run the candidate tilings in turn until
+    # the fastest is kept) and the backward path (timed at its first launch);
+    # they are neither profiled nor timed.
+    n_tune = 0
+    while True:
+        run.round(tau_for(n_tune))
+        n_tune += 1
+        if P.tuning_pending() == 0 or n_tune >= 64:
+            break
     torch.cuda.synchronize()
+    print(f"[bench] {n_tune} tuning rounds", file=sys.stderr, flush=True)
 
     def fused_path(l, ns):  # the backward path the library took (timed in the first round)
         return run.ctx.backward_path(l, cfg.batch, ns) == 1

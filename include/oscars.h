@@ -267,17 +267,21 @@ oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches)
  * testing aid).  Every tiling sums each output in the same order (K in
  * chunks of 1024 summed left to right), so results are bit-identical
  * whatever the tiling; only the speed differs.
- *   OSCARS_TILING_AUTO (default): the first launch of each GEMM configuration
- *     (layer shape, batch, number of active replicas) in the process times
- *     every feasible tiling on the stream (three runs each, the faster of the
- *     last two counting), which waits for that stream once, and keeps the
- *     fastest; while the stream is being captured into a graph
+ *   OSCARS_TILING_AUTO (default): the launches of each GEMM configuration
+ *     (layer shape, batch, number of active replicas) in the process are
+ *     tuned online: while the configuration is being tuned, each launch runs
+ *     one feasible tiling between two events on the stream (two timed
+ *     launches per tiling, read later without waiting), after which the
+ *     tiling with the fastest launch is kept (oscars_tuning_pending counts the
+ *     configurations still being tuned); while the stream is being captured
+ *     into a graph
  *     a fixed rule chooses instead.
  *   L, M, S: 128 x 128, 64 x 128, 64 x 64 output tiles;
  *   W: 128 x 256 (bf16 models, batches above 128); WS, VS: 128 x 256 and
  *     64 x 256 with the K chunks split over workgroups (bf16, batches above
  *     128, more than one K chunk) -- where a forced tiling does not apply, W
  *     or L is used.
+ * Every call (AUTO included) restarts the tuning of every configuration.
  * Returns OSCARS_E_INVALID for a value outside [0, OSCARS_TILING_COUNT). */
 enum {
   OSCARS_TILING_AUTO = 0,
@@ -290,6 +294,13 @@ enum {
   OSCARS_TILING_COUNT = 7
 };
 oscars_status oscars_set_gemm_tiling(int32_t tiling);
+
+/* Number of forward / backward-data GEMM configurations, over the whole
+ * process, whose tiling OSCARS_TILING_AUTO is still tuning (seen at least
+ * once, not yet decided), into *configurations.  A caller that times the
+ * steady state runs rounds until it reads 0.  Returns OSCARS_E_INVALID for a
+ * null pointer. */
+oscars_status oscars_tuning_pending(int32_t* configurations);
 
 /* Backward pass of the hidden layers (l >= 2) of bf16 models, process-wide
  * (a tuning and testing aid).  By default one launch per layer does

@@ -72,6 +72,7 @@ _SIGS = {
     "oscars_profile_begin": (_i32, [_vp, _u32]),
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
     "oscars_set_gemm_tiling": (_i32, [_i32]),
+    "oscars_tuning_pending": (_i32, [_P(_i32)]),
     "oscars_set_backward": (_i32, [_i32]),
     "oscars_backward_path": (_i32, [_vp, _i32, _i32, _i32, _P(_i32)]),
     "oscars_broadcast": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp]),
@@ -200,9 +201,16 @@ TILINGS = {"auto": TILING_AUTO, "L": TILING_L, "M": TILING_M, "S": TILING_S, "W"
 
 
 def set_gemm_tiling(tiling: int):
-    """Process-wide tiling of the forward / backward-data GEMMs (AUTO: timed
-    once per configuration, fastest kept)."""
+    """Process-wide tiling of the forward / backward-data GEMMs (AUTO: tuned
+    online per configuration, fastest kept)."""
     _check(_lib().oscars_set_gemm_tiling(int(tiling)), "oscars_set_gemm_tiling")
+
+
+def tuning_pending() -> int:
+    """GEMM configurations whose AUTO tiling is still being tuned."""
+    n = ctypes.c_int32(0)
+    _check(_lib().oscars_tuning_pending(ctypes.byref(n)), "oscars_tuning_pending")
+    return int(n.value)
 
 
 # Backward pass of hidden bf16 layers (oscars_set_backward); results are

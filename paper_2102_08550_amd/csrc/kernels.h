@@ -80,9 +80,8 @@ hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots,
 //   L 128 x 128, M 64 x 128, S 64 x 64 (register-staged operands);
 //   W 128 x 256 and, split over K chunks, WS (128 x 256) and VS (64 x 256)
 //   (bf16, batches above 128, operands streamed into LDS).
-// AUTO times the feasible tilings at the first launch of each configuration
-// (three runs each, the faster of the last two counting) and keeps the
-// fastest; any other value forces that tiling where it applies
+// AUTO tunes each configuration online: its launches run the feasible
+// tilings in turn, timed (two launches each), until the fastest is kept; any other value forces that tiling where it applies
 // (W for an infeasible split, L where no whole-batch tiling applies).
 enum GemmTiling {
   GEMM_TILING_AUTO = 0,
@@ -95,6 +94,12 @@ enum GemmTiling {
   GEMM_TILING_COUNT = 7
 };
 void set_gemm_tiling(int tiling);
+// Configurations whose AUTO tiling is still being tuned (process-wide).
+int gemm_tuning_pending();
+// While on (for the calling thread), an AUTO configuration not decided yet is
+// decided at its next launch: every feasible tiling timed there and then, the
+// fastest kept (for launches that are themselves being timed).
+void set_gemm_tune_now(bool on);
 
 // Backward pass of a hidden layer (l >= 2) of a bf16 model in one launch:
 // backward-data, backward-weight and the SGD update, with the arguments of

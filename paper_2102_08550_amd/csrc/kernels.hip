@@ -26,6 +26,7 @@
 #include <mutex>
 #include <tuple>
 #include <type_traits>
+#include <vector>
 
 #include "../../include/oscars.h"
 #include "kernels.h"
@@ -1993,6 +1994,56 @@ struct TuneKey {
   }
 };
 
+constexpr int kTuneRuns = 2;  // timed launches per candidate tiling
+struct TuneState {
+  struct Timed {
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    int cand = -1;  // candidate index, -1 when the pair is free
+  };
+  int cand[GEMM_TILING_COUNT] = {};
+  int nc = 0;
+  float best_ms[GEMM_TILING_COUNT] = {};
+  int runs[GEMM_TILING_COUNT] = {};
+  int in_flight[GEMM_TILING_COUNT] = {};
+  int choice = -1;
+  std::vector<Timed> timed;  // event pairs of timed launches (created on demand)
+  // Read every timed launch that has completed.
+  hipError_t collect() {
+    for (Timed& t : timed) {
+      if (t.cand < 0) continue;
+      const hipError_t q = hipEventQuery(t.ev[1]);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) return q;
+      float ms = 0.0f;
+      const hipError_t e = hipEventElapsedTime(&ms, t.ev[0], t.ev[1]);
+      if (e != hipSuccess) return e;
+      const int c = t.cand;
+      if (runs[c] == 0 || ms < best_ms[c]) best_ms[c] = ms;
+      ++runs[c];
+      --in_flight[c];
+      t.cand = -1;
+    }
+    return hipSuccess;
+  }
+  hipError_t free_slot(Timed** out) {
+    for (Timed& t : timed)
+      if (t.cand < 0) {
+        *out = &t;
+        return hipSuccess;
+      }
+    Timed t;
+    hipError_t e = hipEventCreate(&t.ev[0]);
+    if (e == hipSuccess) e = hipEventCreate(&t.ev[1]);
+    if (e != hipSuccess) return e;
+    timed.push_back(t);
+    *out = &timed.back();
+    return hipSuccess;
+  }
+};
+std::mutex g_tune_mu;
+std::map<TuneKey, TuneState> g_tune;  // every device, precision and mode
+thread_local bool t_tune_now = false;  // set_gemm_tune_now
+
 template <bool BF16, int MODE>
 hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
   if constexpr (MODE == GEMM_WGRAD) {
@@ -2016,54 +2067,105 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
     if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone)
       return launch_tiling<BF16, MODE>(g, n_slots, s, static_tiling(BF16, g, n_slots));
 
-    static std::mutex mu;
-    static std::map<TuneKey, int> best;
+    // Online choice: while a configuration is being tuned, each of its launches
+    // runs one candidate tiling between two events (the launches of the real
+    // workload, so caches are as warm or cold as they will be); completed
+    // event pairs are read at later launches without waiting.  Once every
+    // candidate has kTuneRuns timed launches, the one with the smallest time
+    // (its fastest launch) is kept.
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) dev = 0;
     const TuneKey key{dev, BF16, MODE, g.M, g.N, g.K, n_slots, g.gather != nullptr,
                       split_fits(g, n_slots)};
-    std::lock_guard<std::mutex> lock(mu);
-    auto it = best.find(key);
-    if (it != best.end()) return launch_tiling<BF16, MODE>(g, n_slots, s, it->second);
-
-    // First launch of this configuration: every feasible tiling computes the
-    // (identical) result three times, timed; a tiling's time is the faster of
-    // its second and third runs (the first warms caches and code), and the
-    // fastest tiling is kept.
-    static hipEvent_t ev[2] = {nullptr, nullptr};
-    hipError_t e = hipSuccess;
-    for (int i = 0; i < 2 && e == hipSuccess; ++i)
-      if (!ev[i]) e = hipEventCreate(&ev[i]);
-    int choice = static_tiling(BF16, g, n_slots);
-    float best_ms = 0.0f;
-    bool have = false;
-    for (int t = GEMM_TILING_L; t < GEMM_TILING_COUNT && e == hipSuccess; ++t) {
-      if (!tiling_fits(t, BF16, g, n_slots)) continue;
-      float t_best = 0.0f;
-      for (int rep = 0; rep < 3 && e == hipSuccess; ++rep) {
-        float ms = 0.0f;
-        e = hipEventRecord(ev[0], s);
-        if (e == hipSuccess) e = launch_tiling<BF16, MODE>(g, n_slots, s, t);
-        if (e == hipSuccess) e = hipEventRecord(ev[1], s);
-        if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
-        if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev[0], ev[1]);
-        if (rep == 1 || (rep == 2 && ms < t_best)) t_best = ms;
-      }
-      if (e == hipSuccess && (!have || t_best < best_ms)) {
-        best_ms = t_best;
-        choice = t;
-        have = true;
-      }
+    std::lock_guard<std::mutex> lock(g_tune_mu);
+    TuneState& ts = g_tune[key];
+    if (ts.choice >= 0) return launch_tiling<BF16, MODE>(g, n_slots, s, ts.choice);
+    if (ts.nc == 0) {
+      for (int t = GEMM_TILING_L; t < GEMM_TILING_COUNT; ++t)
+        if (tiling_fits(t, BF16, g, n_slots)) ts.cand[ts.nc++] = t;
+      if (ts.nc == 1) ts.choice = ts.cand[0];
+      if (ts.nc <= 1) return launch_tiling<BF16, MODE>(g, n_slots, s, ts.cand[0]);
     }
+    hipError_t e = ts.collect();
     if (e != hipSuccess) return e;
-    best[key] = choice;
-    return hipSuccess;  // the result is in place (every timed run computed it)
+    if (t_tune_now) {
+      // Decided at once: every candidate computes the (identical) result
+      // three times, timed; its time is the faster of the last two runs.
+      TuneState::Timed* slot = nullptr;
+      e = ts.free_slot(&slot);
+      float best_ms = 0.0f;
+      for (int c = 0; c < ts.nc && e == hipSuccess; ++c) {
+        float t_best = 0.0f;
+        for (int rep = 0; rep < 3 && e == hipSuccess; ++rep) {
+          float ms = 0.0f;
+          e = hipEventRecord(slot->ev[0], s);
+          if (e == hipSuccess) e = launch_tiling<BF16, MODE>(g, n_slots, s, ts.cand[c]);
+          if (e == hipSuccess) e = hipEventRecord(slot->ev[1], s);
+          if (e == hipSuccess) e = hipEventSynchronize(slot->ev[1]);
+          if (e == hipSuccess) e = hipEventElapsedTime(&ms, slot->ev[0], slot->ev[1]);
+          if (rep == 1 || (rep == 2 && ms < t_best)) t_best = ms;
+        }
+        if (e == hipSuccess && (c == 0 || t_best < best_ms)) {
+          best_ms = t_best;
+          ts.choice = ts.cand[c];
+        }
+      }
+      return e;  // the result is in place (every timed run computed it)
+    }
+    int next = -1;
+    bool done = true;
+    for (int c = 0; c < ts.nc; ++c) {
+      if (ts.runs[c] + ts.in_flight[c] < kTuneRuns && (next < 0 || ts.runs[c] + ts.in_flight[c] <
+                                                                     ts.runs[next] + ts.in_flight[next]))
+        next = c;
+      if (ts.runs[c] < kTuneRuns) done = false;
+    }
+    if (done) {
+      int c_best = 0;
+      for (int c = 1; c < ts.nc; ++c)
+        if (ts.best_ms[c] < ts.best_ms[c_best]) c_best = c;
+      ts.choice = ts.cand[c_best];
+      return launch_tiling<BF16, MODE>(g, n_slots, s, ts.choice);
+    }
+    if (next < 0)  // every remaining run is in flight: launch the provisional choice
+      return launch_tiling<BF16, MODE>(g, n_slots, s, static_tiling(BF16, g, n_slots));
+    TuneState::Timed* slot = nullptr;
+    e = ts.free_slot(&slot);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(slot->ev[0], s);
+    if (e == hipSuccess) e = launch_tiling<BF16, MODE>(g, n_slots, s, ts.cand[next]);
+    if (e == hipSuccess) e = hipEventRecord(slot->ev[1], s);
+    if (e != hipSuccess) return e;
+    slot->cand = next;
+    ++ts.in_flight[next];
+    return hipSuccess;
   }
 }
 
 }  // namespace
 
-void set_gemm_tiling(int tiling) { g_forced_tiling.store(tiling); }
+void set_gemm_tiling(int tiling) {
+  std::lock_guard<std::mutex> lock(g_tune_mu);
+  g_forced_tiling.store(tiling);
+  // AUTO starts over: every configuration is tuned again at its next launches
+  // (event pairs still in flight are left to complete and are not read).
+  for (auto& kv : g_tune) {
+    TuneState& ts = kv.second;
+    ts.nc = 0;
+    ts.choice = -1;
+    for (int c = 0; c < GEMM_TILING_COUNT; ++c) ts.runs[c] = ts.in_flight[c] = 0;
+    for (TuneState::Timed& t : ts.timed) t.cand = -1;
+  }
+}
+
+void set_gemm_tune_now(bool on) { t_tune_now = on; }
+
+int gemm_tuning_pending() {
+  std::lock_guard<std::mutex> lock(g_tune_mu);
+  int n = 0;
+  for (const auto& kv : g_tune) n += kv.second.nc > 0 && kv.second.choice < 0;  // launched, undecided
+  return n;
+}
 
 hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s) {
   if (bf16) {

@@ -361,6 +361,10 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
   int nc = bwd_fused_splits(f, ns, cand, 7);
   cand[nc++] = 0;
   float best[8] = {};
+  struct TuneNow {  // the separate path's backward-data tiling decided at its first run
+    TuneNow() { set_gemm_tune_now(true); }
+    ~TuneNow() { set_gemm_tune_now(false); }
+  } tune_now;
   for (int rep = 0; rep < 3 && e == hipSuccess; ++rep) {
     for (int i = 0; i < nc && e == hipSuccess; ++i) {
       float ms = 0.0f;
@@ -851,6 +855,12 @@ oscars_status oscars_set_gemm_tiling(int32_t tiling) {
                 "tiling codes of the C ABI and of the launchers agree");
   if (tiling < 0 || tiling >= OSCARS_TILING_COUNT) return OSCARS_E_INVALID;
   set_gemm_tiling(tiling);
+  return OSCARS_OK;
+}
+
+oscars_status oscars_tuning_pending(int32_t* configurations) {
+  if (!configurations) return OSCARS_E_INVALID;
+  *configurations = gemm_tuning_pending();
   return OSCARS_OK;
 }
 

@@ -164,6 +164,42 @@ def test_every_tiling_gives_identical_results(P, cfg):
         P.set_gemm_tiling(len(P.TILINGS))
 
 
+def test_online_tiling_choice_settles(P):
+    """AUTO tunes online: the launches of a configuration run the candidate
+    tilings in turn until the fastest is kept, and the tuning ends; every
+    launch gives the same bits, so the tuned run equals a run with one forced
+    tiling round for round."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    cfg = MASK_CFGS[2]
+    say(f"online tiling {cfg.dtype} dims={cfg.dims} tau={cfg.tau_given}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = [int(t) for t in cfg.tau_given]
+    try:
+        P.set_gemm_tiling(P.TILING_AUTO)  # restarts the tuning of every configuration
+        assert P.tuning_pending() == 0
+        run = OscarsRun(cfg, ds, init)
+        n = 0
+        while True:
+            run.local_steps(tau)
+            n += 1
+            torch.cuda.synchronize()
+            if n == 1:
+                assert P.tuning_pending() > 0
+            elif P.tuning_pending() == 0:
+                break
+            assert n < 40, "tuning did not settle"
+        auto = run.replicas.view(cfg.K, run.n).cpu().numpy().copy()
+        run.close()
+        say(f"  settled after {n} rounds")
+        P.set_gemm_tiling(P.TILING_L)
+        forced, _ = _run_once(P, cfg, ds, init, np.array([tau] * n))
+    finally:
+        P.set_gemm_tiling(P.TILING_AUTO)
+    assert np.array_equal(auto.view(np.uint32), forced.view(np.uint32))
+
+
 BACKWARD_CFGS = [
     # output features of 2056 and 1032: three and two chunks of 1024 (the last
     # ragged), input strips ragged (1032 = 16 x 64 + 8, 200), 37 classes;

@@ -56,6 +56,13 @@ def test_process_wide_knobs_reject_bad_values(P):
     assert lib.oscars_set_gemm_tiling(P.TILING_AUTO) == P.OK
 
 
+def test_tuning_pending_without_launches(P):
+    """No GEMM has run in this process: no configuration is being tuned; a
+    null output pointer is refused."""
+    assert P.tuning_pending() == 0
+    assert P._lib().oscars_tuning_pending(None) == P.E_INVALID
+
+
 def test_load_balance_matches_oracle(P):
     rnd = random.Random(3)
     for _ in range(400):
