@@ -1027,21 +1027,25 @@ struct DmaRowsTile {  // K rows x COLS bf16 (COLS * 2 = 256 bytes per row)
 };
 
 // MFMA operand (8 consecutive K of column col0 + (lane & 31)) from a tile of
-// 256-byte rows, K rows k0 + 8 h .. + 7.
+// 256-byte rows, K rows k0 + 8 h .. + 7.  The two transposing reads are
+// inline asm: after an LDS-DMA load the compiler waits for every vector memory
+// operation in flight (vmcnt(0)) before a ds_read_b64_tr_b16 it emits itself,
+// which drained the next stages' loads at every K step.  The compiler does
+// not wait for these reads either: the caller waits (lgkmcnt) before using
+// the operands, through an asm statement that takes them as operands.
 __device__ __forceinline__ bf16x8 tr_operand(const uint32_t* tile, int k0, int col0, int lane) {
   const int g = lane >> 4, il = lane & 15, a = il & 3, e = il >> 2, h = lane >> 5;
   const int col = col0 + 16 * (g & 1) + 4 * a;
-  s16x4 v[2];
+  u32x2 v[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int k = k0 + 8 * h + 4 * q + e;
     const int byte = k * 256 + trow_chunk(k, col >> 3) * 16 + (col & 4) * 2;
-    v[q] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_s16x4*)(reinterpret_cast<const char*>(tile) + byte));
+    const uint32_t addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+        (const __attribute__((address_space(3))) char*)(reinterpret_cast<const char*>(tile) + byte)));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v[q]) : "v"(addr));
   }
-  const s16x4 lo = v[0], hi = v[1];
-  typedef short s16x8 __attribute__((ext_vector_type(8)));
-  const s16x8 all = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  const u32x4 all = {v[0][0], v[0][1], v[1][0], v[1][1]};
   return __builtin_bit_cast(bf16x8, all);
 }
 
@@ -1128,6 +1132,9 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
       for (int i = 0; i < MI; ++i) a[i] = tr_operand(As, 16 * s, wm * 64 + 32 * i, lane);
 #pragma unroll
       for (int jj = 0; jj < NJ; ++jj) b[jj] = tr_operand(Bs, 16 * s, wn * 64 + 32 * jj, lane);
+      // the operand reads done (tr_operand); the products depend on this wait
+      static_assert(MI == 2 && NJ == 2, "the wait names the four operands");
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]));
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -1433,12 +1440,24 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     };
 
     f32x4 mreg[FB_NB][4];
-    load_delta(tbeg, dreg[1]);
-    load_delta(tbeg + 1, dreg[0]);
+    // Prologue in the loop's own pattern of memory operations (steps
+    // tbeg - 4 .. tbeg - 2: delta t + 3, master t + 4, then the six stores of
+    // chunk t - 1, here out of range), so that the vector-memory counter
+    // state at the loop entry matches the one at its back edge.
 #pragma unroll
-    for (int d = 0; d < 3; ++d)
+    for (int v = 0; v < 3; ++v) {
+      const int t = tbeg - 4 + v;
+      if (v > 0) load_delta(t + 3, dreg[v & 1]);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) mreg[1 + d][q] = master_chunk(tbeg + d, q);
+      for (int q = 0; q < 4; ++q) mreg[1 + v][q] = master_chunk(t + 4, q);
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4{0u, 0u, 0u, 0u}, r_wout, kOob, 0, 2);
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{0u, 0u, 0u, 0u}, r_copy, kOob, 0, 2);
+      }
+    }
 
     // step t = tbeg - 1 + u
     auto step = [&](int t, auto uc) {
