@@ -1952,8 +1952,8 @@ int device_cu_count() {
 }
 
 // Forward / backward-data tilings.  Every tiling sums in the same order, so
-// the choice changes only the speed: the first launch of each configuration
-// times the feasible tilings and keeps the fastest (see select_tiling).
+// the choice changes only the speed: AUTO tunes each configuration online
+// from its own launches and keeps the fastest (gemm_launch).
 bool split_fits(const GemmArgs& g, int n_slots) {
   const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
   const int64_t slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
