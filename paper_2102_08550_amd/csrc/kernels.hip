@@ -1441,9 +1441,10 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
 
     f32x4 mreg[FB_NB][4];
     // Prologue in the loop's own pattern of memory operations (steps
-    // tbeg - 4 .. tbeg - 2: delta t + 3, master t + 4, then the six stores of
-    // chunk t - 1, here out of range), so that the vector-memory counter
-    // state at the loop entry matches the one at its back edge.
+    // tbeg - 4 .. tbeg - 2: delta t + 3 except at the first, whose chunk is
+    // before the range; master t + 4; then the six stores of chunk t - 1,
+    // out of range), so that the vector-memory counter state at the loop
+    // entry matches the one at its back edge.
 #pragma unroll
     for (int v = 0; v < 3; ++v) {
       const int t = tbeg - 4 + v;
