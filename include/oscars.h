@@ -276,7 +276,8 @@ oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches)
  *     configurations still being tuned); while the stream is being captured
  *     into a graph
  *     a fixed rule chooses instead.
- *   L, M, S: 128 x 128, 64 x 128, 64 x 64 output tiles;
+ *   L, M, S: 128 x 128, 64 x 128, 64 x 64 output tiles; LS: 128 x 128 with
+ *     the K chunks split over workgroups (more than one K chunk);
  *   W: 128 x 256 (bf16 models, batches above 128); WS, VS: 128 x 256 and
  *     64 x 256 with the K chunks split over workgroups (bf16, batches above
  *     128, more than one K chunk) -- where a forced tiling does not apply, W
@@ -291,7 +292,8 @@ enum {
   OSCARS_TILING_W = 4,
   OSCARS_TILING_WS = 5,
   OSCARS_TILING_VS = 6,
-  OSCARS_TILING_COUNT = 7
+  OSCARS_TILING_LS = 7,
+  OSCARS_TILING_COUNT = 8
 };
 oscars_status oscars_set_gemm_tiling(int32_t tiling);
 

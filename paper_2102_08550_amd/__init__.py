@@ -195,9 +195,9 @@ def sample_indices(n_rows: int, offsets: Sequence[int], seed: int, k: int, first
 
 # Forward / backward-data GEMM tilings (oscars_set_gemm_tiling); results are
 # bit-identical for every tiling.
-TILING_AUTO, TILING_L, TILING_M, TILING_S, TILING_W, TILING_WS, TILING_VS = range(7)
+TILING_AUTO, TILING_L, TILING_M, TILING_S, TILING_W, TILING_WS, TILING_VS, TILING_LS = range(8)
 TILINGS = {"auto": TILING_AUTO, "L": TILING_L, "M": TILING_M, "S": TILING_S, "W": TILING_W,
-           "WS": TILING_WS, "VS": TILING_VS}
+           "WS": TILING_WS, "VS": TILING_VS, "LS": TILING_LS}
 
 
 def set_gemm_tiling(tiling: int):

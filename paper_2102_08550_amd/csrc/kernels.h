@@ -77,12 +77,15 @@ struct GemmArgs {
 hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s);
 
 // Forward / backward-data tilings (backward-weight always uses one):
-//   L 128 x 128, M 64 x 128, S 64 x 64 (register-staged operands);
+//   L 128 x 128, M 64 x 128, S 64 x 64 (register-staged operands), and LS,
+//   L split over K chunks;
 //   W 128 x 256 and, split over K chunks, WS (128 x 256) and VS (64 x 256)
 //   (bf16, batches above 128, operands streamed into LDS).
 // AUTO tunes each configuration online: its launches run the feasible
-// tilings in turn, timed (two launches each), until the fastest is kept; any other value forces that tiling where it applies
-// (W for an infeasible split, L where no whole-batch tiling applies).
+// tilings in turn, timed (two launches each), until the fastest is kept.
+// Any other value forces that tiling where it applies (L for LS without
+// room for the partials, W for another infeasible split, L where no
+// whole-batch tiling applies).
 enum GemmTiling {
   GEMM_TILING_AUTO = 0,
   GEMM_TILING_L = 1,
@@ -91,7 +94,8 @@ enum GemmTiling {
   GEMM_TILING_W = 4,
   GEMM_TILING_WS = 5,
   GEMM_TILING_VS = 6,
-  GEMM_TILING_COUNT = 7
+  GEMM_TILING_LS = 7,
+  GEMM_TILING_COUNT = 8
 };
 void set_gemm_tiling(int tiling);
 // Configurations whose AUTO tiling is still being tuned (process-wide).

@@ -1966,6 +1966,7 @@ bool tiling_fits(int t, bool bf16, const GemmArgs& g, int n_slots) {
     case GEMM_TILING_L: case GEMM_TILING_M: case GEMM_TILING_S: return true;
     case GEMM_TILING_W: return bf16 && g.N > 128;
     case GEMM_TILING_WS: case GEMM_TILING_VS: return bf16 && g.N > 128 && split_fits(g, n_slots);
+    case GEMM_TILING_LS: return split_fits(g, n_slots);
   }
   return false;
 }
@@ -1980,6 +1981,11 @@ hipError_t launch_tiling(const GemmArgs& g_in, int n_slots, hipStream_t s, int t
       if (t == GEMM_TILING_WS) return gemm_launch_shape<true, MODE, SHAPE_W, true>(g, n_slots, s);
       return gemm_launch_shape<true, MODE, SHAPE_V, true>(g, n_slots, s);
     }
+  }
+  if (t == GEMM_TILING_LS) {
+    GemmArgs g = g_in;
+    g.part_slot = static_cast<int64_t>((g.K + KCHUNK - 1) / KCHUNK) * g.N * g.out_ld;
+    return gemm_launch_shape<BF16, MODE, SHAPE_L, true>(g, n_slots, s);
   }
   if (t == GEMM_TILING_M) return gemm_launch_shape<BF16, MODE, SHAPE_M, false>(g_in, n_slots, s);
   if (t == GEMM_TILING_S) return gemm_launch_shape<BF16, MODE, SHAPE_S, false>(g_in, n_slots, s);
@@ -2079,8 +2085,9 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
     const int forced = g_forced_tiling.load();
     if (forced != GEMM_TILING_AUTO) {
       int t = forced;
-      if (!tiling_fits(t, BF16, g, n_slots)) t = (t == GEMM_TILING_W || !BF16 || g.N <= 128)
-                                                      ? GEMM_TILING_L : GEMM_TILING_W;
+      if (!tiling_fits(t, BF16, g, n_slots))
+        t = (t == GEMM_TILING_W || t == GEMM_TILING_LS || !BF16 || g.N <= 128) ? GEMM_TILING_L
+                                                                                : GEMM_TILING_W;
       return launch_tiling<BF16, MODE>(g, n_slots, s, t);
     }
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;

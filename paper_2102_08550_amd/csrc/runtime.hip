@@ -851,7 +851,8 @@ oscars_status oscars_broadcast(const float* global, float* replicas, int32_t K, 
 }
 
 oscars_status oscars_set_gemm_tiling(int32_t tiling) {
-  static_assert(OSCARS_TILING_COUNT == GEMM_TILING_COUNT && OSCARS_TILING_VS == GEMM_TILING_VS,
+  static_assert(OSCARS_TILING_COUNT == GEMM_TILING_COUNT && OSCARS_TILING_VS == GEMM_TILING_VS &&
+                    OSCARS_TILING_LS == GEMM_TILING_LS,
                 "tiling codes of the C ABI and of the launchers agree");
   if (tiling < 0 || tiling >= OSCARS_TILING_COUNT) return OSCARS_E_INVALID;
   set_gemm_tiling(tiling);
