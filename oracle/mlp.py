@@ -22,8 +22,11 @@ nearest even on the float32 bits).
 
 Pinned by tests: central finite differences in float64 on tiny networks, the
 closed-form gradient of softmax regression, one step of ``torch.optim.SGD``
-on ``nn.Linear``/``ReLU``/``CrossEntropyLoss`` (CPU, float64), and bf16
-rounding against torch's float32 -> bfloat16 conversion.
+on ``nn.Linear``/``ReLU``/``CrossEntropyLoss`` (CPU, float64), bf16
+rounding against torch's float32 -> bfloat16 conversion, and the bf16
+gradient, step and evaluation against an independent torch float64 autograd
+reference that rounds at the points listed above (and at no other), with one
+negative control per rounding point.
 """
 from __future__ import annotations
 
