@@ -2,6 +2,8 @@
 through the oracle on the same seeded inputs, and compare."""
 from __future__ import annotations
 
+import json
+import os
 import sys
 
 import numpy as np
@@ -20,10 +22,46 @@ def say(msg):
 
 
 def rel_err(a_layers, b_layers) -> float:
+    """One norm-wise relative error over every parameter (a summary only: the
+    assertions are per tensor, see tensor_errors)."""
     num = sum(float(np.sum((np.asarray(a, np.float64) - np.asarray(b, np.float64)) ** 2))
               for la, lb in zip(a_layers, b_layers) for a, b in zip(la, lb))
     den = sum(float(np.sum(np.asarray(b, np.float64) ** 2)) for lb in b_layers for b in lb)
     return (num / den) ** 0.5
+
+
+def tensor_errors(a_layers, b_layers):
+    """Per tensor (W1, b1, W2, ...): ``rel`` = ||a - b|| / ||b|| and ``max`` =
+    max |a - b| / max |b|, element by element over the whole tensor."""
+    out = {}
+    for l, (la, lb) in enumerate(zip(a_layers, b_layers), start=1):
+        for kind, a, b in (("W", la[0], lb[0]), ("b", la[1], lb[1])):
+            a = np.asarray(a, np.float64).ravel()
+            b = np.asarray(b, np.float64).ravel()
+            d = np.abs(a - b)
+            out[f"{kind}{l}"] = {
+                "rel": float(np.linalg.norm(d) / max(np.linalg.norm(b), 1e-300)),
+                "max": float(d.max() / max(np.abs(b).max(), 1e-300)),
+            }
+    return out
+
+
+def assert_tensors_close(errs, tol, where=""):
+    """Every tensor within ``tol`` in both measures of tensor_errors."""
+    for t, e in errs.items():
+        assert e["rel"] <= tol and e["max"] <= tol, f"{where} {t}: {e} (tol {tol})"
+
+
+def record(name, payload):
+    """Keep the achieved agreement of a GPU parity test on record: a JSON
+    file per test under gpurun_out/parity/ (the folder that a GPU run hands
+    back)."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    d = os.path.join(root, "gpurun_out", "parity")
+    os.makedirs(d, exist_ok=True)
+    safe = "".join(c if c.isalnum() or c in "-_." else "_" for c in name)
+    with open(os.path.join(d, f"{safe}.json"), "w") as f:
+        json.dump(payload, f, indent=1, sort_keys=True)
 
 
 def oracle_tau(cfg, rounds):
