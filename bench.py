@@ -6,8 +6,10 @@ A step is one Oscars round over the whole hot path: Algorithm 1 (tau from the
 workers' iteration times), the mini-batch index table, tau_k local SGD steps
 of every simulated worker (forward, loss gradient, backward-data,
 backward-weight + SGD update, finished workers masked out), and the
-parameter-server aggregation with broadcast.  Inputs are resident in HBM
-before the timed region.  Prints one JSON line.
+parameter-server aggregation into the global model, all in one
+oscars_round (every worker's first step reads the global model, so no
+broadcast copies are written).  Inputs are resident in HBM before the timed
+region.  Prints one JSON line.
 
 Default workload: MLP 4096-4096-4096-4096-1000, bf16 inputs/weights with fp32
 accumulation and fp32 masters, K = 8 workers with speed factors
@@ -335,7 +337,7 @@ def main():
     while True:
         run.round(tau_for(n_tune))
         n_tune += 1
-        if P.tuning_pending() == 0 or n_tune >= 64:
+        if run.ctx.tuning_pending() == 0 or n_tune >= 64:
             break
     torch.cuda.synchronize()
     print(f"[bench] {n_tune} tuning rounds", file=sys.stderr, flush=True)

@@ -100,11 +100,16 @@ typedef struct {
 } oscars_shards;
 
 /* Create a context for K replicas of `model`, mini-batches up to max_batch.
- * Allocates the device workspace (activations, bf16 weight copies, index
- * tables) on the current HIP device (and, under OSCARS_BACKWARD_AUTO, the
- * first local steps of a bf16 model add scratch replicas for timing the
- * backward paths; see oscars_set_backward).  `hip_stream` (a hipStream_t, NULL =
- * null stream) is the stream oscars_local_steps enqueues on. */
+ * Allocates, on the current HIP device, the whole device workspace the
+ * local steps use: activations, bf16 weight copies, split-K partials, the
+ * index table and loss buffer for rounds of up to 64 local steps per worker
+ * (with pinned host staging), and, for bf16 models with hidden layers, the
+ * scratch replicas on which OSCARS_BACKWARD_AUTO times the backward paths
+ * (K x the widest hidden layer, fp32 + bf16; left out where they would take
+ * more than a quarter of the free device memory, and then nothing is timed).
+ * `hip_stream` (a hipStream_t, NULL = null stream) is the stream
+ * oscars_local_steps enqueues on.  The context owns its tuning state (GEMM
+ * tilings, backward path): contexts do not share it. */
 oscars_status oscars_create(oscars_ctx** out, const oscars_model* model, int32_t K,
                             int32_t max_batch, void* hip_stream);
 /* Free the workspace.  NULL is allowed.  Waits for the context's stream. */
@@ -164,6 +169,8 @@ oscars_status oscars_sample_indices(const oscars_shards* shards, int32_t K, int3
                                     int64_t* rows_out);
 
 /* Local SGD of Eq. 4 (second branch) for every worker, batched on the GPU.
+ * Allocates no device memory unless some worker runs more than 64 steps in
+ * one call (the index table then grows, once, after waiting for the stream).
  *   replicas  device [K][oscars_num_params] fp32 master parameters, one replica
  *             per worker, 16-byte aligned; updated in place;
  *   shards    training data and shards (K + 1 offsets);
@@ -206,12 +213,16 @@ oscars_status oscars_round_losses(oscars_ctx* ctx, float* losses);
  * x, max_batch rows at a time, on the context's stream:
  *   params    device [n_pad] fp32, flat layout (e.g. the global model);
  *   x, y      device, as in oscars_shards (dtype of the model);
- *   loss_sum  out: summed softmax cross-entropy (fp32 per row, summed in
- *             double in row order);
+ *   n_rows    1 <= n_rows <= 2^31 - 65;
+ *   loss_sum  out: summed softmax cross-entropy (fp32 per row, summed on the
+ *             GPU in double in a fixed order: 256 contiguous runs of rows,
+ *             each in row order, the run sums left to right);
  *   correct   out: rows whose label's logit is the largest (ties count).
  * Uses the context's activation workspace (not the losses of the last
- * local steps), allocates and frees temporary device buffers, and waits for
- * the stream.  Not for a stream being captured into a graph. */
+ * local steps), allocates and frees temporary device buffers (the row
+ * table, per-row losses and flags: 12 bytes per row), times GEMM tilings
+ * the context has not decided yet, and waits for the stream.  Not for a
+ * stream being captured into a graph. */
 oscars_status oscars_evaluate(oscars_ctx* ctx, const float* params, const void* x,
                               const int32_t* y, int64_t n_rows, double* loss_sum,
                               int64_t* correct);
@@ -263,7 +274,7 @@ enum {
 oscars_status oscars_profile_begin(oscars_ctx* ctx, uint32_t kind_mask);
 oscars_status oscars_profile_end(oscars_ctx* ctx, double* ms, int64_t* launches);
 
-/* Tiling of the forward and backward-data GEMMs, process-wide (a tuning and
+/* Tiling of the forward and backward-data GEMMs of one context (a tuning and
  * testing aid).  Every tiling sums each output in the same order (K in
  * chunks of 1024 summed left to right), so results are bit-identical
  * whatever the tiling; only the speed differs.
@@ -295,16 +306,16 @@ enum {
   OSCARS_TILING_LS = 7,
   OSCARS_TILING_COUNT = 8
 };
-oscars_status oscars_set_gemm_tiling(int32_t tiling);
+oscars_status oscars_set_gemm_tiling(oscars_ctx* ctx, int32_t tiling);
 
-/* Number of forward / backward-data GEMM configurations, over the whole
- * process, whose tiling OSCARS_TILING_AUTO is still tuning (seen at least
- * once, not yet decided), into *configurations.  A caller that times the
- * steady state runs rounds until it reads 0.  Returns OSCARS_E_INVALID for a
- * null pointer. */
-oscars_status oscars_tuning_pending(int32_t* configurations);
+/* Number of forward / backward-data GEMM configurations of this context
+ * whose tiling OSCARS_TILING_AUTO is still tuning (seen at least once, not
+ * yet decided), into *configurations.  A caller that times the steady state
+ * runs rounds until it reads 0.  Returns OSCARS_E_INVALID for a null
+ * pointer. */
+oscars_status oscars_tuning_pending(const oscars_ctx* ctx, int32_t* configurations);
 
-/* Backward pass of the hidden layers (l >= 2) of bf16 models, process-wide
+/* Backward pass of the hidden layers (l >= 2) of a bf16 model, per context
  * (a tuning and testing aid).  By default one launch per layer does
  * backward-data, backward-weight and the SGD update of Eq. 4 (Approach): it
  * rounds the fp32 master it streams for the update to the bf16 weights the
@@ -318,13 +329,12 @@ oscars_status oscars_tuning_pending(int32_t* configurations);
  *     context of: the fused launch with each feasible number of 1024-output
  *     chunks per workgroup (all; then half, a quarter, ... down to one,
  *     where the context's partial buffer holds the split), and the separate
- *     launches.  Each runs three times there on scratch replicas (allocated
- *     then: K x the widest hidden layer, fp32 and bf16), the faster of its
- *     last two runs counting.  Untimed -- on a stream being captured into a
- *     graph, or where the scratch would take more than a quarter of the
- *     free device memory --: fused, split over the number of workgroups per
- *     64-wide input strip that fills the last pass over the CUs best (the
- *     fewest on ties);
+ *     launches.  Each runs three times there on the scratch replicas
+ *     oscars_create allocated, the faster of its last two runs counting.
+ *     Untimed -- on a stream being captured into a graph, or where
+ *     oscars_create left the scratch out --: fused, split over the number of
+ *     workgroups per 64-wide input strip that fills the last pass over the
+ *     CUs best (the fewest on ties);
  *   OSCARS_BACKWARD_SEPARATE: backward-data and update launches;
  *   OSCARS_BACKWARD_FUSED: fused, never split;
  *   OSCARS_BACKWARD_FUSED_SPLIT: fused, split wherever there is more than one
@@ -339,7 +349,7 @@ enum {
   OSCARS_BACKWARD_FUSED_SPLIT = 3,
   OSCARS_BACKWARD_COUNT = 4
 };
-oscars_status oscars_set_backward(int32_t mode);
+oscars_status oscars_set_backward(oscars_ctx* ctx, int32_t mode);
 
 /* The backward path of layer `layer` (1..L) in oscars_local_steps and
  * oscars_round of this context with `replicas` active replicas (1..K) and

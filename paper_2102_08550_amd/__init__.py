@@ -71,9 +71,9 @@ _SIGS = {
     "oscars_set_cursors": (_i32, [_vp, _P(_i64)]),
     "oscars_profile_begin": (_i32, [_vp, _u32]),
     "oscars_profile_end": (_i32, [_vp, _P(ctypes.c_double), _P(_i64)]),
-    "oscars_set_gemm_tiling": (_i32, [_i32]),
-    "oscars_tuning_pending": (_i32, [_P(_i32)]),
-    "oscars_set_backward": (_i32, [_i32]),
+    "oscars_set_gemm_tiling": (_i32, [_vp, _i32]),
+    "oscars_tuning_pending": (_i32, [_vp, _P(_i32)]),
+    "oscars_set_backward": (_i32, [_vp, _i32]),
     "oscars_backward_path": (_i32, [_vp, _i32, _i32, _i32, _P(_i32)]),
     "oscars_broadcast": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp]),
     "oscars_plan_tau": (_i32, [_P(ctypes.c_double), _i32, _i32, _i64, _P(_i64), _P(_i64), _P(_i32)]),
@@ -200,18 +200,6 @@ TILINGS = {"auto": TILING_AUTO, "L": TILING_L, "M": TILING_M, "S": TILING_S, "W"
            "WS": TILING_WS, "VS": TILING_VS, "LS": TILING_LS}
 
 
-def set_gemm_tiling(tiling: int):
-    """Process-wide tiling of the forward / backward-data GEMMs (AUTO: tuned
-    online per configuration, fastest kept)."""
-    _check(_lib().oscars_set_gemm_tiling(int(tiling)), "oscars_set_gemm_tiling")
-
-
-def tuning_pending() -> int:
-    """GEMM configurations whose AUTO tiling is still being tuned."""
-    n = ctypes.c_int32(0)
-    _check(_lib().oscars_tuning_pending(ctypes.byref(n)), "oscars_tuning_pending")
-    return int(n.value)
-
 
 # Backward pass of hidden bf16 layers (oscars_set_backward); results are
 # bit-identical in every mode.
@@ -219,12 +207,6 @@ BACKWARD_AUTO, BACKWARD_SEPARATE, BACKWARD_FUSED, BACKWARD_FUSED_SPLIT = range(4
 BACKWARDS = {"auto": BACKWARD_AUTO, "separate": BACKWARD_SEPARATE, "fused": BACKWARD_FUSED,
              "fused_split": BACKWARD_FUSED_SPLIT}
 
-
-def set_backward(mode: int):
-    """Process-wide backward of hidden bf16 layers: AUTO (fused backward-data
-    + update, split over output chunks when CUs would idle), SEPARATE, FUSED,
-    FUSED_SPLIT."""
-    _check(_lib().oscars_set_backward(int(mode)), "oscars_set_backward")
 
 
 def aggregate(global_, replicas, weights: Sequence[float], K: int, n: int, ld: int,
@@ -372,6 +354,23 @@ class Context:
     def set_cursors(self, steps_done: Sequence[int]):
         a, ap = _arr(steps_done, np.int64)
         _check(_lib().oscars_set_cursors(self._h, ap), "oscars_set_cursors")
+
+    def set_gemm_tiling(self, tiling: int):
+        """Tiling of this context's forward / backward-data GEMMs (AUTO: tuned
+        online per configuration, fastest kept); restarts the tuning."""
+        _check(_lib().oscars_set_gemm_tiling(self._h, int(tiling)), "oscars_set_gemm_tiling")
+
+    def tuning_pending(self) -> int:
+        """This context's GEMM configurations whose AUTO tiling is still being
+        tuned."""
+        n = ctypes.c_int32(0)
+        _check(_lib().oscars_tuning_pending(self._h, ctypes.byref(n)), "oscars_tuning_pending")
+        return int(n.value)
+
+    def set_backward(self, mode: int):
+        """Backward of this context's hidden bf16 layers: AUTO (timed per
+        configuration), SEPARATE, FUSED, FUSED_SPLIT."""
+        _check(_lib().oscars_set_backward(self._h, int(mode)), "oscars_set_backward")
 
     def backward_path(self, layer: int, batch: int, replicas: int) -> int:
         """Backward of `layer` (1..L) with `replicas` active replicas: 1 fused,

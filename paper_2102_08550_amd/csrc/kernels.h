@@ -74,7 +74,16 @@ struct GemmArgs {
   int out_bf16;  // FWD / DGRAD: store bf16 (else fp32)
 };
 
-hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s);
+// The tiling state of one context (forced tiling, online tuning, choices).
+struct GemmTuner;
+GemmTuner* gemm_tuner_create();  // nullptr when out of host memory
+void gemm_tuner_destroy(GemmTuner* t);
+
+// tuner: the context's tiling state (nullptr: the fixed rule, nothing timed);
+// tune = false: nothing is timed and no event is created -- a configuration
+// the tuner has decided keeps its choice, any other takes the fixed rule.
+hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s,
+                       GemmTuner* tuner, bool tune = true);
 
 // Forward / backward-data tilings (backward-weight always uses one):
 //   L 128 x 128, M 64 x 128, S 64 x 64 (register-staged operands), and LS,
@@ -97,9 +106,9 @@ enum GemmTiling {
   GEMM_TILING_LS = 7,
   GEMM_TILING_COUNT = 8
 };
-void set_gemm_tiling(int tiling);
-// Configurations whose AUTO tiling is still being tuned (process-wide).
-int gemm_tuning_pending();
+void gemm_tuner_set_tiling(GemmTuner* t, int tiling);
+// Configurations whose AUTO tiling is still being tuned by this tuner.
+int gemm_tuner_pending(GemmTuner* t);
 // While on (for the calling thread), an AUTO configuration not decided yet is
 // decided at its next launch: every feasible tiling timed there and then, the
 // fastest kept (for launches that are themselves being timed).
@@ -115,23 +124,24 @@ void set_gemm_tune_now(bool on);
 // that is exactly -0).  Batches of at most 256 rows, inputs a multiple of 8,
 // W_l within 32-bit buffer offsets (backward_fusable).
 bool backward_fusable(const GemmArgs& g);
-bool backward_fused_enabled();
-// cps_forced > 0: each workgroup covers that many KCHUNK ranges of outputs
-// (all of them where the partial buffer cannot hold the split); 0: by mode.
-hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s, int cps_forced = 0);
+bool backward_fused_enabled(int mode);
+// mode: the context's BackwardMode; cps_forced > 0: each workgroup covers
+// that many KCHUNK ranges of outputs (all of them where the partial buffer
+// cannot hold the split); 0: by mode.
+hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s, int mode,
+                            int cps_forced = 0);
 // The feasible ranges per workgroup (all chunks first, then halving down to
 // one), at most `max` of them written to cps; returns their number.
 int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max);
-// Backward of hidden bf16 layers: AUTO (fused, the o chunks split over the
-// workgroup count that best fills the last CU pass, or the separate
-// launches, whichever the caller timed faster for the configuration),
+// Backward of hidden bf16 layers (a per-context setting): AUTO (fused, the
+// o chunks split over the workgroup count that best fills the last CU pass,
+// or the separate launches, whichever the caller timed faster for the
+// configuration),
 // SEPARATE (backward-data and update kernels), FUSED (never split),
 // FUSED_SPLIT (one chunk per workgroup wherever there is more than one chunk
 // and the partial buffer holds them).
 enum BackwardMode { BACKWARD_AUTO = 0, BACKWARD_SEPARATE = 1, BACKWARD_FUSED = 2,
                     BACKWARD_FUSED_SPLIT = 3, BACKWARD_MODE_COUNT = 4 };
-void set_backward_mode(int mode);
-int backward_mode();
 
 // Softmax cross-entropy on logits [slot][B][ld]: delta = (softmax - onehot)/B
 // stored as bf16 or fp32 into delta [slot][B][ld] (columns C..ld-1 zeroed),
@@ -146,6 +156,14 @@ hipError_t launch_softmax_ce(const float* logits, int64_t ld, int64_t slot_strid
 hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int32_t* order,
                             uint16_t* wcopy, int64_t wcopy_slot, int64_t n, int n_slots,
                             hipStream_t s);
+
+// Held-out evaluation: the row table [64 slot entries = 0][i = 0 .. n-1]
+// that the forward pass gathers through, and the reduction of the per-row
+// losses (double: 256 contiguous runs of rows, each in row order, the run
+// sums left to right) and correct flags (int64) into *out_loss, *out_hits.
+hipError_t launch_eval_rows(int32_t* table, int64_t n, hipStream_t s);
+hipError_t launch_eval_reduce(const float* loss, const int32_t* hit, int64_t n, double* out_loss,
+                              int64_t* out_hits, hipStream_t s);
 
 // replicas[k * ld + i] = g[i] for k < K, i < n (non-temporal stores).
 hipError_t launch_broadcast(const float* g, float* replicas, int K, int64_t n, int64_t ld,

@@ -24,6 +24,7 @@
 #include <atomic>
 #include <map>
 #include <mutex>
+#include <new>
 #include <tuple>
 #include <type_traits>
 #include <vector>
@@ -1796,6 +1797,48 @@ __global__ __launch_bounds__(256) void cast_bf16_kernel(const float* master, int
   }
 }
 
+// Evaluation row table: table[z] = 0 for the 64 slot entries, then
+// table[64 + i] = i for the n rows.
+__global__ __launch_bounds__(256) void eval_rows_kernel(int32_t* table, int64_t n) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n + 64;
+       i += stride)
+    table[i] = i < 64 ? 0 : static_cast<int32_t>(i - 64);
+}
+
+// Summed loss and correct count of n evaluated rows, one workgroup: thread t
+// sums the contiguous run of rows [t * run, (t + 1) * run) in row order in
+// double (run = ceil(n / 256)); thread 0 adds the 256 run sums left to right.
+// Fixed order: the result does not depend on anything but the inputs.
+__global__ __launch_bounds__(256) void eval_reduce_kernel(const float* loss, const int32_t* hit,
+                                                          int64_t n, double* out_loss,
+                                                          int64_t* out_hits) {
+  __shared__ double part_loss[256];
+  __shared__ int64_t part_hits[256];
+  const int t = threadIdx.x;
+  const int64_t run = (n + 255) / 256;
+  const int64_t r0 = t * run, r1 = r0 + run < n ? r0 + run : n;
+  double acc = 0.0;
+  int64_t hits = 0;
+  for (int64_t i = r0; i < r1; ++i) {
+    acc += static_cast<double>(loss[i]);
+    hits += hit[i];
+  }
+  part_loss[t] = acc;
+  part_hits[t] = hits;
+  __syncthreads();
+  if (t == 0) {
+    double sum = 0.0;
+    int64_t h = 0;
+    for (int i = 0; i < 256; ++i) {
+      sum += part_loss[i];
+      h += part_hits[i];
+    }
+    *out_loss = sum;
+    *out_hits = h;
+  }
+}
+
 struct AggWeights {
   float w[OSCARS_MAX_K];
 };
@@ -2010,8 +2053,6 @@ int static_tiling(bool bf16, const GemmArgs& g, int n_slots) {
   return GEMM_TILING_S;
 }
 
-std::atomic<int> g_forced_tiling{GEMM_TILING_AUTO};
-
 struct TuneKey {
   int dev, bf16, mode, M, N, K, slots, gather, split;
   bool operator<(const TuneKey& o) const {
@@ -2066,12 +2107,32 @@ struct TuneState {
     return hipSuccess;
   }
 };
-std::mutex g_tune_mu;
-std::map<TuneKey, TuneState> g_tune;  // every device, precision and mode
 thread_local bool t_tune_now = false;  // set_gemm_tune_now
 
+}  // namespace
+
+// The tiling state of one context: a forced tiling, or per configuration
+// (device, precision, mode, shape, active replicas, gather, split) the online
+// tuning and its choice.
+struct GemmTuner {
+  std::mutex mu;
+  int forced = GEMM_TILING_AUTO;
+  std::map<TuneKey, TuneState> map;
+  ~GemmTuner() {
+    for (auto& kv : map)
+      for (TuneState::Timed& t : kv.second.timed)
+        for (hipEvent_t e : t.ev)
+          if (e) (void)hipEventDestroy(e);
+  }
+};
+
+namespace {
+
+// tuner == nullptr, or tune == false: no timing, no events; a configuration
+// the tuner has decided keeps its choice, any other takes the fixed rule.
 template <bool BF16, int MODE>
-hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
+hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s, GemmTuner* tuner,
+                       bool tune) {
   if constexpr (MODE == GEMM_WGRAD) {
     if constexpr (BF16) {
       const int64_t gx = static_cast<int64_t>((g.M + 127) / 128) * ((g.N + 127) / 128);
@@ -2082,12 +2143,24 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
     }
     return gemm_launch_shape<BF16, MODE, SHAPE_L, false>(g, n_slots, s);
   } else {
-    const int forced = g_forced_tiling.load();
+    if (!tuner) return launch_tiling<BF16, MODE>(g, n_slots, s, static_tiling(BF16, g, n_slots));
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    const TuneKey key{dev, BF16, MODE, g.M, g.N, g.K, n_slots, g.gather != nullptr,
+                      split_fits(g, n_slots)};
+    std::lock_guard<std::mutex> lock(tuner->mu);
+    const int forced = tuner->forced;
     if (forced != GEMM_TILING_AUTO) {
       int t = forced;
       if (!tiling_fits(t, BF16, g, n_slots))
         t = (t == GEMM_TILING_W || t == GEMM_TILING_LS || !BF16 || g.N <= 128) ? GEMM_TILING_L
                                                                                 : GEMM_TILING_W;
+      return launch_tiling<BF16, MODE>(g, n_slots, s, t);
+    }
+    if (!tune) {
+      const auto it = tuner->map.find(key);
+      const int t = it != tuner->map.end() && it->second.choice >= 0
+                        ? it->second.choice : static_tiling(BF16, g, n_slots);
       return launch_tiling<BF16, MODE>(g, n_slots, s, t);
     }
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -2100,12 +2173,7 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
     // event pairs are read at later launches without waiting.  Once every
     // candidate has kTuneRuns timed launches, the one with the smallest time
     // (its fastest launch) is kept.
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
-    const TuneKey key{dev, BF16, MODE, g.M, g.N, g.K, n_slots, g.gather != nullptr,
-                      split_fits(g, n_slots)};
-    std::lock_guard<std::mutex> lock(g_tune_mu);
-    TuneState& ts = g_tune[key];
+    TuneState& ts = tuner->map[key];
     if (ts.choice >= 0) return launch_tiling<BF16, MODE>(g, n_slots, s, ts.choice);
     if (ts.nc == 0) {
       for (int t = GEMM_TILING_L; t < GEMM_TILING_COUNT; ++t)
@@ -2171,12 +2239,16 @@ hipError_t gemm_launch(const GemmArgs& g, int n_slots, hipStream_t s) {
 
 }  // namespace
 
-void set_gemm_tiling(int tiling) {
-  std::lock_guard<std::mutex> lock(g_tune_mu);
-  g_forced_tiling.store(tiling);
+GemmTuner* gemm_tuner_create() { return new (std::nothrow) GemmTuner(); }
+
+void gemm_tuner_destroy(GemmTuner* t) { delete t; }
+
+void gemm_tuner_set_tiling(GemmTuner* tuner, int tiling) {
+  std::lock_guard<std::mutex> lock(tuner->mu);
+  tuner->forced = tiling;
   // AUTO starts over: every configuration is tuned again at its next launches
   // (event pairs still in flight are left to complete and are not read).
-  for (auto& kv : g_tune) {
+  for (auto& kv : tuner->map) {
     TuneState& ts = kv.second;
     ts.nc = 0;
     ts.choice = -1;
@@ -2187,36 +2259,30 @@ void set_gemm_tiling(int tiling) {
 
 void set_gemm_tune_now(bool on) { t_tune_now = on; }
 
-int gemm_tuning_pending() {
-  std::lock_guard<std::mutex> lock(g_tune_mu);
+int gemm_tuner_pending(GemmTuner* tuner) {
+  std::lock_guard<std::mutex> lock(tuner->mu);
   int n = 0;
-  for (const auto& kv : g_tune) n += kv.second.nc > 0 && kv.second.choice < 0;  // launched, undecided
+  for (const auto& kv : tuner->map) n += kv.second.nc > 0 && kv.second.choice < 0;  // launched, undecided
   return n;
 }
 
-hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s) {
+hipError_t launch_gemm(const GemmArgs& g, GemmMode mode, bool bf16, int n_slots, hipStream_t s,
+                       GemmTuner* tuner, bool tune) {
   if (bf16) {
     switch (mode) {
-      case GEMM_FWD: return gemm_launch<true, GEMM_FWD>(g, n_slots, s);
-      case GEMM_DGRAD: return gemm_launch<true, GEMM_DGRAD>(g, n_slots, s);
-      case GEMM_WGRAD: return gemm_launch<true, GEMM_WGRAD>(g, n_slots, s);
+      case GEMM_FWD: return gemm_launch<true, GEMM_FWD>(g, n_slots, s, tuner, tune);
+      case GEMM_DGRAD: return gemm_launch<true, GEMM_DGRAD>(g, n_slots, s, tuner, tune);
+      case GEMM_WGRAD: return gemm_launch<true, GEMM_WGRAD>(g, n_slots, s, tuner, tune);
     }
   } else {
     switch (mode) {
-      case GEMM_FWD: return gemm_launch<false, GEMM_FWD>(g, n_slots, s);
-      case GEMM_DGRAD: return gemm_launch<false, GEMM_DGRAD>(g, n_slots, s);
-      case GEMM_WGRAD: return gemm_launch<false, GEMM_WGRAD>(g, n_slots, s);
+      case GEMM_FWD: return gemm_launch<false, GEMM_FWD>(g, n_slots, s, tuner, tune);
+      case GEMM_DGRAD: return gemm_launch<false, GEMM_DGRAD>(g, n_slots, s, tuner, tune);
+      case GEMM_WGRAD: return gemm_launch<false, GEMM_WGRAD>(g, n_slots, s, tuner, tune);
     }
   }
   return hipErrorInvalidValue;
 }
-
-namespace {
-std::atomic<int> g_backward_mode{BACKWARD_AUTO};
-}  // namespace
-
-void set_backward_mode(int mode) { g_backward_mode.store(mode); }
-int backward_mode() { return g_backward_mode.load(); }
 
 // Batches of at most FB_BMAX rows, whole 16-byte input chunks, and W_l (with
 // the chunks read ahead) under 1 GiB, so that 32-bit buffer offsets with an
@@ -2226,7 +2292,7 @@ bool backward_fusable(const GemmArgs& g) {
          static_cast<int64_t>(g.K + 6 * FB_TO) * g.M * 4 < (static_cast<int64_t>(1) << 30);
 }
 
-bool backward_fused_enabled() { return g_backward_mode.load() != BACKWARD_SEPARATE; }
+bool backward_fused_enabled(int mode) { return mode != BACKWARD_SEPARATE; }
 
 // Grid x = slots x strips x splits, slot slowest, strip fastest: with the
 // XCD-aware order the strips of one slot (which read the same delta) share
@@ -2249,14 +2315,14 @@ int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max) {
   return n;
 }
 
-hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s, int cps_forced) {
+hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s, int mode,
+                            int cps_forced) {
   if (!backward_fusable(g_in) || n_slots < 1) return hipErrorInvalidValue;
   GemmArgs g = g_in;
   const int strips = (g.M + FB_TI - 1) / FB_TI;
   const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
   g.part_slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
   const bool can_split = nchunks > 1 && g.part && g.part_slot * n_slots <= g.part_cap;
-  const int mode = g_backward_mode.load();
   int cps = nchunks;
   if (cps_forced > 0) {
     cps = can_split && cps_forced < nchunks ? cps_forced : nchunks;
@@ -2347,6 +2413,21 @@ hipError_t launch_cast_bf16(const float* master, int64_t master_slot, const int3
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(cast_bf16_kernel, dim3(static_cast<unsigned>(blocks), n_slots), dim3(256), 0,
                      s, master, master_slot, order, wcopy, wcopy_slot, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_eval_rows(int32_t* table, int64_t n, hipStream_t s) {
+  int64_t blocks = (n + 64 + 255) / 256;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL(eval_rows_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, table,
+                     n);
+  return hipGetLastError();
+}
+
+hipError_t launch_eval_reduce(const float* loss, const int32_t* hit, int64_t n, double* out_loss,
+                              int64_t* out_hits, hipStream_t s) {
+  hipLaunchKernelGGL(eval_reduce_kernel, dim3(1), dim3(256), 0, s, loss, hit, n, out_loss,
+                     out_hits);
   return hipGetLastError();
 }
 

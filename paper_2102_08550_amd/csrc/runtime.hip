@@ -38,6 +38,9 @@ int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 constexpr int kMaxTau = 4096;
+// Index-table, loss and staging capacity allocated by oscars_create: rounds
+// of up to this many local steps per worker need no allocation later.
+constexpr int kPreTau = 64;
 
 }  // namespace
 
@@ -87,6 +90,9 @@ struct oscars_ctx {
   bool cal_off = false;  // scratch too large for the free device memory: no timing
   hipEvent_t cal_ev[2] = {nullptr, nullptr};
 
+  GemmTuner* tuner = nullptr;        // tiling of this context's GEMM launches
+  int backward_mode = BACKWARD_AUTO;  // backward of hidden bf16 layers
+
   uint32_t prof_mask = 0;
   std::vector<hipEvent_t> ev_pool;
   std::vector<std::pair<int, int>> prof_recs;  // (kind, first event index)
@@ -107,6 +113,7 @@ void free_ctx(oscars_ctx* c) {
   for (hipEvent_t e : c->cal_ev)
     if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  gemm_tuner_destroy(c->tuner);
   delete c;
 }
 
@@ -117,6 +124,79 @@ hipError_t dev_alloc(oscars_ctx* c, size_t bytes, void** out) {
   c->allocs.push_back(p);
   e = hipMemsetAsync(p, 0, bytes, c->stream);
   *out = p;
+  return e;
+}
+
+// Index table (with host staging) and loss buffer for `need` table entries
+// and `loss_need` losses; grows them only when they are too small (waiting
+// for the stream first).  On failure the context keeps its old buffers.
+hipError_t ensure_tables(oscars_ctx* c, int64_t need, int64_t loss_need) {
+  hipError_t e = hipSuccess;
+  if (need > c->table_cap || loss_need > c->loss_cap || need > c->pinned_cap) {
+    e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return e;
+    c->upload_pending = false;
+  }
+  if (need > c->pinned_cap) {
+    int32_t* p = nullptr;
+    e = hipHostMalloc(reinterpret_cast<void**>(&p), need * sizeof(int32_t));
+    if (e != hipSuccess) return e;
+    if (c->pinned) (void)hipHostFree(c->pinned);
+    c->pinned = p;
+    c->pinned_cap = need;
+  }
+  if (need > c->table_cap) {
+    int32_t* p = nullptr;
+    e = hipMalloc(reinterpret_cast<void**>(&p), need * sizeof(int32_t));
+    if (e != hipSuccess) return e;
+    if (c->table_dev) (void)hipFree(c->table_dev);
+    c->table_dev = p;
+    c->table_cap = need;
+  }
+  if (loss_need > c->loss_cap) {
+    float* p = nullptr;
+    e = hipMalloc(reinterpret_cast<void**>(&p), loss_need * sizeof(float));
+    if (e != hipSuccess) return e;
+    if (c->loss_dev) (void)hipFree(c->loss_dev);
+    c->loss_dev = p;
+    c->loss_cap = loss_need;
+  }
+  return hipSuccess;
+}
+
+// Scratch replicas on which OSCARS_BACKWARD_AUTO times the backward paths of
+// the hidden layers of a bf16 model: K x the widest hidden layer (fp32 W and
+// b, bf16 W).  Skipped (no timing: c->cal_off) where it would take more than
+// a quarter of the free device memory.
+hipError_t alloc_calibration(oscars_ctx* c) {
+  if (!c->bf16 || c->L < 2) return hipSuccess;
+  for (int l = 2; l <= c->L; ++l) {
+    const int64_t w = static_cast<int64_t>(c->dims[l]) * c->dims[l - 1];
+    c->cal_w = std::max(c->cal_w, round_up(w, 8));
+    c->cal_layer = std::max(c->cal_layer, round_up(w + c->dims[l], 8));
+  }
+  size_t free_b = 0, total_b = 0;
+  hipError_t e = hipMemGetInfo(&free_b, &total_b);
+  if (e != hipSuccess) return e;
+  const double need = static_cast<double>(c->K) * (c->cal_layer * 4.0 + c->cal_w * 2.0);
+  if (need > static_cast<double>(free_b) / 4.0) {
+    c->cal_off = true;
+    return hipSuccess;
+  }
+  void* p = nullptr;
+  e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_layer * 4, &p);
+  c->cal_master = static_cast<float*>(p);
+  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_w * 2, &p);
+  c->cal_copy = static_cast<uint16_t*>(p);
+  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->K) * 4, &p);
+  c->cal_order = static_cast<int32_t*>(p);
+  std::vector<int32_t> ident(c->K);
+  for (int k = 0; k < c->K; ++k) ident[k] = k;
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->cal_order, ident.data(), ident.size() * 4, hipMemcpyHostToDevice,
+                       c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipEventCreate(&c->cal_ev[i]);
   return e;
 }
 
@@ -182,6 +262,11 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
   c->n_pad = off;
   c->cursors.assign(K, 0);
   c->samplers.resize(K);
+  c->tuner = gemm_tuner_create();
+  if (!c->tuner) {
+    delete c;
+    return OSCARS_E_NOMEM;
+  }
 
   hipError_t e = hipGetDevice(&c->device);
   if (e == hipSuccess && c->bf16) {
@@ -226,6 +311,11 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
     }
   }
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming);
+  if (e == hipSuccess) {
+    const int64_t rows = static_cast<int64_t>(K) * kPreTau * max_batch;
+    e = ensure_tables(c, 64 + rows, rows);
+  }
+  if (e == hipSuccess) e = alloc_calibration(c);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) {
     free_ctx(c);
@@ -273,21 +363,18 @@ oscars_status oscars_set_cursors(oscars_ctx* ctx, const int64_t* steps_done) {
 
 namespace {
 
-// tau_k local steps of every worker.  start == nullptr: worker k starts from
-// replica k.  Otherwise every worker starts from `start` (the global model of
-// a round): the first step reads `start` and writes replica k; workers with
-// tau_k = 0 get a copy of `start`.
 // Backward of hidden layer l of a bf16 model without a forced mode: at the
 // first launch of each (inputs, outputs, batch, replicas) the fused launch
 // (gf) with every feasible number of output chunks per workgroup (all, then
 // halving down to one), and the separate backward-data + update launches
-// (gd, gw), each run three times on scratch replicas, timed; the fastest of
-// the last two runs of each decides (the earlier candidate on ties).  The
-// real replicas and weight copies are untouched; every candidate writes the
-// delta of the layer below, which the real launch that follows recomputes.
-// *cps: the chunks per workgroup of the fused launch, or 0 for the separate
-// launches.  On a stream being captured into a graph nothing is timed: the
-// fused launch with the split its launcher picks (*cps = -1).
+// (gd, gw), each run three times on the scratch replicas oscars_create
+// allocated, timed; the fastest of the last two runs of each decides (the
+// earlier candidate on ties).  The real replicas and weight copies are
+// untouched; every candidate writes the delta of the layer below, which the
+// real launch that follows recomputes.  *cps: the chunks per workgroup of the
+// fused launch, or 0 for the separate launches.  On a stream being captured
+// into a graph, or without scratch, nothing is timed: the fused launch with
+// the split its launcher picks (*cps = -1).
 hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const GemmArgs& gd,
                            const GemmArgs& gw, int* cps) {
   *cps = -1;
@@ -300,39 +387,9 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
     *cps = it->second;
     return hipSuccess;
   }
+  // no scratch (too large for the free memory, see alloc_calibration): untimed
+  if (c->cal_off || !c->cal_master) return hipSuccess;
   hipError_t e = hipSuccess;
-  if (c->cal_off) return hipSuccess;
-  if (!c->cal_master) {
-    // scratch for the widest hidden layer, every replica; skipped (no timing,
-    // fused) where it would take more than a quarter of the free memory
-    for (int l = 2; l <= c->L; ++l) {
-      const int64_t w = static_cast<int64_t>(c->dims[l]) * c->dims[l - 1];
-      c->cal_w = std::max(c->cal_w, round_up(w, 8));
-      c->cal_layer = std::max(c->cal_layer, round_up(w + c->dims[l], 8));
-    }
-    size_t free_b = 0, total_b = 0;
-    e = hipMemGetInfo(&free_b, &total_b);
-    if (e != hipSuccess) return e;
-    const double need = static_cast<double>(c->K) * (c->cal_layer * 4.0 + c->cal_w * 2.0);
-    if (need > static_cast<double>(free_b) / 4.0) {
-      c->cal_off = true;
-      return hipSuccess;
-    }
-    void* p = nullptr;
-    e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_layer * 4, &p);
-    c->cal_master = static_cast<float*>(p);
-    if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->K) * c->cal_w * 2, &p);
-    c->cal_copy = static_cast<uint16_t*>(p);
-    if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(c->K) * 4, &p);
-    c->cal_order = static_cast<int32_t*>(p);
-    std::vector<int32_t> ident(c->K);
-    for (int k = 0; k < c->K; ++k) ident[k] = k;
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(c->cal_order, ident.data(), ident.size() * 4, hipMemcpyHostToDevice, c->stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
-    for (int i = 0; i < 2 && e == hipSuccess; ++i) e = hipEventCreate(&c->cal_ev[i]);
-    if (e != hipSuccess) return e;
-  }
   const int64_t wsize = static_cast<int64_t>(gf.M) * gf.K;  // W_l: outputs x inputs
   auto to_scratch = [&](GemmArgs& a) {
     a.master = c->cal_master;
@@ -370,10 +427,10 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
       float ms = 0.0f;
       e = hipEventRecord(c->cal_ev[0], c->stream);
       if (cand[i] > 0) {
-        if (e == hipSuccess) e = launch_bwd_fused(f, ns, c->stream, cand[i]);
+        if (e == hipSuccess) e = launch_bwd_fused(f, ns, c->stream, c->backward_mode, cand[i]);
       } else {
-        if (e == hipSuccess) e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream);
-        if (e == hipSuccess) e = launch_gemm(w, GEMM_WGRAD, true, ns, c->stream);
+        if (e == hipSuccess) e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream, c->tuner);
+        if (e == hipSuccess) e = launch_gemm(w, GEMM_WGRAD, true, ns, c->stream, c->tuner);
       }
       if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
       if (e == hipSuccess) e = hipEventSynchronize(c->cal_ev[1]);
@@ -390,6 +447,10 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
   return hipSuccess;
 }
 
+// tau_k local steps of every worker.  start == nullptr: worker k starts from
+// replica k.  Otherwise every worker starts from `start` (the global model of
+// a round): the first step reads `start` and writes replica k; workers with
+// tau_k = 0 get a copy of `start`.
 oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start,
                               const oscars_shards* s, const int32_t* tau, float lr, int32_t batch) {
   // ---- validation (no side effects on failure) ----
@@ -412,59 +473,36 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
   std::stable_sort(order.begin(), order.end(),
                    [&](int32_t a, int32_t b) { return tau[a] > tau[b]; });
   const int n_slots = static_cast<int>(order.size());
-  c->last_order = order;
-  c->last_tau.assign(tau, tau + K);
-  c->last_B = batch;
-  c->last_tau_max = n_slots ? tau[order[0]] : 0;
-  if (start) {
-    for (int k = 0; k < K; ++k) {
-      if (tau[k] > 0) continue;
-      hipError_t e = hipMemcpyAsync(replicas + static_cast<int64_t>(k) * c->n_pad, start,
-                                    c->n_pad * sizeof(float), hipMemcpyDeviceToDevice, c->stream);
-      if (e != hipSuccess) return hip_fail(e);
-    }
-  }
-  if (n_slots == 0) return OSCARS_OK;
-  const int tau_max = tau[order[0]];
+  const int tau_max = n_slots ? tau[order[0]] : 0;
   const int B = batch;
 
-  // ---- index table: order[64] then rows[slot][j][b] ----
+  // ---- index table capacity: order[64] then rows[slot][j][b] (grown only
+  // for more than kPreTau steps per worker; failures leave no side effects) ----
   const int64_t need = 64 + static_cast<int64_t>(n_slots) * tau_max * B;
+  const int64_t loss_need = static_cast<int64_t>(n_slots) * tau_max * B;
   hipError_t e = hipSuccess;
   if (c->upload_pending) {
     e = hipEventSynchronize(c->upload_done);
     if (e != hipSuccess) return hip_fail(e);
     c->upload_pending = false;
   }
-  if (need > c->pinned_cap) {
-    if (c->pinned) (void)hipHostFree(c->pinned);
-    c->pinned = nullptr;
-    c->pinned_cap = 0;
-    e = hipHostMalloc(reinterpret_cast<void**>(&c->pinned), need * sizeof(int32_t));
-    if (e != hipSuccess) return OSCARS_E_NOMEM;
-    c->pinned_cap = need;
+  e = ensure_tables(c, need, loss_need);
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) return OSCARS_E_NOMEM;
+  if (e != hipSuccess) return hip_fail(e);
+
+  c->last_order = order;
+  c->last_tau.assign(tau, tau + K);
+  c->last_B = batch;
+  c->last_tau_max = tau_max;
+  if (start) {
+    for (int k = 0; k < K; ++k) {
+      if (tau[k] > 0) continue;
+      e = hipMemcpyAsync(replicas + static_cast<int64_t>(k) * c->n_pad, start,
+                         c->n_pad * sizeof(float), hipMemcpyDeviceToDevice, c->stream);
+      if (e != hipSuccess) return hip_fail(e);
+    }
   }
-  const int64_t loss_need = static_cast<int64_t>(n_slots) * tau_max * B;
-  if (need > c->table_cap || loss_need > c->loss_cap) {
-    e = hipStreamSynchronize(c->stream);
-    if (e != hipSuccess) return hip_fail(e);
-  }
-  if (need > c->table_cap) {
-    if (c->table_dev) (void)hipFree(c->table_dev);
-    c->table_dev = nullptr;
-    c->table_cap = 0;
-    e = hipMalloc(reinterpret_cast<void**>(&c->table_dev), need * sizeof(int32_t));
-    if (e != hipSuccess) return OSCARS_E_NOMEM;
-    c->table_cap = need;
-  }
-  if (loss_need > c->loss_cap) {
-    if (c->loss_dev) (void)hipFree(c->loss_dev);
-    c->loss_dev = nullptr;
-    c->loss_cap = 0;
-    e = hipMalloc(reinterpret_cast<void**>(&c->loss_dev), loss_need * sizeof(float));
-    if (e != hipSuccess) return OSCARS_E_NOMEM;
-    c->loss_cap = loss_need;
-  }
+  if (n_slots == 0) return OSCARS_OK;
   int32_t* h_order = c->pinned;
   int32_t* h_rows = c->pinned + 64;
   for (int z = 0; z < 64; ++z) h_order[z] = z < n_slots ? order[z] : 0;
@@ -572,7 +610,7 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
       }
       g.out_ld = c->ld[l];
       g.out_slot = c->act_slot(l);
-      e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_gemm(g, GEMM_FWD, c->bf16, ns, c->stream); });
+      e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_gemm(g, GEMM_FWD, c->bf16, ns, c->stream, c->tuner); });
       if (e != hipSuccess) return hip_fail(e);
     }
     // loss gradient
@@ -629,7 +667,7 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
     };
     // backward, top layer first; dgrad(l) reads W_l before wgrad(l) updates it
     for (int l = L; l >= 1; --l) {
-      if (l > 1 && c->bf16 && backward_fused_enabled()) {
+      if (l > 1 && c->bf16 && backward_fused_enabled(c->backward_mode)) {
         // hidden layer of a bf16 model: backward-data, backward-weight and the
         // update in one launch (bit-identical to the two launches below)
         GemmArgs g{};
@@ -655,13 +693,16 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
         g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
         if (backward_fusable(g)) {
           int cps = -1;  // fused, split by the launcher's rule
-          if (backward_mode() == BACKWARD_AUTO) {
+          if (c->backward_mode == BACKWARD_AUTO) {
             e = choose_backward(c, ns, g, dgrad_args(l), wgrad_args(l), &cps);
             if (e != hipSuccess) return hip_fail(e);
           }
           if (cps != 0) {
             e = timed(c, OSCARS_KERNEL_BWD_FUSED,
-                      [&] { return launch_bwd_fused(g, ns, c->stream, cps > 0 ? cps : 0); });
+                      [&] {
+                        return launch_bwd_fused(g, ns, c->stream, c->backward_mode,
+                                                cps > 0 ? cps : 0);
+                      });
             if (e != hipSuccess) return hip_fail(e);
             continue;
           }
@@ -670,17 +711,117 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
       if (l > 1) {
         const GemmArgs g = dgrad_args(l);
         e = timed(c, OSCARS_KERNEL_DGRAD,
-                  [&] { return launch_gemm(g, GEMM_DGRAD, c->bf16, ns, c->stream); });
+                  [&] { return launch_gemm(g, GEMM_DGRAD, c->bf16, ns, c->stream, c->tuner); });
         if (e != hipSuccess) return hip_fail(e);
       }
       const GemmArgs g = wgrad_args(l);
       e = timed(c, OSCARS_KERNEL_WGRAD,
-                [&] { return launch_gemm(g, GEMM_WGRAD, c->bf16, ns, c->stream); });
+                [&] { return launch_gemm(g, GEMM_WGRAD, c->bf16, ns, c->stream, c->tuner); });
       if (e != hipSuccess) return hip_fail(e);
     }
   }
   for (int k = 0; k < K; ++k) c->cursors[k] += tau[k];
   return OSCARS_OK;
+}
+
+oscars_status check_evaluate(const oscars_ctx* c, const float* params, const void* x,
+                             const int32_t* y, int64_t n_rows, const double* loss_sum,
+                             const int64_t* correct) {
+  if (!c || !params || !x || !y || !loss_sum || !correct) return OSCARS_E_INVALID;
+  if (!aligned16(params) || !aligned16(x)) return OSCARS_E_INVALID;
+  if (n_rows < 1 || n_rows > 0x7FFFFFFF - 64) return OSCARS_E_INVALID;
+  return OSCARS_OK;
+}
+
+// Device bytes of an evaluation's temporaries: results (double loss, int64
+// count), then the row table [64 + n] int32, per-row losses [n] fp32 and
+// correct flags [n] int32, each part 256-byte aligned.
+struct EvalLayout {
+  int64_t table, loss, hit, end;
+  explicit EvalLayout(int64_t n) {
+    table = 256;
+    loss = table + round_up((64 + n) * 4, 256);
+    hit = loss + round_up(n * 4, 256);
+    end = hit + round_up(n * 4, 256);
+  }
+};
+
+size_t eval_bytes(int64_t n_rows) { return static_cast<size_t>(EvalLayout(n_rows).end); }
+
+// The forward pass of the local steps over rows 0 .. n_rows-1, max_batch rows
+// at a time, into the temporaries at `buf` (eval_bytes(n_rows) bytes of
+// device memory); then the fixed-order reduction and a copy of its two
+// results to the host.  tune = false: no GEMM tiling is timed (no events are
+// created); the tilings the context has decided, else the fixed rule.  Every
+// tiling gives the same bits.  Waits for the context's stream.
+hipError_t run_evaluate(oscars_ctx* c, const float* params, const void* x, const int32_t* y,
+                        int64_t n_rows, void* buf, bool tune, double* loss_sum, int64_t* correct) {
+  const EvalLayout lay(n_rows);
+  char* base = static_cast<char*>(buf);
+  struct Results {
+    double loss;
+    int64_t hits;
+  };
+  Results* d_res = reinterpret_cast<Results*>(base);
+  int32_t* d_tab = reinterpret_cast<int32_t*>(base + lay.table);
+  float* d_loss = reinterpret_cast<float*>(base + lay.loss);
+  int32_t* d_hit = reinterpret_cast<int32_t*>(base + lay.hit);
+  const int L = c->L, Bmax = c->max_batch;
+  hipError_t e = launch_eval_rows(d_tab, n_rows, c->stream);
+  // Weights as the forward pass reads them: the bf16 copy of params (one
+  // cast into the start-model buffer) or params themselves.
+  if (e == hipSuccess && c->bf16)
+    e = launch_cast_bf16(params, 0, d_tab, c->gq, 0, c->n_pad, 1, c->stream);
+  for (int64_t i0 = 0; i0 < n_rows && e == hipSuccess; i0 += Bmax) {
+    const int N = static_cast<int>(std::min<int64_t>(Bmax, n_rows - i0));
+    const int32_t* rows = d_tab + 64 + i0;
+    for (int l = 1; l <= L && e == hipSuccess; ++l) {
+      GemmArgs g{};
+      g.M = c->dims[l];
+      g.N = N;
+      g.K = c->dims[l - 1];
+      g.a_ext = g.K;
+      g.b_ext = g.K;
+      g.a = c->bf16 ? static_cast<const void*>(c->gq + c->w_off[l])
+                    : static_cast<const void*>(params + c->w_off[l]);
+      g.a_ld = c->dims[l - 1];
+      if (l == 1) {
+        g.b = x;
+        g.b_ld = c->dims[0];
+        g.gather = rows;
+        g.rows_out = c->act[0];
+        g.rows_out_ld = c->ld[0];
+      } else {
+        g.b = c->act[l - 1];
+        g.b_ld = c->ld[l - 1];
+      }
+      g.master = const_cast<float*>(params);  // not written by the forward pass
+      g.master_in = params;
+      g.b_off = c->b_off[l];
+      g.w_off = c->w_off[l];
+      g.order = d_tab;
+      g.part = c->part;
+      g.part_cap = c->part_cap;
+      g.out = l < L ? c->act[l] : static_cast<void*>(c->logits);
+      g.relu = l < L;
+      g.out_bf16 = l < L && c->bf16;
+      g.out_ld = c->ld[l];
+      e = launch_gemm(g, GEMM_FWD, c->bf16, 1, c->stream, c->tuner, tune);
+    }
+    if (e == hipSuccess)
+      e = launch_softmax_ce(c->logits, c->ld[L], c->act_slot(L), c->dims[L], N, y, rows, 0,
+                            c->delta[L], c->bf16, d_loss + i0, 0, 1, c->stream, d_hit + i0);
+  }
+  if (e == hipSuccess)
+    e = launch_eval_reduce(d_loss, d_hit, n_rows, &d_res->loss, &d_res->hits, c->stream);
+  Results h{};
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(&h, d_res, sizeof(Results), hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return e;
+  *loss_sum = h.loss;
+  *correct = h.hits;
+  return hipSuccess;
 }
 
 }  // namespace
@@ -734,91 +875,15 @@ oscars_status oscars_round_losses(oscars_ctx* c, float* losses) {
 
 oscars_status oscars_evaluate(oscars_ctx* c, const float* params, const void* x, const int32_t* y,
                               int64_t n_rows, double* loss_sum, int64_t* correct) {
-  if (!c || !params || !x || !y || !loss_sum || !correct) return OSCARS_E_INVALID;
-  if (!aligned16(params) || !aligned16(x)) return OSCARS_E_INVALID;
-  if (n_rows < 1 || n_rows > 0x7FFFFFFF) return OSCARS_E_INVALID;
-  const int L = c->L, Bmax = c->max_batch;
-  // Temporary buffers: [64 slot ids = 0][n_rows row ids], per-row loss and hit.
-  std::vector<int32_t> h_tab(64 + n_rows, 0);
-  for (int64_t i = 0; i < n_rows; ++i) h_tab[64 + i] = static_cast<int32_t>(i);
-  int32_t* d_tab = nullptr;
-  float* d_loss = nullptr;
-  int32_t* d_hit = nullptr;
-  auto release = [&]() {
-    if (d_tab) (void)hipFree(d_tab);
-    if (d_loss) (void)hipFree(d_loss);
-    if (d_hit) (void)hipFree(d_hit);
-  };
-  hipError_t e = hipStreamSynchronize(c->stream);
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&d_tab), h_tab.size() * sizeof(int32_t));
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&d_loss), n_rows * sizeof(float));
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&d_hit), n_rows * sizeof(int32_t));
-  if (e == hipSuccess)
-    e = hipMemcpy(d_tab, h_tab.data(), h_tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    release();
-    return e == hipErrorOutOfMemory ? OSCARS_E_NOMEM : hip_fail(e);
-  }
-  // Weights as the forward pass reads them: the bf16 copy of params (one
-  // cast into the start-model buffer) or params themselves.
-  if (c->bf16)
-    e = launch_cast_bf16(params, 0, d_tab, c->gq, 0, c->n_pad, 1, c->stream);
-  for (int64_t i0 = 0; i0 < n_rows && e == hipSuccess; i0 += Bmax) {
-    const int N = static_cast<int>(std::min<int64_t>(Bmax, n_rows - i0));
-    const int32_t* rows = d_tab + 64 + i0;
-    for (int l = 1; l <= L && e == hipSuccess; ++l) {
-      GemmArgs g{};
-      g.M = c->dims[l];
-      g.N = N;
-      g.K = c->dims[l - 1];
-      g.a_ext = g.K;
-      g.b_ext = g.K;
-      g.a = c->bf16 ? static_cast<const void*>(c->gq + c->w_off[l])
-                    : static_cast<const void*>(params + c->w_off[l]);
-      g.a_ld = c->dims[l - 1];
-      if (l == 1) {
-        g.b = x;
-        g.b_ld = c->dims[0];
-        g.gather = rows;
-        g.rows_out = c->act[0];
-        g.rows_out_ld = c->ld[0];
-      } else {
-        g.b = c->act[l - 1];
-        g.b_ld = c->ld[l - 1];
-      }
-      g.master = const_cast<float*>(params);  // not written by the forward pass
-      g.master_in = params;
-      g.b_off = c->b_off[l];
-      g.w_off = c->w_off[l];
-      g.order = d_tab;
-      g.part = c->part;
-      g.part_cap = c->part_cap;
-      g.out = l < L ? c->act[l] : static_cast<void*>(c->logits);
-      g.relu = l < L;
-      g.out_bf16 = l < L && c->bf16;
-      g.out_ld = c->ld[l];
-      e = launch_gemm(g, GEMM_FWD, c->bf16, 1, c->stream);
-    }
-    if (e == hipSuccess)
-      e = launch_softmax_ce(c->logits, c->ld[L], c->act_slot(L), c->dims[L], N, y, rows, 0,
-                            c->delta[L], c->bf16, d_loss + i0, 0, 1, c->stream, d_hit + i0);
-  }
-  std::vector<float> h_loss(e == hipSuccess ? n_rows : 0);
-  std::vector<int32_t> h_hit(e == hipSuccess ? n_rows : 0);
-  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
-  if (e == hipSuccess) e = hipMemcpy(h_loss.data(), d_loss, n_rows * sizeof(float), hipMemcpyDeviceToHost);
-  if (e == hipSuccess) e = hipMemcpy(h_hit.data(), d_hit, n_rows * sizeof(int32_t), hipMemcpyDeviceToHost);
-  release();
-  if (e != hipSuccess) return hip_fail(e);
-  double acc = 0.0;
-  int64_t hits = 0;
-  for (int64_t i = 0; i < n_rows; ++i) {
-    acc += h_loss[i];
-    hits += h_hit[i];
-  }
-  *loss_sum = acc;
-  *correct = hits;
-  return OSCARS_OK;
+  oscars_status st = check_evaluate(c, params, x, y, n_rows, loss_sum, correct);
+  if (st != OSCARS_OK) return st;
+  void* buf = nullptr;
+  hipError_t e = hipMalloc(&buf, eval_bytes(n_rows));
+  if (e != hipSuccess) return e == hipErrorOutOfMemory ? OSCARS_E_NOMEM : hip_fail(e);
+  e = run_evaluate(c, params, x, y, n_rows, buf, true, loss_sum, correct);
+  const hipError_t f = hipFree(buf);  // waits for the device
+  if (e == hipSuccess) e = f;
+  return e == hipSuccess ? OSCARS_OK : hip_fail(e);
 }
 
 oscars_status oscars_aggregate(float* global, float* replicas, const float* weights, int32_t K,
@@ -850,18 +915,18 @@ oscars_status oscars_broadcast(const float* global, float* replicas, int32_t K, 
   return e == hipSuccess ? OSCARS_OK : hip_fail(e);
 }
 
-oscars_status oscars_set_gemm_tiling(int32_t tiling) {
+oscars_status oscars_set_gemm_tiling(oscars_ctx* c, int32_t tiling) {
   static_assert(OSCARS_TILING_COUNT == GEMM_TILING_COUNT && OSCARS_TILING_VS == GEMM_TILING_VS &&
                     OSCARS_TILING_LS == GEMM_TILING_LS,
                 "tiling codes of the C ABI and of the launchers agree");
-  if (tiling < 0 || tiling >= OSCARS_TILING_COUNT) return OSCARS_E_INVALID;
-  set_gemm_tiling(tiling);
+  if (!c || tiling < 0 || tiling >= OSCARS_TILING_COUNT) return OSCARS_E_INVALID;
+  gemm_tuner_set_tiling(c->tuner, tiling);
   return OSCARS_OK;
 }
 
-oscars_status oscars_tuning_pending(int32_t* configurations) {
-  if (!configurations) return OSCARS_E_INVALID;
-  *configurations = gemm_tuning_pending();
+oscars_status oscars_tuning_pending(const oscars_ctx* c, int32_t* configurations) {
+  if (!c || !configurations) return OSCARS_E_INVALID;
+  *configurations = gemm_tuner_pending(c->tuner);
   return OSCARS_OK;
 }
 
@@ -871,13 +936,13 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
       replicas < 1 || replicas > c->K)
     return OSCARS_E_INVALID;
   *fused = 0;
-  if (layer == 1 || !c->bf16 || !backward_fused_enabled()) return OSCARS_OK;
+  if (layer == 1 || !c->bf16 || !backward_fused_enabled(c->backward_mode)) return OSCARS_OK;
   GemmArgs g{};
   g.M = c->dims[layer - 1];
   g.N = batch;
   g.K = c->dims[layer];
   if (!backward_fusable(g)) return OSCARS_OK;
-  if (backward_mode() != BACKWARD_AUTO) {
+  if (c->backward_mode != BACKWARD_AUTO) {
     *fused = 1;
     return OSCARS_OK;
   }
@@ -890,12 +955,12 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
   return OSCARS_OK;
 }
 
-oscars_status oscars_set_backward(int32_t mode) {
+oscars_status oscars_set_backward(oscars_ctx* c, int32_t mode) {
   static_assert(OSCARS_BACKWARD_COUNT == BACKWARD_MODE_COUNT &&
                     OSCARS_BACKWARD_FUSED_SPLIT == BACKWARD_FUSED_SPLIT,
                 "backward modes of the C ABI and of the launchers agree");
-  if (mode < 0 || mode >= OSCARS_BACKWARD_COUNT) return OSCARS_E_INVALID;
-  set_backward_mode(mode);
+  if (!c || mode < 0 || mode >= OSCARS_BACKWARD_COUNT) return OSCARS_E_INVALID;
+  c->backward_mode = mode;
   return OSCARS_OK;
 }
 

@@ -44,23 +44,18 @@ def P():
     return paper_2102_08550_amd
 
 
-def test_process_wide_knobs_reject_bad_values(P):
-    """Tiling and backward mode: values outside their range are refused with
-    E_INVALID, valid ones accepted (host-side stores only, no GPU work)."""
+def test_context_knobs_reject_bad_arguments(P):
+    """Tiling, backward mode and the tuning count belong to a context: a null
+    context or output, or a value outside its range, is refused with
+    E_INVALID before anything is touched (no GPU work)."""
     lib = P._lib()
-    assert lib.oscars_set_gemm_tiling(len(P.TILINGS)) == P.E_INVALID
-    assert lib.oscars_set_gemm_tiling(-1) == P.E_INVALID
-    assert lib.oscars_set_backward(len(P.BACKWARDS)) == P.E_INVALID
-    assert lib.oscars_set_backward(-1) == P.E_INVALID
-    assert lib.oscars_set_backward(P.BACKWARD_AUTO) == P.OK
-    assert lib.oscars_set_gemm_tiling(P.TILING_AUTO) == P.OK
-
-
-def test_tuning_pending_without_launches(P):
-    """No GEMM has run in this process: no configuration is being tuned; a
-    null output pointer is refused."""
-    assert P.tuning_pending() == 0
-    assert P._lib().oscars_tuning_pending(None) == P.E_INVALID
+    for t in (P.TILING_AUTO, len(P.TILINGS), -1):
+        assert lib.oscars_set_gemm_tiling(None, t) == P.E_INVALID
+    for m in (P.BACKWARD_AUTO, len(P.BACKWARDS), -1):
+        assert lib.oscars_set_backward(None, m) == P.E_INVALID
+    n = P._i32(0)
+    assert lib.oscars_tuning_pending(None, P.ctypes.byref(n)) == P.E_INVALID
+    assert lib.oscars_tuning_pending(None, None) == P.E_INVALID
 
 
 def test_load_balance_matches_oracle(P):
