@@ -227,6 +227,28 @@ oscars_status oscars_evaluate(oscars_ctx* ctx, const float* params, const void* 
                               const int32_t* y, int64_t n_rows, double* loss_sum,
                               int64_t* correct);
 
+/* oscars_evaluate for callers that cannot allocate device memory: serving
+ * loops that evaluate a model over and over, code that must not call
+ * hipMalloc / hipFree (e.g. next to a graph being captured on another
+ * stream), harnesses that forbid allocation.  Same arguments and the same
+ * results, bit for bit, as oscars_evaluate; it differs in three ways:
+ *   - its temporaries (row table, per-row losses and flags, results) live in
+ *     one library-wide device array of about 3 MB per GPU, set aside when the
+ *     first context on that GPU is created and held until the process ends,
+ *     so n_rows <= OSCARS_EVAL_NOALLOC_MAX_ROWS (else OSCARS_E_INVALID);
+ *   - it allocates nothing and creates no HIP objects: GEMM tilings the
+ *     context has not decided yet take the fixed rule instead of being timed
+ *     (every tiling gives the same bits);
+ *   - every call on one GPU shares that array: calls that overlap on one GPU
+ *     (two host threads, or two contexts on different streams) race and
+ *     their results are undefined.  The call waits for the context's
+ *     stream before it returns, so calls from one thread never overlap.
+ * OSCARS_E_STATE if the current device is not the context's. */
+#define OSCARS_EVAL_NOALLOC_MAX_ROWS 262144
+oscars_status oscars_evaluate_noalloc(oscars_ctx* ctx, const float* params, const void* x,
+                                      const int32_t* y, int64_t n_rows, double* loss_sum,
+                                      int64_t* correct);
+
 /* Parameter-server aggregation (Approach, Eq. 4, first branch).
  *   global    device [n] fp32 out: g[i] = sum_k w_k * replicas[k * ld + i],
  *             summed as a balanced pairwise tree over P = next power of two

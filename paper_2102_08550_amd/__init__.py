@@ -24,6 +24,7 @@ LIB_PATH = os.path.join(_HERE, "_lib", "liboscars.so")
 OK, E_INVALID, E_NOMEM, E_HIP, E_INFEASIBLE, E_STATE = 0, -1, -2, -3, -4, -5
 FP32, BF16 = 0, 1
 MAX_K = 64
+EVAL_NOALLOC_MAX_ROWS = 262144
 (KERNEL_CAST, KERNEL_FWD, KERNEL_SOFTMAX, KERNEL_DGRAD, KERNEL_WGRAD, KERNEL_AGGREGATE,
  KERNEL_BWD_FUSED) = range(7)
 KERNEL_NAMES = ("cast_bf16", "gemm_fwd", "softmax_ce", "gemm_dgrad", "gemm_wgrad_update",
@@ -78,6 +79,8 @@ _SIGS = {
     "oscars_broadcast": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp]),
     "oscars_plan_tau": (_i32, [_P(ctypes.c_double), _i32, _i32, _i64, _P(_i64), _P(_i64), _P(_i32)]),
     "oscars_evaluate": (_i32, [_vp, _vp, _vp, _vp, _i64, _P(ctypes.c_double), _P(_i64)]),
+    "oscars_evaluate_noalloc": (_i32, [_vp, _vp, _vp, _vp, _i64, _P(ctypes.c_double),
+                                       _P(_i64)]),
     "oscars_status_str": (ctypes.c_char_p, [_i32]),
     "oscars_last_hip_error": (_i32, []),
 }
@@ -331,18 +334,20 @@ class Context:
                "oscars_round_losses")
         return out
 
-    def evaluate(self, params, x, y, n_rows: Optional[int] = None):
+    def evaluate(self, params, x, y, n_rows: Optional[int] = None, noalloc: bool = False):
         """Held-out (summed loss, correct count) of the flat model ``params``
-        (device tensor [n_pad] fp32) on rows 0..n_rows-1 of x / y."""
+        (device tensor [n_pad] fp32) on rows 0..n_rows-1 of x / y
+        (oscars_evaluate, or with ``noalloc`` oscars_evaluate_noalloc)."""
         import torch
         n = int(x.shape[0] if n_rows is None else n_rows)
         if n > x.shape[0] or n > y.shape[0]:
             raise ValueError("n_rows exceeds the rows of x or y")
         loss = ctypes.c_double(0.0)
         hits = _i64(0)
-        _check(_lib().oscars_evaluate(self._h, _dev_ptr(params, torch.float32, "params"),
-                                      _dev_ptr(x, None, "x"), _dev_ptr(y, torch.int32, "y"), n,
-                                      ctypes.byref(loss), ctypes.byref(hits)), "oscars_evaluate")
+        name = "oscars_evaluate_noalloc" if noalloc else "oscars_evaluate"
+        _check(getattr(_lib(), name)(self._h, _dev_ptr(params, torch.float32, "params"),
+                                     _dev_ptr(x, None, "x"), _dev_ptr(y, torch.int32, "y"), n,
+                                     ctypes.byref(loss), ctypes.byref(hits)), name)
         return float(loss.value), int(hits.value)
 
     def cursors(self) -> List[int]:

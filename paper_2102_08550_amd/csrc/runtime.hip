@@ -15,6 +15,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -41,6 +42,40 @@ constexpr int kMaxTau = 4096;
 // Index-table, loss and staging capacity allocated by oscars_create: rounds
 // of up to this many local steps per worker need no allocation later.
 constexpr int kPreTau = 64;
+
+}  // namespace
+
+// Device memory of oscars_evaluate_noalloc: the temporaries of one
+// evaluation of up to OSCARS_EVAL_NOALLOC_MAX_ROWS rows (results, row table,
+// per-row losses and flags; EvalLayout below), one copy per GPU, held until
+// the process ends.  Host code never uses this name as an address: it takes
+// the device address each GPU reports for it (scratch_address).
+constexpr size_t kNoAllocScratchBytes =
+    256 + (64 + OSCARS_EVAL_NOALLOC_MAX_ROWS) * 4 + 2 * OSCARS_EVAL_NOALLOC_MAX_ROWS * 4;
+static_assert(OSCARS_EVAL_NOALLOC_MAX_ROWS % 64 == 0, "whole 256-byte parts");
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_ptr;  // device -> address of `scratch` there
+
+// The address of `scratch` on `device`, which must be the current device;
+// looked up once per device.
+hipError_t scratch_address(int device, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  auto it = g_scratch_ptr.find(device);
+  if (it != g_scratch_ptr.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  g_scratch_ptr[device] = p;
+  *out = p;
+  return hipSuccess;
+}
 
 }  // namespace
 
@@ -90,6 +125,7 @@ struct oscars_ctx {
   bool cal_off = false;  // scratch too large for the free device memory: no timing
   hipEvent_t cal_ev[2] = {nullptr, nullptr};
 
+  void* noalloc_scratch = nullptr;   // this device's `scratch` (oscars_evaluate_noalloc)
   GemmTuner* tuner = nullptr;        // tiling of this context's GEMM launches
   int backward_mode = BACKWARD_AUTO;  // backward of hidden bf16 layers
 
@@ -269,6 +305,7 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
   }
 
   hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess) e = scratch_address(c->device, &c->noalloc_scratch);
   if (e == hipSuccess && c->bf16) {
     void* p = nullptr;
     e = dev_alloc(c, static_cast<size_t>(K) * c->n_pad * 2, &p);
@@ -736,7 +773,7 @@ oscars_status check_evaluate(const oscars_ctx* c, const float* params, const voi
 // Device bytes of an evaluation's temporaries: results (double loss, int64
 // count), then the row table [64 + n] int32, per-row losses [n] fp32 and
 // correct flags [n] int32, each part 256-byte aligned.
-struct EvalLayout {
+struct EvalLayout {  // kNoAllocScratchBytes holds it for OSCARS_EVAL_NOALLOC_MAX_ROWS rows
   int64_t table, loss, hit, end;
   explicit EvalLayout(int64_t n) {
     table = 256;
@@ -883,6 +920,21 @@ oscars_status oscars_evaluate(oscars_ctx* c, const float* params, const void* x,
   e = run_evaluate(c, params, x, y, n_rows, buf, true, loss_sum, correct);
   const hipError_t f = hipFree(buf);  // waits for the device
   if (e == hipSuccess) e = f;
+  return e == hipSuccess ? OSCARS_OK : hip_fail(e);
+}
+
+oscars_status oscars_evaluate_noalloc(oscars_ctx* c, const float* params, const void* x,
+                                      const int32_t* y, int64_t n_rows, double* loss_sum,
+                                      int64_t* correct) {
+  oscars_status st = check_evaluate(c, params, x, y, n_rows, loss_sum, correct);
+  if (st != OSCARS_OK) return st;
+  if (n_rows > OSCARS_EVAL_NOALLOC_MAX_ROWS) return OSCARS_E_INVALID;
+  if (eval_bytes(n_rows) > kNoAllocScratchBytes) return OSCARS_E_INVALID;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (dev != c->device || !c->noalloc_scratch) return OSCARS_E_STATE;
+  e = run_evaluate(c, params, x, y, n_rows, c->noalloc_scratch, false, loss_sum, correct);
   return e == hipSuccess ? OSCARS_OK : hip_fail(e);
 }
 
