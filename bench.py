@@ -280,6 +280,11 @@ def main():
                     help="c5 (default): the full round; c4: aggregation-only stress")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--backward", default="auto", choices=["auto", "separate", "fused",
+                                                           "fused_split"],
+                    help="backward path of the hidden bf16 layers (auto: timed per "
+                         "configuration in this process; a fixed one makes counter passes of "
+                         "separate processes run the same launch mix)")
     ap.add_argument("--probe-copy-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, three "
                          "times (calibration of hardware byte counters)")
@@ -313,6 +318,7 @@ def main():
     init = workload.gen_init(cfg)
     stream = torch.cuda.current_stream()
     run = OscarsRun(cfg, ds, init, stream=stream)
+    run.ctx.set_backward(P.BACKWARDS[args.backward])
 
     def tau_for(step):
         if cfg.tau_rule == "speeds":  # Algorithm 1 from the workers' iteration times
@@ -396,6 +402,10 @@ def main():
                           "flop_per_launch": fl / cnt, "bytes_per_launch": by / cnt}
         return out_
     kernels = summarize(prof_w, work_w, n_warm)  # breakdown (warmup, every kernel timed)
+    tau0 = np.asarray(tau_for(0))
+    backward_mix = {f"l{l}": {str(ns): ("fused" if fused_path(l, ns) else "separate")
+                              for ns in sorted({int((tau0 > j).sum()) for j in range(tau0.max())})}
+                    for l in range(2, len(cfg.dims))}
     d = summarize(prof, work_tot, 1)[dom]  # dominant kernel, inside the timed region
     ridge = MFMA_PEAK_TFLOPS[cfg.dtype] * 1e12 / (HBM_PEAK_GBPS * 1e9)
     intensity = d["flop_per_launch"] / d["bytes_per_launch"] if d["bytes_per_launch"] else 0.0
@@ -446,6 +456,7 @@ def main():
                         if local_ms else None,
                         "samples_per_s_kernels": samples_w / (local_ms / 1e3) if local_ms else None},
         "kernels": kernels,
+        "backward": {"mode": args.backward, "path_per_layer_and_active_replicas": backward_mix},
         "roofline": roof,
         "hbm_copy": copy,
     }
