@@ -16,6 +16,14 @@ of the cluster is modelled.  A round ends at the barrier of Eq. 1, when the
 last worker finishes: max_k tau_k t_k.  As in Problem Formulation, the time
 of the parameter exchange itself is not counted.
 
+``run_measured`` closes the loop on measured times instead: the workers'
+work differs for real (each worker draws its own mini-batch size, which Eq. 4
+leaves free), every worker's local steps run as launches of their own, and
+its iteration time is the GPU time of those launches (HIP events around each
+launch, summed) divided by its step count.  The load balancer plans the next
+round from these measurements, so a change in a worker's work is followed by
+a new plan.
+
 Paradigms compared (Motivation):
   * ``bsp``    -- synchronous mini-batch SGD by averaging: tau_k = 1;
   * ``local``  -- local SGD without balancing: tau_k = I for every worker;
@@ -227,6 +235,97 @@ def run_paradigm(cfg, dataset, init, eval_set, paradigm: str, schedule: SpeedSch
             "tau_changes": balancer.changes if balancer else 0}
 
 
+class BatchSchedule:
+    """Per-worker mini-batch sizes over the rounds: ``batches`` from round 0
+    on, replaced by ``changes[r]`` from round r on.  A worker whose batch
+    size changes continues its sample stream at step position cursor x new
+    size (Eq. 4 fixes no mini-batch rule; the oracle reads positions the same
+    way)."""
+
+    def __init__(self, batches: Sequence[int], changes: Optional[Dict[int, Sequence[int]]] = None):
+        self.batches = [int(b) for b in batches]
+        self.changes = {int(r): [int(b) for b in v] for r, v in (changes or {}).items()}
+        if any(b < 1 for b in self.batches) or any(b < 1 for v in self.changes.values() for b in v):
+            raise ValueError("batch sizes must be positive")
+        if any(len(v) != len(self.batches) for v in self.changes.values()):
+            raise ValueError("one batch size per worker")
+
+    @property
+    def K(self) -> int:
+        return len(self.batches)
+
+    @property
+    def max_batch(self) -> int:
+        return max([max(self.batches)] + [max(v) for v in self.changes.values()])
+
+    def at(self, r: int) -> List[int]:
+        cur = self.batches
+        for start in sorted(self.changes):
+            if start <= r:
+                cur = self.changes[start]
+        return list(cur)
+
+
+def run_measured(cfg, dataset, init, schedule: BatchSchedule, rounds: int, resolution: int = 4,
+                 return_model: bool = False) -> Dict:
+    """Oscars with the load balancer fed by measured iteration times.
+
+    Round 0 is a probe: every worker takes one step.  In every round worker k
+    runs its tau_k local steps with its own mini-batch size as launches of its
+    own (``oscars_local_steps`` with only worker k active; the result equals
+    the grouped launches bit for bit), HIP events around each of those
+    launches give its GPU time, and t_k = that time / tau_k.  Then the
+    parameter server averages and broadcasts (``oscars_aggregate``).  The
+    next round's tau is Algorithm 1 on the ticks of the measured t
+    (``LoadBalancer``).  Returns per-round records: tau, batch sizes,
+    measured times, ticks, T* and the Eq. 1 barrier of the measured times."""
+    import dataclasses
+
+    import torch
+
+    from . import aggregate
+    from .rounds import OscarsRun
+    K = cfg.K
+    if schedule.K != K:
+        raise ValueError("schedule and workload disagree on K")
+    run = OscarsRun(dataclasses.replace(cfg, batch=schedule.max_batch), dataset, init)
+    balancer = LoadBalancer(K, cfg.M, resolution)
+    kinds = list(range(7))
+    records = []
+    tau = [1] * K
+    try:
+        for r in range(rounds):
+            batches = schedule.at(r)
+            ms = [0.0] * K
+            for k in range(K):
+                if tau[k] == 0:
+                    continue
+                solo = [0] * K
+                solo[k] = tau[k]
+                run.ctx.profile_begin(kinds)
+                run.ctx.local_steps(run.replicas, run.x, run.y, run.offsets, run.seed, solo,
+                                    cfg.lr, batches[k])
+                prof = run.ctx.profile_end()
+                ms[k] = float(sum(v[0] for v in prof.values()))
+            aggregate(run.g, run.replicas, run.weights, K, run.n, run.n, True)
+            t_iter = [m / a for m, a in zip(ms, tau)]
+            rec = {"round": r, "tau": list(tau), "batches": batches, "gpu_ms": ms,
+                   "t_iter_ms": t_iter, "barrier_ms": barrier_time(tau, t_iter),
+                   "idle": idle_fraction(tau, t_iter)}
+            balancer.update(t_iter)
+            rec["next_ticks"], rec["next_T_star"] = list(balancer.ticks), balancer.T_star
+            rec["next_tau"] = list(balancer.tau)
+            records.append(rec)
+            tau = list(balancer.tau)
+        torch.cuda.synchronize()
+        model = run.global_layers() if return_model else None
+        cursors = run.ctx.cursors()
+    finally:
+        run.close()
+    return {"records": records, "model": model, "cursors": cursors,
+            "tau_changes": balancer.changes}
+
+
 def time_to_loss(result: Dict, target: float) -> Optional[float]:
     """Emulated clock at the first evaluation at or below ``target``."""
     for rec in result["records"]:
@@ -281,6 +380,18 @@ def compare(cfg, schedule: SpeedSchedule, time_budget_steps: float, local_steps:
     return out
 
 
+def _measured_cfg():
+    """The workload of the measured-time run: an fp32 MLP wide enough that a
+    worker's step time grows with its mini-batch size."""
+    import workload
+    return workload.Config("measured-1024-2048-2048-10-fp32", (1024, 2048, 2048, 10), workload.FP32,
+                           K=4, n_rows=8000, batch=1024, tau_rule="given", lr=0.02, seed=24,
+                           mean_scale=0.3)
+
+
+MEASURED_BATCHES = (64, 128, 512, 1024)
+
+
 def main(argv=None):
     import workload
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
@@ -292,7 +403,24 @@ def main(argv=None):
     ap.add_argument("--mean-scale", type=float, default=0.1)
     ap.add_argument("--eval-every", type=int, default=1)
     ap.add_argument("--out", default=None, help="also write the JSON here")
+    ap.add_argument("--measured", type=int, default=0, metavar="ROUNDS",
+                    help="instead: this many rounds with the plan from measured times on the "
+                         "1024-2048-2048-10 fp32 MLP, 4 workers with batches 64, 128, 512, 1024 "
+                         "reversed half way")
     args = ap.parse_args(argv)
+    if args.measured > 0:
+        cfg = _measured_cfg()
+        sched = BatchSchedule(MEASURED_BATCHES,
+                              {args.measured // 2: tuple(reversed(MEASURED_BATCHES))})
+        res = run_measured(cfg, workload.gen_dataset(cfg), workload.gen_init(cfg), sched,
+                           args.measured, resolution=args.resolution)
+        res.pop("model")
+        line = json.dumps(res)
+        print(line)
+        if args.out:
+            with open(args.out, "w") as f:
+                f.write(line + "\n")
+        return 0
     cfg = workload.scaled(workload.C2, mean_scale=args.mean_scale)
     schedule = SpeedSchedule(cfg.speeds, changes={args.budget / 2: tuple(reversed(cfg.speeds))},
                              jitter=args.jitter, seed=cfg.seed)

@@ -75,3 +75,15 @@ def test_fixed_paradigms(C):
     assert C.plan_round("local", 3, [1.0, 2.0, 3.0], None, 5) == [5, 5, 5]
     with pytest.raises(ValueError):
         C.plan_round("asp", 3, [1.0, 2.0, 3.0], None, 5)
+
+
+def test_batch_schedule(C):
+    s = C.BatchSchedule([64, 128, 512, 1024], {3: [1024, 512, 128, 64], 5: [8, 8, 8, 8]})
+    assert s.K == 4 and s.max_batch == 1024
+    assert s.at(0) == s.at(2) == [64, 128, 512, 1024]
+    assert s.at(3) == s.at(4) == [1024, 512, 128, 64]
+    assert s.at(9) == [8, 8, 8, 8]
+    with pytest.raises(ValueError):
+        C.BatchSchedule([64, 0])
+    with pytest.raises(ValueError):
+        C.BatchSchedule([64, 32], {1: [8]})

@@ -9,13 +9,20 @@ Algorithm 1 on measured times; Eq. 1 for the barrier).
 * Each paradigm run through ``run_paradigm`` (real rounds on the GPU,
   emulated cluster clock): the load balancer's tau sequence equals the
   oracle's plans replayed on the same clock, and the final global model and
-  its held-out loss match the oracle's run with that tau sequence."""
+  its held-out loss match the oracle's run with that tau sequence.
+* The load balancer fed by measured iteration times (``run_measured``):
+  workers with different mini-batch sizes, each worker's launches timed with
+  HIP events; every plan equals the oracle's Algorithm 1 on the same
+  measured times, the plan follows a change of the workers' work, and the
+  final global model matches the oracle's run with the same tau and batch
+  sequences, tensor by tensor."""
 import numpy as np
 import pytest
 
 import oracle
 import workload
-from _parity import BF16_TOL, FP32_TOL, oracle_rounds, rel_err, say
+from _parity import (BF16_TOL, FP32_TOL, assert_tensors_close, oracle_rounds, record,
+                     rel_err, say, tensor_errors)
 
 pytestmark = pytest.mark.gpu
 
@@ -123,3 +130,51 @@ def test_paradigm_matches_oracle(P, paradigm):
     assert abs(last["eval_loss"] - ref_loss / 500) <= FP32_TOL * max(1.0, ref_loss / 500)
     # the emulated clock is the sum of the barriers
     assert last["clock"] >= budget and last["samples"] == sum(map(sum, taus)) * cfg.batch
+
+
+def test_measured_balancing_follows_the_work(P):
+    from paper_2102_08550_amd import controller as C
+    cfg = C._measured_cfg()
+    K, res_ticks = cfg.K, 4
+    say(f"measured balancing {cfg.name} batches {C.MEASURED_BATCHES}, reversed from round 3")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    sched = C.BatchSchedule(C.MEASURED_BATCHES, {3: tuple(reversed(C.MEASURED_BATCHES))})
+    res = C.run_measured(cfg, ds, init, sched, rounds=5, resolution=res_ticks, return_model=True)
+    recs = res["records"]
+    for rec in recs:
+        say(f"  round {rec['round']}: batches {rec['batches']} tau {rec['tau']} "
+            f"t_iter {[round(t, 4) for t in rec['t_iter_ms']]} ms -> next tau {rec['next_tau']}")
+        ticks, T, tau = oracle.plan_from_measured(list(rec["t_iter_ms"]), res_ticks, cfg.M)
+        assert (rec["next_ticks"], rec["next_T_star"], rec["next_tau"]) == (ticks, T, tau)
+    for a, b in zip(recs, recs[1:]):
+        assert b["tau"] == a["next_tau"]
+    assert recs[0]["tau"] == [1] * K
+    # larger mini-batches take longer: planned from the batches 64 .. 1024,
+    # worker 0 takes more steps than worker 3; from the reversed batches
+    # (measured in round 3), fewer
+    assert recs[1]["t_iter_ms"][3] > recs[1]["t_iter_ms"][0]
+    assert recs[2]["tau"][0] > recs[2]["tau"][3]
+    assert recs[3]["t_iter_ms"][0] > recs[3]["t_iter_ms"][3]
+    assert recs[4]["tau"][0] < recs[4]["tau"][3]
+    # the oracle's run with the same tau and batch sequences
+    X = ds.x_f32().astype(np.float64)
+    off = oracle.shard_offsets(cfg.n_rows, K)
+    seed = workload.sampler_seed(cfg)
+    g = [(W.astype(np.float64), b.astype(np.float64)) for W, b in init]
+    s = [0] * K
+    w = oracle.paper_weights(K)
+    for rec in recs:
+        reps = []
+        for k in range(K):
+            xk, _ = oracle.worker_local_steps(g, X, ds.y, off, seed, k, s[k], rec["tau"][k],
+                                              cfg.lr, rec["batches"][k], False)
+            reps.append(xk)
+            s[k] += rec["tau"][k]
+        g = [(oracle.tree_aggregate([r[l][0] for r in reps], w),
+              oracle.tree_aggregate([r[l][1] for r in reps], w)) for l in range(len(g))]
+    assert res["cursors"] == s
+    errs = tensor_errors(res["model"], g)
+    record("measured-balancing", {"records": recs, "tensors": errs, "tol": FP32_TOL})
+    say(f"  final model: worst per-tensor error {max(max(e.values()) for e in errs.values()):.2e}")
+    assert_tensors_close(errs, FP32_TOL, "measured balancing")
