@@ -23,3 +23,4 @@ from .sampler import (SplitMix64, batch_rows, epoch_permutation,  # noqa: F401
 from .aggregate import paper_weights, tree_aggregate  # noqa: F401
 from .mlp import bf16_round, evaluate, loss_and_grads, sgd_step  # noqa: F401
 from .local_sgd import OracleRun, run_rounds, worker_local_steps  # noqa: F401
+from . import cnn  # noqa: F401

@@ -17,7 +17,7 @@ SGD, and equal tau with uniform weights is periodic model averaging.
 from __future__ import annotations
 
 import dataclasses
-from typing import Dict, List, Optional, Sequence
+from typing import Callable, Dict, List, Optional, Sequence
 
 import numpy as np
 
@@ -36,13 +36,18 @@ class OracleRun:
 
 def worker_local_steps(x0: Params, X: np.ndarray, y: np.ndarray, offsets: Sequence[int],
                        seed: int, k: int, first_step: int, tau: int, lr: float, B: int,
-                       bf16: bool, cache: Optional[Dict] = None):
-    """Worker k runs tau SGD steps from x0 on its own shard.  Returns (x, mean loss)."""
+                       bf16: bool, cache: Optional[Dict] = None, step: Optional[Callable] = None):
+    """Worker k runs tau SGD steps from x0 on its own shard.  Returns (x, mean
+    loss).  ``step(params, Xb, yb, lr) -> (params, loss)`` is the model's SGD
+    step (default: the fully connected network of ``mlp``)."""
     x = [(W.copy(), b.copy()) for W, b in x0]
     losses = []
     for j in range(tau):
         rows = batch_rows(seed, offsets, k, first_step + j, B, cache)
-        x, loss = sgd_step(x, X[rows], y[rows], lr, bf16)
+        if step is None:
+            x, loss = sgd_step(x, X[rows], y[rows], lr, bf16)
+        else:
+            x, loss = step(x, X[rows], y[rows], lr)
         losses.append(loss)
     return x, (float(np.mean(losses)) if losses else float("nan"))
 
@@ -56,10 +61,12 @@ def _flatten(p: Params) -> List[np.ndarray]:
 
 def run_rounds(init: Params, X: np.ndarray, y: np.ndarray, K: int, tau_rounds: np.ndarray,
                lr: float, B: int, seed: int, bf16: bool, weights: Optional[Sequence[float]] = None,
-               steps_done: Optional[Sequence[int]] = None) -> OracleRun:
+               steps_done: Optional[Sequence[int]] = None,
+               step: Optional[Callable] = None) -> OracleRun:
     """Run ``len(tau_rounds)`` rounds; ``tau_rounds[r][k]`` is worker k's step
     count in round r.  ``X`` holds the inputs as float64 (bf16 values for bf16
-    workloads), ``init`` the starting global model."""
+    workloads), ``init`` the starting global model, ``step`` the model's SGD
+    step (see worker_local_steps)."""
     offsets = shard_offsets(X.shape[0], K)
     g = [(np.asarray(W, np.float64).copy(), np.asarray(b, np.float64).copy()) for W, b in init]
     w = np.full(K, 1.0 / K) if weights is None else np.asarray(weights, np.float64)
@@ -71,7 +78,7 @@ def run_rounds(init: Params, X: np.ndarray, y: np.ndarray, K: int, tau_rounds: n
         replicas, round_losses = [], []
         for k in range(K):
             xk, lk = worker_local_steps(g, X, y, offsets, seed, k, s[k], int(tau[k]), lr, B,
-                                        bf16, cache)
+                                        bf16, cache, step)
             replicas.append(xk)
             round_losses.append(lk)
             s[k] += int(tau[k])
