@@ -81,6 +81,50 @@ def gemm_work(cfg, tau, fused_path=None):
     return work
 
 
+def cnn_work(cfg, tau):
+    """Algorithmic FLOPs and bytes of one round of the convolutional workload
+    (oscars_round), per kind: conv layers as implicit GEMMs (2 FLOPs per
+    multiply-add of every kernel tap; bytes: input, weights and output once),
+    average pooling with the forward kinds, the classifier with its kinds, the
+    weight updates' fp32 read and write of their parameters."""
+    import numpy as np
+    B = cfg.batch
+    tau = np.asarray(tau)
+    work = {k: [0.0, 0.0] for k in ("gemm_fwd", "gemm_dgrad", "gemm_wgrad_update", "softmax_ce",
+                                    "aggregate")}
+    H, W, C = cfg.image
+    geo = []
+    for co, st in cfg.conv:
+        Ho, Wo = (H - 1) // st + 1, (W - 1) // st + 1
+        geo.append((H, W, C, Ho, Wo, co))
+        H, W, C = Ho, Wo, co
+    classes = cfg.n_classes
+    work["aggregate"][1] += (cfg.K + 1) * cfg.n_params * 4.0
+    for j in range(int(tau.max())):
+        ns = int((tau > j).sum())
+        for l, (h, w, c, ho, wo, co) in enumerate(geo):
+            macs = B * ho * wo * co * 9 * c
+            act_in, act_out, wts = B * h * w * c * 4, B * ho * wo * co * 4, (9 * c * co + co) * 4
+            work["gemm_fwd"][0] += ns * 2.0 * macs
+            work["gemm_fwd"][1] += ns * (act_in + wts + act_out)
+            if l > 0:
+                work["gemm_dgrad"][0] += ns * 2.0 * macs
+                work["gemm_dgrad"][1] += ns * (act_out + wts + 2 * act_in)  # reads the mask too
+            work["gemm_wgrad_update"][0] += ns * 2.0 * macs
+            work["gemm_wgrad_update"][1] += ns * (act_out + act_in + 2 * wts)
+        pooled = B * C * 4
+        work["gemm_fwd"][1] += ns * (B * H * W * C * 4 + pooled)  # pooling
+        work["gemm_fwd"][0] += ns * 2.0 * B * C * classes
+        work["gemm_fwd"][1] += ns * (pooled + (C * classes + classes) * 4 + B * classes * 4)
+        work["gemm_dgrad"][0] += ns * 2.0 * B * C * classes
+        work["gemm_dgrad"][1] += ns * (B * classes * 4 + C * classes * 4 + pooled)
+        work["gemm_dgrad"][1] += ns * (pooled + 2 * B * H * W * C * 4)  # pooling backward
+        work["gemm_wgrad_update"][0] += ns * 2.0 * B * C * classes
+        work["gemm_wgrad_update"][1] += ns * (B * classes * 4 + pooled + 2 * (C * classes + classes) * 4)
+        work["softmax_ce"][1] += ns * B * classes * 8
+    return work
+
+
 def kernel_source_hash() -> str:
     p = os.path.join(ROOT, "paper_2102_08550_amd", "csrc", "kernels.hip")
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
@@ -150,8 +194,12 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
             for j in range(int(tau[k])):
                 rows = oracle.batch_rows(seed, off, k, done[k] + j, cfg.batch, cache)
                 xb = workload.bf16_bits_to_f32(ds.x[rows]) if cfg.dtype == "bf16" else ds.x[rows]
-                x, _ = oracle.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr,
-                                       cfg.dtype == "bf16")
+                if cfg.is_cnn:
+                    x, _ = oracle.cnn.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr,
+                                               cfg.image, cfg.strides)
+                else:
+                    x, _ = oracle.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr,
+                                           cfg.dtype == "bf16")
                 steps += 1
                 if time.perf_counter() - t0 > budget_s:
                     break
@@ -276,8 +324,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"],
-                    help="c5 (default): the full round; c4: aggregation-only stress")
+    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5", "c6"],
+                    help="c5 (default): the full round; c4: aggregation-only stress; c6: the "
+                         "convolutional workload")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--backward", default="auto", choices=["auto", "separate", "fused",
@@ -359,7 +408,8 @@ def main():
         tau = tau_for(s)
         run.round(tau)
         samples_w += int(np.sum(tau)) * cfg.batch
-        for kname, (fl, by) in gemm_work(cfg, tau, fused_path).items():
+        for kname, (fl, by) in (cnn_work(cfg, tau) if cfg.is_cnn
+                                else gemm_work(cfg, tau, fused_path)).items():
             a = work_w.setdefault(kname, [0.0, 0.0])
             a[0] += fl
             a[1] += by
@@ -381,7 +431,7 @@ def main():
             run.ctx.profile_begin([dom_kind])
         run.round(tau)
         if s == args.steps - 1:
-            work_tot = gemm_work(cfg, tau, fused_path)
+            work_tot = cnn_work(cfg, tau) if cfg.is_cnn else gemm_work(cfg, tau, fused_path)
         samples += int(np.sum(tau)) * cfg.batch
     torch.cuda.synchronize()
     t1 = time.perf_counter()

@@ -112,6 +112,44 @@ typedef struct {
  * tilings, backward path): contexts do not share it. */
 oscars_status oscars_create(oscars_ctx** out, const oscars_model* model, int32_t K,
                             int32_t max_batch, void* hip_stream);
+/*
+ * Convolutional model: the stand-in for the paper's own workload, a
+ * convolutional network trained on CIFAR-10 images (Evaluation Setup).  fp32
+ * throughout, like the paper's PyTorch.
+ *   height, width, channels  the input image; a dataset row holds
+ *             height x width x channels fp32 values, channels fastest (NHWC);
+ *             height, width <= 4096, the row at most 2^24 values;
+ *   n_conv    1 <= n_conv <= OSCARS_MAX_LAYERS - 1 conv layers, each a 3 x 3
+ *             convolution with one row and column of zero padding on every
+ *             side, a bias per output channel and ReLU:
+ *               Z[b][i][j][o] = bias[o] + sum_{r,s,c} X[b][s i + r - 1][s j + s' - 1][c] W[o][r][s'][c]
+ *             with output extent (input - 1) / stride + 1;
+ *   conv_channels  host [n_conv]: output channels, 1 .. OSCARS_MAX_WIDTH;
+ *   conv_strides   host [n_conv]: 1 or 2;
+ *   classes   then every channel averaged over all positions, a linear
+ *             classifier to `classes` logits (with bias), softmax cross-entropy
+ *             averaged over the batch.
+ * Flat parameter layout of one replica: [W_1 ([C_1][3][3][C_0]), b_1, ...,
+ * W_n, b_n, W_fc ([classes][C_n]), b_fc], each segment starting on a
+ * 64-element boundary (oscars_layer_offsets: layers 1 .. n_conv + 1).
+ * Every other call (local steps, rounds, aggregation, evaluation, cursors)
+ * takes the context as for the fully connected model; x is the fp32 images.
+ */
+typedef struct {
+  int32_t height, width, channels;
+  int32_t n_conv;
+  const int32_t* conv_channels;
+  const int32_t* conv_strides;
+  int32_t classes;
+} oscars_cnn_model;
+
+/* Create a context for K replicas of a convolutional model (see above), mini-
+ * batches up to max_batch; allocates its whole device workspace (activations
+ * and their gradients per conv layer, pooled features, logits, weight-gradient
+ * partials, the index table) on the current device. */
+oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* model, int32_t K,
+                                int32_t max_batch, void* hip_stream);
+
 /* Free the workspace.  NULL is allowed.  Waits for the context's stream. */
 void oscars_destroy(oscars_ctx* ctx);
 /* Replace the stream later calls enqueue on. */

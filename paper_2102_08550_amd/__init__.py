@@ -47,6 +47,11 @@ class _Model(ctypes.Structure):
     _fields_ = [("n_layers", _i32), ("dims", _P(_i32)), ("dtype", _i32)]
 
 
+class _CnnModel(ctypes.Structure):
+    _fields_ = [("height", _i32), ("width", _i32), ("channels", _i32), ("n_conv", _i32),
+                ("conv_channels", _P(_i32)), ("conv_strides", _P(_i32)), ("classes", _i32)]
+
+
 class _Shards(ctypes.Structure):
     _fields_ = [("x", _vp), ("y", _vp), ("n_rows", _i64), ("offsets", _P(_i64)), ("seed", _u64)]
 
@@ -56,6 +61,7 @@ _LIB = None
 # name -> (restype, argtypes)
 _SIGS = {
     "oscars_create": (_i32, [_P(_vp), _P(_Model), _i32, _i32, _vp]),
+    "oscars_create_cnn": (_i32, [_P(_vp), _P(_CnnModel), _i32, _i32, _vp]),
     "oscars_destroy": (None, [_vp]),
     "oscars_set_stream": (_i32, [_vp, _vp]),
     "oscars_num_params": (_i64, [_vp]),
@@ -239,17 +245,38 @@ def broadcast(global_, replicas, K: int, n: int, ld: int, stream=None):
 
 
 class Context:
-    """K replicas of a ReLU MLP (dims = (d, h_1, ..., C)) and their workspace."""
+    """K replicas of a ReLU MLP (dims = (d, h_1, ..., C)) and their workspace;
+    or, with ``cnn = (image, conv)``, of the convolutional model: image =
+    (H, W, C), conv = ((out channels, stride), ...), dims = (H W C, classes),
+    fp32 (oscars_create_cnn)."""
 
-    def __init__(self, dims: Sequence[int], dtype: int, K: int, max_batch: int, stream=None):
+    def __init__(self, dims: Sequence[int], dtype: int, K: int, max_batch: int, stream=None,
+                 cnn=None):
         self.dims = [int(v) for v in dims]
         self.dtype = int(dtype)
         self.K = int(K)
-        self._dims_arr, dp = _arr(self.dims, np.int32)
-        model = _Model(len(self.dims) - 1, dp, self.dtype)
         h = _vp()
-        _check(_lib().oscars_create(ctypes.byref(h), ctypes.byref(model), self.K, int(max_batch),
-                                    _stream_handle(stream)), "oscars_create")
+        if cnn is None:
+            self._dims_arr, dp = _arr(self.dims, np.int32)
+            model = _Model(len(self.dims) - 1, dp, self.dtype)
+            self.shapes = [(o, i) for i, o in zip(self.dims[:-1], self.dims[1:])]
+            _check(_lib().oscars_create(ctypes.byref(h), ctypes.byref(model), self.K,
+                                        int(max_batch), _stream_handle(stream)), "oscars_create")
+        else:
+            image, conv = [int(v) for v in cnn[0]], [(int(o), int(st)) for o, st in cnn[1]]
+            if self.dtype != FP32 or len(self.dims) != 2 or len(image) != 3:
+                raise ValueError("convolutional models are fp32 with dims (H W C, classes)")
+            self._ch, chp = _arr([o for o, _ in conv], np.int32)
+            self._st, stp = _arr([st for _, st in conv], np.int32)
+            model = _CnnModel(image[0], image[1], image[2], len(conv), chp, stp, self.dims[-1])
+            self.shapes, cin = [], image[2]
+            for o, _ in conv:
+                self.shapes.append((o, 3, 3, cin))
+                cin = o
+            self.shapes.append((self.dims[-1], cin))
+            _check(_lib().oscars_create_cnn(ctypes.byref(h), ctypes.byref(model), self.K,
+                                            int(max_batch), _stream_handle(stream)),
+                   "oscars_create_cnn")
         self._h = h
         self.n_pad = int(_lib().oscars_num_params(h))
 
@@ -284,10 +311,10 @@ class Context:
 
     def unpack(self, flat: np.ndarray):
         out = []
-        for l in range(1, len(self.dims)):
+        for l, shape in enumerate(self.shapes, start=1):
             wo, bo = self.layer_offsets(l)
-            i, o = self.dims[l - 1], self.dims[l]
-            out.append((flat[wo:wo + o * i].reshape(o, i), flat[bo:bo + o]))
+            size = int(np.prod(shape))
+            out.append((flat[wo:wo + size].reshape(shape), flat[bo:bo + shape[0]]))
         return out
 
     def _step_args(self, replicas, x, y, offsets, seed, tau):

@@ -44,7 +44,7 @@ def build(verbose: bool = False) -> str:
     objdir = os.path.join(OUT, "obj")
     os.makedirs(objdir, exist_ok=True)
     objs = []
-    for src in ("kernels.hip", "runtime.hip"):
+    for src in ("kernels.hip", "conv_kernels.hip", "runtime.hip"):
         obj = os.path.join(objdir, src + ".o")
         _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)

@@ -1,0 +1,71 @@
+// Launchers of the convolutional workload's kernels (device code in
+// conv_kernels.hip): 3 x 3 convolutions with padding 1 as implicit GEMMs on
+// fp32 MFMA, global average pooling, and the linear classifier, grouped over
+// the active replica slots like the fully connected kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace oscars {
+
+enum ConvPass {
+  CONV_FWD = 0,    // Z[p][o] = b[o] + sum_{r,s,c} in[tap(p, r, s)][c] W[o][r][s][c]; ReLU
+  CONV_DGRAD = 1,  // dIn[q][c] = sum_{r,s,o} dZ[p(q, r, s)][o] W[o][r][s][c] where mask > 0
+  CONV_WGRAD = 2,  // dW[o][r][s][c] = sum_p dZ[p][o] in[tap(p, r, s)][c]; db[o] = sum_p dZ[p][o]
+  FC_FWD = 3,      // logits[b][o] = bias[o] + sum_c pooled[b][c] W[o][c]
+  FC_DGRAD = 4,    // dpooled[b][c] = sum_o delta[b][o] W[o][c]
+  FC_WGRAD = 5     // dW[o][c] = sum_b delta[b][o] pooled[b][c]; db[o] = sum_b delta[b][o]
+};
+
+// One grouped launch over n_slots replica slots (slot z works on replica
+// order[z]).  Every per-slot pointer is the slot-0 address; the kernel adds z
+// (activations, gradients, partials) or order[z] (parameters) times its
+// stride.  Layouts: images and activations [batch][H][W][C] fp32 (channels
+// fastest); conv weights [Cout][3][3][Cin], classifier weights
+// [classes][channels], each followed by its bias, at w_off / b_off of the
+// flat replica.
+struct ConvArgs {
+  int B;                  // batch rows
+  int H, W, C;            // the layer's input (FC: C = pooled channels, H = W = 1)
+  int Ho, Wo, Co;         // the layer's output (FC: Co = classes)
+  int stride;             // 1 or 2 (conv)
+  const float* in;        // conv input [B][H][W][C] (or, with gather, dataset rows); FC: pooled
+  int64_t in_slot, in_ld;             // slot stride; row stride of a gathered dataset row
+  const int32_t* gather;  // layer 1: dataset row of each batch row, [slot] stride gather_slot
+  int64_t gather_slot;
+  const float* dout;      // DGRAD / WGRAD: gradient of the layer output [B][Ho][Wo][Co]
+  int64_t dout_slot, dout_ld;         // FC: delta [B][dout_ld]
+  const float* master_in; // parameters read (weights; bias in FWD), by order[z]
+  int64_t master_in_slot;
+  int64_t w_off, b_off;
+  float* out;             // FWD: activations (FC: logits [B][out_ld]); DGRAD: gradient of the input
+  int64_t out_slot, out_ld;
+  const float* mask;      // CONV_DGRAD: the input activation (ReLU mask, > 0)
+  int64_t mask_slot;
+  float* part;            // WGRAD: partial sums [slot][split][Co][N]
+  int64_t part_slot;
+  int splits;             // WGRAD: number of K ranges (output pixels or batch rows)
+  int64_t k_per_split;
+  const int32_t* order;
+};
+
+hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s);
+
+// WGRAD epilogue: sum the partials of each weight in split order, then the
+// SGD update master <- master - lr sum (W) and the bias from the last column;
+// master[order[z]] with stride master_slot; reads master_in like ConvArgs.
+hipError_t launch_conv_update(const ConvArgs& a, ConvPass pass, float* master,
+                              int64_t master_slot, float lr, int n_slots, hipStream_t s);
+
+// pooled[z][b][c] = (sum over the H W positions of act[z][b][.][c], in
+// position order) / (H W).
+hipError_t launch_avgpool(const float* act, int64_t act_slot, float* pooled, int64_t pooled_slot,
+                          int B, int HW, int C, int n_slots, hipStream_t s);
+// dZ[z][b][p][c] = dpooled[z][b][c] / (H W) where act[z][b][p][c] > 0, else 0.
+hipError_t launch_avgpool_backward(const float* dpooled, int64_t dpooled_slot, const float* act,
+                                   int64_t act_slot, float* dz, int B, int HW, int C,
+                                   int n_slots, hipStream_t s);
+
+}  // namespace oscars

@@ -20,6 +20,7 @@
 #include <vector>
 
 #include "../../include/oscars.h"
+#include "conv.h"
 #include "host_logic.h"
 #include "kernels.h"
 
@@ -42,6 +43,8 @@ constexpr int kMaxTau = 4096;
 // Index-table, loss and staging capacity allocated by oscars_create: rounds
 // of up to this many local steps per worker need no allocation later.
 constexpr int kPreTau = 64;
+// Output pixels per weight-gradient partial of a conv layer.
+constexpr int64_t kConvPixelsPerSplit = 2048;
 
 }  // namespace
 
@@ -126,6 +129,19 @@ struct oscars_ctx {
   hipEvent_t cal_ev[2] = {nullptr, nullptr};
 
   void* noalloc_scratch = nullptr;   // this device's `scratch` (oscars_evaluate_noalloc)
+  // Convolutional model (oscars_create_cnn): conv layers l = 1..L-1, the
+  // classifier is layer L.  geometry[l] for l = 0 (the image) .. L-1.
+  bool cnn = false;
+  std::vector<int> img_h, img_w, img_c, conv_stride;
+  std::vector<float*> cact, cdz;   // [K][max_batch][h][w][c] per conv layer (1..L-1)
+  float* pooled = nullptr;         // [K][max_batch][c of layer L-1]
+  float* dpooled = nullptr;
+  float* cpart = nullptr;          // weight-gradient partials [K][part slot]
+  int64_t cpart_slot = 0;
+  int64_t cnn_slot(int l) const {
+    return static_cast<int64_t>(max_batch) * img_h[l] * img_w[l] * img_c[l];
+  }
+
   GemmTuner* tuner = nullptr;        // tiling of this context's GEMM launches
   int backward_mode = BACKWARD_AUTO;  // backward of hidden bf16 layers
 
@@ -362,6 +378,118 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* m, int32_t K, 
   return OSCARS_OK;
 }
 
+oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int32_t K,
+                                int32_t max_batch, void* hip_stream) {
+  if (!out || !m || !m->conv_channels || !m->conv_strides) return OSCARS_E_INVALID;
+  if (m->n_conv < 1 || m->n_conv > OSCARS_MAX_LAYERS - 1) return OSCARS_E_INVALID;
+  if (m->height < 1 || m->width < 1 || m->channels < 1 || m->height > 4096 ||
+      m->width > 4096 || m->channels > OSCARS_MAX_WIDTH)
+    return OSCARS_E_INVALID;
+  if (static_cast<int64_t>(m->height) * m->width * m->channels > (int64_t{1} << 24))
+    return OSCARS_E_INVALID;
+  if (m->classes < 1 || m->classes > OSCARS_MAX_WIDTH) return OSCARS_E_INVALID;
+  if (K < 1 || K > OSCARS_MAX_K || max_batch < 1 || max_batch > OSCARS_MAX_BATCH)
+    return OSCARS_E_INVALID;
+  for (int l = 0; l < m->n_conv; ++l) {
+    if (m->conv_channels[l] < 1 || m->conv_channels[l] > OSCARS_MAX_WIDTH) return OSCARS_E_INVALID;
+    if (m->conv_strides[l] != 1 && m->conv_strides[l] != 2) return OSCARS_E_INVALID;
+  }
+  oscars_ctx* c = new (std::nothrow) oscars_ctx();
+  if (!c) return OSCARS_E_NOMEM;
+  const int Lc = m->n_conv;
+  c->cnn = true;
+  c->L = Lc + 1;
+  c->dims.assign(c->L + 1, 0);
+  c->dims[0] = m->height * m->width * m->channels;
+  for (int l = 1; l <= Lc; ++l) c->dims[l] = m->conv_channels[l - 1];
+  c->dims[c->L] = m->classes;
+  c->bf16 = false;
+  c->esize = 4;
+  c->K = K;
+  c->max_batch = max_batch;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->img_h.assign(Lc + 1, 0);
+  c->img_w.assign(Lc + 1, 0);
+  c->img_c.assign(Lc + 1, 0);
+  c->conv_stride.assign(Lc + 1, 1);
+  c->img_h[0] = m->height;
+  c->img_w[0] = m->width;
+  c->img_c[0] = m->channels;
+  for (int l = 1; l <= Lc; ++l) {
+    c->conv_stride[l] = m->conv_strides[l - 1];
+    c->img_h[l] = (c->img_h[l - 1] - 1) / c->conv_stride[l] + 1;
+    c->img_w[l] = (c->img_w[l - 1] - 1) / c->conv_stride[l] + 1;
+    c->img_c[l] = m->conv_channels[l - 1];
+  }
+  c->w_off.assign(c->L + 1, 0);
+  c->b_off.assign(c->L + 1, 0);
+  c->ld.assign(c->L + 1, 0);
+  int64_t off = 0;
+  for (int l = 1; l <= c->L; ++l) {
+    const int64_t w = l <= Lc ? 9LL * c->img_c[l - 1] * c->img_c[l]
+                              : static_cast<int64_t>(m->classes) * c->img_c[Lc];
+    c->w_off[l] = off;
+    off = round_up(off + w, 64);
+    c->b_off[l] = off;
+    off = round_up(off + c->dims[l], 64);
+  }
+  c->ld[c->L] = round_up(m->classes, 64);
+  c->n_pad = off;
+  c->cursors.assign(K, 0);
+  c->samplers.resize(K);
+  c->act.assign(c->L + 1, nullptr);
+  c->delta.assign(c->L + 1, nullptr);
+  c->cact.assign(Lc + 1, nullptr);
+  c->cdz.assign(Lc + 1, nullptr);
+  c->tuner = gemm_tuner_create();
+  if (!c->tuner) {
+    delete c;
+    return OSCARS_E_NOMEM;
+  }
+  // weight-gradient partials per slot: the largest layer's splits x outputs
+  int64_t part = static_cast<int64_t>(m->classes) * (c->img_c[Lc] + 1);
+  for (int l = 1; l <= Lc; ++l) {
+    const int64_t pixels = static_cast<int64_t>(max_batch) * c->img_h[l] * c->img_w[l];
+    const int64_t splits = (pixels + kConvPixelsPerSplit - 1) / kConvPixelsPerSplit;
+    part = std::max<int64_t>(part, splits * c->img_c[l] * (9LL * c->img_c[l - 1] + 1));
+  }
+  c->cpart_slot = round_up(part, 64);
+
+  hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess) e = scratch_address(c->device, &c->noalloc_scratch);
+  void* p = nullptr;
+  for (int l = 1; l <= Lc && e == hipSuccess; ++l) {
+    const size_t bytes = static_cast<size_t>(K) * c->cnn_slot(l) * 4;
+    e = dev_alloc(c, bytes, &p);
+    c->cact[l] = static_cast<float*>(p);
+    if (e == hipSuccess) e = dev_alloc(c, bytes, &p);
+    c->cdz[l] = static_cast<float*>(p);
+  }
+  const size_t pooled_bytes = static_cast<size_t>(K) * max_batch * c->img_c[Lc] * 4;
+  if (e == hipSuccess) e = dev_alloc(c, pooled_bytes, &p);
+  c->pooled = static_cast<float*>(p);
+  if (e == hipSuccess) e = dev_alloc(c, pooled_bytes, &p);
+  c->dpooled = static_cast<float*>(p);
+  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(c->L) * 4, &p);
+  c->logits = static_cast<float*>(p);
+  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(c->L) * 4, &p);
+  c->delta[c->L] = p;
+  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(K) * c->cpart_slot * 4, &p);
+  c->cpart = static_cast<float*>(p);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming);
+  if (e == hipSuccess) {
+    const int64_t rows = static_cast<int64_t>(K) * kPreTau * max_batch;
+    e = ensure_tables(c, 64 + rows, rows);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) {
+    free_ctx(c);
+    return e == hipErrorOutOfMemory ? OSCARS_E_NOMEM : hip_fail(e);
+  }
+  *out = c;
+  return OSCARS_OK;
+}
+
 void oscars_destroy(oscars_ctx* ctx) { free_ctx(ctx); }
 
 oscars_status oscars_set_stream(oscars_ctx* ctx, void* hip_stream) {
@@ -399,6 +527,146 @@ oscars_status oscars_set_cursors(oscars_ctx* ctx, const int64_t* steps_done) {
 }  // extern "C"
 
 namespace {
+
+ConvArgs conv_layer_args(const oscars_ctx* c, int l, const float* master_in, int64_t master_in_slot,
+                         const int32_t* order, int B) {
+  ConvArgs a{};
+  a.B = B;
+  a.order = order;
+  a.master_in = master_in;
+  a.master_in_slot = master_in_slot;
+  a.w_off = c->w_off[l];
+  a.b_off = c->b_off[l];
+  if (l < c->L) {
+    a.H = c->img_h[l - 1];
+    a.W = c->img_w[l - 1];
+    a.C = c->img_c[l - 1];
+    a.Ho = c->img_h[l];
+    a.Wo = c->img_w[l];
+    a.Co = c->img_c[l];
+    a.stride = c->conv_stride[l];
+  } else {  // classifier
+    a.H = a.W = a.Ho = a.Wo = 1;
+    a.C = c->img_c[c->L - 1];
+    a.Co = c->dims[c->L];
+    a.stride = 1;
+  }
+  return a;
+}
+
+// Forward pass of the convolutional model for n_slots slots: conv layers
+// (layer 1 gathers the dataset rows `rows` of each slot), average pooling,
+// classifier logits into c->logits.
+hipError_t cnn_forward(oscars_ctx* c, const float* master_in, int64_t master_in_slot,
+                       const int32_t* order, const void* x, const int32_t* rows,
+                       int64_t rows_slot, int B, int ns) {
+  const int L = c->L;
+  hipError_t e = hipSuccess;
+  for (int l = 1; l < L && e == hipSuccess; ++l) {
+    ConvArgs a = conv_layer_args(c, l, master_in, master_in_slot, order, B);
+    if (l == 1) {
+      a.in = static_cast<const float*>(x);
+      a.in_ld = c->dims[0];
+      a.gather = rows;
+      a.gather_slot = rows_slot;
+    } else {
+      a.in = c->cact[l - 1];
+      a.in_slot = c->cnn_slot(l - 1);
+    }
+    a.out = c->cact[l];
+    a.out_slot = c->cnn_slot(l);
+    e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_conv(a, CONV_FWD, ns, c->stream); });
+  }
+  const int HW = c->img_h[L - 1] * c->img_w[L - 1], Cl = c->img_c[L - 1];
+  const int64_t pslot = static_cast<int64_t>(c->max_batch) * Cl;
+  if (e == hipSuccess)
+    e = timed(c, OSCARS_KERNEL_FWD, [&] {
+      return launch_avgpool(c->cact[L - 1], c->cnn_slot(L - 1), c->pooled, pslot, B, HW, Cl, ns,
+                            c->stream);
+    });
+  if (e == hipSuccess) {
+    ConvArgs a = conv_layer_args(c, L, master_in, master_in_slot, order, B);
+    a.in = c->pooled;
+    a.in_slot = pslot;
+    a.out = c->logits;
+    a.out_slot = c->act_slot(L);
+    a.out_ld = c->ld[L];
+    e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_conv(a, FC_FWD, ns, c->stream); });
+  }
+  return e;
+}
+
+// One local step of every active slot of the convolutional model after its
+// forward pass and loss gradient (in c->delta[L]): classifier backward-data
+// and update, pooling backward with the last ReLU mask, then per conv layer
+// (top down) backward-data (masked by the layer below) and the weight update.
+// Backward-data of a layer reads its weights before its update writes them.
+hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
+                        int64_t master_in_slot, const int32_t* order, const void* x,
+                        const int32_t* rows, int64_t rows_slot, int B, int ns, float lr) {
+  const int L = c->L;
+  const int Cl = c->img_c[L - 1], HW = c->img_h[L - 1] * c->img_w[L - 1];
+  const int64_t pslot = static_cast<int64_t>(c->max_batch) * Cl;
+  hipError_t e = hipSuccess;
+  {
+    ConvArgs a = conv_layer_args(c, L, master_in, master_in_slot, order, B);
+    a.in = c->pooled;
+    a.in_slot = pslot;
+    a.dout = static_cast<const float*>(c->delta[L]);
+    a.dout_slot = c->act_slot(L);
+    a.dout_ld = c->ld[L];
+    a.out = c->dpooled;
+    a.out_slot = pslot;
+    a.out_ld = Cl;
+    e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, FC_DGRAD, ns, c->stream); });
+    a.part = c->cpart;
+    a.part_slot = c->cpart_slot;
+    a.splits = 1;
+    a.k_per_split = B;
+    if (e == hipSuccess)
+      e = timed(c, OSCARS_KERNEL_WGRAD, [&] {
+        hipError_t r = launch_conv(a, FC_WGRAD, ns, c->stream);
+        return r == hipSuccess ? launch_conv_update(a, FC_WGRAD, replicas, c->n_pad, lr, ns, c->stream)
+                               : r;
+      });
+  }
+  if (e == hipSuccess)
+    e = timed(c, OSCARS_KERNEL_DGRAD, [&] {
+      return launch_avgpool_backward(c->dpooled, pslot, c->cact[L - 1], c->cnn_slot(L - 1),
+                                     c->cdz[L - 1], B, HW, Cl, ns, c->stream);
+    });
+  for (int l = L - 1; l >= 1 && e == hipSuccess; --l) {
+    ConvArgs a = conv_layer_args(c, l, master_in, master_in_slot, order, B);
+    a.dout = c->cdz[l];
+    a.dout_slot = c->cnn_slot(l);
+    if (l > 1) {
+      a.out = c->cdz[l - 1];
+      a.out_slot = c->cnn_slot(l - 1);
+      a.mask = c->cact[l - 1];
+      a.mask_slot = c->cnn_slot(l - 1);
+      e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, CONV_DGRAD, ns, c->stream); });
+      if (e != hipSuccess) break;
+      a.in = c->cact[l - 1];
+      a.in_slot = c->cnn_slot(l - 1);
+    } else {
+      a.in = static_cast<const float*>(x);
+      a.in_ld = c->dims[0];
+      a.gather = rows;
+      a.gather_slot = rows_slot;
+    }
+    const int64_t pixels = static_cast<int64_t>(B) * a.Ho * a.Wo;
+    a.k_per_split = kConvPixelsPerSplit;
+    a.splits = static_cast<int>((pixels + kConvPixelsPerSplit - 1) / kConvPixelsPerSplit);
+    a.part = c->cpart;
+    a.part_slot = c->cpart_slot;
+    e = timed(c, OSCARS_KERNEL_WGRAD, [&] {
+      hipError_t r = launch_conv(a, CONV_WGRAD, ns, c->stream);
+      return r == hipSuccess ? launch_conv_update(a, CONV_WGRAD, replicas, c->n_pad, lr, ns, c->stream)
+                             : r;
+    });
+  }
+  return e;
+}
 
 // Backward of hidden layer l of a bf16 model without a forced mode: at the
 // first launch of each (inputs, outputs, batch, replicas) the fused launch
@@ -559,6 +827,31 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
   c->upload_pending = true;
   const int32_t* d_order = c->table_dev;
   const int32_t* d_rows = c->table_dev + 64;
+
+  if (c->cnn) {
+    for (int j = 0; j < tau_max; ++j) {
+      int ns = 0;
+      while (ns < n_slots && tau[order[ns]] > j) ++ns;
+      const int32_t* rows_j = d_rows + static_cast<int64_t>(j) * B;
+      const int64_t rows_slot = static_cast<int64_t>(tau_max) * B;
+      const bool from_start = start && j == 0;
+      const float* min = from_start ? start : replicas;
+      const int64_t min_slot = from_start ? 0 : c->n_pad;
+      e = cnn_forward(c, min, min_slot, d_order, s->x, rows_j, rows_slot, B, ns);
+      if (e == hipSuccess)
+        e = timed(c, OSCARS_KERNEL_SOFTMAX, [&] {
+          return launch_softmax_ce(c->logits, c->ld[c->L], c->act_slot(c->L), c->dims[c->L], B,
+                                   s->y, rows_j, rows_slot, c->delta[c->L], false,
+                                   c->loss_dev + static_cast<int64_t>(j) * B, rows_slot, ns,
+                                   c->stream);
+        });
+      if (e == hipSuccess)
+        e = cnn_backward(c, replicas, min, min_slot, d_order, s->x, rows_j, rows_slot, B, ns, lr);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    for (int k = 0; k < K; ++k) c->cursors[k] += tau[k];
+    return OSCARS_OK;
+  }
 
   // ---- bf16 working copies: of the start model once, else of every active replica ----
   if (c->bf16) {
@@ -804,6 +1097,8 @@ hipError_t run_evaluate(oscars_ctx* c, const float* params, const void* x, const
   float* d_loss = reinterpret_cast<float*>(base + lay.loss);
   int32_t* d_hit = reinterpret_cast<int32_t*>(base + lay.hit);
   const int L = c->L, Bmax = c->max_batch;
+  const uint32_t prof_mask = c->prof_mask;  // evaluation launches are never profiled
+  c->prof_mask = 0;
   hipError_t e = launch_eval_rows(d_tab, n_rows, c->stream);
   // Weights as the forward pass reads them: the bf16 copy of params (one
   // cast into the start-model buffer) or params themselves.
@@ -812,6 +1107,13 @@ hipError_t run_evaluate(oscars_ctx* c, const float* params, const void* x, const
   for (int64_t i0 = 0; i0 < n_rows && e == hipSuccess; i0 += Bmax) {
     const int N = static_cast<int>(std::min<int64_t>(Bmax, n_rows - i0));
     const int32_t* rows = d_tab + 64 + i0;
+    if (c->cnn) {
+      e = cnn_forward(c, params, 0, d_tab, x, rows, 0, N, 1);
+      if (e == hipSuccess)
+        e = launch_softmax_ce(c->logits, c->ld[L], c->act_slot(L), c->dims[L], N, y, rows, 0,
+                              c->delta[L], false, d_loss + i0, 0, 1, c->stream, d_hit + i0);
+      continue;
+    }
     for (int l = 1; l <= L && e == hipSuccess; ++l) {
       GemmArgs g{};
       g.M = c->dims[l];
@@ -849,6 +1151,7 @@ hipError_t run_evaluate(oscars_ctx* c, const float* params, const void* x, const
       e = launch_softmax_ce(c->logits, c->ld[L], c->act_slot(L), c->dims[L], N, y, rows, 0,
                             c->delta[L], c->bf16, d_loss + i0, 0, 1, c->stream, d_hit + i0);
   }
+  c->prof_mask = prof_mask;
   if (e == hipSuccess)
     e = launch_eval_reduce(d_loss, d_hit, n_rows, &d_res->loss, &d_res->hits, c->stream);
   Results h{};

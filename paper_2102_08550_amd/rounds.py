@@ -36,7 +36,8 @@ class OscarsRun:
         import torch
         self.cfg = cfg
         self.dtype = BF16 if cfg.dtype == "bf16" else FP32
-        self.ctx = Context(cfg.dims, self.dtype, cfg.K, cfg.batch, stream=stream)
+        self.ctx = Context(cfg.dims, self.dtype, cfg.K, cfg.batch, stream=stream,
+                           cnn=(cfg.image, cfg.conv) if getattr(cfg, "conv", ()) else None)
         dev = torch.device("cuda")
         if self.dtype == BF16:
             self.x = torch.from_numpy(np.ascontiguousarray(dataset.x).view(np.int16)).to(dev)

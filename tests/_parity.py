@@ -113,13 +113,21 @@ def gpu_rounds(cfg, ds, init, tau_rounds, check_agg=True, fused=False):
     return globals_, losses
 
 
+def oracle_step(cfg):
+    """The oracle's SGD step of the workload's model (None: the fully
+    connected network)."""
+    if not cfg.is_cnn:
+        return None
+    return lambda p, Xb, yb, lr: oracle.cnn.sgd_step(p, Xb, yb, lr, cfg.image, cfg.strides)
+
+
 def oracle_rounds(cfg, ds, init, tau_rounds):
     X = ds.x_f32().astype(np.float64)
     out, g, s, losses = [], init, None, []
     for tau in tau_rounds:
         res = oracle.run_rounds(g, X, ds.y, cfg.K, np.array([tau]), cfg.lr, cfg.batch,
                                 workload.sampler_seed(cfg), cfg.dtype == workload.BF16,
-                                steps_done=s)
+                                steps_done=s, step=oracle_step(cfg))
         g, s = res.params, res.steps_done
         out.append(g)
         losses.append(res.losses[0])

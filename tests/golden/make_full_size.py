@@ -1,9 +1,10 @@
 """Writes the expected values of the full-size trajectory tests: the oracle's
-run of the two bf16 MLP workloads over all their rounds (Approach, Eq. 4:
+run of the two bf16 MLP workloads and the convolutional workload over all
+their rounds (Approach, Eq. 4:
 every round each worker runs its tau_k local SGD steps from the global model,
 then the 1/K average).
 
-    python tests/golden/make_full_size.py [c3] [c5]
+    python tests/golden/make_full_size.py [c3] [c5] [c6]
 
 writes ``tests/golden/full_size_<name>.npz``.  Only ``oracle`` (the
 arithmetic) and ``workload`` (the seeded inputs) are called.  A full copy of
@@ -20,7 +21,7 @@ keeps, per round:
   * ``val_<t>``                [len(CHECK)][len(idx)] values at those indices
                                after the rounds in ``check_rounds`` (float32);
   * ``check_rounds``           1-based round numbers kept.
-Runtime on 8 cores: a few minutes for c3, about ten for c5.
+Runtime on 8 cores: about three minutes each.
 """
 from __future__ import annotations
 
@@ -86,9 +87,13 @@ def make(name: str) -> str:
     g = [(W.astype(np.float64), b.astype(np.float64)) for W, b in init]
     steps = None
     seed = workload.sampler_seed(cfg)
+    step = None
+    if cfg.is_cnn:
+        step = lambda p, Xb, yb, lr: oracle.cnn.sgd_step(p, Xb, yb, lr, cfg.image,  # noqa: E731
+                                                         cfg.strides)
     for r in range(cfg.rounds):
         res = oracle.run_rounds(g, X, ds.y, cfg.K, tau[r:r + 1], cfg.lr, cfg.batch, seed,
-                                cfg.dtype == workload.BF16, steps_done=steps)
+                                cfg.dtype == workload.BF16, steps_done=steps, step=step)
         g, steps = res.params, res.steps_done
         out["loss"][r] = res.losses[0]
         tensors = {}
@@ -108,5 +113,5 @@ def make(name: str) -> str:
 
 
 if __name__ == "__main__":
-    for n in (sys.argv[1:] or ["c3", "c5"]):
+    for n in (sys.argv[1:] or ["c3", "c5", "c6"]):
         print("wrote", make(n), flush=True)

@@ -1,0 +1,208 @@
+"""GPU parity of the convolutional workload (the stand-in for the paper's
+CIFAR-10 convolutional network, Evaluation Setup; Approach, Eq. 4) against
+the oracle, on the same seeded inputs, through the C ABI.
+
+* Trajectories tensor by tensor (each conv W_l, b_l and the classifier),
+  element by element, within the fp32 tolerance: small images with ragged
+  tiles in every dimension, strides 1 and 2, split weight gradients, batch 1,
+  a worker idle; as local steps + aggregation and as oscars_round.
+* Masking independence (grouped == solo, bit for bit) and determinism.
+* The full-size workload (32 x 32 x 3 images, 8 workers, all 5 rounds) in the
+  benchmark's launch configuration against the oracle's run stored by
+  tests/golden/make_full_size.py.
+* Held-out evaluation (and the allocation-free variant) against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import workload
+from _parity import (FP32_TOL, assert_tensors_close, gpu_rounds, oracle_rounds, record, say,
+                     tensor_errors)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2102_08550_amd
+    return paper_2102_08550_amd
+
+
+def _cfg(name, image, conv, K, n_rows, batch, tau, rounds, seed, lr=0.1, classes=10):
+    return workload.Config(name, (image[0] * image[1] * image[2], classes), workload.FP32, K=K,
+                           n_rows=n_rows, batch=batch, tau_rule="given", tau_given=tau, lr=lr,
+                           rounds=rounds, seed=seed, image=image, conv=conv, mean_scale=0.5)
+
+
+TRAJ = {
+    # 12 x 10 images: 2400 output pixels at batch 20 (ragged 64-pixel tiles,
+    # two weight-gradient ranges), channels 16 / 24 / 40 (ragged column
+    # tiles), K of 27, 144 and 216 (ragged 16-steps), stride-2 layers on odd
+    # sizes (10 -> 5 -> 3)
+    "small": _cfg("cnn-small", (12, 10, 3), ((16, 1), (24, 2), (40, 2)), K=4, n_rows=600,
+                  batch=20, tau=(3, 1, 0, 2), rounds=3, seed=41),
+    # more than 64 channels and classes, one conv layer, batch 1
+    "wide-b1": _cfg("cnn-wide-b1", (5, 7, 2), ((72, 2),), K=3, n_rows=40, batch=1,
+                    tau=(2, 3, 1), rounds=2, seed=42, classes=70),
+    # the full workload's layers on 16 x 16 images, batch 64 (pixels per
+    # weight-gradient range: several ranges per layer)
+    "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
+                           K=4, tau_rule="given", tau_given=(4, 2, 1, 3), rounds=2),
+}
+CASES = [(n, False) for n in TRAJ] + [("small", True), ("c6s", True)]
+
+
+@pytest.mark.parametrize("name,fused", CASES,
+                         ids=[f"{n}-{'round' if f else 'steps+agg'}" for n, f in CASES])
+def test_cnn_trajectory_matches_oracle(P, name, fused):
+    cfg = TRAJ[name]
+    say(f"cnn trajectory {name} fused={fused}: image={cfg.image} conv={cfg.conv} K={cfg.K} "
+        f"B={cfg.batch}")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = np.array([cfg.tau_given] * cfg.rounds)
+    g_gpu, l_gpu = gpu_rounds(cfg, ds, init, tau, fused=fused)
+    g_ref, l_ref = oracle_rounds(cfg, ds, init, tau)
+    per_round = [tensor_errors(a, b) for a, b in zip(g_gpu, g_ref)]
+    worst = [max(max(e["rel"], e["max"]) for e in pr.values()) for pr in per_round]
+    say(f"  worst per-tensor error per round: {[f'{e:.2e}' for e in worst]}")
+    # the change the rounds made, against the oracle's change
+    upd = tensor_errors([(a - W0, c - b0) for (a, c), (W0, b0) in zip(g_gpu[-1], init)],
+                        [(a - W0, c - b0) for (a, c), (W0, b0) in zip(g_ref[-1], init)])
+    record(f"cnn-trajectory-{name}-{'round' if fused else 'steps'}",
+           {"tol": FP32_TOL, "tensors": per_round, "update": upd})
+    for r in range(cfg.rounds):
+        assert_tensors_close(per_round[r], FP32_TOL, f"round {r + 1}")
+        for k in range(cfg.K):
+            if tau[r][k] == 0:
+                assert np.isnan(l_gpu[r][k])
+            else:
+                assert abs(l_gpu[r][k] - l_ref[r][k]) <= FP32_TOL * abs(l_ref[r][k]), (r, k)
+    assert_tensors_close(upd, 1e-2, "update")
+
+
+def _run_once(cfg, ds, init, tau):
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    run = OscarsRun(cfg, ds, init)
+    run.local_steps(list(tau))
+    torch.cuda.synchronize()
+    reps = run.replicas.view(cfg.K, run.n).cpu().numpy().copy()
+    run.close()
+    return reps
+
+
+def test_cnn_masking_independence_and_determinism(P):
+    cfg = TRAJ["small"]
+    say("cnn masking")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau = (3, 1, 2, 2)
+    grouped = _run_once(cfg, ds, init, tau)
+    again = _run_once(cfg, ds, init, tau)
+    assert np.array_equal(grouped.view(np.uint32), again.view(np.uint32))
+    for k in range(cfg.K):
+        solo_tau = [0] * cfg.K
+        solo_tau[k] = tau[k]
+        solo = _run_once(cfg, ds, init, solo_tau)
+        assert np.array_equal(solo[k].view(np.uint32), grouped[k].view(np.uint32)), k
+
+
+def _load_golden(name):
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                        f"full_size_{name}.npz")
+    with np.load(path, allow_pickle=False) as z:
+        return {k: z[k] for k in z.files}
+
+
+def test_cnn_full_size_trajectory(P):
+    """C6 at full size, all rounds, oscars_round, against the stored oracle run:
+    aggregate bit for bit with the oracle's tree over the GPU's replicas every
+    round, losses, tensor norms, and elements at the check rounds."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun, tau_schedule
+    cfg = workload.C6
+    gold = _load_golden("c6")
+    say(f"full-size {cfg.name}: generating data")
+    ds = workload.gen_dataset(cfg)
+    init = workload.gen_init(cfg)
+    tau_all = tau_schedule(cfg)
+    assert np.array_equal(tau_all, gold["tau"])
+    checks = [int(c) for c in gold["check_rounds"]]
+    run = OscarsRun(cfg, ds, init)
+    log = {"tol": FP32_TOL, "rounds": []}
+    try:
+        for r in range(cfg.rounds):
+            tau = tau_all[r].tolist()
+            run.round(tau)
+            losses = run.ctx.round_losses()
+            torch.cuda.synchronize()
+            reps = run.replicas.view(cfg.K, run.n).cpu().numpy()
+            g = run.g.cpu().numpy()
+            expect = oracle.tree_aggregate([reps[k] for k in range(cfg.K)],
+                                           oracle.paper_weights(cfg.K))
+            assert np.array_equal(g.view(np.uint32), expect.view(np.uint32)), r
+            entry = {"round": r + 1, "loss_rel": [], "norm_rel": {}}
+            for k in range(cfg.K):
+                ref = float(gold["loss"][r][k])
+                e = abs(float(losses[k]) - ref) / max(abs(ref), 1e-2)
+                entry["loss_rel"].append(e)
+                assert e <= FP32_TOL, (r + 1, k, float(losses[k]), ref)
+            tensors = {}
+            for l, (W, b) in enumerate(run.ctx.unpack(g), start=1):
+                tensors[f"W{l}"], tensors[f"b{l}"] = W.ravel(), b.ravel()
+            for t, v in tensors.items():
+                n_ref = gold[f"norm_{t}"][r]
+                entry["norm_rel"][t] = abs(np.linalg.norm(v.astype(np.float64)) - n_ref) / n_ref
+                assert entry["norm_rel"][t] <= FP32_TOL, (r + 1, t)
+            if r + 1 in checks:
+                c = checks.index(r + 1)
+                entry["sampled"] = {}
+                for t, v in tensors.items():
+                    ref = gold[f"val_{t}"][c].astype(np.float64)
+                    d = np.abs(v[gold[f"idx_{t}"]].astype(np.float64) - ref)
+                    entry["sampled"][t] = {"rel": float(np.linalg.norm(d) / np.linalg.norm(ref)),
+                                           "max": float(d.max() / gold[f"absmax_{t}"][r])}
+                assert_tensors_close(entry["sampled"], FP32_TOL, f"round {r + 1}")
+            say(f"  round {r + 1}: loss rel <= {max(entry['loss_rel']):.2e}, norm rel <= "
+                f"{max(entry['norm_rel'].values()):.2e}")
+            log["rounds"].append(entry)
+    finally:
+        record("full-size-c6", log)
+        run.close()
+
+
+def test_cnn_evaluate_matches_oracle(P):
+    import torch
+    cfg = TRAJ["small"]
+    say("cnn evaluate")
+    init = workload.gen_init(cfg)
+    ctx = P.Context(cfg.dims, P.FP32, cfg.K, cfg.batch, cnn=(cfg.image, cfg.conv))
+    try:
+        params = torch.from_numpy(ctx.pack(init)).cuda()
+        ev = workload.gen_eval_set(cfg, 3 * cfg.batch + 7)
+        x = torch.from_numpy(ev.x).cuda()
+        y = torch.from_numpy(ev.y.astype(np.int32)).cuda()
+        loss, hits = ctx.evaluate(params, x, y)
+        loss2, hits2 = ctx.evaluate(params, x, y, noalloc=True)
+        ref_loss, ref_hits = oracle.cnn.evaluate(
+            [(W.astype(np.float64), b.astype(np.float64)) for W, b in init],
+            ev.x.astype(np.float64), ev.y, cfg.image, cfg.strides)
+        say(f"  loss {loss} vs {ref_loss}, correct {hits} vs {ref_hits}")
+        assert abs(loss - ref_loss) <= FP32_TOL * abs(ref_loss)
+        assert abs(hits - ref_hits) <= 1
+        assert (loss2, hits2) == (loss, hits)
+    finally:
+        ctx.close()
+
+
+def test_cnn_create_rejects_bad_models(P):
+    for image, conv, classes in (((0, 4, 3), ((8, 1),), 10), ((4, 4, 3), ((8, 3),), 10),
+                                 ((4, 4, 3), ((0, 1),), 10), ((4, 4, 3), (), 10),
+                                 ((4, 4, 3), ((8, 1),), 0)):
+        with pytest.raises((P.OscarsError, ValueError)):
+            P.Context((image[0] * image[1] * image[2], classes), P.FP32, 2, 4,
+                      cnn=(image, conv))

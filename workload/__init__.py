@@ -20,7 +20,11 @@ Setup, which is not available here):
   Rows are drawn in fixed chunks of ``_CHUNK`` rows so that the stream does not
   depend on available memory.
 * init: for each layer, W[out][in] then b[out] ~ U(-1/sqrt(in), +1/sqrt(in)),
-  float32 (the ``nn.Linear`` convention).
+  float32 (the ``nn.Linear`` convention); convolutional workloads draw each
+  conv layer's W[out][3][3][in] and b[out] ~ U(-1/sqrt(9 in), +1/sqrt(9 in))
+  (the ``nn.Conv2d`` convention), then the classifier as a linear layer.
+* convolutional workloads (the stand-in for the paper's CIFAR-10 images):
+  a row is an H x W x C image, channels fastest, drawn from the same mixture.
 """
 from __future__ import annotations
 
@@ -58,9 +62,17 @@ class Config:
     sigma: float = 0.02  # aggregation-only: spread of the replicas around g
     staleness_max: int = 4
     mean_scale: float = 1.0  # class means ~ N(0, mean_scale^2 I): smaller overlaps the classes more
+    image: Tuple[int, ...] = ()  # convolutional workloads: (H, W, C) of a row
+    conv: Tuple[Tuple[int, int], ...] = ()  # convolutional workloads: (out channels, stride) per 3x3 layer
+
+    @property
+    def is_cnn(self) -> bool:
+        return bool(self.conv)
 
     @property
     def n_layers(self) -> int:
+        if self.conv:  # conv layers, then the classifier
+            return len(self.conv) + 1
         return max(len(self.dims) - 1, 0)
 
     @property
@@ -73,7 +85,17 @@ class Config:
 
     @property
     def n_params(self) -> int:
+        if self.is_cnn:
+            n, cin = 0, self.image[2]
+            for co, _ in self.conv:
+                n += 9 * cin * co + co
+                cin = co
+            return n + self.n_classes * cin + self.n_classes
         return sum(o * i + o for i, o in zip(self.dims[:-1], self.dims[1:]))
+
+    @property
+    def strides(self) -> Tuple[int, ...]:
+        return tuple(s for _, s in self.conv)
 
 
 # The five workloads the hot path is measured on.  C3/C5 learning rates are not
@@ -92,7 +114,16 @@ C5 = Config("mlp-4096x4-1000-bf16-K8", (4096, 4096, 4096, 4096, 1000), BF16, K=8
             n_rows=200000, batch=256, tau_rule="speeds", speeds=(1, 1, 2, 2, 3, 4, 6, 8),
             lr=0.05, rounds=5, seed=5)
 
-CONFIGS = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5}
+# Convolutional workload: CIFAR-shaped 32 x 32 x 3 images, 10 classes, three
+# 3 x 3 conv layers (32, 64, 128 channels; strides 1, 2, 2), global average
+# pooling, a linear classifier; fp32 like the paper's PyTorch; batch 128 as
+# in the paper's convergence experiment; 8 workers with the speed factors of
+# the 784-512-256-10 workload.
+C6 = Config("cnn-32x32x3-c32-c64s2-c128s2-fp32-K8", (3072, 10), FP32, K=8, n_rows=50000,
+            batch=128, tau_rule="speeds", speeds=(1, 1, 1, 1, 2, 2, 4, 8), lr=0.05, rounds=5,
+            seed=6, image=(32, 32, 3), conv=((32, 1), (64, 2), (128, 2)))
+
+CONFIGS = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c6": C6}
 
 
 def scaled(cfg: Config, **changes) -> Config:
@@ -165,9 +196,23 @@ def gen_dataset(cfg: Config) -> Dataset:
 
 
 def gen_init(cfg: Config) -> List[Tuple[np.ndarray, np.ndarray]]:
-    """Initial parameters as a list of (W[out][in], b[out]) float32 arrays."""
+    """Initial parameters as a list of (W[out][in], b[out]) float32 arrays
+    (convolutional workloads: W[out][3][3][in] per conv layer, then the
+    classifier's W[classes][channels])."""
     g = _streams(cfg)[2]
     layers = []
+    if cfg.is_cnn:
+        cin = cfg.image[2]
+        for co, _ in cfg.conv:
+            a = 1.0 / math.sqrt(9 * cin)
+            W = g.uniform(-a, a, size=(co, 3, 3, cin)).astype(np.float32)
+            b = g.uniform(-a, a, size=(co,)).astype(np.float32)
+            layers.append((W, b))
+            cin = co
+        a = 1.0 / math.sqrt(cin)
+        layers.append((g.uniform(-a, a, size=(cfg.n_classes, cin)).astype(np.float32),
+                       g.uniform(-a, a, size=(cfg.n_classes,)).astype(np.float32)))
+        return layers
     for fan_in, fan_out in zip(cfg.dims[:-1], cfg.dims[1:]):
         a = 1.0 / math.sqrt(fan_in)
         W = g.uniform(-a, a, size=(fan_out, fan_in)).astype(np.float32)
