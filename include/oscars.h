@@ -118,7 +118,8 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* model, int32_t
  * throughout, like the paper's PyTorch.
  *   height, width, channels  the input image; a dataset row holds
  *             height x width x channels fp32 values, channels fastest (NHWC);
- *             height, width <= 4096, the row at most 2^24 values;
+ *             height, width <= 4096, the row at most 2^24 values, and
+ *             max_batch x every layer's activations below 2^31 values;
  *   n_conv    1 <= n_conv <= OSCARS_MAX_LAYERS - 1 conv layers, each a 3 x 3
  *             convolution with one row and column of zero padding on every
  *             side, a bias per output channel and ReLU:

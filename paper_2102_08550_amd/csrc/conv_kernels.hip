@@ -49,35 +49,183 @@ __host__ __device__ inline Dims pass_dims(const ConvArgs& a, int pass) {
   }
 }
 
-// Input tap k = (r 3 + s) C + c of output pixel `pix` = (b Ho + i) Wo + j:
-// input[b][stride i + r - 1][stride j + s - 1][c], zero outside the image.
-__device__ __forceinline__ float conv_tap(const ConvArgs& a, const float* in,
-                                          const int32_t* rows, int64_t pix, int64_t k) {
-  const int64_t hw = static_cast<int64_t>(a.Ho) * a.Wo;
-  const int b = static_cast<int>(pix / hw), p = static_cast<int>(pix % hw);
-  const int i = p / a.Wo, j = p % a.Wo;
-  const int rs = static_cast<int>(k / a.C), c = static_cast<int>(k % a.C);
-  const int hi = a.stride * i + rs / 3 - 1, wi = a.stride * j + rs % 3 - 1;
-  if (hi < 0 || hi >= a.H || wi < 0 || wi >= a.W) return 0.0f;
-  const float* img = rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
-                          : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
-  return img[(static_cast<int64_t>(hi) * a.W + wi) * a.C + c];
-}
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// Output-gradient tap k = (r 3 + s) Cout + o of input pixel q = (b H + hi) W + wi:
-// dZ[b][i][j][o] where stride i + r - 1 = hi and stride j + s - 1 = wi, else 0.
-__device__ __forceinline__ float dgrad_tap(const ConvArgs& a, const float* dz, int64_t q,
-                                           int64_t k) {
-  const int64_t hw = static_cast<int64_t>(a.H) * a.W;
-  const int b = static_cast<int>(q / hw), p = static_cast<int>(q % hw);
-  const int hi = p / a.W, wi = p % a.W;
-  const int rs = static_cast<int>(k / a.Co), o = static_cast<int>(k % a.Co);
-  const int ti = hi + 1 - rs / 3, tj = wi + 1 - rs % 3;
-  if (ti < 0 || tj < 0 || ti % a.stride != 0 || tj % a.stride != 0) return 0.0f;
-  const int i = ti / a.stride, j = tj / a.stride;
-  if (i >= a.Ho || j >= a.Wo) return 0.0f;
-  return dz[((static_cast<int64_t>(b) * a.Ho + i) * a.Wo + j) * a.Co + o];
-}
+// Loaders.  A thread gathers, per K step, four consecutive K elements of one
+// A row (m0 + t / 4) and of one B row (n0 + t / 4).  What depends only on
+// the row (the pixel's image and position, or the weight tap of a column) is
+// decoded once per workgroup; the K index is decoded once per step and
+// stepped through the four elements.  Where the four elements are
+// consecutive channels of one tap (channel counts a multiple of 4) they are
+// one 16-byte load.  Sizes fit 32-bit indices (oscars_create_cnn checks).
+template <int PASS>
+struct ConvLoader {
+  const ConvArgs& a;
+  int kend;
+  // A row
+  bool am = false;
+  const float* arow = nullptr;
+  int ah = 0, aw = 0;
+  int am_idx = 0;
+  // B row
+  bool bn = false, bones = false;
+  int bn_idx = 0, br = 0, bs = 0, bc = 0;
+  const float* in = nullptr;
+  const int32_t* rows = nullptr;
+  const float* dz = nullptr;
+  const float* Wt = nullptr;
+
+  __device__ ConvLoader(const ConvArgs& a_, int kend_, int m, int M, int n, int N, const float* in_,
+                        const int32_t* rows_, const float* dz_, const float* Wt_)
+      : a(a_), kend(kend_), am(m < M), am_idx(m), bn(n < N), bn_idx(n), in(in_), rows(rows_),
+        dz(dz_), Wt(Wt_) {
+    if constexpr (PASS == CONV_FWD) {
+      if (am) {
+        const int hw = a.Ho * a.Wo, b = m / hw, p = m - b * hw, i = p / a.Wo, j = p - i * a.Wo;
+        arow = image(b);
+        ah = a.stride * i - 1;
+        aw = a.stride * j - 1;
+      }
+    } else if constexpr (PASS == CONV_DGRAD) {
+      if (am) {
+        const int hw = a.H * a.W, b = m / hw, p = m - b * hw, hi = p / a.W, wi = p - hi * a.W;
+        arow = dz + static_cast<int64_t>(b) * a.Ho * a.Wo * a.Co;
+        ah = hi + 1;
+        aw = wi + 1;
+      }
+    } else if constexpr (PASS == CONV_WGRAD) {
+      if (bn) {
+        bones = n == 9 * a.C;
+        if (!bones) {
+          const int rs = n / a.C;
+          bc = n - rs * a.C;
+          br = rs / 3;
+          bs = rs - 3 * br;
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ const float* image(int b) const {
+    return rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
+                : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+  }
+
+  __device__ __forceinline__ void fetch(int k, float (&ra)[4], float (&rb)[4]) const {
+    if constexpr (PASS == CONV_FWD) {
+      int rs = k / a.C, c = k - rs * a.C;
+      if ((a.C & 3) == 0) {
+        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        const int r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
+        if (am && k < kend && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W)
+          v = *reinterpret_cast<const f32x4*>(arow + (hi * a.W + wi) * a.C + c);
+        for (int e = 0; e < 4; ++e) ra[e] = v[e];
+      } else {
+        for (int e = 0; e < 4; ++e) {
+          float v = 0.0f;
+          const int r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
+          if (am && k + e < kend && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W)
+            v = arow[(hi * a.W + wi) * a.C + c];
+          ra[e] = v;
+          if (++c == a.C) {
+            c = 0;
+            ++rs;
+          }
+        }
+      }
+      const int K9 = 9 * a.C;
+      if ((K9 & 3) == 0) {
+        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (bn && k < kend) v = *reinterpret_cast<const f32x4*>(Wt + static_cast<int64_t>(bn_idx) * K9 + k);
+        for (int e = 0; e < 4; ++e) rb[e] = v[e];
+      } else {
+        for (int e = 0; e < 4; ++e)
+          rb[e] = (bn && k + e < kend) ? Wt[static_cast<int64_t>(bn_idx) * K9 + k + e] : 0.0f;
+      }
+    } else if constexpr (PASS == CONV_DGRAD) {
+      int rs = k / a.Co, o = k - rs * a.Co;
+      auto tap = [&](int rs_, int& off) -> bool {
+        const int r = rs_ / 3, ti = ah - r, tj = aw - (rs_ - 3 * r);
+        if (ti < 0 || tj < 0) return false;
+        int i = ti, j = tj;
+        if (a.stride == 2) {
+          if ((ti | tj) & 1) return false;
+          i = ti >> 1;
+          j = tj >> 1;
+        }
+        if (i >= a.Ho || j >= a.Wo) return false;
+        off = (i * a.Wo + j) * a.Co;
+        return true;
+      };
+      if ((a.Co & 3) == 0) {
+        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        int off = 0;
+        if (am && k < kend && tap(rs, off)) v = *reinterpret_cast<const f32x4*>(arow + off + o);
+        for (int e = 0; e < 4; ++e) ra[e] = v[e];
+      } else {
+        int rs2 = rs, o2 = o;
+        for (int e = 0; e < 4; ++e) {
+          int off = 0;
+          ra[e] = (am && k + e < kend && tap(rs2, off)) ? arow[off + o2] : 0.0f;
+          if (++o2 == a.Co) {
+            o2 = 0;
+            ++rs2;
+          }
+        }
+      }
+      const int K9 = 9 * a.C;
+      for (int e = 0; e < 4; ++e) {
+        rb[e] = (bn && k + e < kend) ? Wt[static_cast<int64_t>(o) * K9 + rs * a.C + bn_idx] : 0.0f;
+        if (++o == a.Co) {
+          o = 0;
+          ++rs;
+        }
+      }
+    } else if constexpr (PASS == CONV_WGRAD) {
+      for (int e = 0; e < 4; ++e)
+        ra[e] = (am && k + e < kend) ? dz[static_cast<int64_t>(k + e) * a.Co + am_idx] : 0.0f;
+      const int hw = a.Ho * a.Wo;
+      int b = k / hw, p = k - b * hw, i = p / a.Wo, j = p - i * a.Wo;
+      for (int e = 0; e < 4; ++e) {
+        float v = 0.0f;
+        if (bn && k + e < kend) {
+          if (bones) {
+            v = 1.0f;
+          } else {
+            const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
+            if (hi >= 0 && hi < a.H && wi >= 0 && wi < a.W) v = image(b)[(hi * a.W + wi) * a.C + bc];
+          }
+        }
+        rb[e] = v;
+        if (++j == a.Wo) {
+          j = 0;
+          if (++i == a.Ho) {
+            i = 0;
+            ++b;
+          }
+        }
+      }
+    } else if constexpr (PASS == FC_FWD) {
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = k + e < kend;
+        ra[e] = (am && ok) ? in[am_idx * a.C + k + e] : 0.0f;
+        rb[e] = (bn && ok) ? Wt[bn_idx * a.C + k + e] : 0.0f;
+      }
+    } else if constexpr (PASS == FC_DGRAD) {
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = k + e < kend;
+        ra[e] = (am && ok) ? dz[static_cast<int64_t>(am_idx) * a.dout_ld + k + e] : 0.0f;
+        rb[e] = (bn && ok) ? Wt[(k + e) * a.C + bn_idx] : 0.0f;
+      }
+    } else {  // FC_WGRAD
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = k + e < kend;
+        ra[e] = (am && ok) ? dz[static_cast<int64_t>(k + e) * a.dout_ld + am_idx] : 0.0f;
+        rb[e] = (bn && ok) ? (bn_idx == a.C ? 1.0f : in[(k + e) * a.C + bn_idx]) : 0.0f;
+      }
+    }
+  }
+};
 
 template <int PASS>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
@@ -85,57 +233,29 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   __shared__ float As[2][CK][CLD];
   __shared__ float Bs[2][CK][CLD];
   const Dims d = pass_dims(a, PASS);
+  const int M = static_cast<int>(d.M), N = static_cast<int>(d.N), K = static_cast<int>(d.K);
   const int z = blockIdx.y;
   const int rep = a.order[z];
-  const int64_t gm = (d.M + CT - 1) / CT, gn = (d.N + CT - 1) / CT;
-  int64_t tile = blockIdx.x;
-  int split = 0;
+  const int gm = (M + CT - 1) / CT, gn = (N + CT - 1) / CT;
+  int tile = blockIdx.x, split = 0;
   if constexpr (WG) {
-    split = static_cast<int>(tile / (gm * gn));
-    tile %= gm * gn;
+    split = tile / (gm * gn);
+    tile -= split * gm * gn;
   }
-  const int64_t m0 = tile / gn * CT, n0 = tile % gn * CT;
-  const int64_t kbeg = WG ? split * a.k_per_split : 0;
-  const int64_t kend = WG ? (d.K < kbeg + a.k_per_split ? d.K : kbeg + a.k_per_split) : d.K;
+  const int m0 = tile / gn * CT, n0 = (tile - tile / gn * gn) * CT;
+  const int kbeg = WG ? split * static_cast<int>(a.k_per_split) : 0;
+  const int kend = WG ? (K - kbeg < a.k_per_split ? K : kbeg + static_cast<int>(a.k_per_split)) : K;
 
   const float* in = a.in ? a.in + z * a.in_slot : nullptr;
   const int32_t* rows = a.gather ? a.gather + z * a.gather_slot : nullptr;
   const float* dz = a.dout ? a.dout + z * a.dout_slot : nullptr;
   const float* par = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
-  const float* Wt = par + a.w_off;
-
-  auto A = [&](int64_t m, int64_t k) -> float {
-    if constexpr (PASS == CONV_FWD) return conv_tap(a, in, rows, m, k);
-    if constexpr (PASS == CONV_DGRAD) return dgrad_tap(a, dz, m, k);
-    if constexpr (PASS == CONV_WGRAD) return dz[k * a.Co + m];
-    if constexpr (PASS == FC_FWD) return in[m * a.C + k];
-    if constexpr (PASS == FC_DGRAD) return dz[m * a.dout_ld + k];
-    return dz[k * a.dout_ld + m];  // FC_WGRAD
-  };
-  auto Bv = [&](int64_t n, int64_t k) -> float {
-    if constexpr (PASS == CONV_FWD) return Wt[n * 9 * a.C + k];
-    if constexpr (PASS == CONV_DGRAD) return Wt[(k % a.Co) * 9 * a.C + (k / a.Co) * a.C + n];
-    if constexpr (PASS == CONV_WGRAD) return n == 9LL * a.C ? 1.0f : conv_tap(a, in, rows, k, n);
-    if constexpr (PASS == FC_FWD) return Wt[n * a.C + k];
-    if constexpr (PASS == FC_DGRAD) return Wt[k * a.C + n];
-    return n == a.C ? 1.0f : in[k * a.C + n];  // FC_WGRAD
-  };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, r = lane & 31, h = lane >> 5;
-  // loader: thread t gathers rows m0 + t / 4 (A) and n0 + t / 4 (B), K
-  // elements 4 (t % 4) .. 4 (t % 4) + 3 of the step
   const int lr = tid >> 2, lk = (tid & 3) * 4;
+  const ConvLoader<PASS> ld(a, kend, m0 + lr, M, n0 + lr, N, in, rows, dz, par + a.w_off);
   float ra[4], rb[4];
-  auto gather = [&](int64_t k0) {
-    const int64_t m = m0 + lr, n = n0 + lr;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t k = k0 + lk + e;
-      ra[e] = (m < d.M && k < kend) ? A(m, k) : 0.0f;
-      rb[e] = (n < d.N && k < kend) ? Bv(n, k) : 0.0f;
-    }
-  };
   auto stash = [&](int buf) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -147,13 +267,13 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   f32x16 acc;
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-  const int64_t nk = (kend - kbeg + CK - 1) / CK;
-  gather(kbeg);
+  const int nk = (kend - kbeg + CK - 1) / CK;
+  ld.fetch(kbeg + lk, ra, rb);
   stash(0);
   __syncthreads();
-  for (int64_t t = 0; t < nk; ++t) {
-    const int buf = static_cast<int>(t & 1);
-    if (t + 1 < nk) gather(kbeg + (t + 1) * CK);
+  for (int t = 0; t < nk; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nk) ld.fetch(kbeg + (t + 1) * CK + lk, ra, rb);
     // MFMA u contracts k = 2u (lanes 0-31) and 2u + 1 (lanes 32-63)
 #pragma unroll
     for (int u = 0; u < CK / 2; ++u)
@@ -164,24 +284,24 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
 
   // accumulator i of lane (r, h): row 8 (i / 4) + 4 h + i % 4, column r
-  const int64_t col = n0 + wn * 32 + r;
+  const int col = n0 + wn * 32 + r;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const int64_t row = m0 + wm * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-    if (row >= d.M || col >= d.N) continue;
+    const int row = m0 + wm * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+    if (row >= M || col >= N) continue;
     const float v = acc[i];
     if constexpr (PASS == CONV_FWD) {
       const float zv = v + par[a.b_off + col];
-      a.out[z * a.out_slot + row * a.Co + col] = zv > 0.0f ? zv : 0.0f;
+      a.out[z * a.out_slot + static_cast<int64_t>(row) * a.Co + col] = zv > 0.0f ? zv : 0.0f;
     } else if constexpr (PASS == FC_FWD) {
-      a.out[z * a.out_slot + row * a.out_ld + col] = v + par[a.b_off + col];
+      a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v + par[a.b_off + col];
     } else if constexpr (PASS == CONV_DGRAD) {
-      const int64_t at = row * a.C + col;
+      const int64_t at = static_cast<int64_t>(row) * a.C + col;
       a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? v : 0.0f;
     } else if constexpr (PASS == FC_DGRAD) {
-      a.out[z * a.out_slot + row * a.out_ld + col] = v;
+      a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v;
     } else {
-      a.part[z * a.part_slot + (split * d.M + row) * d.N + col] = v;
+      a.part[z * a.part_slot + (static_cast<int64_t>(split) * M + row) * N + col] = v;
     }
   }
 }

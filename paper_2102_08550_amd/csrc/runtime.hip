@@ -44,7 +44,7 @@ constexpr int kMaxTau = 4096;
 // of up to this many local steps per worker need no allocation later.
 constexpr int kPreTau = 64;
 // Output pixels per weight-gradient partial of a conv layer.
-constexpr int64_t kConvPixelsPerSplit = 2048;
+constexpr int64_t kConvPixelsPerSplit = 512;
 
 }  // namespace
 
@@ -420,6 +420,13 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
     c->img_h[l] = (c->img_h[l - 1] - 1) / c->conv_stride[l] + 1;
     c->img_w[l] = (c->img_w[l - 1] - 1) / c->conv_stride[l] + 1;
     c->img_c[l] = m->conv_channels[l - 1];
+  }
+  for (int l = 0; l <= Lc; ++l) {  // per-slot activations within 32-bit indices
+    if (static_cast<int64_t>(max_batch) * c->img_h[l] * c->img_w[l] * c->img_c[l] >=
+        (int64_t{1} << 31)) {
+      delete c;
+      return OSCARS_E_INVALID;
+    }
   }
   c->w_off.assign(c->L + 1, 0);
   c->b_off.assign(c->L + 1, 0);
