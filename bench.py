@@ -334,6 +334,11 @@ def main():
                     help="backward path of the hidden bf16 layers (auto: timed per "
                          "configuration in this process; a fixed one makes counter passes of "
                          "separate processes run the same launch mix)")
+    ap.add_argument("--schedule", default="grouped", choices=["grouped", "replica"],
+                    help="grouped (default): one oscars_round, every local step of all active "
+                         "workers in one launch per layer and pass; replica: the same round "
+                         "worker after worker (a broadcast, each worker's tau_k steps alone, "
+                         "then the average), to measure a replica-major order")
     ap.add_argument("--probe-copy-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, three "
                          "times (calibration of hardware byte counters)")
@@ -369,6 +374,18 @@ def main():
     run = OscarsRun(cfg, ds, init, stream=stream)
     run.ctx.set_backward(P.BACKWARDS[args.backward])
 
+    def do_round(tau):
+        if args.schedule == "grouped":
+            run.round(tau)
+            return
+        # replica-major: every worker's steps back to back, from the global model
+        P.broadcast(run.g, run.replicas, cfg.K, run.n, run.n)
+        for k in sorted(range(cfg.K), key=lambda k: -int(tau[k])):
+            solo = [0] * cfg.K
+            solo[k] = int(tau[k])
+            run.local_steps(solo)
+        P.aggregate(run.g, run.replicas, run.weights, cfg.K, run.n, run.n, False)
+
     def tau_for(step):
         if cfg.tau_rule == "speeds":  # Algorithm 1 from the workers' iteration times
             return P.load_balance(workload.speeds_to_t_iter(cfg.speeds), cfg.M)[1]
@@ -390,7 +407,7 @@ def main():
     # they are neither profiled nor timed.
     n_tune = 0
     while True:
-        run.round(tau_for(n_tune))
+        do_round(tau_for(n_tune))
         n_tune += 1
         if run.ctx.tuning_pending() == 0 or n_tune >= 64:
             break
@@ -406,7 +423,7 @@ def main():
     samples_w = 0
     for s in range(1, n_warm + 1):
         tau = tau_for(s)
-        run.round(tau)
+        do_round(tau)
         samples_w += int(np.sum(tau)) * cfg.batch
         for kname, (fl, by) in (cnn_work(cfg, tau) if cfg.is_cnn
                                 else gemm_work(cfg, tau, fused_path)).items():
@@ -429,7 +446,7 @@ def main():
         tau = tau_for(args.warmup + s)
         if s == args.steps - 1:
             run.ctx.profile_begin([dom_kind])
-        run.round(tau)
+        do_round(tau)
         if s == args.steps - 1:
             work_tot = cnn_work(cfg, tau) if cfg.is_cnn else gemm_work(cfg, tau, fused_path)
         samples += int(np.sum(tau)) * cfg.batch
@@ -507,6 +524,7 @@ def main():
                         "samples_per_s_kernels": samples_w / (local_ms / 1e3) if local_ms else None},
         "kernels": kernels,
         "backward": {"mode": args.backward, "path_per_layer_and_active_replicas": backward_mix},
+        "schedule": args.schedule,
         "roofline": roof,
         "hbm_copy": copy,
     }
