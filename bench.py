@@ -130,21 +130,22 @@ def kernel_source_hash() -> str:
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
 
-def pmc_traffic(kernel: str, workload_name: str, algorithmic_bytes: float):
+def pmc_traffic(kernel: str, workload_name: str, algorithmic_bytes: float, mix=None):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None.  The
-    summary holds measured / algorithmic bytes per launch (FETCH_SIZE over
-    the fetch pass's algorithmic bytes plus WRITE_SIZE over the write
-    pass's): the backward path of each configuration is timed per process,
-    so a counter pass may run a different mix of launches than this one;
-    the ratio times this run's algorithmic bytes per launch follows the
-    launches timed here."""
+    summary, if it was taken on the current kernel source and, where the
+    summary records it, with the same backward path per layer and active
+    replica count as this run (`mix`); else None.  The summary holds
+    measured / algorithmic bytes per launch (FETCH_SIZE over the fetch
+    pass's algorithmic bytes plus WRITE_SIZE over the write pass's); the
+    ratio times this run's algorithmic bytes per launch gives the bytes."""
     try:
         data = json.load(open(PMC_FILE))
     except (OSError, ValueError):
         return None
     ent = data.get(workload_name, {}).get(kernel)
     if not ent or ent.get("kernels_sha256_16") != kernel_source_hash() or not ent.get("ratio"):
+        return None
+    if mix is not None and ent.get("backward_mix") not in (None, mix):
         return None
     return ent["ratio"] * algorithmic_bytes
 
@@ -469,10 +470,6 @@ def main():
                           "flop_per_launch": fl / cnt, "bytes_per_launch": by / cnt}
         return out_
     kernels = summarize(prof_w, work_w, n_warm)  # breakdown (warmup, every kernel timed)
-    tau0 = np.asarray(tau_for(0))
-    backward_mix = {f"l{l}": {str(ns): ("fused" if fused_path(l, ns) else "separate")
-                              for ns in sorted({int((tau0 > j).sum()) for j in range(tau0.max())})}
-                    for l in range(2, len(cfg.dims))}
     d = summarize(prof, work_tot, 1)[dom]  # dominant kernel, inside the timed region
     ridge = MFMA_PEAK_TFLOPS[cfg.dtype] * 1e12 / (HBM_PEAK_GBPS * 1e9)
     intensity = d["flop_per_launch"] / d["bytes_per_launch"] if d["bytes_per_launch"] else 0.0
@@ -482,7 +479,12 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": d["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = pmc_traffic(dom, args.workload, d["bytes_per_launch"])
+    tau0 = np.asarray(tau_for(0))
+    backward_mix = {f"l{l}": {str(ns): ("fused" if fused_path(l, ns) else "separate")
+                              for ns in sorted({int((tau0 > j).sum()) for j in range(tau0.max())})}
+                    for l in range(2, len(cfg.dims))}
+    mix = backward_mix if args.schedule == "grouped" else {"schedule": "replica"}
+    roof["traffic"] = pmc_traffic(dom, args.workload, d["bytes_per_launch"], mix)
     if roof["traffic"] is not None:
         roof["traffic_basis"] = ("committed counter passes' measured/algorithmic bytes per launch "
                                  "x this run's algorithmic bytes per launch")

@@ -35,3 +35,16 @@ def test_traffic_is_null_once_the_kernels_changed(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "PMC_FILE", str(tmp_path / "missing.json"))
     assert bench.pmc_traffic("gemm_bwd_fused", "c5", 1000.0) is None
 
+
+
+def test_traffic_needs_the_same_launch_mix(tmp_path, monkeypatch):
+    """A summary that records the backward path per layer and replica count
+    applies only to runs that took the same paths."""
+    p = tmp_path / "pmc.json"
+    mix = {"l2": {"8": "fused", "1": "separate"}}
+    json.dump({"c5": {"gemm_bwd_fused": {"kernels_sha256_16": bench.kernel_source_hash(),
+                                         "ratio": 1.1, "backward_mix": mix}}}, open(p, "w"))
+    monkeypatch.setattr(bench, "PMC_FILE", str(p))
+    assert bench.pmc_traffic("gemm_bwd_fused", "c5", 1000.0, mix) == pytest.approx(1100.0)
+    other = {"l2": {"8": "fused", "1": "fused"}}
+    assert bench.pmc_traffic("gemm_bwd_fused", "c5", 1000.0, other) is None
