@@ -130,14 +130,20 @@ def kernel_source_hash() -> str:
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
 
-def pmc_traffic(kernel: str, workload_name: str, algorithmic_bytes: float, mix=None):
+MIX_TOLERANCE = 0.05
+
+
+def pmc_traffic(kernel: str, workload_name: str, algorithmic_bytes: float, mix=None,
+                mix_bytes=None):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source and, where the
-    summary records it, with the same backward path per layer and active
-    replica count as this run (`mix`); else None.  The summary holds
-    measured / algorithmic bytes per launch (FETCH_SIZE over the fetch
-    pass's algorithmic bytes plus WRITE_SIZE over the write pass's); the
-    ratio times this run's algorithmic bytes per launch gives the bytes."""
+    summary, if it was taken on the current kernel source and on a launch mix
+    close to this run's; else None.  The summary holds measured / algorithmic
+    bytes per launch (FETCH_SIZE over the fetch pass's algorithmic bytes plus
+    WRITE_SIZE over the write pass's); the ratio times this run's algorithmic
+    bytes per launch gives the bytes.  Where the summary records its backward
+    path per layer and active replica count and it differs from this run's
+    (`mix`), the kind's algorithmic bytes per round under the two mixes
+    (`mix_bytes(mix)`) must agree within MIX_TOLERANCE."""
     try:
         data = json.load(open(PMC_FILE))
     except (OSError, ValueError):
@@ -145,8 +151,13 @@ def pmc_traffic(kernel: str, workload_name: str, algorithmic_bytes: float, mix=N
     ent = data.get(workload_name, {}).get(kernel)
     if not ent or ent.get("kernels_sha256_16") != kernel_source_hash() or not ent.get("ratio"):
         return None
-    if mix is not None and ent.get("backward_mix") not in (None, mix):
-        return None
+    theirs = ent.get("backward_mix")
+    if mix is not None and theirs is not None and theirs != mix:
+        if mix_bytes is None or "schedule" in theirs or "schedule" in mix:
+            return None
+        ours, other = mix_bytes(mix), mix_bytes(theirs)
+        if not ours or abs(other - ours) > MIX_TOLERANCE * ours:
+            return None
     return ent["ratio"] * algorithmic_bytes
 
 
@@ -484,7 +495,13 @@ def main():
                               for ns in sorted({int((tau0 > j).sum()) for j in range(tau0.max())})}
                     for l in range(2, len(cfg.dims))}
     mix = backward_mix if args.schedule == "grouped" else {"schedule": "replica"}
-    roof["traffic"] = pmc_traffic(dom, args.workload, d["bytes_per_launch"], mix)
+
+    def mix_bytes(m):  # the dominant kind's algorithmic bytes per round under mix m
+        if cfg.is_cnn:
+            return cnn_work(cfg, tau0)[dom][1]
+        path = lambda l, ns: m.get(f"l{l}", {}).get(str(ns), "fused") == "fused"  # noqa: E731
+        return gemm_work(cfg, tau0, path)[dom][1]
+    roof["traffic"] = pmc_traffic(dom, args.workload, d["bytes_per_launch"], mix, mix_bytes)
     if roof["traffic"] is not None:
         roof["traffic_basis"] = ("committed counter passes' measured/algorithmic bytes per launch "
                                  "x this run's algorithmic bytes per launch")
@@ -513,12 +530,14 @@ def main():
         "kernels_note": "per-kernel breakdown from the warmup rounds (events around every "
                         "launch); the roofline kernel is timed by events around its launches "
                         "in the last timed round",
-        "aggregation": {"GBps": kernels["aggregate"]["GBps"],
-                        "frac_hbm_peak": kernels["aggregate"]["GBps"] / HBM_PEAK_GBPS,
-                        "avg_us": kernels["aggregate"]["avg_us"],
-                        "bytes_per_round": kernels["aggregate"]["bytes_per_launch"],
-                        "note": "K-way average into the global model; oscars_round starts the "
-                                "next round's workers from it, so no broadcast copies are written"},
+        "aggregation": ({"GBps": kernels["aggregate"]["GBps"],
+                         "frac_hbm_peak": kernels["aggregate"]["GBps"] / HBM_PEAK_GBPS,
+                         "avg_us": kernels["aggregate"]["avg_us"],
+                         "bytes_per_round": kernels["aggregate"]["bytes_per_launch"],
+                         "note": "K-way average into the global model; oscars_round starts the "
+                                 "next round's workers from it, so no broadcast copies are "
+                                 "written"}
+                        if "aggregate" in kernels else None),
         "local_steps": {"kernel_ms_per_round": local_ms / n_warm,
                         "TFLOPs": flops / (local_ms / 1e3) / 1e12 if local_ms else None,
                         "frac_mfma_peak": flops / (local_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS[cfg.dtype]

@@ -391,7 +391,9 @@ oscars_status oscars_tuning_pending(const oscars_ctx* ctx, int32_t* configuratio
  *     chunks per workgroup (all; then half, a quarter, ... down to one,
  *     where the context's partial buffer holds the split), and the separate
  *     launches.  Each runs three times there on the scratch replicas
- *     oscars_create allocated, the faster of its last two runs counting.
+ *     oscars_create allocated, the faster of its last two runs counting; a
+ *     later candidate is taken only when it is more than 5% faster than the
+ *     earlier pick.
  *     Untimed -- on a stream being captured into a graph, or where
  *     oscars_create left the scratch out --: fused, split over the number of
  *     workgroups per 64-wide input strip that fills the last pass over the

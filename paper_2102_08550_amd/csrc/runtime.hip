@@ -43,6 +43,8 @@ constexpr int kMaxTau = 4096;
 // Index-table, loss and staging capacity allocated by oscars_create: rounds
 // of up to this many local steps per worker need no allocation later.
 constexpr int kPreTau = 64;
+// Backward path timing: how much faster a later candidate must be to be taken.
+constexpr float kBackwardMargin = 0.05f;
 // Output pixels per weight-gradient partial of a conv layer.
 constexpr int64_t kConvPixelsPerSplit = 512;
 
@@ -751,9 +753,13 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
     }
   }
   if (e != hipSuccess) return e;
+  // A later candidate replaces the pick only when it is faster by more than
+  // kBackwardMargin: near ties (within the run-to-run spread of these
+  // timings) go to the earlier candidate, so that separate processes on one
+  // box take the same paths.
   int pick = 0;
   for (int i = 1; i < nc; ++i)
-    if (best[i] < best[pick]) pick = i;
+    if (best[i] < best[pick] * (1.0f - kBackwardMargin)) pick = i;
   *cps = cand[pick];
   c->bwd_fused_choice[key] = *cps;
   return hipSuccess;

@@ -48,3 +48,16 @@ def test_traffic_needs_the_same_launch_mix(tmp_path, monkeypatch):
     assert bench.pmc_traffic("gemm_bwd_fused", "c5", 1000.0, mix) == pytest.approx(1100.0)
     other = {"l2": {"8": "fused", "1": "fused"}}
     assert bench.pmc_traffic("gemm_bwd_fused", "c5", 1000.0, other) is None
+
+
+def test_traffic_accepts_a_mix_of_nearly_the_same_bytes(tmp_path, monkeypatch):
+    p = tmp_path / "pmc.json"
+    theirs = {"l2": {"1": "fused"}}
+    json.dump({"c5": {"gemm_bwd_fused": {"kernels_sha256_16": bench.kernel_source_hash(),
+                                         "ratio": 1.1, "backward_mix": theirs}}}, open(p, "w"))
+    monkeypatch.setattr(bench, "PMC_FILE", str(p))
+    ours = {"l2": {"1": "separate"}}
+    close = lambda m: 1000.0 if m == ours else 1020.0  # noqa: E731
+    far = lambda m: 1000.0 if m == ours else 1200.0  # noqa: E731
+    assert bench.pmc_traffic("gemm_bwd_fused", "c5", 500.0, ours, close) == pytest.approx(550.0)
+    assert bench.pmc_traffic("gemm_bwd_fused", "c5", 500.0, ours, far) is None
