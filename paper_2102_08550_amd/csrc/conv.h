@@ -31,6 +31,8 @@ struct ConvArgs {
   int H, W, C;            // the layer's input (FC: C = pooled channels, H = W = 1)
   int Ho, Wo, Co;         // the layer's output (FC: Co = classes)
   int stride;             // 1 or 2 (conv)
+  int cls;                // CONV_DGRAD with stride 2: parity class of the input pixels, 2 (hi & 1)
+                          // + (wi & 1); a launch per class (see conv_kernels.hip)
   const float* in;        // conv input [B][H][W][C] (or, with gather, dataset rows); FC: pooled
   int64_t in_slot, in_ld;             // slot stride; row stride of a gathered dataset row
   const int32_t* gather;  // layer 1: dataset row of each batch row, [slot] stride gather_slot

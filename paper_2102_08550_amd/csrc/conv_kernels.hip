@@ -13,6 +13,11 @@
 //   FC_WGRAD    classes         channels + 1   batch          delta[k][m]          pooled[k][n] (1)
 //
 // with k = (r 3 + s) Cin + c for the conv taps (the layout of W[o][3][3][c]).
+// Backward-data of a stride-2 layer runs one launch per parity class of the
+// input pixels: input row hi receives output row i through tap r only where
+// hi + 1 - r = 2 i, so even rows take tap r = 1 and odd rows taps 0 and 2
+// (likewise columns).  Each class gathers only its 1, 2 or 4 taps (K = taps x
+// Cout), a quarter of the 9-tap work on average.
 // A workgroup computes a 64 x 64 tile of C with four waves of 32 x 32, fp32
 // MFMA 32x32x2, K in steps of 16: the next step's operands are gathered into
 // registers while the current step's MFMAs read LDS (two LDS buffers, one
@@ -38,10 +43,21 @@ struct Dims {
   int64_t M, N, K;
 };
 
+// Stride-2 backward-data class `cls`: input rows hi = 2 i + (cls >> 1), columns
+// wi = 2 j + (cls & 1); per dimension one tap (r = 1) for even, two (r = 0, 2)
+// for odd positions.
+__host__ __device__ inline int cls_rows(const ConvArgs& a) { return (a.H - (a.cls >> 1) + 1) / 2; }
+__host__ __device__ inline int cls_cols(const ConvArgs& a) { return (a.W - (a.cls & 1) + 1) / 2; }
+__host__ __device__ inline int cls_taps(int odd) { return odd ? 2 : 1; }
+
 __host__ __device__ inline Dims pass_dims(const ConvArgs& a, int pass) {
   switch (pass) {
     case CONV_FWD: return {static_cast<int64_t>(a.B) * a.Ho * a.Wo, a.Co, 9LL * a.C};
-    case CONV_DGRAD: return {static_cast<int64_t>(a.B) * a.H * a.W, a.C, 9LL * a.Co};
+    case CONV_DGRAD:
+      if (a.stride == 2)
+        return {static_cast<int64_t>(a.B) * cls_rows(a) * cls_cols(a), a.C,
+                static_cast<int64_t>(cls_taps(a.cls >> 1)) * cls_taps(a.cls & 1) * a.Co};
+      return {static_cast<int64_t>(a.B) * a.H * a.W, a.C, 9LL * a.Co};
     case CONV_WGRAD: return {a.Co, 9LL * a.C + 1, static_cast<int64_t>(a.B) * a.Ho * a.Wo};
     case FC_FWD: return {a.B, a.Co, a.C};
     case FC_DGRAD: return {a.B, a.C, a.Co};
@@ -88,7 +104,8 @@ struct ConvLoader {
       }
     } else if constexpr (PASS == CONV_DGRAD) {
       if (am) {
-        const int hw = a.H * a.W, b = m / hw, p = m - b * hw, hi = p / a.W, wi = p - hi * a.W;
+        int b, hi, wi;
+        dgrad_pixel(a, m, b, hi, wi);
         arow = dz + static_cast<int64_t>(b) * a.Ho * a.Wo * a.Co;
         ah = hi + 1;
         aw = wi + 1;
@@ -103,6 +120,37 @@ struct ConvLoader {
           bs = rs - 3 * br;
         }
       }
+    }
+  }
+
+  // Input pixel (b, hi, wi) of backward-data row m.
+  static __device__ __forceinline__ void dgrad_pixel(const ConvArgs& a, int m, int& b, int& hi,
+                                                     int& wi) {
+    if (a.stride == 2) {
+      const int rows = cls_rows(a), cols = cls_cols(a), hw = rows * cols;
+      b = m / hw;
+      const int p = m - b * hw, i = p / cols;
+      hi = 2 * i + (a.cls >> 1);
+      wi = 2 * (p - i * cols) + (a.cls & 1);
+    } else {
+      const int hw = a.H * a.W;
+      b = m / hw;
+      const int p = m - b * hw;
+      hi = p / a.W;
+      wi = p - hi * a.W;
+    }
+  }
+
+  // Kernel tap (r, s) of backward-data tap index t: all nine (t = 3 r + s)
+  // for stride 1; the class's one, two or four for stride 2.
+  __device__ __forceinline__ void dgrad_tap_rs(int t, int& r, int& s) const {
+    if (a.stride == 2) {
+      const int ns = cls_taps(a.cls & 1), tr = t / ns, ts = t - tr * ns;
+      r = (a.cls >> 1) ? 2 * tr : 1;
+      s = (a.cls & 1) ? 2 * ts : 1;
+    } else {
+      r = t / 3;
+      s = t - 3 * r;
     }
   }
 
@@ -143,14 +191,18 @@ struct ConvLoader {
           rb[e] = (bn && k + e < kend) ? Wt[static_cast<int64_t>(bn_idx) * K9 + k + e] : 0.0f;
       }
     } else if constexpr (PASS == CONV_DGRAD) {
-      int rs = k / a.Co, o = k - rs * a.Co;
-      auto tap = [&](int rs_, int& off) -> bool {
-        const int r = rs_ / 3, ti = ah - r, tj = aw - (rs_ - 3 * r);
+      int t = k / a.Co, o = k - t * a.Co;
+      // output-gradient row of tap t for this input pixel, or false where the
+      // tap lands outside the output (or, for stride 2 and all nine taps,
+      // between output rows)
+      auto tap = [&](int t_, int& off) -> bool {
+        int r, sc;
+        dgrad_tap_rs(t_, r, sc);
+        const int ti = ah - r, tj = aw - sc;
         if (ti < 0 || tj < 0) return false;
         int i = ti, j = tj;
         if (a.stride == 2) {
-          if ((ti | tj) & 1) return false;
-          i = ti >> 1;
+          i = ti >> 1;  // even by the class's choice of taps
           j = tj >> 1;
         }
         if (i >= a.Ho || j >= a.Wo) return false;
@@ -160,25 +212,31 @@ struct ConvLoader {
       if ((a.Co & 3) == 0) {
         f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
         int off = 0;
-        if (am && k < kend && tap(rs, off)) v = *reinterpret_cast<const f32x4*>(arow + off + o);
+        if (am && k < kend && tap(t, off)) v = *reinterpret_cast<const f32x4*>(arow + off + o);
         for (int e = 0; e < 4; ++e) ra[e] = v[e];
       } else {
-        int rs2 = rs, o2 = o;
+        int t2 = t, o2 = o;
         for (int e = 0; e < 4; ++e) {
           int off = 0;
-          ra[e] = (am && k + e < kend && tap(rs2, off)) ? arow[off + o2] : 0.0f;
+          ra[e] = (am && k + e < kend && tap(t2, off)) ? arow[off + o2] : 0.0f;
           if (++o2 == a.Co) {
             o2 = 0;
-            ++rs2;
+            ++t2;
           }
         }
       }
       const int K9 = 9 * a.C;
       for (int e = 0; e < 4; ++e) {
-        rb[e] = (bn && k + e < kend) ? Wt[static_cast<int64_t>(o) * K9 + rs * a.C + bn_idx] : 0.0f;
+        float v = 0.0f;
+        if (bn && k + e < kend) {
+          int r, sc;
+          dgrad_tap_rs(t, r, sc);
+          v = Wt[static_cast<int64_t>(o) * K9 + (3 * r + sc) * a.C + bn_idx];
+        }
+        rb[e] = v;
         if (++o == a.Co) {
           o = 0;
-          ++rs;
+          ++t;
         }
       }
     } else if constexpr (PASS == CONV_WGRAD) {
@@ -296,7 +354,9 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     } else if constexpr (PASS == FC_FWD) {
       a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v + par[a.b_off + col];
     } else if constexpr (PASS == CONV_DGRAD) {
-      const int64_t at = static_cast<int64_t>(row) * a.C + col;
+      int b, hi, wi;
+      ConvLoader<PASS>::dgrad_pixel(a, row, b, hi, wi);
+      const int64_t at = ((static_cast<int64_t>(b) * a.H + hi) * a.W + wi) * a.C + col;
       a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? v : 0.0f;
     } else if constexpr (PASS == FC_DGRAD) {
       a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v;
@@ -357,6 +417,8 @@ __global__ __launch_bounds__(256) void avgpool_backward_kernel(const float* dpoo
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
   const Dims d = pass_dims(a, pass);
+  if (pass == CONV_DGRAD && a.stride == 2 && d.M == 0 && n_slots >= 1)
+    return hipSuccess;  // a parity class without pixels (an extent of 1)
   if (n_slots < 1 || d.M < 1 || d.N < 1 || d.K < 1) return hipErrorInvalidValue;
   int64_t gx = ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
   if (pass == CONV_WGRAD || pass == FC_WGRAD) {

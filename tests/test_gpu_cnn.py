@@ -46,6 +46,10 @@ TRAJ = {
     # more than 64 channels and classes, one conv layer, batch 1
     "wide-b1": _cfg("cnn-wide-b1", (5, 7, 2), ((72, 2),), K=3, n_rows=40, batch=1,
                     tau=(2, 3, 1), rounds=2, seed=42, classes=70),
+    # stride-2 backward-data whose odd-column class is empty (width 1) and a
+    # 2-row image
+    "thin": _cfg("cnn-thin", (3, 1, 4), ((8, 1), (12, 2), (8, 2)), K=2, n_rows=30, batch=7,
+                 tau=(2, 3), rounds=2, seed=43),
     # the full workload's layers on 16 x 16 images, batch 64 (pixels per
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
