@@ -230,8 +230,9 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
         "value": steps * cfg.batch / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
         "host": host_info(),
         "sample": f"{steps} local SGD steps of batch {cfg.batch} (workers' steps of {rounds} "
-                  f"round(s), each worker from the round's start model; {dt:.1f} s, float64 "
-                  f"with bf16 rounding points); aggregation of {cfg.K} x {n_slice} fp32 slices",
+                  f"round(s), each worker from the round's start model; {dt:.1f} s, float64"
+                  f"{' with bf16 rounding points' if cfg.dtype == 'bf16' else ''}); aggregation of "
+                  f"{cfg.K} x {n_slice} fp32 slices",
         "aggregate_GBps": (cfg.K + 1) * n_slice * 4 / dta / 1e9,
     }
 
