@@ -218,7 +218,12 @@ oscars_status oscars_sample_indices(const oscars_shards* shards, int32_t K, int3
  *   lr        learning rate eta, finite and > 0;
  *   batch     mini-batch size, 1 <= batch <= max_batch of the context.
  * Worker k continues its sample stream where its previous call stopped (its
- * cursor advances by tau[k]).  Replicas with tau[k] <= j get no work in step j. */
+ * cursor advances by tau[k]).  Replicas with tau[k] <= j get no work in step j.
+ * The batches' rows are drawn on the host and uploaded from a staging buffer
+ * that the next call reuses: a call first waits until the stream has run the
+ * previous call's upload (the host stays at most one call ahead).  Hence
+ * OSCARS_E_STATE, with no side effects, when the context's stream is being
+ * captured into a graph. */
 oscars_status oscars_local_steps(oscars_ctx* ctx, float* replicas, const oscars_shards* shards,
                                  const int32_t* tau, float lr, int32_t batch);
 
@@ -236,7 +241,8 @@ oscars_status oscars_local_steps(oscars_ctx* ctx, float* replicas, const oscars_
  * Equivalent to copying global into every replica, oscars_local_steps and
  * oscars_aggregate(global, replicas, weights, K, n, n, 0), bit for bit, but
  * without writing K copies of the model: the first step reads the global
- * model directly. */
+ * model directly.  Waits for the previous upload, and refuses a stream being
+ * captured into a graph (OSCARS_E_STATE), as oscars_local_steps. */
 oscars_status oscars_round(oscars_ctx* ctx, float* global, float* replicas,
                            const oscars_shards* shards, const int32_t* tau, float lr,
                            int32_t batch, const float* weights);

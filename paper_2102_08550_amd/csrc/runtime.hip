@@ -787,6 +787,13 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
     if (s->offsets[k + 1] <= s->offsets[k]) return OSCARS_E_INVALID;
     if (tau[k] < 0 || tau[k] > kMaxTau) return OSCARS_E_INVALID;
   }
+  // Not on a stream being captured into a graph: every call draws its
+  // batches on the host and waits for the previous call's index upload, which
+  // a graph could neither redraw nor wait for.
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(c->stream, &cap);
+  if (e != hipSuccess) return hip_fail(e);
+  if (cap != hipStreamCaptureStatusNone) return OSCARS_E_STATE;
 
   // ---- slots: workers with work, by tau descending, ties by index ----
   std::vector<int32_t> order;
@@ -802,7 +809,6 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
   // for more than kPreTau steps per worker; failures leave no side effects) ----
   const int64_t need = 64 + static_cast<int64_t>(n_slots) * tau_max * B;
   const int64_t loss_need = static_cast<int64_t>(n_slots) * tau_max * B;
-  hipError_t e = hipSuccess;
   if (c->upload_pending) {
     e = hipEventSynchronize(c->upload_done);
     if (e != hipSuccess) return hip_fail(e);

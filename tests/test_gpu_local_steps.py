@@ -440,6 +440,46 @@ def test_local_steps_rejects_bad_arguments(P):
         P.Context((64, 72, 10), P.FP32, 65, 16)
 
 
+def test_local_steps_refuse_graph_capture(P):
+    """The local steps draw every call's batches on the host and wait for the
+    previous call's index upload, so a stream being captured is refused with
+    E_STATE before anything is enqueued; eager calls then go on unchanged."""
+    import torch
+    from paper_2102_08550_amd.rounds import OscarsRun
+    cfg = workload.scaled(workload.C2, dims=(64, 72, 10), n_rows=400, batch=16, K=4, rounds=1,
+                          tau_rule="given")
+    ds = workload.gen_dataset(cfg)
+    s = torch.cuda.Stream()
+    run = OscarsRun(cfg, ds, workload.gen_init(cfg), stream=s)
+    taus = [1, 2, 1, 3]
+    run.round(taus)  # an earlier call whose upload the next one would wait for
+    torch.cuda.synchronize()
+    g_before, r_before = run.g.clone(), run.replicas.clone()
+    cur = run.ctx.cursors()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s, capture_error_mode="relaxed"):
+        with pytest.raises(P.OscarsError) as ei:
+            run.round(taus)
+        assert ei.value.status == P.E_STATE
+        with pytest.raises(P.OscarsError) as ei:
+            run.local_steps(taus)
+        assert ei.value.status == P.E_STATE
+    torch.cuda.synchronize()
+    assert run.ctx.cursors() == cur
+    assert torch.equal(run.g, g_before) and torch.equal(run.replicas, r_before)
+    # the refused calls left no state behind: the next eager round matches a
+    # fresh context resumed at the same cursors
+    run.round(taus)
+    ref = OscarsRun(cfg, ds, workload.gen_init(cfg))
+    ref.g.copy_(g_before)
+    ref.ctx.set_cursors(cur)
+    ref.round(taus)
+    torch.cuda.synchronize()
+    assert torch.equal(run.g, ref.g)
+    run.close()
+    ref.close()
+
+
 def _load_golden(name):
     import os
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
