@@ -32,7 +32,8 @@ struct ConvArgs {
   int Ho, Wo, Co;         // the layer's output (FC: Co = classes)
   int stride;             // 1 or 2 (conv)
   int cls;                // CONV_DGRAD with stride 2: parity class of the input pixels, 2 (hi & 1)
-                          // + (wi & 1); a launch per class (see conv_kernels.hip)
+                          // + (wi & 1), or -1 for all four classes in one launch (see
+                          // conv_kernels.hip)
   const float* in;        // conv input [B][H][W][C] (or, with gather, dataset rows); FC: pooled
   int64_t in_slot, in_ld;             // slot stride; row stride of a gathered dataset row
   const int32_t* gather;  // layer 1: dataset row of each batch row, [slot] stride gather_slot
@@ -55,14 +56,16 @@ struct ConvArgs {
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s);
 
-// WGRAD epilogue: sum the partials of each weight in split order, then the
+// WGRAD epilogue: sum the partials of each weight (eight groups of
+// consecutive splits, each in split order, the group sums in order), then the
 // SGD update master <- master - lr sum (W) and the bias from the last column;
 // master[order[z]] with stride master_slot; reads master_in like ConvArgs.
 hipError_t launch_conv_update(const ConvArgs& a, ConvPass pass, float* master,
                               int64_t master_slot, float lr, int n_slots, hipStream_t s);
 
-// pooled[z][b][c] = (sum over the H W positions of act[z][b][.][c], in
-// position order) / (H W).
+// pooled[z][b][c] = (sum over the H W positions of act[z][b][.][c]: eight
+// groups of consecutive positions, each in position order, the group sums in
+// order) / (H W).
 hipError_t launch_avgpool(const float* act, int64_t act_slot, float* pooled, int64_t pooled_slot,
                           int B, int HW, int C, int n_slots, hipStream_t s);
 // dZ[z][b][p][c] = dpooled[z][b][c] / (H W) where act[z][b][p][c] > 0, else 0.

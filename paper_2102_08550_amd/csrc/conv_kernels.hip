@@ -13,11 +13,12 @@
 //   FC_WGRAD    classes         channels + 1   batch          delta[k][m]          pooled[k][n] (1)
 //
 // with k = (r 3 + s) Cin + c for the conv taps (the layout of W[o][3][3][c]).
-// Backward-data of a stride-2 layer runs one launch per parity class of the
-// input pixels: input row hi receives output row i through tap r only where
-// hi + 1 - r = 2 i, so even rows take tap r = 1 and odd rows taps 0 and 2
-// (likewise columns).  Each class gathers only its 1, 2 or 4 taps (K = taps x
-// Cout), a quarter of the 9-tap work on average.
+// Backward-data of a stride-2 layer treats each parity class of the input
+// pixels as a GEMM of its own: input row hi receives output row i through tap
+// r only where hi + 1 - r = 2 i, so even rows take tap r = 1 and odd rows taps
+// 0 and 2 (likewise columns).  Each class gathers only its 1, 2 or 4 taps
+// (K = taps x Cout), a quarter of the 9-tap work on average; the four classes
+// share one launch (their tiles concatenated, the most taps first).
 // A workgroup computes a 64 x 64 tile of C with four waves of 32 x 32, fp32
 // MFMA 32x32x2, K in steps of 16: the next step's operands are gathered into
 // registers while the current step's MFMAs read LDS (two LDS buffers, one
@@ -27,6 +28,8 @@
 // inputs, whichever slots share a launch.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "conv.h"
 
@@ -66,6 +69,19 @@ __host__ __device__ inline Dims pass_dims(const ConvArgs& a, int pass) {
 }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Kernel tap (r, s) of backward-data tap index t: all nine (t = 3 r + s) for
+// stride 1; the class's one, two or four for stride 2.
+__device__ __forceinline__ void dgrad_tap(const ConvArgs& a, int t, int& r, int& s) {
+  if (a.stride == 2) {
+    const int ns = cls_taps(a.cls & 1), tr = t / ns, ts = t - tr * ns;
+    r = (a.cls >> 1) ? 2 * tr : 1;
+    s = (a.cls & 1) ? 2 * ts : 1;
+  } else {
+    r = t / 3;
+    s = t - 3 * r;
+  }
+}
 
 // Loaders.  A thread gathers, per K step, four consecutive K elements of one
 // A row (m0 + t / 4) and of one B row (n0 + t / 4).  What depends only on
@@ -141,22 +157,70 @@ struct ConvLoader {
     }
   }
 
-  // Kernel tap (r, s) of backward-data tap index t: all nine (t = 3 r + s)
-  // for stride 1; the class's one, two or four for stride 2.
   __device__ __forceinline__ void dgrad_tap_rs(int t, int& r, int& s) const {
-    if (a.stride == 2) {
-      const int ns = cls_taps(a.cls & 1), tr = t / ns, ts = t - tr * ns;
-      r = (a.cls >> 1) ? 2 * tr : 1;
-      s = (a.cls & 1) ? 2 * ts : 1;
-    } else {
-      r = t / 3;
-      s = t - 3 * r;
-    }
+    dgrad_tap(a, t, r, s);
   }
 
   __device__ __forceinline__ const float* image(int b) const {
     return rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
                 : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+  }
+
+  // Backward-data operands: A, the output-gradient taps of this input pixel
+  // (four consecutive output channels of one tap); B, the weights of this
+  // input channel (column) for four consecutive K.
+  __device__ __forceinline__ void dgrad_a(int k, float (&ra)[4]) const {
+    int t = k / a.Co, o = k - t * a.Co;
+    // output-gradient row of tap t for this input pixel, or false where the
+    // tap lands outside the output (or, for stride 2 and all nine taps,
+    // between output rows)
+    auto tap = [&](int t_, int& off) -> bool {
+      int r, sc;
+      dgrad_tap_rs(t_, r, sc);
+      const int ti = ah - r, tj = aw - sc;
+      if (ti < 0 || tj < 0) return false;
+      int i = ti, j = tj;
+      if (a.stride == 2) {
+        i = ti >> 1;  // even by the class's choice of taps
+        j = tj >> 1;
+      }
+      if (i >= a.Ho || j >= a.Wo) return false;
+      off = (i * a.Wo + j) * a.Co;
+      return true;
+    };
+    if ((a.Co & 3) == 0) {
+      f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+      int off = 0;
+      if (am && k < kend && tap(t, off)) v = *reinterpret_cast<const f32x4*>(arow + off + o);
+      for (int e = 0; e < 4; ++e) ra[e] = v[e];
+    } else {
+      int t2 = t, o2 = o;
+      for (int e = 0; e < 4; ++e) {
+        int off = 0;
+        ra[e] = (am && k + e < kend && tap(t2, off)) ? arow[off + o2] : 0.0f;
+        if (++o2 == a.Co) {
+          o2 = 0;
+          ++t2;
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void dgrad_b(int k, float (&rb)[4]) const {
+    int t = k / a.Co, o = k - t * a.Co;
+    const int K9 = 9 * a.C;
+    for (int e = 0; e < 4; ++e) {
+      float v = 0.0f;
+      if (bn && k + e < kend) {
+        int r, sc;
+        dgrad_tap_rs(t, r, sc);
+        v = Wt[static_cast<int64_t>(o) * K9 + (3 * r + sc) * a.C + bn_idx];
+      }
+      rb[e] = v;
+      if (++o == a.Co) {
+        o = 0;
+        ++t;
+      }
+    }
   }
 
   __device__ __forceinline__ void fetch(int k, float (&ra)[4], float (&rb)[4]) const {
@@ -191,54 +255,8 @@ struct ConvLoader {
           rb[e] = (bn && k + e < kend) ? Wt[static_cast<int64_t>(bn_idx) * K9 + k + e] : 0.0f;
       }
     } else if constexpr (PASS == CONV_DGRAD) {
-      int t = k / a.Co, o = k - t * a.Co;
-      // output-gradient row of tap t for this input pixel, or false where the
-      // tap lands outside the output (or, for stride 2 and all nine taps,
-      // between output rows)
-      auto tap = [&](int t_, int& off) -> bool {
-        int r, sc;
-        dgrad_tap_rs(t_, r, sc);
-        const int ti = ah - r, tj = aw - sc;
-        if (ti < 0 || tj < 0) return false;
-        int i = ti, j = tj;
-        if (a.stride == 2) {
-          i = ti >> 1;  // even by the class's choice of taps
-          j = tj >> 1;
-        }
-        if (i >= a.Ho || j >= a.Wo) return false;
-        off = (i * a.Wo + j) * a.Co;
-        return true;
-      };
-      if ((a.Co & 3) == 0) {
-        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-        int off = 0;
-        if (am && k < kend && tap(t, off)) v = *reinterpret_cast<const f32x4*>(arow + off + o);
-        for (int e = 0; e < 4; ++e) ra[e] = v[e];
-      } else {
-        int t2 = t, o2 = o;
-        for (int e = 0; e < 4; ++e) {
-          int off = 0;
-          ra[e] = (am && k + e < kend && tap(t2, off)) ? arow[off + o2] : 0.0f;
-          if (++o2 == a.Co) {
-            o2 = 0;
-            ++t2;
-          }
-        }
-      }
-      const int K9 = 9 * a.C;
-      for (int e = 0; e < 4; ++e) {
-        float v = 0.0f;
-        if (bn && k + e < kend) {
-          int r, sc;
-          dgrad_tap_rs(t, r, sc);
-          v = Wt[static_cast<int64_t>(o) * K9 + (3 * r + sc) * a.C + bn_idx];
-        }
-        rb[e] = v;
-        if (++o == a.Co) {
-          o = 0;
-          ++t;
-        }
-      }
+      dgrad_a(k, ra);
+      dgrad_b(k, rb);
     } else if constexpr (PASS == CONV_WGRAD) {
       for (int e = 0; e < 4; ++e)
         ra[e] = (am && k + e < kend) ? dz[static_cast<int64_t>(k + e) * a.Co + am_idx] : 0.0f;
@@ -285,17 +303,148 @@ struct ConvLoader {
   }
 };
 
-template <int PASS>
+// Backward-data weights gathered along N (input channels a multiple of 4): a
+// thread takes four consecutive input channels nq .. nq + 3 of one K element
+// (tap t, output channel o), W[o][r][s][nq .. nq + 3], one 16-byte load.
+struct DgradWeightLoader {
+  const ConvArgs& a;
+  int kend;
+  int nq;
+  bool bn;
+  const float* Wt;
+  __device__ DgradWeightLoader(const ConvArgs& a_, int kend_, int n, int N, const float* Wt_)
+      : a(a_), kend(kend_), nq(n), bn(n < N), Wt(Wt_) {}
+  __device__ __forceinline__ void fetch(int k, float (&rb)[4]) const {
+    f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (bn && k < kend) {
+      const int t = k / a.Co, o = k - t * a.Co;
+      int r, sc;
+      dgrad_tap(a, t, r, sc);
+      v = *reinterpret_cast<const f32x4*>(Wt + static_cast<int64_t>(o) * 9 * a.C +
+                                          (3 * r + sc) * a.C + nq);
+    }
+    for (int e = 0; e < 4; ++e) rb[e] = v[e];
+  }
+};
+
+// Backward-weight loader.  Both operands are contiguous along M or N (dZ is
+// [pixel][Cout], an input tap [pixel][Cin]), so a thread gathers, per K step,
+// four consecutive rows of A (output channels) and four consecutive columns
+// of B (the channels of one tap, or the bias column) of one K element, an
+// output pixel whose position is decoded once for both: one 16-byte load each
+// where the channel counts are multiples of 4.
+struct WgradLoader {
+  const ConvArgs& a;
+  int kend;
+  int mq, nq;         // the thread's first row and column
+  int M, N;
+  bool avec, bvec;    // the four rows / the four columns in one 16-byte load
+  int br = 0, bs = 0, bc = 0;  // tap and channel of column nq
+  const float* in;
+  const int32_t* rows;
+  const float* dz;
+
+  __device__ WgradLoader(const ConvArgs& a_, int kend_, int m, int M_, int n, int N_,
+                         const float* in_, const int32_t* rows_, const float* dz_, const float*)
+      : a(a_), kend(kend_), mq(m), nq(n), M(M_), N(N_), in(in_), rows(rows_), dz(dz_) {
+    const int K9 = 9 * a.C;
+    avec = (a.Co & 3) == 0 && mq + 3 < M;
+    bvec = (a.C & 3) == 0 && nq + 3 < K9;
+    if (nq < K9) {
+      const int rs = nq / a.C;
+      bc = nq - rs * a.C;
+      br = rs / 3;
+      bs = rs - 3 * br;
+    }
+  }
+
+  __device__ __forceinline__ const float* image(int b) const {
+    return rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
+                : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+  }
+
+  __device__ __forceinline__ void fetch(int k, float (&ra)[4], float (&rb)[4]) const {
+    const bool ok = k < kend;
+    int b = 0, i = 0, j = 0;
+    if (ok) {
+      const int hw = a.Ho * a.Wo, p = k - (k / hw) * hw;
+      b = k / hw;
+      i = p / a.Wo;
+      j = p - i * a.Wo;
+    }
+    const float* zrow = dz + static_cast<int64_t>(k) * a.Co;
+    if (avec) {
+      f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (ok) v = *reinterpret_cast<const f32x4*>(zrow + mq);
+      for (int e = 0; e < 4; ++e) ra[e] = v[e];
+    } else {
+      for (int e = 0; e < 4; ++e) ra[e] = (ok && mq + e < M) ? zrow[mq + e] : 0.0f;
+    }
+    if (bvec) {
+      f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+      const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
+      if (ok && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W)
+        v = *reinterpret_cast<const f32x4*>(image(b) + (hi * a.W + wi) * a.C + bc);
+      for (int e = 0; e < 4; ++e) rb[e] = v[e];
+    } else {
+      const int K9 = 9 * a.C;
+      for (int e = 0; e < 4; ++e) {
+        const int n = nq + e;
+        float v = 0.0f;
+        if (ok && n < N) {
+          if (n == K9) {
+            v = 1.0f;  // the bias column
+          } else {
+            const int rs = n / a.C, c = n - rs * a.C, r = rs / 3, sc = rs - 3 * r;
+            const int hi = a.stride * i + r - 1, wi = a.stride * j + sc - 1;
+            if (hi >= 0 && hi < a.H && wi >= 0 && wi < a.W) v = image(b)[(hi * a.W + wi) * a.C + c];
+          }
+        }
+        rb[e] = v;
+      }
+    }
+  }
+};
+
+// Tiles of one stride-2 backward-data class.
+__host__ __device__ inline int64_t dgrad_class_tiles(ConvArgs a, int cls) {
+  a.cls = cls;
+  const Dims d = pass_dims(a, CONV_DGRAD);
+  return ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
+}
+// The classes of a stride-2 backward-data launch in workgroup order: the
+// most taps (longest K) first, so that the short ones fill the last pass.
+__host__ __device__ inline int dgrad_class_at(int i) { return i == 0 ? 3 : i == 1 ? 1 : i == 2 ? 2 : 0; }
+
+// TR (input channels a multiple of 4): backward-weight gathers both operands
+// along M and N (WgradLoader), backward-data its weights along N
+// (DgradWeightLoader); otherwise ConvLoader gathers both along K (layer 1's
+// three channels: one decoded column per thread beats four scalar columns).
+template <int PASS, bool TR = false>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   constexpr bool WG = PASS == CONV_WGRAD || PASS == FC_WGRAD;
-  __shared__ float As[2][CK][CLD];
-  __shared__ float Bs[2][CK][CLD];
+  __shared__ __attribute__((aligned(16))) float As[2][CK][CLD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][CK][CLD];
+  int tile = blockIdx.x, split = 0;
+  if constexpr (PASS == CONV_DGRAD) {
+    if (a.stride == 2 && a.cls < 0) {
+      // all four parity classes in one launch: the workgroup's class and its
+      // tile within the class
+      int i = 0;
+      for (; i < 4; ++i) {
+        const int t = static_cast<int>(dgrad_class_tiles(a, dgrad_class_at(i)));
+        if (tile < t) break;
+        tile -= t;
+      }
+      if (i == 4) return;  // past the last class (the grid is their sum)
+      a.cls = dgrad_class_at(i);
+    }
+  }
   const Dims d = pass_dims(a, PASS);
   const int M = static_cast<int>(d.M), N = static_cast<int>(d.N), K = static_cast<int>(d.K);
   const int z = blockIdx.y;
   const int rep = a.order[z];
   const int gm = (M + CT - 1) / CT, gn = (N + CT - 1) / CT;
-  int tile = blockIdx.x, split = 0;
   if constexpr (WG) {
     split = tile / (gm * gn);
     tile -= split * gm * gn;
@@ -311,14 +460,41 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, r = lane & 31, h = lane >> 5;
-  const int lr = tid >> 2, lk = (tid & 3) * 4;
-  const ConvLoader<PASS> ld(a, kend, m0 + lr, M, n0 + lr, N, in, rows, dz, par + a.w_off);
+  // a thread's share of each K step: one row of A and of B and four
+  // consecutive K (lr, lk .. lk + 3), or, for backward-weight, four
+  // consecutive rows and columns (lr .. lr + 3) and one K (lk)
+  static_assert(!TR || PASS == CONV_WGRAD || PASS == CONV_DGRAD, "M / N gathers");
+  constexpr bool TRA = TR && PASS == CONV_WGRAD;  // A gathered along M
+  // (lr, lk): the thread's A row and K offset, (lrb, lkb) its B row and K
+  // offset; four consecutive K of one row, or four consecutive rows of one K
+  const int lr = TRA ? 4 * (tid & 15) : tid >> 2;
+  const int lk = TRA ? tid >> 4 : (tid & 3) * 4;
+  const int lrb = TR ? 4 * (tid & 15) : tid >> 2;
+  const int lkb = TR ? tid >> 4 : (tid & 3) * 4;
+  typedef typename std::conditional<TRA, WgradLoader, ConvLoader<PASS>>::type Loader;
+  const Loader ld(a, kend, m0 + lr, M, n0 + lrb, N, in, rows, dz, par + a.w_off);
+  const DgradWeightLoader wl(a, kend, n0 + lrb, N, par + a.w_off);
   float ra[4], rb[4];
+  auto load = [&](int k0) {
+    if constexpr (TR && PASS == CONV_DGRAD) {
+      ld.dgrad_a(k0 + lk, ra);
+      wl.fetch(k0 + lkb, rb);
+    } else {
+      ld.fetch(k0 + lk, ra, rb);
+    }
+  };
   auto stash = [&](int buf) {
+    if constexpr (TRA) {
+      *reinterpret_cast<f32x4*>(&As[buf][lk][lr]) = f32x4{ra[0], ra[1], ra[2], ra[3]};
+    } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      As[buf][lk + e][lr] = ra[e];
-      Bs[buf][lk + e][lr] = rb[e];
+      for (int e = 0; e < 4; ++e) As[buf][lk + e][lr] = ra[e];
+    }
+    if constexpr (TR) {
+      *reinterpret_cast<f32x4*>(&Bs[buf][lkb][lrb]) = f32x4{rb[0], rb[1], rb[2], rb[3]};
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Bs[buf][lkb + e][lrb] = rb[e];
     }
   };
 
@@ -326,12 +502,12 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
   const int nk = (kend - kbeg + CK - 1) / CK;
-  ld.fetch(kbeg + lk, ra, rb);
+  load(kbeg);
   stash(0);
   __syncthreads();
   for (int t = 0; t < nk; ++t) {
     const int buf = t & 1;
-    if (t + 1 < nk) ld.fetch(kbeg + (t + 1) * CK + lk, ra, rb);
+    if (t + 1 < nk) load(kbeg + (t + 1) * CK);
     // MFMA u contracts k = 2u (lanes 0-31) and 2u + 1 (lanes 32-63)
 #pragma unroll
     for (int u = 0; u < CK / 2; ++u)
@@ -366,38 +542,74 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
 }
 
-// Sum of the partials of weight (m, n) in split order, then
-// master <- master_in - lr sum: W[m][n] for n < N - 1, the bias b[m] for the
-// last column.
+// Sum of the partials of weight (m, n), then master <- master_in - lr sum:
+// W[m][n] for n < N - 1, the bias b[m] for the last column.  The ranges are
+// summed in UG groups of consecutive ranges, each group in range order by one
+// thread, then the group sums in group order; the order depends on the number
+// of ranges only, not on how many replicas share the launch.  A workgroup
+// takes UW consecutive weights (a half-wave's loads read consecutive partials
+// of one range).
+constexpr int UW = 32, UG = 8;
+static_assert(UW * UG == 256, "one thread per (weight, group)");
+
 template <int PASS>
 __global__ __launch_bounds__(256) void conv_update_kernel(ConvArgs a, float* master,
                                                           int64_t master_slot, float lr) {
   const Dims d = pass_dims(a, PASS);
   const int z = blockIdx.y;
   const int rep = a.order[z];
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (e >= d.M * d.N) return;
-  const int64_t m = e / d.N, n = e % d.N;
+  const int64_t MN = d.M * d.N;
+  const int w = threadIdx.x % UW, grp = threadIdx.x / UW;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * UW + w;
+  const int per = (a.splits + UG - 1) / UG;
+  const int s0 = grp * per, s1 = min(a.splits, s0 + per);
   const float* part = a.part + z * a.part_slot;
   float sum = 0.0f;
-  for (int s = 0; s < a.splits; ++s) sum += part[s * d.M * d.N + e];
+  if (e < MN)
+    for (int s = s0; s < s1; ++s) sum += part[s * MN + e];
+  __shared__ float group_sum[UG][UW];
+  group_sum[grp][w] = sum;
+  __syncthreads();
+  if (grp != 0 || e >= MN) return;
+  float tot = group_sum[0][w];
+#pragma unroll
+  for (int g = 1; g < UG; ++g) tot += group_sum[g][w];
+  const int64_t m = e / d.N, n = e % d.N;
   const float* src = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
   float* dst = master + static_cast<int64_t>(rep) * master_slot;
   const int64_t at = n < d.N - 1 ? a.w_off + m * (d.N - 1) + n : a.b_off + m;
-  dst[at] = fmaf(-lr, sum, src[at]);
+  dst[at] = fmaf(-lr, tot, src[at]);
 }
+
+// pooled[b][c] = (sum over the positions) / (H W): the positions in PG groups
+// of consecutive positions, each in position order by one thread, then the
+// group sums in group order.  A workgroup takes PW consecutive channels of one
+// batch row (a half-wave's loads read consecutive channels of one position).
+constexpr int PW = 32, PG = 8;
+static_assert(PW * PG == 256, "one thread per (channel, group)");
 
 __global__ __launch_bounds__(256) void avgpool_kernel(const float* act, int64_t act_slot,
                                                       float* pooled, int64_t pooled_slot, int B,
                                                       int HW, int C) {
   const int z = blockIdx.y;
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (e >= static_cast<int64_t>(B) * C) return;
-  const int64_t b = e / C, c = e % C;
-  const float* src = act + z * act_slot + b * HW * C + c;
+  const int cb = (C + PW - 1) / PW;
+  const int b = blockIdx.x / cb, c = (blockIdx.x % cb) * PW + threadIdx.x % PW;
+  const int grp = threadIdx.x / PW;
+  const int per = (HW + PG - 1) / PG;
+  const int p0 = grp * per, p1 = min(HW, p0 + per);
   float sum = 0.0f;
-  for (int p = 0; p < HW; ++p) sum += src[static_cast<int64_t>(p) * C];
-  pooled[z * pooled_slot + e] = sum / static_cast<float>(HW);
+  if (c < C) {
+    const float* src = act + z * act_slot + (static_cast<int64_t>(b) * HW) * C + c;
+    for (int p = p0; p < p1; ++p) sum += src[static_cast<int64_t>(p) * C];
+  }
+  __shared__ float group_sum[PG][PW];
+  group_sum[grp][threadIdx.x % PW] = sum;
+  __syncthreads();
+  if (grp != 0 || c >= C) return;
+  float tot = group_sum[0][threadIdx.x];
+#pragma unroll
+  for (int g = 1; g < PG; ++g) tot += group_sum[g][threadIdx.x];
+  pooled[z * pooled_slot + static_cast<int64_t>(b) * C + c] = tot / static_cast<float>(HW);
 }
 
 __global__ __launch_bounds__(256) void avgpool_backward_kernel(const float* dpooled,
@@ -416,9 +628,24 @@ __global__ __launch_bounds__(256) void avgpool_backward_kernel(const float* dpoo
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
+  if (pass == CONV_DGRAD && a.stride == 2) {
+    if (n_slots < 1 || a.cls > 3 || a.B < 1 || a.C < 1 || a.Co < 1) return hipErrorInvalidValue;
+    int64_t gx = 0;
+    if (a.cls < 0)
+      for (int i = 0; i < 4; ++i) gx += dgrad_class_tiles(a, i);
+    else
+      gx = dgrad_class_tiles(a, a.cls);
+    if (gx == 0) return hipSuccess;  // no pixels (extents of 1)
+    if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if ((a.C & 3) == 0)
+      hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, true>),
+                         dim3(static_cast<unsigned>(gx), n_slots), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, false>),
+                         dim3(static_cast<unsigned>(gx), n_slots), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   const Dims d = pass_dims(a, pass);
-  if (pass == CONV_DGRAD && a.stride == 2 && d.M == 0 && n_slots >= 1)
-    return hipSuccess;  // a parity class without pixels (an extent of 1)
   if (n_slots < 1 || d.M < 1 || d.N < 1 || d.K < 1) return hipErrorInvalidValue;
   int64_t gx = ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
   if (pass == CONV_WGRAD || pass == FC_WGRAD) {
@@ -431,8 +658,18 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   const dim3 grid(static_cast<unsigned>(gx), n_slots), block(256);
   switch (pass) {
     case CONV_FWD: hipLaunchKernelGGL(conv_gemm_kernel<CONV_FWD>, grid, block, 0, s, a); break;
-    case CONV_DGRAD: hipLaunchKernelGGL(conv_gemm_kernel<CONV_DGRAD>, grid, block, 0, s, a); break;
-    case CONV_WGRAD: hipLaunchKernelGGL(conv_gemm_kernel<CONV_WGRAD>, grid, block, 0, s, a); break;
+    case CONV_DGRAD:
+      if ((a.C & 3) == 0)
+        hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, true>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, false>), grid, block, 0, s, a);
+      break;
+    case CONV_WGRAD:
+      if ((a.C & 3) == 0)
+        hipLaunchKernelGGL((conv_gemm_kernel<CONV_WGRAD, true>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((conv_gemm_kernel<CONV_WGRAD, false>), grid, block, 0, s, a);
+      break;
     case FC_FWD: hipLaunchKernelGGL(conv_gemm_kernel<FC_FWD>, grid, block, 0, s, a); break;
     case FC_DGRAD: hipLaunchKernelGGL(conv_gemm_kernel<FC_DGRAD>, grid, block, 0, s, a); break;
     case FC_WGRAD: hipLaunchKernelGGL(conv_gemm_kernel<FC_WGRAD>, grid, block, 0, s, a); break;
@@ -444,8 +681,8 @@ hipError_t launch_conv_update(const ConvArgs& a, ConvPass pass, float* master,
                               int64_t master_slot, float lr, int n_slots, hipStream_t s) {
   if (pass != CONV_WGRAD && pass != FC_WGRAD) return hipErrorInvalidValue;
   const Dims d = pass_dims(a, pass);
-  const int64_t blocks = (d.M * d.N + 255) / 256;
-  if (blocks > 0x7FFFFFFF || n_slots < 1) return hipErrorInvalidValue;
+  const int64_t blocks = (d.M * d.N + UW - 1) / UW;
+  if (blocks > 0x7FFFFFFF || n_slots < 1 || a.splits < 1) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(blocks), n_slots), block(256);
   if (pass == CONV_WGRAD)
     hipLaunchKernelGGL(conv_update_kernel<CONV_WGRAD>, grid, block, 0, s, a, master, master_slot, lr);
@@ -456,8 +693,8 @@ hipError_t launch_conv_update(const ConvArgs& a, ConvPass pass, float* master,
 
 hipError_t launch_avgpool(const float* act, int64_t act_slot, float* pooled, int64_t pooled_slot,
                           int B, int HW, int C, int n_slots, hipStream_t s) {
-  const int64_t blocks = (static_cast<int64_t>(B) * C + 255) / 256;
-  if (blocks > 0x7FFFFFFF || n_slots < 1) return hipErrorInvalidValue;
+  const int64_t blocks = static_cast<int64_t>(B) * ((C + PW - 1) / PW);
+  if (blocks > 0x7FFFFFFF || n_slots < 1 || B < 1 || HW < 1 || C < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(avgpool_kernel, dim3(static_cast<unsigned>(blocks), n_slots), dim3(256), 0, s,
                      act, act_slot, pooled, pooled_slot, B, HW, C);
   return hipGetLastError();

@@ -653,11 +653,9 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
       a.out_slot = c->cnn_slot(l - 1);
       a.mask = c->cact[l - 1];
       a.mask_slot = c->cnn_slot(l - 1);
-      // stride 2: one launch per parity class of the input pixels
-      for (int cls = 0; cls < (a.stride == 2 ? 4 : 1) && e == hipSuccess; ++cls) {
-        a.cls = cls;
-        e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, CONV_DGRAD, ns, c->stream); });
-      }
+      // stride 2: the four parity classes of the input pixels in one launch
+      a.cls = -1;
+      e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, CONV_DGRAD, ns, c->stream); });
       if (e != hipSuccess) break;
       a.in = c->cact[l - 1];
       a.in_slot = c->cnn_slot(l - 1);
