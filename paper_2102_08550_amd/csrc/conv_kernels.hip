@@ -542,6 +542,138 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Thin input layers (at most 3 input channels, at most 32 output channels in
+// fours; layer 1 of an RGB network).  Their GEMMs are too narrow for 64 x 64
+// tiles (K = 9 Cin <= 27 in the forward, N = 9 Cin + 1 in backward-weight) and
+// their input channels too few for vector gathers, so they get kernels of
+// their own.  (Backward-data is never needed: layer 1 has no layer below.)
+
+__host__ __device__ inline bool thin_layer(const ConvArgs& a) {
+  return a.C >= 1 && a.C <= 3 && a.Co >= 4 && a.Co <= 32 && (a.Co & 3) == 0;
+}
+
+// Forward, one output pixel per thread and all CO output channels:
+// Z[p][o] = (sum over the taps t = (3 r + s) Cin + c, in t order, of
+// in(tap) W[o][t]) + b[o], then ReLU.  The weights sit in LDS as [t][o], so
+// every lane reads the same words (broadcast).
+template <int CO>
+__global__ __launch_bounds__(256) void conv_thin_fwd_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float w_s[27 * CO + CO];
+  const int z = blockIdx.y;
+  const int rep = a.order[z];
+  const float* par = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
+  const int KT = 9 * a.C;
+  for (int i = threadIdx.x; i < KT * CO; i += 256) {
+    const int o = i / KT, t = i - o * KT;
+    w_s[t * CO + o] = par[a.w_off + i];
+  }
+  for (int i = threadIdx.x; i < CO; i += 256) w_s[KT * CO + i] = par[a.b_off + i];
+  __syncthreads();
+  const int hw = a.Ho * a.Wo;
+  const int64_t p = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (p >= static_cast<int64_t>(a.B) * hw) return;
+  const int b = static_cast<int>(p / hw), q = static_cast<int>(p - static_cast<int64_t>(b) * hw);
+  const int i = q / a.Wo, j = q - i * a.Wo;
+  const float* in = a.in + z * a.in_slot;
+  const float* img = a.gather
+                         ? in + static_cast<int64_t>(a.gather[z * a.gather_slot + b]) * a.in_ld
+                         : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+  float acc[CO];
+#pragma unroll
+  for (int o = 0; o < CO; ++o) acc[o] = 0.0f;
+  for (int r = 0; r < 3; ++r)
+    for (int sc = 0; sc < 3; ++sc) {
+      const int hi = a.stride * i + r - 1, wi = a.stride * j + sc - 1;
+      const bool inside = hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+      for (int c = 0; c < a.C; ++c) {
+        const float x = inside ? img[(hi * a.W + wi) * a.C + c] : 0.0f;
+        const float* w = w_s + ((3 * r + sc) * a.C + c) * CO;
+#pragma unroll
+        for (int o = 0; o < CO; o += 4) {
+          const f32x4 wv = *reinterpret_cast<const f32x4*>(w + o);
+          acc[o] = fmaf(x, wv[0], acc[o]);
+          acc[o + 1] = fmaf(x, wv[1], acc[o + 1]);
+          acc[o + 2] = fmaf(x, wv[2], acc[o + 2]);
+          acc[o + 3] = fmaf(x, wv[3], acc[o + 3]);
+        }
+      }
+    }
+  float* out = a.out + z * a.out_slot + p * CO;
+  const float* bias = w_s + KT * CO;
+#pragma unroll
+  for (int o = 0; o < CO; o += 4) {
+    f32x4 v;
+    for (int e = 0; e < 4; ++e) {
+      const float zv = acc[o + e] + bias[o + e];
+      v[e] = zv > 0.0f ? zv : 0.0f;
+    }
+    *reinterpret_cast<f32x4*>(out + o) = v;
+  }
+}
+
+// Backward-weight partial of one range of output pixels (workgroup = range,
+// as the weight-gradient passes of conv_gemm_kernel): C[o][n] = sum over the
+// range's pixels p of dZ[p][o] x(p, n), with x(p, n) the input tap of column
+// n < 9 Cin and 1 for the bias column.  The whole 32 x 32 block is one MFMA
+// accumulator: each wave runs the 32x32x2 fp32 MFMA over a quarter of the
+// range (two pixels per MFMA, operands loaded by the lanes straight from
+// memory: lane l holds dZ[p + l / 32][l % 32] and x(p + l / 32, l % 32)),
+// and the four quarters are added in wave order.
+__global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
+  __shared__ float red[4][32][33];
+  const int z = blockIdx.y;
+  const int split = blockIdx.x;
+  const int M = a.Co, N = 9 * a.C + 1;
+  const int hw = a.Ho * a.Wo;
+  const int K = a.B * hw;
+  const int kbeg = split * static_cast<int>(a.k_per_split);
+  const int kend = K - kbeg < a.k_per_split ? K : kbeg + static_cast<int>(a.k_per_split);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+  const int quarter = (kend - kbeg + 3) / 4;
+  const int wb = kbeg + wave * quarter;
+  const int we = wb + quarter < kend ? wb + quarter : kend;
+  // this lane's B column: tap (r, s) and channel c, the bias column, or none
+  const int n = l32;
+  const int rs = n / a.C, nc = n - rs * a.C, nr = rs / 3, ns = rs - 3 * nr;
+  const bool ntap = n < N - 1, nbias = n == N - 1;
+  const bool mrow = l32 < M;
+  const float* dz = a.dout + z * a.dout_slot;
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+  for (int p0 = wb; p0 < we; p0 += 2) {
+    const int p = p0 + h;
+    float av = 0.0f, bv = 0.0f;
+    if (p < we) {
+      if (mrow) av = dz[static_cast<int64_t>(p) * M + l32];
+      if (ntap) {
+        const int b = p / hw, q = p - b * hw, i = q / a.Wo, j = q - i * a.Wo;
+        const int hi = a.stride * i + nr - 1, wi = a.stride * j + ns - 1;
+        if (hi >= 0 && hi < a.H && wi >= 0 && wi < a.W) {
+          const float* in = a.in + z * a.in_slot;
+          const float* img =
+              a.gather ? in + static_cast<int64_t>(a.gather[z * a.gather_slot + b]) * a.in_ld
+                       : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+          bv = img[(hi * a.W + wi) * a.C + nc];
+        }
+      } else if (nbias) {
+        bv = 1.0f;
+      }
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+  }
+  // accumulator e of lane (l32, h): row 8 (e / 4) + 4 h + e % 4, column l32
+#pragma unroll
+  for (int e = 0; e < 16; ++e) red[wave][8 * (e >> 2) + 4 * h + (e & 3)][l32] = acc[e];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < M * N; idx += 256) {
+    const int m = idx / N, c = idx - m * N;
+    const float v = ((red[0][m][c] + red[1][m][c]) + red[2][m][c]) + red[3][m][c];
+    a.part[z * a.part_slot + (static_cast<int64_t>(split) * M + m) * N + c] = v;
+  }
+}
+
 // Sum of the partials of weight (m, n), then master <- master_in - lr sum:
 // W[m][n] for n < N - 1, the bias b[m] for the last column.  The ranges are
 // summed in UG groups of consecutive ranges, each group in range order by one
@@ -647,6 +779,30 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   }
   const Dims d = pass_dims(a, pass);
   if (n_slots < 1 || d.M < 1 || d.N < 1 || d.K < 1) return hipErrorInvalidValue;
+  if (pass == CONV_FWD && thin_layer(a)) {
+    const int64_t blocks = (d.M + 255) / 256;  // one output pixel per thread
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(blocks), n_slots), block(256);
+    switch (a.Co / 4) {
+      case 1: hipLaunchKernelGGL(conv_thin_fwd_kernel<4>, grid, block, 0, s, a); break;
+      case 2: hipLaunchKernelGGL(conv_thin_fwd_kernel<8>, grid, block, 0, s, a); break;
+      case 3: hipLaunchKernelGGL(conv_thin_fwd_kernel<12>, grid, block, 0, s, a); break;
+      case 4: hipLaunchKernelGGL(conv_thin_fwd_kernel<16>, grid, block, 0, s, a); break;
+      case 5: hipLaunchKernelGGL(conv_thin_fwd_kernel<20>, grid, block, 0, s, a); break;
+      case 6: hipLaunchKernelGGL(conv_thin_fwd_kernel<24>, grid, block, 0, s, a); break;
+      case 7: hipLaunchKernelGGL(conv_thin_fwd_kernel<28>, grid, block, 0, s, a); break;
+      default: hipLaunchKernelGGL(conv_thin_fwd_kernel<32>, grid, block, 0, s, a); break;
+    }
+    return hipGetLastError();
+  }
+  if (pass == CONV_WGRAD && thin_layer(a)) {
+    if (a.splits < 1 || a.k_per_split < 2 || (a.k_per_split & 1) ||
+        static_cast<int64_t>(a.splits) * a.k_per_split < d.K)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_thin_wgrad_kernel, dim3(static_cast<unsigned>(a.splits), n_slots),
+                       dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   int64_t gx = ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
   if (pass == CONV_WGRAD || pass == FC_WGRAD) {
     if (a.splits < 1 || a.k_per_split < 1 ||
