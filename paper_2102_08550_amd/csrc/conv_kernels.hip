@@ -543,6 +543,102 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Backward-data with at most 32 input channels (a multiple of 4): 128 x 32
+// tiles, the four waves stacked along M, where a 64 x 64 tile would leave half
+// of its columns empty.  The operands are gathered as in
+// conv_gemm_kernel<CONV_DGRAD, true> (each thread two A rows, four
+// consecutive K of each; the first 128 threads four consecutive weight
+// columns of one K), the LDS tiles hold the same K steps, and so every sum
+// is the same.
+constexpr int NM = 128, NN = 32;
+
+__host__ __device__ inline bool dgrad_narrow(const ConvArgs& a) {
+  return (a.C & 3) == 0 && a.C >= 4 && a.C <= NN;
+}
+__host__ __device__ inline int64_t dgrad_narrow_tiles(const ConvArgs& a) {
+  const Dims d = pass_dims(a, CONV_DGRAD);
+  return ((d.M + NM - 1) / NM) * ((d.N + NN - 1) / NN);
+}
+
+__global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float As[2][CK][NM + 4];
+  __shared__ __attribute__((aligned(16))) float Bs[2][CK][NN + 4];
+  int tile = blockIdx.x;
+  if (a.stride == 2 && a.cls < 0) {
+    int i = 0;
+    for (; i < 4; ++i) {
+      ConvArgs ac = a;
+      ac.cls = dgrad_class_at(i);
+      const int t = static_cast<int>(dgrad_narrow_tiles(ac));
+      if (tile < t) break;
+      tile -= t;
+    }
+    if (i == 4) return;  // past the last class (the grid is their sum)
+    a.cls = dgrad_class_at(i);
+  }
+  const Dims d = pass_dims(a, CONV_DGRAD);
+  const int M = static_cast<int>(d.M), N = static_cast<int>(d.N), K = static_cast<int>(d.K);
+  const int z = blockIdx.y;
+  const int rep = a.order[z];
+  const int gn = (N + NN - 1) / NN;
+  const int m0 = tile / gn * NM, n0 = (tile - tile / gn * gn) * NN;
+  const float* dz = a.dout + z * a.dout_slot;
+  const float* par = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r = lane & 31, h = lane >> 5;
+  const int lr = tid >> 2, lk = (tid & 3) * 4;      // A rows lr and lr + 64
+  const bool bload = tid < NN * CK / 4;             // B: four columns of one K
+  const int lrb = 4 * (tid & 7), lkb = (tid >> 3) & (CK - 1);
+  const ConvLoader<CONV_DGRAD> ld0(a, K, m0 + lr, M, n0, N, nullptr, nullptr, dz, par + a.w_off);
+  const ConvLoader<CONV_DGRAD> ld1(a, K, m0 + lr + 64, M, n0, N, nullptr, nullptr, dz,
+                                   par + a.w_off);
+  const DgradWeightLoader wl(a, K, n0 + lrb, N, par + a.w_off);
+  float ra0[4], ra1[4], rb[4];
+  auto load = [&](int k0) {
+    ld0.dgrad_a(k0 + lk, ra0);
+    ld1.dgrad_a(k0 + lk, ra1);
+    if (bload) wl.fetch(k0 + lkb, rb);
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      As[buf][lk + e][lr] = ra0[e];
+      As[buf][lk + e][lr + 64] = ra1[e];
+    }
+    if (bload) *reinterpret_cast<f32x4*>(&Bs[buf][lkb][lrb]) = f32x4{rb[0], rb[1], rb[2], rb[3]};
+  };
+
+  f32x16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+  const int nk = (K + CK - 1) / CK;
+  load(0);
+  stash(0);
+  __syncthreads();
+  for (int t = 0; t < nk; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nk) load((t + 1) * CK);
+#pragma unroll
+    for (int u = 0; u < CK / 2; ++u)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[buf][2 * u + h][wave * 32 + r],
+                                                 Bs[buf][2 * u + h][r], acc, 0, 0, 0);
+    if (t + 1 < nk) stash(buf ^ 1);
+    __syncthreads();
+  }
+
+  const int col = n0 + r;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int row = m0 + wave * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+    if (row >= M || col >= N) continue;
+    int b, hi, wi;
+    ConvLoader<CONV_DGRAD>::dgrad_pixel(a, row, b, hi, wi);
+    const int64_t at = ((static_cast<int64_t>(b) * a.H + hi) * a.W + wi) * a.C + col;
+    a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? acc[i] : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Thin input layers (at most 3 input channels, at most 32 output channels in
 // fours; layer 1 of an RGB network).  Their GEMMs are too narrow for 64 x 64
 // tiles (K = 9 Cin <= 27 in the forward, N = 9 Cin + 1 in backward-weight) and
@@ -760,6 +856,25 @@ __global__ __launch_bounds__(256) void avgpool_backward_kernel(const float* dpoo
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
+  if (pass == CONV_DGRAD && dgrad_narrow(a)) {
+    if (n_slots < 1 || a.cls > 3 || a.B < 1 || a.Co < 1 || (a.stride == 2 && a.cls < -1))
+      return hipErrorInvalidValue;
+    int64_t gx = 0;
+    if (a.stride == 2 && a.cls < 0) {
+      for (int i = 0; i < 4; ++i) {
+        ConvArgs ac = a;
+        ac.cls = i;
+        gx += dgrad_narrow_tiles(ac);
+      }
+    } else {
+      gx = dgrad_narrow_tiles(a);
+    }
+    if (gx == 0) return hipSuccess;  // no pixels (extents of 1)
+    if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_dgrad_narrow_kernel, dim3(static_cast<unsigned>(gx), n_slots),
+                       dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   if (pass == CONV_DGRAD && a.stride == 2) {
     if (n_slots < 1 || a.cls > 3 || a.B < 1 || a.C < 1 || a.Co < 1) return hipErrorInvalidValue;
     int64_t gx = 0;

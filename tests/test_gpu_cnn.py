@@ -50,6 +50,11 @@ TRAJ = {
     # 2-row image
     "thin": _cfg("cnn-thin", (3, 1, 4), ((8, 1), (12, 2), (8, 2)), K=2, n_rows=30, batch=7,
                  tau=(2, 3), rounds=2, seed=43),
+    # a stride-1 layer with a layer below (stride-1 backward-data), narrow
+    # layers (8 and 12 input channels: 128 x 32 backward-data tiles), a thin
+    # first layer with 8 output channels, odd image sizes
+    "s1": _cfg("cnn-s1", (9, 11, 3), ((8, 1), (12, 1), (20, 2)), K=3, n_rows=200, batch=9,
+               tau=(2, 1, 3), rounds=2, seed=44),
     # the full workload's layers on 16 x 16 images, batch 64 (pixels per
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
