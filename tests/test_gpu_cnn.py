@@ -55,6 +55,10 @@ TRAJ = {
     # first layer with 8 output channels, odd image sizes
     "s1": _cfg("cnn-s1", (9, 11, 3), ((8, 1), (12, 1), (20, 2)), K=3, n_rows=200, batch=9,
                tau=(2, 1, 3), rounds=2, seed=44),
+    # one input channel and a stride-2 thin first layer (12 output channels,
+    # N = 10 weight-gradient columns), then a stride-1 layer
+    "gray-s2": _cfg("cnn-gray-s2", (10, 9, 1), ((12, 2), (16, 1)), K=2, n_rows=120, batch=5,
+                    tau=(3, 2), rounds=2, seed=45),
     # the full workload's layers on 16 x 16 images, batch 64 (pixels per
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
