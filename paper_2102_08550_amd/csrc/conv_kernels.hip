@@ -38,6 +38,9 @@ namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+// A compile-time integer passed as an argument (static register indices).
+template <int U> struct Pi { static constexpr int value = U; };
+
 constexpr int CT = 64;       // tile rows and columns
 constexpr int CK = 16;       // K per step
 constexpr int CLD = CT + 4;  // LDS row pitch (floats)
@@ -45,6 +48,12 @@ constexpr int CLD = CT + 4;  // LDS row pitch (floats)
 struct Dims {
   int64_t M, N, K;
 };
+
+// Loads never sit behind a branch in the vector loaders: a lane with nothing
+// to load (padding, a row or K past the end) reads these zeros instead, so
+// that the compiler's memory-counter waits stay exact and a load of the next
+// K steps can stay in flight across a wait for the current one.
+__device__ __attribute__((aligned(16))) float k_conv_zero[4];
 
 // Stride-2 backward-data class `cls`: input rows hi = 2 i + (cls >> 1), columns
 // wi = 2 j + (cls & 1); per dimension one tap (r = 1) for even, two (r = 0, 2)
@@ -164,6 +173,35 @@ struct ConvLoader {
   __device__ __forceinline__ const float* image(int b) const {
     return rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
                 : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+  }
+
+  // Forward with channel counts a multiple of 4: four consecutive K of the A
+  // row are four channels of one input tap, of the B row four consecutive
+  // weights; one 16-byte load each.
+  __device__ __forceinline__ void fwd_vec(int k, float (&ra)[4], float (&rb)[4]) const {
+    const int rs = k / a.C, c = k - rs * a.C, r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
+    const bool aok = am && k < kend && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+    const f32x4 va =
+        *reinterpret_cast<const f32x4*>(aok ? arow + (hi * a.W + wi) * a.C + c : k_conv_zero);
+    const bool bok = bn && k < kend;
+    const f32x4 vb = *reinterpret_cast<const f32x4*>(
+        bok ? Wt + static_cast<int64_t>(bn_idx) * 9 * a.C + k : k_conv_zero);
+    for (int e = 0; e < 4; ++e) {
+      ra[e] = va[e];
+      rb[e] = vb[e];
+    }
+  }
+  // Backward-data A with output channels a multiple of 4 (see dgrad_a).
+  __device__ __forceinline__ void dgrad_a_vec(int k, float (&ra)[4]) const {
+    const int t = k / a.Co, o = k - t * a.Co;
+    int r, sc;
+    dgrad_tap_rs(t, r, sc);
+    const int ti = ah - r, tj = aw - sc;
+    const int i = a.stride == 2 ? ti >> 1 : ti, j = a.stride == 2 ? tj >> 1 : tj;
+    const bool ok = am && k < kend && ti >= 0 && tj >= 0 && i < a.Ho && j < a.Wo;
+    const f32x4 v =
+        *reinterpret_cast<const f32x4*>(ok ? arow + (i * a.Wo + j) * a.Co + o : k_conv_zero);
+    for (int e = 0; e < 4; ++e) ra[e] = v[e];
   }
 
   // Backward-data operands: A, the output-gradient taps of this input pixel
@@ -315,96 +353,72 @@ struct DgradWeightLoader {
   __device__ DgradWeightLoader(const ConvArgs& a_, int kend_, int n, int N, const float* Wt_)
       : a(a_), kend(kend_), nq(n), bn(n < N), Wt(Wt_) {}
   __device__ __forceinline__ void fetch(int k, float (&rb)[4]) const {
-    f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (bn && k < kend) {
-      const int t = k / a.Co, o = k - t * a.Co;
-      int r, sc;
-      dgrad_tap(a, t, r, sc);
-      v = *reinterpret_cast<const f32x4*>(Wt + static_cast<int64_t>(o) * 9 * a.C +
-                                          (3 * r + sc) * a.C + nq);
-    }
+    const int t = k / a.Co, o = k - t * a.Co;
+    int r, sc;
+    dgrad_tap(a, t, r, sc);
+    const bool ok = bn && k < kend;
+    const f32x4 v = *reinterpret_cast<const f32x4*>(
+        ok ? Wt + static_cast<int64_t>(o) * 9 * a.C + (3 * r + sc) * a.C + nq : k_conv_zero);
     for (int e = 0; e < 4; ++e) rb[e] = v[e];
   }
 };
 
-// Backward-weight loader.  Both operands are contiguous along M or N (dZ is
-// [pixel][Cout], an input tap [pixel][Cin]), so a thread gathers, per K step,
-// four consecutive rows of A (output channels) and four consecutive columns
-// of B (the channels of one tap, or the bias column) of one K element, an
-// output pixel whose position is decoded once for both: one 16-byte load each
-// where the channel counts are multiples of 4.
+// Backward-weight loader for channel counts that are multiples of 4.  Both
+// operands are contiguous along M or N (dZ is [pixel][Cout], an input tap
+// [pixel][Cin]), so a thread gathers, per K step, four consecutive rows of A
+// (output channels) and four consecutive columns of B (the channels of one
+// tap) of one K element, an output pixel whose position is decoded once for
+// both: one 16-byte load each.  With Cin a multiple of 4 a column group lies
+// inside one tap, or is the bias column's group (column 9 Cin: ones) or past
+// the end.
 struct WgradLoader {
   const ConvArgs& a;
   int kend;
   int mq, nq;         // the thread's first row and column
-  int M, N;
-  bool avec, bvec;    // the four rows / the four columns in one 16-byte load
+  bool arow_ok;       // rows mq .. mq + 3 inside (Cout a multiple of 4)
+  bool btap, bbias;   // columns: four channels of one tap / the bias group
   int br = 0, bs = 0, bc = 0;  // tap and channel of column nq
   const float* in;
   const int32_t* rows;
   const float* dz;
 
-  __device__ WgradLoader(const ConvArgs& a_, int kend_, int m, int M_, int n, int N_,
+  __device__ WgradLoader(const ConvArgs& a_, int kend_, int m, int M, int n, int N,
                          const float* in_, const int32_t* rows_, const float* dz_, const float*)
-      : a(a_), kend(kend_), mq(m), nq(n), M(M_), N(N_), in(in_), rows(rows_), dz(dz_) {
+      : a(a_), kend(kend_), mq(m), nq(n), in(in_), rows(rows_), dz(dz_) {
     const int K9 = 9 * a.C;
-    avec = (a.Co & 3) == 0 && mq + 3 < M;
-    bvec = (a.C & 3) == 0 && nq + 3 < K9;
-    if (nq < K9) {
-      const int rs = nq / a.C;
-      bc = nq - rs * a.C;
-      br = rs / 3;
-      bs = rs - 3 * br;
-    }
-  }
-
-  __device__ __forceinline__ const float* image(int b) const {
-    return rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
-                : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+    arow_ok = mq < M;
+    btap = nq < K9;
+    bbias = nq == K9 && nq < N;
+    const int rs = nq / a.C;
+    bc = nq - rs * a.C;
+    br = rs / 3;
+    bs = rs - 3 * br;
   }
 
   __device__ __forceinline__ void fetch(int k, float (&ra)[4], float (&rb)[4]) const {
     const bool ok = k < kend;
-    int b = 0, i = 0, j = 0;
-    if (ok) {
-      const int hw = a.Ho * a.Wo, p = k - (k / hw) * hw;
-      b = k / hw;
-      i = p / a.Wo;
-      j = p - i * a.Wo;
+    const int kk = ok ? k : 0;  // a valid pixel to decode
+    const int hw = a.Ho * a.Wo, b = kk / hw, p = kk - b * hw, i = p / a.Wo, j = p - i * a.Wo;
+    const f32x4 va = *reinterpret_cast<const f32x4*>(
+        ok && arow_ok ? dz + static_cast<int64_t>(k) * a.Co + mq : k_conv_zero);
+    const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
+    const bool tap_ok = ok && btap && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+    const float* img = rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
+                            : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+    const f32x4 vb = *reinterpret_cast<const f32x4*>(
+        tap_ok ? img + (hi * a.W + wi) * a.C + bc : k_conv_zero);
+    for (int e = 0; e < 4; ++e) {
+      ra[e] = va[e];
+      rb[e] = vb[e];
     }
-    const float* zrow = dz + static_cast<int64_t>(k) * a.Co;
-    if (avec) {
-      f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-      if (ok) v = *reinterpret_cast<const f32x4*>(zrow + mq);
-      for (int e = 0; e < 4; ++e) ra[e] = v[e];
-    } else {
-      for (int e = 0; e < 4; ++e) ra[e] = (ok && mq + e < M) ? zrow[mq + e] : 0.0f;
-    }
-    if (bvec) {
-      f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-      const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
-      if (ok && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W)
-        v = *reinterpret_cast<const f32x4*>(image(b) + (hi * a.W + wi) * a.C + bc);
-      for (int e = 0; e < 4; ++e) rb[e] = v[e];
-    } else {
-      const int K9 = 9 * a.C;
-      for (int e = 0; e < 4; ++e) {
-        const int n = nq + e;
-        float v = 0.0f;
-        if (ok && n < N) {
-          if (n == K9) {
-            v = 1.0f;  // the bias column
-          } else {
-            const int rs = n / a.C, c = n - rs * a.C, r = rs / 3, sc = rs - 3 * r;
-            const int hi = a.stride * i + r - 1, wi = a.stride * j + sc - 1;
-            if (hi >= 0 && hi < a.H && wi >= 0 && wi < a.W) v = image(b)[(hi * a.W + wi) * a.C + c];
-          }
-        }
-        rb[e] = v;
-      }
-    }
+    rb[0] = ok && bbias ? 1.0f : rb[0];
   }
 };
+
+// Channel counts for the vector loaders (conv_gemm_kernel<PASS, true>).
+__host__ __device__ inline bool vector_loaders(const ConvArgs& a) {
+  return (a.C & 3) == 0 && (a.Co & 3) == 0;
+}
 
 // Tiles of one stride-2 backward-data class.
 __host__ __device__ inline int64_t dgrad_class_tiles(ConvArgs a, int cls) {
@@ -416,10 +430,11 @@ __host__ __device__ inline int64_t dgrad_class_tiles(ConvArgs a, int cls) {
 // most taps (longest K) first, so that the short ones fill the last pass.
 __host__ __device__ inline int dgrad_class_at(int i) { return i == 0 ? 3 : i == 1 ? 1 : i == 2 ? 2 : 0; }
 
-// TR (input channels a multiple of 4): backward-weight gathers both operands
-// along M and N (WgradLoader), backward-data its weights along N
-// (DgradWeightLoader); otherwise ConvLoader gathers both along K (layer 1's
-// three channels: one decoded column per thread beats four scalar columns).
+// TR (channel counts multiples of 4, see vector_loaders): vector loaders
+// without branches around their loads -- the forward gathers along K as
+// ConvLoader does, backward-weight gathers both operands along M and N
+// (WgradLoader), backward-data its weights along N (DgradWeightLoader);
+// otherwise ConvLoader's general gathers along K.
 template <int PASS, bool TR = false>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   constexpr bool WG = PASS == CONV_WGRAD || PASS == FC_WGRAD;
@@ -463,38 +478,44 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // a thread's share of each K step: one row of A and of B and four
   // consecutive K (lr, lk .. lk + 3), or, for backward-weight, four
   // consecutive rows and columns (lr .. lr + 3) and one K (lk)
-  static_assert(!TR || PASS == CONV_WGRAD || PASS == CONV_DGRAD, "M / N gathers");
+  static_assert(!TR || PASS == CONV_FWD || PASS == CONV_WGRAD || PASS == CONV_DGRAD,
+                "vector loaders: convolution passes");
   constexpr bool TRA = TR && PASS == CONV_WGRAD;  // A gathered along M
+  constexpr bool TRB = TR && PASS != CONV_FWD;    // B gathered along N
   // (lr, lk): the thread's A row and K offset, (lrb, lkb) its B row and K
   // offset; four consecutive K of one row, or four consecutive rows of one K
   const int lr = TRA ? 4 * (tid & 15) : tid >> 2;
   const int lk = TRA ? tid >> 4 : (tid & 3) * 4;
-  const int lrb = TR ? 4 * (tid & 15) : tid >> 2;
-  const int lkb = TR ? tid >> 4 : (tid & 3) * 4;
+  const int lrb = TRB ? 4 * (tid & 15) : tid >> 2;
+  const int lkb = TRB ? tid >> 4 : (tid & 3) * 4;
   typedef typename std::conditional<TRA, WgradLoader, ConvLoader<PASS>>::type Loader;
   const Loader ld(a, kend, m0 + lr, M, n0 + lrb, N, in, rows, dz, par + a.w_off);
   const DgradWeightLoader wl(a, kend, n0 + lrb, N, par + a.w_off);
-  float ra[4], rb[4];
-  auto load = [&](int k0) {
+  float ra[2][4], rb[2][4];
+  auto load = [&](int k0, auto P) {
+    constexpr int p = decltype(P)::value;
     if constexpr (TR && PASS == CONV_DGRAD) {
-      ld.dgrad_a(k0 + lk, ra);
-      wl.fetch(k0 + lkb, rb);
+      ld.dgrad_a_vec(k0 + lk, ra[p]);
+      wl.fetch(k0 + lkb, rb[p]);
+    } else if constexpr (TR && PASS == CONV_FWD) {
+      ld.fwd_vec(k0 + lk, ra[p], rb[p]);
     } else {
-      ld.fetch(k0 + lk, ra, rb);
+      ld.fetch(k0 + lk, ra[p], rb[p]);
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](auto P) {
+    constexpr int p = decltype(P)::value;  // register set p into LDS buffer p
     if constexpr (TRA) {
-      *reinterpret_cast<f32x4*>(&As[buf][lk][lr]) = f32x4{ra[0], ra[1], ra[2], ra[3]};
+      *reinterpret_cast<f32x4*>(&As[p][lk][lr]) = f32x4{ra[p][0], ra[p][1], ra[p][2], ra[p][3]};
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) As[buf][lk + e][lr] = ra[e];
+      for (int e = 0; e < 4; ++e) As[p][lk + e][lr] = ra[p][e];
     }
-    if constexpr (TR) {
-      *reinterpret_cast<f32x4*>(&Bs[buf][lkb][lrb]) = f32x4{rb[0], rb[1], rb[2], rb[3]};
+    if constexpr (TRB) {
+      *reinterpret_cast<f32x4*>(&Bs[p][lkb][lrb]) = f32x4{rb[p][0], rb[p][1], rb[p][2], rb[p][3]};
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) Bs[buf][lkb + e][lrb] = rb[e];
+      for (int e = 0; e < 4; ++e) Bs[p][lkb + e][lrb] = rb[p][e];
     }
   };
 
@@ -502,20 +523,30 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
   const int nk = (kend - kbeg + CK - 1) / CK;
-  load(kbeg);
-  stash(0);
+  // Two register sets: step t + 2 is gathered while step t is multiplied and
+  // step t + 1 (gathered a step earlier) goes into the other LDS buffer.
+  // Gathers past kend read nothing and give zeros.
+  load(kbeg, Pi<0>());
+  stash(Pi<0>());
+  load(kbeg + CK, Pi<1>());
   __syncthreads();
-  for (int t = 0; t < nk; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < nk) load(kbeg + (t + 1) * CK);
+  auto step = [&](int t, auto P) {  // register set and LDS buffer p = t & 1
+    constexpr int p = decltype(P)::value;
+    load(kbeg + (t + 2) * CK, P);
     // MFMA u contracts k = 2u (lanes 0-31) and 2u + 1 (lanes 32-63)
 #pragma unroll
     for (int u = 0; u < CK / 2; ++u)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[buf][2 * u + h][wm * 32 + r],
-                                                 Bs[buf][2 * u + h][wn * 32 + r], acc, 0, 0, 0);
-    if (t + 1 < nk) stash(buf ^ 1);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][wm * 32 + r],
+                                                 Bs[p][2 * u + h][wn * 32 + r], acc, 0, 0, 0);
+    stash(Pi<p ^ 1>());
     __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < nk; t += 2) {
+    step(t, Pi<0>());
+    step(t + 1, Pi<1>());
   }
+  if (t < nk) step(t, Pi<0>());
 
   // accumulator i of lane (r, h): row 8 (i / 4) + 4 h + i % 4, column r
   const int col = n0 + wn * 32 + r;
@@ -553,7 +584,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 constexpr int NM = 128, NN = 32;
 
 __host__ __device__ inline bool dgrad_narrow(const ConvArgs& a) {
-  return (a.C & 3) == 0 && a.C >= 4 && a.C <= NN;
+  return (a.C & 3) == 0 && (a.Co & 3) == 0 && a.C >= 4 && a.C <= NN;
 }
 __host__ __device__ inline int64_t dgrad_narrow_tiles(const ConvArgs& a) {
   const Dims d = pass_dims(a, CONV_DGRAD);
@@ -595,8 +626,8 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
   const DgradWeightLoader wl(a, K, n0 + lrb, N, par + a.w_off);
   float ra0[4], ra1[4], rb[4];
   auto load = [&](int k0) {
-    ld0.dgrad_a(k0 + lk, ra0);
-    ld1.dgrad_a(k0 + lk, ra1);
+    ld0.dgrad_a_vec(k0 + lk, ra0);
+    ld1.dgrad_a_vec(k0 + lk, ra1);
     if (bload) wl.fetch(k0 + lkb, rb);
   };
   auto stash = [&](int buf) {
@@ -884,7 +915,7 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
       gx = dgrad_class_tiles(a, a.cls);
     if (gx == 0) return hipSuccess;  // no pixels (extents of 1)
     if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
-    if ((a.C & 3) == 0)
+    if (vector_loaders(a))
       hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, true>),
                          dim3(static_cast<unsigned>(gx), n_slots), dim3(256), 0, s, a);
     else
@@ -928,15 +959,20 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(gx), n_slots), block(256);
   switch (pass) {
-    case CONV_FWD: hipLaunchKernelGGL(conv_gemm_kernel<CONV_FWD>, grid, block, 0, s, a); break;
+    case CONV_FWD:
+      if (vector_loaders(a))
+        hipLaunchKernelGGL((conv_gemm_kernel<CONV_FWD, true>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((conv_gemm_kernel<CONV_FWD, false>), grid, block, 0, s, a);
+      break;
     case CONV_DGRAD:
-      if ((a.C & 3) == 0)
+      if (vector_loaders(a))
         hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, true>), grid, block, 0, s, a);
       else
         hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, false>), grid, block, 0, s, a);
       break;
     case CONV_WGRAD:
-      if ((a.C & 3) == 0)
+      if (vector_loaders(a))
         hipLaunchKernelGGL((conv_gemm_kernel<CONV_WGRAD, true>), grid, block, 0, s, a);
       else
         hipLaunchKernelGGL((conv_gemm_kernel<CONV_WGRAD, false>), grid, block, 0, s, a);
