@@ -769,26 +769,40 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-  for (int p0 = wb; p0 < we; p0 += 2) {
-    const int p = p0 + h;
-    float av = 0.0f, bv = 0.0f;
-    if (p < we) {
-      if (mrow) av = dz[static_cast<int64_t>(p) * M + l32];
-      if (ntap) {
-        const int b = p / hw, q = p - b * hw, i = q / a.Wo, j = q - i * a.Wo;
-        const int hi = a.stride * i + nr - 1, wi = a.stride * j + ns - 1;
-        if (hi >= 0 && hi < a.H && wi >= 0 && wi < a.W) {
-          const float* in = a.in + z * a.in_slot;
-          const float* img =
-              a.gather ? in + static_cast<int64_t>(a.gather[z * a.gather_slot + b]) * a.in_ld
-                       : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
-          bv = img[(hi * a.W + wi) * a.C + nc];
+  // UB MFMAs per batch, all their operands loaded first (no load behind a
+  // branch: a lane with nothing to load reads the zero array).  The lane's
+  // pixel p0 + 2 u + h is decoded once per wave and then advanced by two.
+  constexpr int UB = 8;
+  const float* in = a.in + z * a.in_slot;
+  const int32_t* rows = a.gather ? a.gather + z * a.gather_slot : nullptr;
+  const int p_first = wb < we ? wb + h : 0;
+  int pb = p_first / hw, pi = (p_first - pb * hw) / a.Wo, pj = p_first - pb * hw - pi * a.Wo;
+  for (int p0 = wb; p0 < we; p0 += 2 * UB) {
+    float av[UB], bv[UB];
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int p = p0 + 2 * u + h;
+      const bool ok = p < we;
+      const int hi = a.stride * pi + nr - 1, wi = a.stride * pj + ns - 1;
+      const bool tap_ok = ok && ntap && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+      const int bsafe = ok ? pb : 0;
+      const float* img = rows ? in + static_cast<int64_t>(rows[bsafe]) * a.in_ld
+                              : in + static_cast<int64_t>(bsafe) * a.H * a.W * a.C;
+      av[u] = *(ok && mrow ? dz + static_cast<int64_t>(p) * M + l32 : k_conv_zero);
+      const float x = *(tap_ok ? img + (hi * a.W + wi) * a.C + nc : k_conv_zero);
+      bv[u] = ok && nbias ? 1.0f : x;
+      // next pixel of this lane: two further on
+      for (int step = 0; step < 2; ++step)
+        if (++pj == a.Wo) {
+          pj = 0;
+          if (++pi == a.Ho) {
+            pi = 0;
+            ++pb;
+          }
         }
-      } else if (nbias) {
-        bv = 1.0f;
-      }
     }
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < UB; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[u], bv[u], acc, 0, 0, 0);
   }
   // accumulator e of lane (l32, h): row 8 (e / 4) + 4 h + e % 4, column l32
 #pragma unroll
