@@ -20,12 +20,16 @@
 // (K = taps x Cout), a quarter of the 9-tap work on average; the four classes
 // share one launch (their tiles concatenated, the most taps first).
 // A workgroup computes a 64 x 64 tile of C with four waves of 32 x 32, fp32
-// MFMA 32x32x2, K in steps of 16: the next step's operands are gathered into
+// MFMA 32x32x2, K in steps of 16: later steps' operands are gathered into
 // registers while the current step's MFMAs read LDS (two LDS buffers, one
-// barrier per step).  The weight-gradient passes split K into ranges, one
-// partial sum per range, which the update kernel adds in range order before
-// applying the SGD step of Eq. 4 -- so results depend on nothing but the
-// inputs, whichever slots share a launch.
+// barrier per step; two register sets where the channel counts allow loaders
+// without branches).  Backward-data into at most 32 channels uses 128 x 32
+// tiles, and layers with at most three input channels (layer 1) have a
+// direct forward and a one-accumulator backward-weight of their own.  The
+// weight-gradient passes split K into ranges, one partial sum per range,
+// which the update kernel adds in a fixed order (eight groups of consecutive
+// ranges) before applying the SGD step of Eq. 4 -- so results depend on
+// nothing but the inputs, whichever slots share a launch.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
