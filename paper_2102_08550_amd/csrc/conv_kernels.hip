@@ -58,6 +58,8 @@ struct Dims {
 // that the compiler's memory-counter waits stay exact and a load of the next
 // K steps can stay in flight across a wait for the current one.
 __device__ __attribute__((aligned(16))) float k_conv_zero[4];
+// and ones for the bias column of a weight gradient
+__device__ __attribute__((aligned(16))) float k_conv_one[4] = {1.0f, 1.0f, 1.0f, 1.0f};
 
 // Stride-2 backward-data class `cls`: input rows hi = 2 i + (cls >> 1), columns
 // wi = 2 j + (cls & 1); per dimension one tap (r = 1) for even, two (r = 0, 2)
@@ -684,62 +686,76 @@ __host__ __device__ inline bool thin_layer(const ConvArgs& a) {
   return a.C >= 1 && a.C <= 3 && a.Co >= 4 && a.Co <= 32 && (a.Co & 3) == 0;
 }
 
-// Forward, one output pixel per thread and all CO output channels:
-// Z[p][o] = (sum over the taps t = (3 r + s) Cin + c, in t order, of
-// in(tap) W[o][t]) + b[o], then ReLU.  The weights sit in LDS as [t][o], so
-// every lane reads the same words (broadcast).
-template <int CO>
+// Forward on the fp32 MFMA: Z[p][o] = (sum over the taps t = (3 r + s) Cin + c
+// of in(tap) W[o][t]) + b[o], then ReLU.  A 32 x 32 block is 32 output pixels
+// (rows) by the output channels (columns; zero weights past Cout).  K is the
+// 9 Cin taps padded to 2 J: MFMA j contracts tap j (lanes 0-31) and tap J + j
+// (lanes 32-63).  Each lane keeps its column's J weights in registers and
+// gathers its pixel's taps straight from memory; a wave takes TB consecutive
+// blocks and loads all their taps before its first MFMA.  A store of one
+// accumulator register writes two output pixels' channels (whole lines).
+constexpr int THIN_TB = 2;
+constexpr int tap_rs(int t, int cin) { return t / cin; }
+constexpr int tap_c(int t, int cin) { return t % cin; }
+
+template <int CIN>
 __global__ __launch_bounds__(256) void conv_thin_fwd_kernel(ConvArgs a) {
-  __shared__ __attribute__((aligned(16))) float w_s[27 * CO + CO];
+  constexpr int KT = 9 * CIN, J = (KT + 1) / 2;
   const int z = blockIdx.y;
-  const int rep = a.order[z];
-  const float* par = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
-  const int KT = 9 * a.C;
-  for (int i = threadIdx.x; i < KT * CO; i += 256) {
-    const int o = i / KT, t = i - o * KT;
-    w_s[t * CO + o] = par[a.w_off + i];
+  const int lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+  const float* par = a.master_in + static_cast<int64_t>(a.order[z]) * a.master_in_slot;
+  const bool col_ok = l32 < a.Co;
+  float wv[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int t = j + J * h;
+    wv[j] = *(col_ok && t < KT ? par + a.w_off + static_cast<int64_t>(l32) * KT + t
+                               : k_conv_zero);
   }
-  for (int i = threadIdx.x; i < CO; i += 256) w_s[KT * CO + i] = par[a.b_off + i];
-  __syncthreads();
+  const float bias = *(col_ok ? par + a.b_off + l32 : k_conv_zero);
   const int hw = a.Ho * a.Wo;
-  const int64_t p = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (p >= static_cast<int64_t>(a.B) * hw) return;
-  const int b = static_cast<int>(p / hw), q = static_cast<int>(p - static_cast<int64_t>(b) * hw);
-  const int i = q / a.Wo, j = q - i * a.Wo;
+  const int64_t M = static_cast<int64_t>(a.B) * hw;
+  const int64_t p0 =
+      (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * (32 * THIN_TB);
   const float* in = a.in + z * a.in_slot;
-  const float* img = a.gather
-                         ? in + static_cast<int64_t>(a.gather[z * a.gather_slot + b]) * a.in_ld
-                         : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
-  float acc[CO];
+  float xv[THIN_TB][J];
 #pragma unroll
-  for (int o = 0; o < CO; ++o) acc[o] = 0.0f;
-  for (int r = 0; r < 3; ++r)
-    for (int sc = 0; sc < 3; ++sc) {
-      const int hi = a.stride * i + r - 1, wi = a.stride * j + sc - 1;
-      const bool inside = hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
-      for (int c = 0; c < a.C; ++c) {
-        const float x = inside ? img[(hi * a.W + wi) * a.C + c] : 0.0f;
-        const float* w = w_s + ((3 * r + sc) * a.C + c) * CO;
+  for (int u = 0; u < THIN_TB; ++u) {
+    const int64_t p = p0 + 32 * u + l32;
+    const bool pok = p < M;
+    const int64_t ps = pok ? p : 0;
+    const int b = static_cast<int>(ps / hw);
+    const int q = static_cast<int>(ps - static_cast<int64_t>(b) * hw);
+    const int i = q / a.Wo, jj = q - i * a.Wo;
+    const float* img =
+        a.gather ? in + static_cast<int64_t>(a.gather[z * a.gather_slot + b]) * a.in_ld
+                 : in + static_cast<int64_t>(b) * a.H * a.W * CIN;
 #pragma unroll
-        for (int o = 0; o < CO; o += 4) {
-          const f32x4 wv = *reinterpret_cast<const f32x4*>(w + o);
-          acc[o] = fmaf(x, wv[0], acc[o]);
-          acc[o + 1] = fmaf(x, wv[1], acc[o + 1]);
-          acc[o + 2] = fmaf(x, wv[2], acc[o + 2]);
-          acc[o + 3] = fmaf(x, wv[3], acc[o + 3]);
-        }
-      }
+    for (int j = 0; j < J; ++j) {
+      // tap j or J + j: (r, s) and channel fixed at compile time for each half
+      const int rs = h ? tap_rs(j + J, CIN) : tap_rs(j, CIN);
+      const int c = h ? tap_c(j + J, CIN) : tap_c(j, CIN);
+      const int r = rs / 3, sc = rs - 3 * r;
+      const int hi = a.stride * i + r - 1, wi = a.stride * jj + sc - 1;
+      const bool ok = pok && j + J * h < KT && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+      xv[u][j] = *(ok ? img + (hi * a.W + wi) * CIN + c : k_conv_zero);
     }
-  float* out = a.out + z * a.out_slot + p * CO;
-  const float* bias = w_s + KT * CO;
+  }
+  float* out = a.out + z * a.out_slot;
 #pragma unroll
-  for (int o = 0; o < CO; o += 4) {
-    f32x4 v;
-    for (int e = 0; e < 4; ++e) {
-      const float zv = acc[o + e] + bias[o + e];
-      v[e] = zv > 0.0f ? zv : 0.0f;
+  for (int u = 0; u < THIN_TB; ++u) {
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(xv[u][j], wv[j], acc, 0, 0, 0);
+    // accumulator e of lane (l32, h): pixel row 8 (e / 4) + 4 h + e % 4, channel l32
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t p = p0 + 32 * u + 8 * (e >> 2) + 4 * h + (e & 3);
+      const float v = acc[e] + bias;
+      if (p < M && col_ok) out[p * a.Co + l32] = v > 0.0f ? v : 0.0f;
     }
-    *reinterpret_cast<f32x4*>(out + o) = v;
   }
 }
 
@@ -751,8 +767,11 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_kernel(ConvArgs a) {
 // range (two pixels per MFMA, operands loaded by the lanes straight from
 // memory: lane l holds dZ[p + l / 32][l % 32] and x(p + l / 32, l % 32)),
 // and the four quarters are added in wave order.
+constexpr int THIN_WG_PIXELS = 512;  // output pixels per range at most
+
 __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
   __shared__ float red[4][32][33];
+  __shared__ int row_s[THIN_WG_PIXELS + 1];  // images a range touches at most
   const int z = blockIdx.y;
   const int split = blockIdx.x;
   const int M = a.Co, N = 9 * a.C + 1;
@@ -773,29 +792,37 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-  // UB MFMAs per batch, all their operands loaded first (no load behind a
-  // branch: a lane with nothing to load reads the zero array).  The lane's
-  // pixel p0 + 2 u + h is decoded once per wave and then advanced by two.
-  constexpr int UB = 8;
+  // UB MFMAs per batch, operands in two register sets: batch t + 1 is loaded
+  // while batch t is multiplied (no load behind a branch: a lane with nothing
+  // to load reads the zero array, so the memory-counter waits stay exact).
+  // The lane's next pixel pn = p0 + 2 u + h is decoded once per wave and then
+  // advanced by two.
+  constexpr int UB = 16;
+  // The dataset rows (or batch rows) of the range's images, staged in LDS
+  // once: an input load then waits only for an LDS read, not for a gather
+  // load queued behind the other loads in flight.
   const float* in = a.in + z * a.in_slot;
-  const int32_t* rows = a.gather ? a.gather + z * a.gather_slot : nullptr;
+  const int64_t img_stride = a.gather ? a.in_ld : static_cast<int64_t>(a.H) * a.W * a.C;
+  const int b_first = kbeg / hw, nrows = (kend - 1) / hw - b_first + 1;
+  for (int i = threadIdx.x; i < nrows; i += 256)
+    row_s[i] = a.gather ? a.gather[z * a.gather_slot + b_first + i] : b_first + i;
+  __syncthreads();
+  int pn = wb + h;
   const int p_first = wb < we ? wb + h : 0;
   int pb = p_first / hw, pi = (p_first - pb * hw) / a.Wo, pj = p_first - pb * hw - pi * a.Wo;
-  for (int p0 = wb; p0 < we; p0 += 2 * UB) {
-    float av[UB], bv[UB];
+  float av[2][UB], bv[2][UB];
+  auto load = [&](auto P) {
+    constexpr int q = decltype(P)::value;
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int p = p0 + 2 * u + h;
-      const bool ok = p < we;
+      const bool ok = pn < we;
       const int hi = a.stride * pi + nr - 1, wi = a.stride * pj + ns - 1;
       const bool tap_ok = ok && ntap && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
-      const int bsafe = ok ? pb : 0;
-      const float* img = rows ? in + static_cast<int64_t>(rows[bsafe]) * a.in_ld
-                              : in + static_cast<int64_t>(bsafe) * a.H * a.W * a.C;
-      av[u] = *(ok && mrow ? dz + static_cast<int64_t>(p) * M + l32 : k_conv_zero);
-      const float x = *(tap_ok ? img + (hi * a.W + wi) * a.C + nc : k_conv_zero);
-      bv[u] = ok && nbias ? 1.0f : x;
-      // next pixel of this lane: two further on
+      const float* img = in + static_cast<int64_t>(row_s[ok ? pb - b_first : 0]) * img_stride;
+      av[q][u] = *(ok && mrow ? dz + static_cast<int64_t>(pn) * M + l32 : k_conv_zero);
+      bv[q][u] = *(tap_ok ? img + (hi * a.W + wi) * a.C + nc
+                          : (ok && nbias ? k_conv_one : k_conv_zero));
+      pn += 2;
       for (int step = 0; step < 2; ++step)
         if (++pj == a.Wo) {
           pj = 0;
@@ -805,9 +832,23 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
           }
         }
     }
+  };
+  auto mul = [&](auto P) {
+    constexpr int q = decltype(P)::value;
 #pragma unroll
-    for (int u = 0; u < UB; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[u], bv[u], acc, 0, 0, 0);
+    for (int u = 0; u < UB; ++u)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[q][u], bv[q][u], acc, 0, 0, 0);
+  };
+  const int nb = we > wb ? (we - wb + 2 * UB - 1) / (2 * UB) : 0;
+  load(Pi<0>());
+  int t = 0;
+  for (; t + 1 < nb; t += 2) {
+    load(Pi<1>());
+    mul(Pi<0>());
+    load(Pi<0>());
+    mul(Pi<1>());
   }
+  if (t < nb) mul(Pi<0>());
   // accumulator e of lane (l32, h): row 8 (e / 4) + 4 h + e % 4, column l32
 #pragma unroll
   for (int e = 0; e < 16; ++e) red[wave][8 * (e >> 2) + 4 * h + (e & 3)][l32] = acc[e];
@@ -842,8 +883,18 @@ __global__ __launch_bounds__(256) void conv_update_kernel(ConvArgs a, float* mas
   const int s0 = grp * per, s1 = min(a.splits, s0 + per);
   const float* part = a.part + z * a.part_slot;
   float sum = 0.0f;
-  if (e < MN)
-    for (int s = s0; s < s1; ++s) sum += part[s * MN + e];
+  if (e < MN) {
+    // sixteen partials loaded at a time, then added in range order
+    int s = s0;
+    for (; s + 16 <= s1; s += 16) {
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = part[(s + u) * MN + e];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) sum += v[u];
+    }
+    for (; s < s1; ++s) sum += part[s * MN + e];
+  }
   __shared__ float group_sum[UG][UW];
   group_sum[grp][w] = sum;
   __syncthreads();
@@ -944,24 +995,20 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   const Dims d = pass_dims(a, pass);
   if (n_slots < 1 || d.M < 1 || d.N < 1 || d.K < 1) return hipErrorInvalidValue;
   if (pass == CONV_FWD && thin_layer(a)) {
-    const int64_t blocks = (d.M + 255) / 256;  // one output pixel per thread
+    const int64_t blocks = (d.M + 4 * 32 * THIN_TB - 1) / (4 * 32 * THIN_TB);
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(blocks), n_slots), block(256);
-    switch (a.Co / 4) {
-      case 1: hipLaunchKernelGGL(conv_thin_fwd_kernel<4>, grid, block, 0, s, a); break;
-      case 2: hipLaunchKernelGGL(conv_thin_fwd_kernel<8>, grid, block, 0, s, a); break;
-      case 3: hipLaunchKernelGGL(conv_thin_fwd_kernel<12>, grid, block, 0, s, a); break;
-      case 4: hipLaunchKernelGGL(conv_thin_fwd_kernel<16>, grid, block, 0, s, a); break;
-      case 5: hipLaunchKernelGGL(conv_thin_fwd_kernel<20>, grid, block, 0, s, a); break;
-      case 6: hipLaunchKernelGGL(conv_thin_fwd_kernel<24>, grid, block, 0, s, a); break;
-      case 7: hipLaunchKernelGGL(conv_thin_fwd_kernel<28>, grid, block, 0, s, a); break;
-      default: hipLaunchKernelGGL(conv_thin_fwd_kernel<32>, grid, block, 0, s, a); break;
+    switch (a.C) {
+      case 1: hipLaunchKernelGGL(conv_thin_fwd_kernel<1>, grid, block, 0, s, a); break;
+      case 2: hipLaunchKernelGGL(conv_thin_fwd_kernel<2>, grid, block, 0, s, a); break;
+      default: hipLaunchKernelGGL(conv_thin_fwd_kernel<3>, grid, block, 0, s, a); break;
     }
     return hipGetLastError();
   }
   if (pass == CONV_WGRAD && thin_layer(a)) {
     if (a.splits < 1 || a.k_per_split < 2 || (a.k_per_split & 1) ||
-        static_cast<int64_t>(a.splits) * a.k_per_split < d.K)
+        a.k_per_split > THIN_WG_PIXELS || static_cast<int64_t>(a.splits) * a.k_per_split < d.K ||
+        static_cast<int64_t>(a.splits - 1) * a.k_per_split >= d.K)
       return hipErrorInvalidValue;
     hipLaunchKernelGGL(conv_thin_wgrad_kernel, dim3(static_cast<unsigned>(a.splits), n_slots),
                        dim3(256), 0, s, a);
