@@ -81,12 +81,21 @@ def gemm_work(cfg, tau, fused_path=None):
     return work
 
 
+def head_fused(hw, c, classes):
+    """Whether the library runs the classifier head of a local step as one
+    launch: the last conv activation of a batch row, its pooled vector, its
+    pooling gradient and the logits fit one workgroup's LDS (12288 floats)."""
+    return hw * c + 2 * c + classes <= 12288
+
+
 def cnn_work(cfg, tau):
     """Algorithmic FLOPs and bytes of one round of the convolutional workload
     (oscars_round), per kind: conv layers as implicit GEMMs (2 FLOPs per
     multiply-add of every kernel tap; bytes: input, weights and output once),
-    average pooling with the forward kinds, the classifier with its kinds, the
-    weight updates' fp32 read and write of their parameters."""
+    the classifier head (pooling, classifier, softmax and their backward-data)
+    as softmax_ce where it is one launch, else pooling and the classifier with
+    the forward and backward-data kinds; the weight updates' fp32 read and
+    write of their parameters."""
     import numpy as np
     B = cfg.batch
     tau = np.asarray(tau)
@@ -112,16 +121,22 @@ def cnn_work(cfg, tau):
                 work["gemm_dgrad"][1] += ns * (act_out + wts + 2 * act_in)  # reads the mask too
             work["gemm_wgrad_update"][0] += ns * 2.0 * macs
             work["gemm_wgrad_update"][1] += ns * (act_out + act_in + 2 * wts)
-        pooled = B * C * 4
-        work["gemm_fwd"][1] += ns * (B * H * W * C * 4 + pooled)  # pooling
-        work["gemm_fwd"][0] += ns * 2.0 * B * C * classes
-        work["gemm_fwd"][1] += ns * (pooled + (C * classes + classes) * 4 + B * classes * 4)
-        work["gemm_dgrad"][0] += ns * 2.0 * B * C * classes
-        work["gemm_dgrad"][1] += ns * (B * classes * 4 + C * classes * 4 + pooled)
-        work["gemm_dgrad"][1] += ns * (pooled + 2 * B * H * W * C * 4)  # pooling backward
+        pooled, act, fc = B * C * 4, B * H * W * C * 4, (C * classes + classes) * 4
+        if head_fused(H * W, C, classes):
+            # one launch (booked as softmax_ce): the last activation read once, pooled,
+            # logits, loss, delta and the gradient at the last conv output written
+            work["softmax_ce"][0] += ns * 4.0 * B * C * classes
+            work["softmax_ce"][1] += ns * (2 * act + pooled + fc + 2 * B * classes * 4)
+        else:
+            work["gemm_fwd"][1] += ns * (act + pooled)  # pooling
+            work["gemm_fwd"][0] += ns * 2.0 * B * C * classes
+            work["gemm_fwd"][1] += ns * (pooled + fc + B * classes * 4)
+            work["gemm_dgrad"][0] += ns * 2.0 * B * C * classes
+            work["gemm_dgrad"][1] += ns * (B * classes * 4 + C * classes * 4 + pooled)
+            work["gemm_dgrad"][1] += ns * (pooled + 2 * act)  # pooling backward
+            work["softmax_ce"][1] += ns * B * classes * 8
         work["gemm_wgrad_update"][0] += ns * 2.0 * B * C * classes
-        work["gemm_wgrad_update"][1] += ns * (B * classes * 4 + pooled + 2 * (C * classes + classes) * 4)
-        work["softmax_ce"][1] += ns * B * classes * 8
+        work["gemm_wgrad_update"][1] += ns * (B * classes * 4 + pooled + 2 * fc)
     return work
 
 

@@ -73,4 +73,45 @@ hipError_t launch_avgpool_backward(const float* dpooled, int64_t dpooled_slot, c
                                    int64_t act_slot, float* dz, int B, int HW, int C,
                                    int n_slots, hipStream_t s);
 
+// The classifier head of one local step (average pooling, linear classifier,
+// softmax cross-entropy, the classifier's backward-data and the pooling
+// backward), grouped over slots like ConvArgs: slot z uses the parameters of
+// replica order[z].
+struct HeadArgs {
+  int B, HW, C, classes;          // batch rows, positions and channels of the last conv
+                                  // layer's output, classes
+  const float* act;               // that output [B][HW][C] (after ReLU), slot stride act_slot
+  int64_t act_slot;
+  const float* master_in;         // parameters read, by order[z]: classifier W [classes][C]
+  int64_t master_in_slot;         // at w_off, its bias at b_off
+  int64_t w_off, b_off;
+  const int32_t* order;
+  const int32_t* y;               // labels of the dataset rows
+  const int32_t* gather;          // dataset row of each batch row, [slot] stride gather_slot
+  int64_t gather_slot;
+  float* pooled;                  // out: pooled[b][c], slot stride pooled_slot
+  int64_t pooled_slot;
+  float* delta;                   // out: logit gradient [b][delta_ld], slot stride delta_slot
+  int64_t delta_slot, delta_ld;
+  float* loss;                    // out: per-row loss, slot stride loss_slot
+  int64_t loss_slot;
+  float* dz;                      // out: gradient at the last conv output [B][HW][C]
+  int64_t dz_slot;
+};
+
+// Whether the head of these sizes fits one workgroup's LDS (else the
+// separate pooling, classifier and softmax launches are used).
+bool conv_head_fits(int HW, int C, int classes);
+
+// Forward and backward of the head up to the last conv output's gradient,
+// one workgroup per (slot, batch row): pooled, logits, loss, delta (the
+// classifier's input to its weight gradient) and dz.
+hipError_t launch_conv_head(const HeadArgs& h, int n_slots, hipStream_t s);
+
+// The classifier's weight gradient from pooled and delta (the batch in
+// eight groups of consecutive rows, each in row order, the group sums in
+// order) and its SGD update: master[order[z]] <- master_in - lr dW.
+hipError_t launch_conv_head_update(const HeadArgs& h, float* master, int64_t master_slot,
+                                   float lr, int n_slots, hipStream_t s);
+
 }  // namespace oscars

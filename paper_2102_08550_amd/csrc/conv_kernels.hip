@@ -953,6 +953,163 @@ __global__ __launch_bounds__(256) void avgpool_backward_kernel(const float* dpoo
   dz[z * act_slot + e] = act[z * act_slot + e] > 0.0f ? g : 0.0f;
 }
 
+// The classifier head of one batch row b of slot z in one workgroup: the
+// row's last conv activation act[b] is staged in LDS once and serves the
+// pooling and the ReLU mask of the pooling backward.
+//   pooled[c] = (sum over the positions p, in order, of act[p][c]) / HW
+//   logit[o] = bias[o] + sum_c pooled[c] W[o][c]  (one wave per class: each
+//              lane over its channels c = lane, lane + 64, ..., then an
+//              xor-butterfly over the lanes)
+//   softmax cross-entropy as softmax_ce_kernel: loss = log(sum_o exp(logit[o]
+//   - max)) - (logit[label] - max); delta[o] = (softmax[o] - [o = label]) / B
+//   dz[p][c] = (sum over o, in order, of delta[o] W[o][c]) / HW where
+//              act[p][c] > 0, else 0
+// LDS: HW C + 2 C + classes floats.
+constexpr int HEAD_LDS_FLOATS = 12288;
+
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  for (int d = 32; d >= 1; d >>= 1) v = fmaxf(v, __shfl_xor(v, d));
+  return v;
+}
+
+__global__ __launch_bounds__(256) void conv_head_kernel(HeadArgs h) {
+  extern __shared__ float head_s[];
+  const int z = blockIdx.y, b = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int n = h.HW * h.C;
+  float* a_s = head_s;               // act[b], n floats
+  float* pool_s = a_s + n;           // C
+  float* dp_s = pool_s + h.C;        // C
+  float* lg_s = dp_s + h.C;          // classes: logits, then delta
+  const float* act_b = h.act + z * h.act_slot + static_cast<int64_t>(b) * n;
+  const bool vec = (n & 3) == 0 && (reinterpret_cast<uintptr_t>(act_b) & 15) == 0;
+  if (vec) {
+    for (int i = 4 * tid; i < n; i += 1024)
+      *reinterpret_cast<f32x4*>(a_s + i) = *reinterpret_cast<const f32x4*>(act_b + i);
+  } else {
+    for (int i = tid; i < n; i += 256) a_s[i] = act_b[i];
+  }
+  __syncthreads();
+  const float inv_hw = 1.0f / static_cast<float>(h.HW);
+  for (int c = tid; c < h.C; c += 256) {
+    float sum = 0.0f;
+    for (int p = 0; p < h.HW; ++p) sum += a_s[p * h.C + c];
+    const float v = sum / static_cast<float>(h.HW);
+    pool_s[c] = v;
+    h.pooled[z * h.pooled_slot + static_cast<int64_t>(b) * h.C + c] = v;
+  }
+  __syncthreads();
+  const float* par = h.master_in + static_cast<int64_t>(h.order[z]) * h.master_in_slot;
+  const float* Wc = par + h.w_off;
+  for (int o = wave; o < h.classes; o += 4) {
+    float v = 0.0f;
+    for (int c = lane; c < h.C; c += 64) v = fmaf(pool_s[c], Wc[static_cast<int64_t>(o) * h.C + c], v);
+    v = wave_sum(v);
+    if (lane == 0) lg_s[o] = par[h.b_off + o] + v;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int label = h.y[h.gather[z * h.gather_slot + b]];
+    const bool label_ok = label >= 0 && label < h.classes;
+    float mx = -INFINITY;
+    for (int o = lane; o < h.classes; o += 64) mx = fmaxf(mx, lg_s[o]);
+    mx = wave_max(mx);
+    float sum = 0.0f;
+    for (int o = lane; o < h.classes; o += 64) sum += expf(lg_s[o] - mx);
+    sum = wave_sum(sum);
+    const float zl = label_ok ? lg_s[label] : 0.0f;
+    const float invB = 1.0f / static_cast<float>(h.B);
+    float* drow = h.delta + z * h.delta_slot + static_cast<int64_t>(b) * h.delta_ld;
+    for (int o = lane; o < h.delta_ld; o += 64) {
+      float dv = 0.0f;
+      if (o < h.classes) {
+        dv = (expf(lg_s[o] - mx) / sum - (o == label ? 1.0f : 0.0f)) * invB;
+        lg_s[o] = dv;
+      }
+      drow[o] = dv;
+    }
+    if (lane == 0)
+      h.loss[z * h.loss_slot + b] = label_ok ? logf(sum) - (zl - mx) : __builtin_nanf("");
+  }
+  __syncthreads();
+  for (int c = tid; c < h.C; c += 256) {
+    float v = 0.0f;
+    for (int o = 0; o < h.classes; ++o) v = fmaf(lg_s[o], Wc[static_cast<int64_t>(o) * h.C + c], v);
+    dp_s[c] = v * inv_hw;
+  }
+  __syncthreads();
+  float* dz_b = h.dz + z * h.dz_slot + static_cast<int64_t>(b) * n;
+  if (vec && (h.C & 3) == 0 && (reinterpret_cast<uintptr_t>(dz_b) & 15) == 0) {
+    for (int i = 4 * tid; i < n; i += 1024) {
+      const int c = i % h.C;
+      const f32x4 av = *reinterpret_cast<const f32x4*>(a_s + i);
+      f32x4 g;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) g[e] = av[e] > 0.0f ? dp_s[c + e] : 0.0f;
+      *reinterpret_cast<f32x4*>(dz_b + i) = g;
+    }
+  } else {
+    for (int i = tid; i < n; i += 256) dz_b[i] = a_s[i] > 0.0f ? dp_s[i % h.C] : 0.0f;
+  }
+}
+
+// The classifier's weight gradient and update: weight e = (o, c) of the
+// classes x (C + 1) matrix (c = C: the bias) takes
+// sum_b delta[b][o] pooled[b][c] (pooled = 1 for the bias) over the batch in
+// HG groups of consecutive rows, each in row order by one thread, then the
+// group sums in group order; master <- master_in - lr sum.
+constexpr int HW32 = 32, HG = 8;
+static_assert(HW32 * HG == 256, "one thread per (weight, group)");
+
+__global__ __launch_bounds__(256) void conv_head_update_kernel(HeadArgs h, float* master,
+                                                               int64_t master_slot, float lr) {
+  const int z = blockIdx.y;
+  const int N = h.C + 1;
+  const int w = threadIdx.x % HW32, grp = threadIdx.x / HW32;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * HW32 + w;
+  const int64_t MN = static_cast<int64_t>(h.classes) * N;
+  const int per = (h.B + HG - 1) / HG;
+  const int b0 = grp * per, b1 = min(h.B, b0 + per);
+  float sum = 0.0f;
+  if (e < MN) {
+    const int o = static_cast<int>(e / N), c = static_cast<int>(e - static_cast<int64_t>(o) * N);
+    const float* dcol = h.delta + z * h.delta_slot + o;
+    // the bias column reads ones
+    const float* pcol = c < h.C ? h.pooled + z * h.pooled_slot + c : k_conv_one;
+    const int64_t ps = c < h.C ? h.C : 0;
+    int bb = b0;
+    for (; bb + 8 <= b1; bb += 8) {
+      float dv[8], pv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        dv[u] = dcol[static_cast<int64_t>(bb + u) * h.delta_ld];
+        pv[u] = pcol[(bb + u) * ps];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum = fmaf(dv[u], pv[u], sum);
+    }
+    for (; bb < b1; ++bb)
+      sum = fmaf(dcol[static_cast<int64_t>(bb) * h.delta_ld], pcol[bb * ps], sum);
+  }
+  __shared__ float group_sum[HG][HW32];
+  group_sum[grp][w] = sum;
+  __syncthreads();
+  if (grp != 0 || e >= MN) return;
+  float tot = group_sum[0][w];
+#pragma unroll
+  for (int g = 1; g < HG; ++g) tot += group_sum[g][w];
+  const int o = static_cast<int>(e / N), c = static_cast<int>(e - static_cast<int64_t>(o) * N);
+  const int rep = h.order[z];
+  const float* src = h.master_in + static_cast<int64_t>(rep) * h.master_in_slot;
+  float* dst = master + static_cast<int64_t>(rep) * master_slot;
+  const int64_t at = c < h.C ? h.w_off + static_cast<int64_t>(o) * h.C + c : h.b_off + o;
+  dst[at] = fmaf(-lr, tot, src[at]);
+}
+
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
@@ -1079,6 +1236,32 @@ hipError_t launch_avgpool_backward(const float* dpooled, int64_t dpooled_slot, c
   if (blocks > 0x7FFFFFFF || n_slots < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(avgpool_backward_kernel, dim3(static_cast<unsigned>(blocks), n_slots),
                      dim3(256), 0, s, dpooled, dpooled_slot, act, act_slot, dz, B, HW, C);
+  return hipGetLastError();
+}
+
+bool conv_head_fits(int HW, int C, int classes) {
+  if (HW < 1 || C < 1 || classes < 1) return false;
+  const int64_t need = static_cast<int64_t>(HW) * C + 2LL * C + classes;
+  return need <= HEAD_LDS_FLOATS;
+}
+
+hipError_t launch_conv_head(const HeadArgs& h, int n_slots, hipStream_t s) {
+  if (n_slots < 1 || h.B < 1 || !conv_head_fits(h.HW, h.C, h.classes) || h.delta_ld < h.classes)
+    return hipErrorInvalidValue;
+  const size_t lds = (static_cast<size_t>(h.HW) * h.C + 2 * h.C + h.classes) * sizeof(float);
+  hipLaunchKernelGGL(conv_head_kernel, dim3(static_cast<unsigned>(h.B), n_slots), dim3(256), lds, s,
+                     h);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_head_update(const HeadArgs& h, float* master, int64_t master_slot,
+                                   float lr, int n_slots, hipStream_t s) {
+  if (n_slots < 1 || h.B < 1 || h.C < 1 || h.classes < 1) return hipErrorInvalidValue;
+  const int64_t MN = static_cast<int64_t>(h.classes) * (h.C + 1);
+  const int64_t blocks = (MN + HW32 - 1) / HW32;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_head_update_kernel, dim3(static_cast<unsigned>(blocks), n_slots),
+                     dim3(256), 0, s, h, master, master_slot, lr);
   return hipGetLastError();
 }
 

@@ -563,12 +563,45 @@ ConvArgs conv_layer_args(const oscars_ctx* c, int l, const float* master_in, int
   return a;
 }
 
+// The classifier head of local step j (conv_head_kernel): whether it fits
+// one workgroup is checked by the caller (conv_head_fits).
+HeadArgs head_args(const oscars_ctx* c, const float* master_in, int64_t master_in_slot,
+                   const int32_t* order, const int32_t* y, const int32_t* rows,
+                   int64_t rows_slot, int B, float* loss) {
+  const int L = c->L;
+  HeadArgs h{};
+  h.B = B;
+  h.HW = c->img_h[L - 1] * c->img_w[L - 1];
+  h.C = c->img_c[L - 1];
+  h.classes = c->dims[L];
+  h.act = c->cact[L - 1];
+  h.act_slot = c->cnn_slot(L - 1);
+  h.master_in = master_in;
+  h.master_in_slot = master_in_slot;
+  h.w_off = c->w_off[L];
+  h.b_off = c->b_off[L];
+  h.order = order;
+  h.y = y;
+  h.gather = rows;
+  h.gather_slot = rows_slot;
+  h.pooled = c->pooled;
+  h.pooled_slot = static_cast<int64_t>(c->max_batch) * h.C;
+  h.delta = static_cast<float*>(c->delta[L]);
+  h.delta_slot = c->act_slot(L);
+  h.delta_ld = c->ld[L];
+  h.loss = loss;
+  h.loss_slot = rows_slot;
+  h.dz = c->cdz[L - 1];
+  h.dz_slot = c->cnn_slot(L - 1);
+  return h;
+}
+
 // Forward pass of the convolutional model for n_slots slots: conv layers
-// (layer 1 gathers the dataset rows `rows` of each slot), average pooling,
-// classifier logits into c->logits.
+// (layer 1 gathers the dataset rows `rows` of each slot), then, with
+// `with_head`, average pooling and the classifier logits into c->logits.
 hipError_t cnn_forward(oscars_ctx* c, const float* master_in, int64_t master_in_slot,
                        const int32_t* order, const void* x, const int32_t* rows,
-                       int64_t rows_slot, int B, int ns) {
+                       int64_t rows_slot, int B, int ns, bool with_head = true) {
   const int L = c->L;
   hipError_t e = hipSuccess;
   for (int l = 1; l < L && e == hipSuccess; ++l) {
@@ -586,6 +619,7 @@ hipError_t cnn_forward(oscars_ctx* c, const float* master_in, int64_t master_in_
     a.out_slot = c->cnn_slot(l);
     e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_conv(a, CONV_FWD, ns, c->stream); });
   }
+  if (!with_head) return e;
   const int HW = c->img_h[L - 1] * c->img_w[L - 1], Cl = c->img_c[L - 1];
   const int64_t pslot = static_cast<int64_t>(c->max_batch) * Cl;
   if (e == hipSuccess)
@@ -609,15 +643,24 @@ hipError_t cnn_forward(oscars_ctx* c, const float* master_in, int64_t master_in_
 // forward pass and loss gradient (in c->delta[L]): classifier backward-data
 // and update, pooling backward with the last ReLU mask, then per conv layer
 // (top down) backward-data (masked by the layer below) and the weight update.
+// With `head` (conv_head_kernel ran instead of the pooling, classifier and
+// softmax launches, and already wrote the gradient at the last conv output),
+// the classifier's update alone precedes the conv layers.
 // Backward-data of a layer reads its weights before its update writes them.
 hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
                         int64_t master_in_slot, const int32_t* order, const void* x,
-                        const int32_t* rows, int64_t rows_slot, int B, int ns, float lr) {
+                        const int32_t* rows, int64_t rows_slot, int B, int ns, float lr,
+                        const HeadArgs* head) {
   const int L = c->L;
   const int Cl = c->img_c[L - 1], HW = c->img_h[L - 1] * c->img_w[L - 1];
   const int64_t pslot = static_cast<int64_t>(c->max_batch) * Cl;
   hipError_t e = hipSuccess;
-  {
+  if (head) {
+    // conv_head_kernel left the gradient at the last conv output in cdz[L - 1]
+    e = timed(c, OSCARS_KERNEL_WGRAD, [&] {
+      return launch_conv_head_update(*head, replicas, c->n_pad, lr, ns, c->stream);
+    });
+  } else {
     ConvArgs a = conv_layer_args(c, L, master_in, master_in_slot, order, B);
     a.in = c->pooled;
     a.in_slot = pslot;
@@ -639,7 +682,7 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
                                : r;
       });
   }
-  if (e == hipSuccess)
+  if (e == hipSuccess && !head)
     e = timed(c, OSCARS_KERNEL_DGRAD, [&] {
       return launch_avgpool_backward(c->dpooled, pslot, c->cact[L - 1], c->cnn_slot(L - 1),
                                      c->cdz[L - 1], B, HW, Cl, ns, c->stream);
@@ -858,16 +901,21 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
       const bool from_start = start && j == 0;
       const float* min = from_start ? start : replicas;
       const int64_t min_slot = from_start ? 0 : c->n_pad;
-      e = cnn_forward(c, min, min_slot, d_order, s->x, rows_j, rows_slot, B, ns);
+      float* loss_j = c->loss_dev + static_cast<int64_t>(j) * B;
+      const HeadArgs head =
+          head_args(c, min, min_slot, d_order, s->y, rows_j, rows_slot, B, loss_j);
+      const bool fused_head = conv_head_fits(head.HW, head.C, head.classes);
+      e = cnn_forward(c, min, min_slot, d_order, s->x, rows_j, rows_slot, B, ns, !fused_head);
       if (e == hipSuccess)
         e = timed(c, OSCARS_KERNEL_SOFTMAX, [&] {
+          if (fused_head) return launch_conv_head(head, ns, c->stream);
           return launch_softmax_ce(c->logits, c->ld[c->L], c->act_slot(c->L), c->dims[c->L], B,
-                                   s->y, rows_j, rows_slot, c->delta[c->L], false,
-                                   c->loss_dev + static_cast<int64_t>(j) * B, rows_slot, ns,
-                                   c->stream);
+                                   s->y, rows_j, rows_slot, c->delta[c->L], false, loss_j,
+                                   rows_slot, ns, c->stream);
         });
       if (e == hipSuccess)
-        e = cnn_backward(c, replicas, min, min_slot, d_order, s->x, rows_j, rows_slot, B, ns, lr);
+        e = cnn_backward(c, replicas, min, min_slot, d_order, s->x, rows_j, rows_slot, B, ns, lr,
+                         fused_head ? &head : nullptr);
       if (e != hipSuccess) return hip_fail(e);
     }
     for (int k = 0; k < K; ++k) c->cursors[k] += tau[k];

@@ -5,7 +5,9 @@ the oracle, on the same seeded inputs, through the C ABI.
 * Trajectories tensor by tensor (each conv W_l, b_l and the classifier),
   element by element, within the fp32 tolerance: small images with ragged
   tiles in every dimension, strides 1 and 2, split weight gradients, batch 1,
-  a worker idle; as local steps + aggregation and as oscars_round.
+  a worker idle, the classifier head in one launch and (a last activation too
+  large for it) in separate launches; as local steps + aggregation and as
+  oscars_round.
 * Masking independence (grouped == solo, bit for bit) and determinism.
 * The full-size workload (32 x 32 x 3 images, 8 workers, all 5 rounds) in the
   benchmark's launch configuration against the oracle's run stored by
@@ -59,6 +61,10 @@ TRAJ = {
     # N = 10 weight-gradient columns), then a stride-1 layer
     "gray-s2": _cfg("cnn-gray-s2", (10, 9, 1), ((12, 2), (16, 1)), K=2, n_rows=120, batch=5,
                     tau=(3, 2), rounds=2, seed=45),
+    # a last conv output too large for the one-launch classifier head (32 x 32
+    # x 16 per batch row): pooling, classifier and softmax as separate launches
+    "big-head": _cfg("cnn-big-head", (32, 32, 3), ((16, 1),), K=2, n_rows=24, batch=3,
+                     tau=(2, 1), rounds=1, seed=46),
     # the full workload's layers on 16 x 16 images, batch 64 (pixels per
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
