@@ -49,12 +49,22 @@ struct ConvArgs {
   int64_t mask_slot;
   float* part;            // WGRAD: partial sums [slot][split][Co][N]
   int64_t part_slot;
-  int splits;             // WGRAD: number of K ranges (output pixels or batch rows)
-  int64_t k_per_split;
+  int splits;             // WGRAD: number of K ranges (of output pixels, output rows of layers
+  int64_t k_per_split;    // with at most 3 input channels, or batch rows; conv_wgrad_ranges)
   const int32_t* order;
 };
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s);
+
+// Output pixels per weight-gradient range of the 64 x 64 conv tiles.
+constexpr int CONV_WGRAD_PIXELS = 512;
+
+// The K ranges a CONV_WGRAD launch of these sizes expects (ConvArgs.splits,
+// ConvArgs.k_per_split): ranges of CONV_WGRAD_PIXELS output pixels, or, for
+// layers with at most three input channels whose staged input rows fit a
+// workgroup's LDS, of whole output rows (as many as fill 512 pixel slots of
+// the row width rounded up to 32).
+void conv_wgrad_ranges(const ConvArgs& a, int* splits, int64_t* k_per_split);
 
 // WGRAD epilogue: sum the partials of each weight (eight groups of
 // consecutive splits, each in split order, the group sums in order), then the

@@ -759,96 +759,133 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_kernel(ConvArgs a) {
   }
 }
 
-// Backward-weight partial of one range of output pixels (workgroup = range,
-// as the weight-gradient passes of conv_gemm_kernel): C[o][n] = sum over the
-// range's pixels p of dZ[p][o] x(p, n), with x(p, n) the input tap of column
-// n < 9 Cin and 1 for the bias column.  The whole 32 x 32 block is one MFMA
-// accumulator: each wave runs the 32x32x2 fp32 MFMA over a quarter of the
-// range (two pixels per MFMA, operands loaded by the lanes straight from
-// memory: lane l holds dZ[p + l / 32][l % 32] and x(p + l / 32, l % 32)),
-// and the four quarters are added in wave order.
-constexpr int THIN_WG_PIXELS = 512;  // output pixels per range at most
+// Backward-weight partial of one range of whole output rows (workgroup =
+// range): C[o][n] = sum over the range's pixels p of dZ[p][o] x(p, n), with
+// x(p, n) the input tap of column n < 9 Cin and 1 for the bias column.  The
+// input rows the range's taps read are staged in LDS first, zero-padded:
+// for range row q and tap row r, input row stride i + r - 1 of its image,
+// with a zero column on the left and zeros past the right edge up to the
+// last column a 32-pixel block of the row can reach.  A tap then needs no
+// bounds test and its LDS offset steps by a constant from pixel to pixel.
+// The whole 32 x 32 block is one MFMA accumulator: wave w takes range rows
+// w, w + 4, ..., each in blocks of 32 pixels, one 32x32x2 fp32 MFMA per
+// pixel pair (lane l holds dZ[p + l / 32][l % 32] and x(p + l / 32, l % 32)),
+// dZ of the next block loaded while the current one is multiplied; the four
+// waves' sums are added in wave order.
+constexpr int THIN_WG_PIXELS = 512;   // a range's pixel slots (rows x padded width) at most
+constexpr int THIN_STAGE_MAX = 11264;  // staged floats at most (44 KB, with red: under 64 KB)
 
+__host__ __device__ inline int thin_wo_pad(const ConvArgs& a) { return (a.Wo + 31) / 32 * 32; }
+__host__ __device__ inline int thin_rows_per_range(const ConvArgs& a) {
+  const int r = THIN_WG_PIXELS / thin_wo_pad(a);
+  return r > 1 ? r : 1;
+}
+__host__ __device__ inline int thin_row_width(const ConvArgs& a) {
+  return a.stride * thin_wo_pad(a) + 2;
+}
+__host__ __device__ inline int64_t thin_stage_floats(const ConvArgs& a) {
+  return static_cast<int64_t>(thin_rows_per_range(a)) * 3 * thin_row_width(a) * a.C;
+}
+__host__ __device__ inline bool thin_wgrad(const ConvArgs& a) {
+  return thin_layer(a) && (a.stride == 1 || a.stride == 2) && thin_stage_floats(a) <= THIN_STAGE_MAX;
+}
+
+template <int CIN, int STRIDE>
 __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
+  extern __shared__ float x_s[];  // [range row][tap row][width][CIN]
   __shared__ float red[4][32][33];
-  __shared__ int row_s[THIN_WG_PIXELS + 1];  // images a range touches at most
+  constexpr int N = 9 * CIN + 1;
   const int z = blockIdx.y;
-  const int split = blockIdx.x;
-  const int M = a.Co, N = 9 * a.C + 1;
-  const int hw = a.Ho * a.Wo;
-  const int K = a.B * hw;
-  const int kbeg = split * static_cast<int>(a.k_per_split);
-  const int kend = K - kbeg < a.k_per_split ? K : kbeg + static_cast<int>(a.k_per_split);
+  const int M = a.Co;
+  const int R = thin_rows_per_range(a), wop = thin_wo_pad(a), width = thin_row_width(a);
+  const int per_row = width * CIN;
+  const int rows_total = a.B * a.Ho;
+  const int r0 = blockIdx.x * R;
+  const int nr_rows = rows_total - r0 < R ? rows_total - r0 : R;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
-  const int quarter = (kend - kbeg + 3) / 4;
-  const int wb = kbeg + wave * quarter;
-  const int we = wb + quarter < kend ? wb + quarter : kend;
+  const float* in = a.in + z * a.in_slot;
+  // staging: first the source offset of every staged row (-1: a padding row),
+  // then the elements, eight loads per thread in flight (a padding element
+  // reads the zero array)
+  __shared__ int64_t src_s[3 * (THIN_WG_PIXELS / 32)];
+  if (threadIdx.x < 3 * R) {
+    const int sr = threadIdx.x, q = sr / 3, r = sr - 3 * q;
+    int64_t off = -1;
+    if (q < nr_rows) {
+      const int orow = r0 + q, b = orow / a.Ho, i = orow - b * a.Ho;
+      const int hi = STRIDE * i + r - 1;
+      if (hi >= 0 && hi < a.H) {
+        const int64_t img = a.gather ? static_cast<int64_t>(a.gather[z * a.gather_slot + b]) * a.in_ld
+                                     : static_cast<int64_t>(b) * a.H * a.W * CIN;
+        off = img + static_cast<int64_t>(hi) * a.W * CIN;
+      }
+    }
+    src_s[sr] = off;
+  }
+  __syncthreads();
+  const int n_stage = 3 * R * per_row;
+  for (int e0 = threadIdx.x; e0 < n_stage; e0 += 8 * 256) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + 256 * u;
+      const int sr = e < n_stage ? e / per_row : 0, col = e - sr * per_row;
+      const int64_t off = src_s[sr];
+      const bool ok = e < n_stage && off >= 0 && col >= CIN && col < (a.W + 1) * CIN;
+      v[u] = *(ok ? in + off + (col - CIN) : k_conv_zero);  // staged column 0: padding
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (e0 + 256 * u < n_stage) x_s[e0 + 256 * u] = v[u];
+  }
   // this lane's B column: tap (r, s) and channel c, the bias column, or none
-  const int n = l32;
-  const int rs = n / a.C, nc = n - rs * a.C, nr = rs / 3, ns = rs - 3 * nr;
-  const bool ntap = n < N - 1, nbias = n == N - 1;
+  const int rs = l32 / CIN, nc = l32 - rs * CIN, nr = rs / 3, ns = rs - 3 * nr;
+  const bool ntap = l32 < N - 1;
+  const float bconst = l32 == N - 1 ? 1.0f : 0.0f;
+  const int tap_off = ntap ? (nr * width + ns) * CIN + nc : 0;
   const bool mrow = l32 < M;
   const float* dz = a.dout + z * a.dout_slot;
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-  // UB MFMAs per batch, operands in two register sets: batch t + 1 is loaded
-  // while batch t is multiplied (no load behind a branch: a lane with nothing
-  // to load reads the zero array, so the memory-counter waits stay exact).
-  // The lane's next pixel pn = p0 + 2 u + h is decoded once per wave and then
-  // advanced by two.
-  constexpr int UB = 16;
-  // The dataset rows (or batch rows) of the range's images, staged in LDS
-  // once: an input load then waits only for an LDS read, not for a gather
-  // load queued behind the other loads in flight.
-  const float* in = a.in + z * a.in_slot;
-  const int64_t img_stride = a.gather ? a.in_ld : static_cast<int64_t>(a.H) * a.W * a.C;
-  const int b_first = kbeg / hw, nrows = (kend - 1) / hw - b_first + 1;
-  for (int i = threadIdx.x; i < nrows; i += 256)
-    row_s[i] = a.gather ? a.gather[z * a.gather_slot + b_first + i] : b_first + i;
   __syncthreads();
-  int pn = wb + h;
-  const int p_first = wb < we ? wb + h : 0;
-  int pb = p_first / hw, pi = (p_first - pb * hw) / a.Wo, pj = p_first - pb * hw - pi * a.Wo;
-  float av[2][UB], bv[2][UB];
-  auto load = [&](auto P) {
-    constexpr int q = decltype(P)::value;
-#pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const bool ok = pn < we;
-      const int hi = a.stride * pi + nr - 1, wi = a.stride * pj + ns - 1;
-      const bool tap_ok = ok && ntap && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
-      const float* img = in + static_cast<int64_t>(row_s[ok ? pb - b_first : 0]) * img_stride;
-      av[q][u] = *(ok && mrow ? dz + static_cast<int64_t>(pn) * M + l32 : k_conv_zero);
-      bv[q][u] = *(tap_ok ? img + (hi * a.W + wi) * a.C + nc
-                          : (ok && nbias ? k_conv_one : k_conv_zero));
-      pn += 2;
-      for (int step = 0; step < 2; ++step)
-        if (++pj == a.Wo) {
-          pj = 0;
-          if (++pi == a.Ho) {
-            pi = 0;
-            ++pb;
-          }
-        }
-    }
-  };
-  auto mul = [&](auto P) {
-    constexpr int q = decltype(P)::value;
+  // batches of this wave: (range row q = wave + 4 (t / nj), pixel block t % nj)
+  const int nj = wop / 32;
+  const int my_rows = nr_rows > wave ? (nr_rows - wave + 3) / 4 : 0;
+  const int nb = my_rows * nj;
+  constexpr int UB = 16;
+  float av[2][UB];
+  auto load = [&](int t, auto P) {  // dZ of batch t (zeros past the wave's batches)
+    constexpr int qs = decltype(P)::value;
+    const int q = wave + 4 * (t / nj), jb = t - (t / nj) * nj;
+    const bool bok = t < nb;
+    const int64_t prow = static_cast<int64_t>(bok ? r0 + q : 0) * a.Wo;
+    const int jlim = bok ? a.Wo - 32 * jb - h : 0;  // slots 2 u below it hold pixels
+    const float* base = dz + (prow + 32 * jb + h) * M + l32;
 #pragma unroll
     for (int u = 0; u < UB; ++u)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[q][u], bv[q][u], acc, 0, 0, 0);
+      av[qs][u] = *(mrow && 2 * u < jlim ? base + static_cast<int64_t>(2 * u) * M : k_conv_zero);
   };
-  const int nb = we > wb ? (we - wb + 2 * UB - 1) / (2 * UB) : 0;
-  load(Pi<0>());
+  auto mul = [&](int t, auto P) {
+    constexpr int qs = decltype(P)::value;
+    const int q = wave + 4 * (t / nj), jb = t - (t / nj) * nj;
+    const float* xrow = x_s + q * 3 * per_row + (STRIDE * (32 * jb + h)) * CIN + tap_off;
+    float bv[UB];
+#pragma unroll
+    for (int u = 0; u < UB; ++u) bv[u] = ntap ? xrow[2 * STRIDE * CIN * u] : bconst;
+#pragma unroll
+    for (int u = 0; u < UB; ++u)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[qs][u], bv[u], acc, 0, 0, 0);
+  };
+  load(0, Pi<0>());
   int t = 0;
   for (; t + 1 < nb; t += 2) {
-    load(Pi<1>());
-    mul(Pi<0>());
-    load(Pi<0>());
-    mul(Pi<1>());
+    load(t + 1, Pi<1>());
+    mul(t, Pi<0>());
+    load(t + 2, Pi<0>());
+    mul(t + 1, Pi<1>());
   }
-  if (t < nb) mul(Pi<0>());
+  if (t < nb) mul(t, Pi<0>());
   // accumulator e of lane (l32, h): row 8 (e / 4) + 4 h + e % 4, column l32
 #pragma unroll
   for (int e = 0; e < 16; ++e) red[wave][8 * (e >> 2) + 4 * h + (e & 3)][l32] = acc[e];
@@ -856,7 +893,7 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
   for (int idx = threadIdx.x; idx < M * N; idx += 256) {
     const int m = idx / N, c = idx - m * N;
     const float v = ((red[0][m][c] + red[1][m][c]) + red[2][m][c]) + red[3][m][c];
-    a.part[z * a.part_slot + (static_cast<int64_t>(split) * M + m) * N + c] = v;
+    a.part[z * a.part_slot + (static_cast<int64_t>(blockIdx.x) * M + m) * N + c] = v;
   }
 }
 
@@ -1162,13 +1199,20 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
     }
     return hipGetLastError();
   }
-  if (pass == CONV_WGRAD && thin_layer(a)) {
-    if (a.splits < 1 || a.k_per_split < 2 || (a.k_per_split & 1) ||
-        a.k_per_split > THIN_WG_PIXELS || static_cast<int64_t>(a.splits) * a.k_per_split < d.K ||
-        static_cast<int64_t>(a.splits - 1) * a.k_per_split >= d.K)
-      return hipErrorInvalidValue;
-    hipLaunchKernelGGL(conv_thin_wgrad_kernel, dim3(static_cast<unsigned>(a.splits), n_slots),
-                       dim3(256), 0, s, a);
+  if (pass == CONV_WGRAD && thin_wgrad(a)) {
+    const int R = thin_rows_per_range(a);
+    if (a.k_per_split != R || a.splits != (a.B * a.Ho + R - 1) / R) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(a.splits), n_slots), block(256);
+    const size_t lds = static_cast<size_t>(thin_stage_floats(a)) * sizeof(float);
+    const int key = 2 * a.C + (a.stride == 2 ? 1 : 0);
+    switch (key) {
+      case 2: hipLaunchKernelGGL((conv_thin_wgrad_kernel<1, 1>), grid, block, lds, s, a); break;
+      case 3: hipLaunchKernelGGL((conv_thin_wgrad_kernel<1, 2>), grid, block, lds, s, a); break;
+      case 4: hipLaunchKernelGGL((conv_thin_wgrad_kernel<2, 1>), grid, block, lds, s, a); break;
+      case 5: hipLaunchKernelGGL((conv_thin_wgrad_kernel<2, 2>), grid, block, lds, s, a); break;
+      case 6: hipLaunchKernelGGL((conv_thin_wgrad_kernel<3, 1>), grid, block, lds, s, a); break;
+      default: hipLaunchKernelGGL((conv_thin_wgrad_kernel<3, 2>), grid, block, lds, s, a); break;
+    }
     return hipGetLastError();
   }
   int64_t gx = ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
@@ -1263,6 +1307,18 @@ hipError_t launch_conv_head_update(const HeadArgs& h, float* master, int64_t mas
   hipLaunchKernelGGL(conv_head_update_kernel, dim3(static_cast<unsigned>(blocks), n_slots),
                      dim3(256), 0, s, h, master, master_slot, lr);
   return hipGetLastError();
+}
+
+void conv_wgrad_ranges(const ConvArgs& a, int* splits, int64_t* k_per_split) {
+  if (thin_wgrad(a)) {
+    const int R = thin_rows_per_range(a);
+    *k_per_split = R;
+    *splits = (a.B * a.Ho + R - 1) / R;
+    return;
+  }
+  const int64_t pixels = static_cast<int64_t>(a.B) * a.Ho * a.Wo;
+  *k_per_split = CONV_WGRAD_PIXELS;
+  *splits = static_cast<int>((pixels + CONV_WGRAD_PIXELS - 1) / CONV_WGRAD_PIXELS);
 }
 
 }  // namespace oscars

@@ -45,8 +45,6 @@ constexpr int kMaxTau = 4096;
 constexpr int kPreTau = 64;
 // Backward path timing: how much faster a later candidate must be to be taken.
 constexpr float kBackwardMargin = 0.05f;
-// Output pixels per weight-gradient partial of a conv layer.
-constexpr int64_t kConvPixelsPerSplit = 512;
 
 }  // namespace
 
@@ -458,9 +456,19 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
   // weight-gradient partials per slot: the largest layer's splits x outputs
   int64_t part = static_cast<int64_t>(m->classes) * (c->img_c[Lc] + 1);
   for (int l = 1; l <= Lc; ++l) {
-    const int64_t pixels = static_cast<int64_t>(max_batch) * c->img_h[l] * c->img_w[l];
-    const int64_t splits = (pixels + kConvPixelsPerSplit - 1) / kConvPixelsPerSplit;
-    part = std::max<int64_t>(part, splits * c->img_c[l] * (9LL * c->img_c[l - 1] + 1));
+    ConvArgs a{};
+    a.B = max_batch;
+    a.H = c->img_h[l - 1];
+    a.W = c->img_w[l - 1];
+    a.C = c->img_c[l - 1];
+    a.Ho = c->img_h[l];
+    a.Wo = c->img_w[l];
+    a.Co = c->img_c[l];
+    a.stride = c->conv_stride[l];
+    int splits = 0;
+    int64_t per = 0;
+    conv_wgrad_ranges(a, &splits, &per);
+    part = std::max<int64_t>(part, static_cast<int64_t>(splits) * a.Co * (9LL * a.C + 1));
   }
   c->cpart_slot = round_up(part, 64);
 
@@ -708,9 +716,7 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
       a.gather = rows;
       a.gather_slot = rows_slot;
     }
-    const int64_t pixels = static_cast<int64_t>(B) * a.Ho * a.Wo;
-    a.k_per_split = kConvPixelsPerSplit;
-    a.splits = static_cast<int>((pixels + kConvPixelsPerSplit - 1) / kConvPixelsPerSplit);
+    conv_wgrad_ranges(a, &a.splits, &a.k_per_split);
     a.part = c->cpart;
     a.part_slot = c->cpart_slot;
     e = timed(c, OSCARS_KERNEL_WGRAD, [&] {

@@ -61,6 +61,9 @@ TRAJ = {
     # N = 10 weight-gradient columns), then a stride-1 layer
     "gray-s2": _cfg("cnn-gray-s2", (10, 9, 1), ((12, 2), (16, 1)), K=2, n_rows=120, batch=5,
                     tau=(3, 2), rounds=2, seed=45),
+    # two input channels, a thin first layer of 4 output channels
+    "two-ch": _cfg("cnn-two-ch", (7, 6, 2), ((4, 1), (8, 2)), K=2, n_rows=60, batch=6,
+                   tau=(2, 3), rounds=2, seed=47),
     # a last conv output too large for the one-launch classifier head (32 x 32
     # x 16 per batch row): pooling, classifier and softmax as separate launches
     "big-head": _cfg("cnn-big-head", (32, 32, 3), ((16, 1),), K=2, n_rows=24, batch=3,
