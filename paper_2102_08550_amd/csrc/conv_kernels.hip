@@ -790,24 +790,16 @@ __host__ __device__ inline bool thin_wgrad(const ConvArgs& a) {
   return thin_layer(a) && (a.stride == 1 || a.stride == 2) && thin_stage_floats(a) <= THIN_STAGE_MAX;
 }
 
+// Stages the input rows of range rows [r0, r0 + nr_rows) in LDS, zero-padded
+// (x_s[(3 q + r) per_row + col CIN + c] = input row STRIDE i + r - 1, column
+// col - 1, of range row q's image, or 0): first the source offset of every
+// staged row (-1: a padding row), then the elements, eight loads per thread
+// in flight (a padding element reads the zero array).  Ends with a barrier.
 template <int CIN, int STRIDE>
-__global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
-  extern __shared__ float x_s[];  // [range row][tap row][width][CIN]
-  __shared__ float red[4][32][33];
-  constexpr int N = 9 * CIN + 1;
-  const int z = blockIdx.y;
-  const int M = a.Co;
-  const int R = thin_rows_per_range(a), wop = thin_wo_pad(a), width = thin_row_width(a);
-  const int per_row = width * CIN;
-  const int rows_total = a.B * a.Ho;
-  const int r0 = blockIdx.x * R;
-  const int nr_rows = rows_total - r0 < R ? rows_total - r0 : R;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
-  const float* in = a.in + z * a.in_slot;
-  // staging: first the source offset of every staged row (-1: a padding row),
-  // then the elements, eight loads per thread in flight (a padding element
-  // reads the zero array)
+__device__ __forceinline__ void thin_stage(const ConvArgs& a, int z, int r0, int R, int nr_rows,
+                                           int per_row, float* x_s) {
   __shared__ int64_t src_s[3 * (THIN_WG_PIXELS / 32)];
+  const float* in = a.in + z * a.in_slot;
   if (threadIdx.x < 3 * R) {
     const int sr = threadIdx.x, q = sr / 3, r = sr - 3 * q;
     int64_t off = -1;
@@ -838,6 +830,23 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
     for (int u = 0; u < 8; ++u)
       if (e0 + 256 * u < n_stage) x_s[e0 + 256 * u] = v[u];
   }
+  __syncthreads();
+}
+
+template <int CIN, int STRIDE>
+__global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
+  extern __shared__ float x_s[];  // [range row][tap row][width][CIN]
+  __shared__ float red[4][32][33];
+  constexpr int N = 9 * CIN + 1;
+  const int z = blockIdx.y;
+  const int M = a.Co;
+  const int R = thin_rows_per_range(a), wop = thin_wo_pad(a), width = thin_row_width(a);
+  const int per_row = width * CIN;
+  const int rows_total = a.B * a.Ho;
+  const int r0 = blockIdx.x * R;
+  const int nr_rows = rows_total - r0 < R ? rows_total - r0 : R;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+  thin_stage<CIN, STRIDE>(a, z, r0, R, nr_rows, per_row, x_s);
   // this lane's B column: tap (r, s) and channel c, the bias column, or none
   const int rs = l32 / CIN, nc = l32 - rs * CIN, nr = rs / 3, ns = rs - 3 * nr;
   const bool ntap = l32 < N - 1;
@@ -848,7 +857,6 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-  __syncthreads();
   // batches of this wave: (range row q = wave + 4 (t / nj), pixel block t % nj)
   const int nj = wop / 32;
   const int my_rows = nr_rows > wave ? (nr_rows - wave + 3) / 4 : 0;
@@ -894,6 +902,65 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
     const int m = idx / N, c = idx - m * N;
     const float v = ((red[0][m][c] + red[1][m][c]) + red[2][m][c]) + red[3][m][c];
     a.part[z * a.part_slot + (static_cast<int64_t>(blockIdx.x) * M + m) * N + c] = v;
+  }
+}
+
+// Forward over whole output rows (the ranges of conv_thin_wgrad_kernel, input
+// rows staged the same way): Z[p][o] = (sum over the taps of in(tap) W[o][t])
+// + b[o], then ReLU, as conv_thin_fwd_kernel (same MFMA blocks and k order:
+// tap j in lanes 0-31, tap J + j in lanes 32-63), but each tap is an LDS read
+// at a per-lane offset fixed for the whole launch.  Wave w takes range rows
+// w, w + 4, ..., each in blocks of 32 pixels.
+template <int CIN, int STRIDE>
+__global__ __launch_bounds__(256) void conv_thin_fwd_rows_kernel(ConvArgs a) {
+  extern __shared__ float x_s[];
+  constexpr int KT = 9 * CIN, J = (KT + 1) / 2;
+  const int z = blockIdx.y;
+  const int R = thin_rows_per_range(a), wop = thin_wo_pad(a), width = thin_row_width(a);
+  const int per_row = width * CIN;
+  const int rows_total = a.B * a.Ho;
+  const int r0 = blockIdx.x * R;
+  const int nr_rows = rows_total - r0 < R ? rows_total - r0 : R;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+  const float* par = a.master_in + static_cast<int64_t>(a.order[z]) * a.master_in_slot;
+  const bool col_ok = l32 < a.Co;
+  float wv[J];
+  int toff[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int t = j + J * h;
+    wv[j] = *(col_ok && t < KT ? par + a.w_off + static_cast<int64_t>(l32) * KT + t
+                               : k_conv_zero);
+    const int rs = h ? tap_rs(j + J, CIN) : tap_rs(j, CIN);
+    const int c = h ? tap_c(j + J, CIN) : tap_c(j, CIN);
+    const int r = rs / 3, sc = rs - 3 * r;
+    toff[j] = t < KT ? (r * width + sc) * CIN + c : 0;  // padding taps have zero weights
+  }
+  const float bias = *(col_ok ? par + a.b_off + l32 : k_conv_zero);
+  thin_stage<CIN, STRIDE>(a, z, r0, R, nr_rows, per_row, x_s);
+  const int nj = wop / 32;
+  const int my_rows = nr_rows > wave ? (nr_rows - wave + 3) / 4 : 0;
+  float* out = a.out + z * a.out_slot;
+  for (int t = 0; t < my_rows * nj; ++t) {
+    const int q = wave + 4 * (t / nj), jb = t - (t / nj) * nj;
+    const float* xp = x_s + q * 3 * per_row + STRIDE * (32 * jb + l32) * CIN;
+    float xv[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) xv[j] = xp[toff[j]];
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(xv[j], wv[j], acc, 0, 0, 0);
+    // accumulator e of lane (l32, h): pixel 8 (e / 4) + 4 h + e % 4 of the block, channel l32
+    const int jlim = a.Wo - 32 * jb;
+    float* orow = out + (static_cast<int64_t>(r0 + q) * a.Wo + 32 * jb) * a.Co + l32;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int pj = 8 * (e >> 2) + 4 * h + (e & 3);
+      const float v = acc[e] + bias;
+      if (pj < jlim && col_ok) orow[pj * a.Co] = v > 0.0f ? v : 0.0f;
+    }
   }
 }
 
@@ -1188,6 +1255,20 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   }
   const Dims d = pass_dims(a, pass);
   if (n_slots < 1 || d.M < 1 || d.N < 1 || d.K < 1) return hipErrorInvalidValue;
+  if (pass == CONV_FWD && thin_wgrad(a)) {
+    const int R = thin_rows_per_range(a);
+    const dim3 grid(static_cast<unsigned>((a.B * a.Ho + R - 1) / R), n_slots), block(256);
+    const size_t lds = static_cast<size_t>(thin_stage_floats(a)) * sizeof(float);
+    switch (2 * a.C + (a.stride == 2 ? 1 : 0)) {
+      case 2: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<1, 1>), grid, block, lds, s, a); break;
+      case 3: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<1, 2>), grid, block, lds, s, a); break;
+      case 4: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<2, 1>), grid, block, lds, s, a); break;
+      case 5: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<2, 2>), grid, block, lds, s, a); break;
+      case 6: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<3, 1>), grid, block, lds, s, a); break;
+      default: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<3, 2>), grid, block, lds, s, a); break;
+    }
+    return hipGetLastError();
+  }
   if (pass == CONV_FWD && thin_layer(a)) {
     const int64_t blocks = (d.M + 4 * 32 * THIN_TB - 1) / (4 * 32 * THIN_TB);
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;

@@ -64,6 +64,10 @@ TRAJ = {
     # two input channels, a thin first layer of 4 output channels
     "two-ch": _cfg("cnn-two-ch", (7, 6, 2), ((4, 1), (8, 2)), K=2, n_rows=60, batch=6,
                    tau=(2, 3), rounds=2, seed=47),
+    # rows too wide for the first layer's staged input rows (1300 pixels):
+    # its per-pixel forward and the generic weight-gradient tiles
+    "wide-row": _cfg("cnn-wide-row", (2, 1300, 3), ((4, 1),), K=2, n_rows=8, batch=2,
+                     tau=(1, 2), rounds=1, seed=48),
     # a last conv output too large for the one-launch classifier head (32 x 32
     # x 16 per batch row): pooling, classifier and softmax as separate launches
     "big-head": _cfg("cnn-big-head", (32, 32, 3), ((16, 1),), K=2, n_rows=24, batch=3,
