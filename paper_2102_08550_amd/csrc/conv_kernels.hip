@@ -89,14 +89,59 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // stride 1; the class's one, two or four for stride 2.
 __device__ __forceinline__ void dgrad_tap(const ConvArgs& a, int t, int& r, int& s) {
   if (a.stride == 2) {
-    const int ns = cls_taps(a.cls & 1), tr = t / ns, ts = t - tr * ns;
+    const int oc = a.cls & 1, tr = t >> oc, ts = t - (tr << oc);  // cls_taps(oc) = 1 << oc
     r = (a.cls >> 1) ? 2 * tr : 1;
-    s = (a.cls & 1) ? 2 * ts : 1;
+    s = oc ? 2 * ts : 1;
   } else {
     r = t / 3;
     s = t - 3 * r;
   }
 }
+
+// A thread's K sequence k0, k0 + CK, k0 + 2 CK, ... split as k = q D + r:
+// one division when constructed, then next() steps by CK without dividing
+// (CK = dq D + dr, split once).
+struct KCursor {
+  int q, r, D, dq, dr;
+  __device__ KCursor(int k0, int D_) : D(D_) {
+    q = k0 / D;
+    r = k0 - q * D;
+    dq = CK / D;
+    dr = CK - dq * D;
+  }
+  __device__ __forceinline__ void next() {
+    r += dr;
+    q += dq;
+    const bool w = r >= D;
+    r = w ? r - D : r;
+    q = w ? q + 1 : q;
+  }
+};
+
+// The same for an output pixel k = (b Ho + i) Wo + j.
+struct PixCursor {
+  int b, i, j, Ho, Wo, di, dj;
+  __device__ PixCursor(int k0, int Ho_, int Wo_) : Ho(Ho_), Wo(Wo_) {
+    const int hw = Ho * Wo;
+    b = k0 / hw;
+    const int p = k0 - b * hw;
+    i = p / Wo;
+    j = p - i * Wo;
+    di = CK / Wo;
+    dj = CK - di * Wo;
+  }
+  __device__ __forceinline__ void next() {
+    j += dj;
+    i += di;
+    const bool w = j >= Wo;
+    j = w ? j - Wo : j;
+    i = w ? i + 1 : i;
+    while (i >= Ho) {  // once at most unless the image has fewer than CK / Wo + 1 rows
+      i -= Ho;
+      ++b;
+    }
+  }
+};
 
 // Loaders.  A thread gathers, per K step, four consecutive K elements of one
 // A row (m0 + t / 4) and of one B row (n0 + t / 4).  What depends only on
@@ -184,8 +229,9 @@ struct ConvLoader {
   // Forward with channel counts a multiple of 4: four consecutive K of the A
   // row are four channels of one input tap, of the B row four consecutive
   // weights; one 16-byte load each.
-  __device__ __forceinline__ void fwd_vec(int k, float (&ra)[4], float (&rb)[4]) const {
-    const int rs = k / a.C, c = k - rs * a.C, r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
+  __device__ __forceinline__ void fwd_vec(int k, const KCursor& kc, float (&ra)[4],
+                                          float (&rb)[4]) const {
+    const int rs = kc.q, c = kc.r, r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
     const bool aok = am && k < kend && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
     const f32x4 va =
         *reinterpret_cast<const f32x4*>(aok ? arow + (hi * a.W + wi) * a.C + c : k_conv_zero);
@@ -198,8 +244,8 @@ struct ConvLoader {
     }
   }
   // Backward-data A with output channels a multiple of 4 (see dgrad_a).
-  __device__ __forceinline__ void dgrad_a_vec(int k, float (&ra)[4]) const {
-    const int t = k / a.Co, o = k - t * a.Co;
+  __device__ __forceinline__ void dgrad_a_vec(int k, const KCursor& kc, float (&ra)[4]) const {
+    const int t = kc.q, o = kc.r;
     int r, sc;
     dgrad_tap_rs(t, r, sc);
     const int ti = ah - r, tj = aw - sc;
@@ -358,8 +404,8 @@ struct DgradWeightLoader {
   const float* Wt;
   __device__ DgradWeightLoader(const ConvArgs& a_, int kend_, int n, int N, const float* Wt_)
       : a(a_), kend(kend_), nq(n), bn(n < N), Wt(Wt_) {}
-  __device__ __forceinline__ void fetch(int k, float (&rb)[4]) const {
-    const int t = k / a.Co, o = k - t * a.Co;
+  __device__ __forceinline__ void fetch(int k, const KCursor& kc, float (&rb)[4]) const {
+    const int t = kc.q, o = kc.r;
     int r, sc;
     dgrad_tap(a, t, r, sc);
     const bool ok = bn && k < kend;
@@ -401,10 +447,10 @@ struct WgradLoader {
     bs = rs - 3 * br;
   }
 
-  __device__ __forceinline__ void fetch(int k, float (&ra)[4], float (&rb)[4]) const {
+  __device__ __forceinline__ void fetch(int k, const PixCursor& pc, float (&ra)[4],
+                                        float (&rb)[4]) const {
     const bool ok = k < kend;
-    const int kk = ok ? k : 0;  // a valid pixel to decode
-    const int hw = a.Ho * a.Wo, b = kk / hw, p = kk - b * hw, i = p / a.Wo, j = p - i * a.Wo;
+    const int b = ok ? pc.b : 0, i = pc.i, j = pc.j;  // a valid image past the end
     const f32x4 va = *reinterpret_cast<const f32x4*>(
         ok && arow_ok ? dz + static_cast<int64_t>(k) * a.Co + mq : k_conv_zero);
     const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
@@ -497,14 +543,23 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   typedef typename std::conditional<TRA, WgradLoader, ConvLoader<PASS>>::type Loader;
   const Loader ld(a, kend, m0 + lr, M, n0 + lrb, N, in, rows, dz, par + a.w_off);
   const DgradWeightLoader wl(a, kend, n0 + lrb, N, par + a.w_off);
+  // the vector loaders' K decode, stepped along with the loads (consecutive K steps)
+  KCursor ka(kbeg + lk, PASS == CONV_FWD ? a.C : a.Co), kb(kbeg + lkb, a.Co);
+  PixCursor pc(TRA ? kbeg + lk : 0, a.Ho > 0 ? a.Ho : 1, a.Wo > 0 ? a.Wo : 1);
   float ra[2][4], rb[2][4];
   auto load = [&](int k0, auto P) {
     constexpr int p = decltype(P)::value;
     if constexpr (TR && PASS == CONV_DGRAD) {
-      ld.dgrad_a_vec(k0 + lk, ra[p]);
-      wl.fetch(k0 + lkb, rb[p]);
+      ld.dgrad_a_vec(k0 + lk, ka, ra[p]);
+      wl.fetch(k0 + lkb, kb, rb[p]);
+      ka.next();
+      kb.next();
     } else if constexpr (TR && PASS == CONV_FWD) {
-      ld.fwd_vec(k0 + lk, ra[p], rb[p]);
+      ld.fwd_vec(k0 + lk, ka, ra[p], rb[p]);
+      ka.next();
+    } else if constexpr (TRA) {
+      ld.fetch(k0 + lk, pc, ra[p], rb[p]);
+      pc.next();
     } else {
       ld.fetch(k0 + lk, ra[p], rb[p]);
     }
@@ -630,11 +685,14 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
   const ConvLoader<CONV_DGRAD> ld1(a, K, m0 + lr + 64, M, n0, N, nullptr, nullptr, dz,
                                    par + a.w_off);
   const DgradWeightLoader wl(a, K, n0 + lrb, N, par + a.w_off);
+  KCursor ka(lk, a.Co), kb(lkb, a.Co);  // stepped along with the loads
   float ra0[4], ra1[4], rb[4];
   auto load = [&](int k0) {
-    ld0.dgrad_a_vec(k0 + lk, ra0);
-    ld1.dgrad_a_vec(k0 + lk, ra1);
-    if (bload) wl.fetch(k0 + lkb, rb);
+    ld0.dgrad_a_vec(k0 + lk, ka, ra0);
+    ld1.dgrad_a_vec(k0 + lk, ka, ra1);
+    if (bload) wl.fetch(k0 + lkb, kb, rb);
+    ka.next();
+    kb.next();
   };
   auto stash = [&](int buf) {
 #pragma unroll
