@@ -143,6 +143,38 @@ struct PixCursor {
   }
 };
 
+// Input pixels of consecutive backward-data rows (the class's pixel grid for
+// stride 2, the image for stride 1): decoded once, then stepped forward.
+struct DgradRowWalker {
+  const ConvArgs& a;
+  int b, i, j, rows, cols;
+  __device__ DgradRowWalker(const ConvArgs& a_, int m) : a(a_) {
+    rows = a.stride == 2 ? cls_rows(a) : a.H;
+    cols = a.stride == 2 ? cls_cols(a) : a.W;
+    const int hw = rows * cols;
+    b = m / hw;
+    const int p = m - b * hw;
+    i = p / cols;
+    j = p - i * cols;
+  }
+  __device__ __forceinline__ void advance(int d) {
+    j += d;
+    while (j >= cols) {
+      j -= cols;
+      if (++i == rows) {
+        i = 0;
+        ++b;
+      }
+    }
+  }
+  // offset of channel 0 of the pixel in [B][H][W][C]
+  __device__ __forceinline__ int64_t offset() const {
+    const int hi = a.stride == 2 ? 2 * i + (a.cls >> 1) : i;
+    const int wi = a.stride == 2 ? 2 * j + (a.cls & 1) : j;
+    return ((static_cast<int64_t>(b) * a.H + hi) * a.W + wi) * a.C;
+  }
+};
+
 // Loaders.  A thread gathers, per K step, four consecutive K elements of one
 // A row (m0 + t / 4) and of one B row (n0 + t / 4).  What depends only on
 // the row (the pixel's image and position, or the weight tap of a column) is
@@ -611,6 +643,19 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 
   // accumulator i of lane (r, h): row 8 (i / 4) + 4 h + i % 4, column r
   const int col = n0 + wn * 32 + r;
+  if constexpr (PASS == CONV_DGRAD) {
+    // the rows' input pixels by stepping: +1 within a group of four, +5 between
+    DgradRowWalker wk(a, m0 + wm * 32 + 4 * h);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i > 0) wk.advance((i & 3) ? 1 : 5);
+      const int row = m0 + wm * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+      if (row >= M || col >= N) continue;
+      const int64_t at = wk.offset() + col;
+      a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? acc[i] : 0.0f;
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int row = m0 + wm * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
@@ -621,11 +666,6 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       a.out[z * a.out_slot + static_cast<int64_t>(row) * a.Co + col] = zv > 0.0f ? zv : 0.0f;
     } else if constexpr (PASS == FC_FWD) {
       a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v + par[a.b_off + col];
-    } else if constexpr (PASS == CONV_DGRAD) {
-      int b, hi, wi;
-      ConvLoader<PASS>::dgrad_pixel(a, row, b, hi, wi);
-      const int64_t at = ((static_cast<int64_t>(b) * a.H + hi) * a.W + wi) * a.C + col;
-      a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? v : 0.0f;
     } else if constexpr (PASS == FC_DGRAD) {
       a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v;
     } else {
@@ -722,13 +762,13 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
   }
 
   const int col = n0 + r;
+  DgradRowWalker wk(a, m0 + wave * 32 + 4 * h);  // stepped as in conv_gemm_kernel
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
+    if (i > 0) wk.advance((i & 3) ? 1 : 5);
     const int row = m0 + wave * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
     if (row >= M || col >= N) continue;
-    int b, hi, wi;
-    ConvLoader<CONV_DGRAD>::dgrad_pixel(a, row, b, hi, wi);
-    const int64_t at = ((static_cast<int64_t>(b) * a.H + hi) * a.W + wi) * a.C + col;
+    const int64_t at = wk.offset() + col;
     a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? acc[i] : 0.0f;
   }
 }
