@@ -98,16 +98,16 @@ __device__ __forceinline__ void dgrad_tap(const ConvArgs& a, int t, int& r, int&
   }
 }
 
-// A thread's K sequence k0, k0 + CK, k0 + 2 CK, ... split as k = q D + r:
-// one division when constructed, then next() steps by CK without dividing
-// (CK = dq D + dr, split once).
+// A thread's K sequence k0, k0 + CK, k0 + 2 CK, ... (or another step) split
+// as k = q D + r: one division when constructed, then next() steps without
+// dividing (step = dq D + dr, split once).
 struct KCursor {
   int q, r, D, dq, dr;
-  __device__ KCursor(int k0, int D_) : D(D_) {
+  __device__ KCursor(int k0, int D_, int step = CK) : D(D_) {
     q = k0 / D;
     r = k0 - q * D;
-    dq = CK / D;
-    dr = CK - dq * D;
+    dq = step / D;
+    dr = step - dq * D;
   }
   __device__ __forceinline__ void next() {
     r += dr;
@@ -871,18 +871,21 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_kernel(ConvArgs a) {
 // dZ of the next block loaded while the current one is multiplied; the four
 // waves' sums are added in wave order.
 constexpr int THIN_WG_PIXELS = 512;   // a range's pixel slots (rows x padded width) at most
+// The forward's workgroups take the same ranges (ranges of 128 or 256 pixel
+// slots, more workgroups, ran the C6 layer 1 slower over a round).
+constexpr int THIN_FWD_PIXELS = THIN_WG_PIXELS;
 constexpr int THIN_STAGE_MAX = 11264;  // staged floats at most (44 KB, with red: under 64 KB)
 
 __host__ __device__ inline int thin_wo_pad(const ConvArgs& a) { return (a.Wo + 31) / 32 * 32; }
-__host__ __device__ inline int thin_rows_per_range(const ConvArgs& a) {
-  const int r = THIN_WG_PIXELS / thin_wo_pad(a);
+__host__ __device__ inline int thin_rows_per_range(const ConvArgs& a, int pixels = THIN_WG_PIXELS) {
+  const int r = pixels / thin_wo_pad(a);
   return r > 1 ? r : 1;
 }
 __host__ __device__ inline int thin_row_width(const ConvArgs& a) {
   return a.stride * thin_wo_pad(a) + 2;
 }
-__host__ __device__ inline int64_t thin_stage_floats(const ConvArgs& a) {
-  return static_cast<int64_t>(thin_rows_per_range(a)) * 3 * thin_row_width(a) * a.C;
+__host__ __device__ inline int64_t thin_stage_floats(const ConvArgs& a, int pixels = THIN_WG_PIXELS) {
+  return static_cast<int64_t>(thin_rows_per_range(a, pixels)) * 3 * thin_row_width(a) * a.C;
 }
 __host__ __device__ inline bool thin_wgrad(const ConvArgs& a) {
   return thin_layer(a) && (a.stride == 1 || a.stride == 2) && thin_stage_floats(a) <= THIN_STAGE_MAX;
@@ -914,15 +917,17 @@ __device__ __forceinline__ void thin_stage(const ConvArgs& a, int z, int r0, int
   }
   __syncthreads();
   const int n_stage = 3 * R * per_row;
+  KCursor ec(threadIdx.x, per_row, 256);  // element e = staged row q, column r
   for (int e0 = threadIdx.x; e0 < n_stage; e0 += 8 * 256) {
     float v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int e = e0 + 256 * u;
-      const int sr = e < n_stage ? e / per_row : 0, col = e - sr * per_row;
-      const int64_t off = src_s[sr];
+      const int col = ec.r;
+      const int64_t off = src_s[e < n_stage ? ec.q : 0];
       const bool ok = e < n_stage && off >= 0 && col >= CIN && col < (a.W + 1) * CIN;
       v[u] = *(ok ? in + off + (col - CIN) : k_conv_zero);  // staged column 0: padding
+      ec.next();
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u)
@@ -1014,7 +1019,8 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_rows_kernel(ConvArgs a) {
   extern __shared__ float x_s[];
   constexpr int KT = 9 * CIN, J = (KT + 1) / 2;
   const int z = blockIdx.y;
-  const int R = thin_rows_per_range(a), wop = thin_wo_pad(a), width = thin_row_width(a);
+  const int R = thin_rows_per_range(a, THIN_FWD_PIXELS), wop = thin_wo_pad(a);
+  const int width = thin_row_width(a);
   const int per_row = width * CIN;
   const int rows_total = a.B * a.Ho;
   const int r0 = blockIdx.x * R;
@@ -1354,9 +1360,9 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   const Dims d = pass_dims(a, pass);
   if (n_slots < 1 || d.M < 1 || d.N < 1 || d.K < 1) return hipErrorInvalidValue;
   if (pass == CONV_FWD && thin_wgrad(a)) {
-    const int R = thin_rows_per_range(a);
+    const int R = thin_rows_per_range(a, THIN_FWD_PIXELS);
     const dim3 grid(static_cast<unsigned>((a.B * a.Ho + R - 1) / R), n_slots), block(256);
-    const size_t lds = static_cast<size_t>(thin_stage_floats(a)) * sizeof(float);
+    const size_t lds = static_cast<size_t>(thin_stage_floats(a, THIN_FWD_PIXELS)) * sizeof(float);
     switch (2 * a.C + (a.stride == 2 ? 1 : 0)) {
       case 2: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<1, 1>), grid, block, lds, s, a); break;
       case 3: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<1, 2>), grid, block, lds, s, a); break;
