@@ -57,7 +57,7 @@ struct ConvArgs {
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s);
 
 // Output pixels per weight-gradient range of the 64 x 64 conv tiles.
-constexpr int CONV_WGRAD_PIXELS = 512;
+constexpr int CONV_WGRAD_PIXELS = 256;
 
 // The K ranges a CONV_WGRAD launch of these sizes expects (ConvArgs.splits,
 // ConvArgs.k_per_split): ranges of CONV_WGRAD_PIXELS output pixels, or, for
