@@ -47,7 +47,7 @@ struct ConvArgs {
   int64_t out_slot, out_ld;
   const float* mask;      // CONV_DGRAD: the input activation (ReLU mask, > 0)
   int64_t mask_slot;
-  float* part;            // WGRAD: partial sums [slot][split][Co][N]
+  float* part;            // WGRAD: partial sums [slot][split][Co][N] (launch_conv_updates)
   int64_t part_slot;
   int splits;             // WGRAD: number of K ranges (of output pixels, output rows of layers
   int64_t k_per_split;    // with at most 3 input channels, or batch rows; conv_wgrad_ranges)
@@ -66,12 +66,6 @@ constexpr int CONV_WGRAD_PIXELS = 256;
 // the row width rounded up to 32).
 void conv_wgrad_ranges(const ConvArgs& a, int* splits, int64_t* k_per_split);
 
-// WGRAD epilogue: sum the partials of each weight (eight groups of
-// consecutive splits, each in split order, the group sums in order), then the
-// SGD update master <- master - lr sum (W) and the bias from the last column;
-// master[order[z]] with stride master_slot; reads master_in like ConvArgs.
-hipError_t launch_conv_update(const ConvArgs& a, ConvPass pass, float* master,
-                              int64_t master_slot, float lr, int n_slots, hipStream_t s);
 
 // pooled[z][b][c] = (sum over the H W positions of act[z][b][.][c]: eight
 // groups of consecutive positions, each in position order, the group sums in
@@ -118,10 +112,28 @@ bool conv_head_fits(int HW, int C, int classes);
 // classifier's input to its weight gradient) and dz.
 hipError_t launch_conv_head(const HeadArgs& h, int n_slots, hipStream_t s);
 
-// The classifier's weight gradient from pooled and delta (the batch in
-// eight groups of consecutive rows, each in row order, the group sums in
-// order) and its SGD update: master[order[z]] <- master_in - lr dW.
-hipError_t launch_conv_head_update(const HeadArgs& h, float* master, int64_t master_slot,
-                                   float lr, int n_slots, hipStream_t s);
+// One layer's parameters for launch_conv_updates: W [M][N - 1] at w_off and
+// the bias [M] at b_off of the flat replica, and their gradient as
+// weight-gradient partials [slot][split][M][N] (bias last; slot stride
+// part_slot), or, with part == nullptr, the classifier's gradient formed from
+// HeadArgs' pooled and delta (M = classes, N = C + 1).
+struct UpdateBlock {
+  const float* part;
+  int64_t part_slot;
+  int splits, M, N;
+  int64_t w_off, b_off;
+};
+constexpr int MAX_UPDATE_BLOCKS = 4;
+
+// The SGD updates of up to MAX_UPDATE_BLOCKS layers in one launch (after every
+// backward-data launch that reads their weights): each gradient summed in a
+// fixed order (partials: eight groups of consecutive ranges, each in range
+// order, the group sums in order; the classifier's: eight groups of
+// consecutive batch rows likewise), then master[order[z]] <- master_in - lr
+// gradient (master_in likewise by order[z]).
+hipError_t launch_conv_updates(const UpdateBlock* blocks, int n_blocks, const HeadArgs* head,
+                               const float* master_in, int64_t master_in_slot, const int32_t* order,
+                               float* master, int64_t master_slot, float lr, int n_slots,
+                               hipStream_t s);
 
 }  // namespace oscars

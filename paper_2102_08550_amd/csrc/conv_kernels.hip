@@ -1068,40 +1068,79 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_rows_kernel(ConvArgs a) {
   }
 }
 
-// Sum of the partials of weight (m, n), then master <- master_in - lr sum:
-// W[m][n] for n < N - 1, the bias b[m] for the last column.  The ranges are
-// summed in UG groups of consecutive ranges, each group in range order by one
-// thread, then the group sums in group order; the order depends on the number
-// of ranges only, not on how many replicas share the launch.  A workgroup
-// takes UW consecutive weights (a half-wave's loads read consecutive partials
-// of one range).
+// All SGD updates of one local step in one launch, after every layer's
+// backward-data has read its weights.  Block j of u is a layer's weights
+// W[m][n] (n < N - 1) and bias b[m] (n = N - 1); a workgroup takes UW
+// consecutive weights of one block.  The gradient of weight (m, n) is
+//   with partials (a weight-gradient launch's ranges): the sum of the
+//     ranges' partials in UG groups of consecutive ranges, each group in
+//     range order by one thread (sixteen partials loaded at a time), then
+//     the group sums in group order;
+//   without (the classifier after conv_head_kernel): the sum over the batch
+//     of delta[b][m] pooled[b][n] (pooled = 1 for the bias) in UG groups of
+//     consecutive rows, each in row order, then the group sums in order.
+// The order depends on the sizes only, not on how many replicas share the
+// launch.  master[order[z]] <- master_in[order[z]] - lr (gradient).
 constexpr int UW = 32, UG = 8;
 static_assert(UW * UG == 256, "one thread per (weight, group)");
 
-template <int PASS>
-__global__ __launch_bounds__(256) void conv_update_kernel(ConvArgs a, float* master,
-                                                          int64_t master_slot, float lr) {
-  const Dims d = pass_dims(a, PASS);
+struct UpdateAll {
+  UpdateBlock blk[MAX_UPDATE_BLOCKS];
+  int64_t first[MAX_UPDATE_BLOCKS + 1];  // first workgroup of each block
+  int n;
+  const float* master_in;
+  int64_t master_in_slot;
+  const int32_t* order;
+};
+
+__global__ __launch_bounds__(256) void conv_update_all_kernel(UpdateAll u, HeadArgs h,
+                                                              float* master, int64_t master_slot,
+                                                              float lr) {
+  int j = 0;
+  while (j + 1 < u.n && blockIdx.x >= u.first[j + 1]) ++j;
+  const UpdateBlock ub = u.blk[j];
   const int z = blockIdx.y;
-  const int rep = a.order[z];
-  const int64_t MN = d.M * d.N;
+  const int rep = u.order[z];
+  const int64_t MN = static_cast<int64_t>(ub.M) * ub.N;
   const int w = threadIdx.x % UW, grp = threadIdx.x / UW;
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * UW + w;
-  const int per = (a.splits + UG - 1) / UG;
-  const int s0 = grp * per, s1 = min(a.splits, s0 + per);
-  const float* part = a.part + z * a.part_slot;
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) - u.first[j]) * UW + w;
+  const int64_t m = e / ub.N, n = e - m * ub.N;
   float sum = 0.0f;
   if (e < MN) {
-    // sixteen partials loaded at a time, then added in range order
-    int s = s0;
-    for (; s + 16 <= s1; s += 16) {
-      float v[16];
+    if (ub.part) {
+      const int per = (ub.splits + UG - 1) / UG;
+      const int s0 = grp * per, s1 = min(ub.splits, s0 + per);
+      const float* part = ub.part + z * ub.part_slot;
+      int sp = s0;
+      for (; sp + 16 <= s1; sp += 16) {
+        float v[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = part[(s + u) * MN + e];
+        for (int q = 0; q < 16; ++q) v[q] = part[(sp + q) * MN + e];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) sum += v[u];
+        for (int q = 0; q < 16; ++q) sum += v[q];
+      }
+      for (; sp < s1; ++sp) sum += part[sp * MN + e];
+    } else {
+      const int per = (h.B + UG - 1) / UG;
+      const int b0 = grp * per, b1 = min(h.B, b0 + per);
+      const float* dcol = h.delta + z * h.delta_slot + m;
+      // the bias column reads ones
+      const float* pcol = n < ub.N - 1 ? h.pooled + z * h.pooled_slot + n : k_conv_one;
+      const int64_t ps = n < ub.N - 1 ? ub.N - 1 : 0;
+      int bb = b0;
+      for (; bb + 8 <= b1; bb += 8) {
+        float dv[8], pv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          dv[q] = dcol[static_cast<int64_t>(bb + q) * h.delta_ld];
+          pv[q] = pcol[(bb + q) * ps];
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sum = fmaf(dv[q], pv[q], sum);
+      }
+      for (; bb < b1; ++bb)
+        sum = fmaf(dcol[static_cast<int64_t>(bb) * h.delta_ld], pcol[bb * ps], sum);
     }
-    for (; s < s1; ++s) sum += part[s * MN + e];
   }
   __shared__ float group_sum[UG][UW];
   group_sum[grp][w] = sum;
@@ -1110,10 +1149,9 @@ __global__ __launch_bounds__(256) void conv_update_kernel(ConvArgs a, float* mas
   float tot = group_sum[0][w];
 #pragma unroll
   for (int g = 1; g < UG; ++g) tot += group_sum[g][w];
-  const int64_t m = e / d.N, n = e % d.N;
-  const float* src = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
+  const float* src = u.master_in + static_cast<int64_t>(rep) * u.master_in_slot;
   float* dst = master + static_cast<int64_t>(rep) * master_slot;
-  const int64_t at = n < d.N - 1 ? a.w_off + m * (d.N - 1) + n : a.b_off + m;
+  const int64_t at = n < ub.N - 1 ? ub.w_off + m * (ub.N - 1) + n : ub.b_off + m;
   dst[at] = fmaf(-lr, tot, src[at]);
 }
 
@@ -1265,59 +1303,6 @@ __global__ __launch_bounds__(256) void conv_head_kernel(HeadArgs h) {
   }
 }
 
-// The classifier's weight gradient and update: weight e = (o, c) of the
-// classes x (C + 1) matrix (c = C: the bias) takes
-// sum_b delta[b][o] pooled[b][c] (pooled = 1 for the bias) over the batch in
-// HG groups of consecutive rows, each in row order by one thread, then the
-// group sums in group order; master <- master_in - lr sum.
-constexpr int HW32 = 32, HG = 8;
-static_assert(HW32 * HG == 256, "one thread per (weight, group)");
-
-__global__ __launch_bounds__(256) void conv_head_update_kernel(HeadArgs h, float* master,
-                                                               int64_t master_slot, float lr) {
-  const int z = blockIdx.y;
-  const int N = h.C + 1;
-  const int w = threadIdx.x % HW32, grp = threadIdx.x / HW32;
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * HW32 + w;
-  const int64_t MN = static_cast<int64_t>(h.classes) * N;
-  const int per = (h.B + HG - 1) / HG;
-  const int b0 = grp * per, b1 = min(h.B, b0 + per);
-  float sum = 0.0f;
-  if (e < MN) {
-    const int o = static_cast<int>(e / N), c = static_cast<int>(e - static_cast<int64_t>(o) * N);
-    const float* dcol = h.delta + z * h.delta_slot + o;
-    // the bias column reads ones
-    const float* pcol = c < h.C ? h.pooled + z * h.pooled_slot + c : k_conv_one;
-    const int64_t ps = c < h.C ? h.C : 0;
-    int bb = b0;
-    for (; bb + 8 <= b1; bb += 8) {
-      float dv[8], pv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        dv[u] = dcol[static_cast<int64_t>(bb + u) * h.delta_ld];
-        pv[u] = pcol[(bb + u) * ps];
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) sum = fmaf(dv[u], pv[u], sum);
-    }
-    for (; bb < b1; ++bb)
-      sum = fmaf(dcol[static_cast<int64_t>(bb) * h.delta_ld], pcol[bb * ps], sum);
-  }
-  __shared__ float group_sum[HG][HW32];
-  group_sum[grp][w] = sum;
-  __syncthreads();
-  if (grp != 0 || e >= MN) return;
-  float tot = group_sum[0][w];
-#pragma unroll
-  for (int g = 1; g < HG; ++g) tot += group_sum[g][w];
-  const int o = static_cast<int>(e / N), c = static_cast<int>(e - static_cast<int64_t>(o) * N);
-  const int rep = h.order[z];
-  const float* src = h.master_in + static_cast<int64_t>(rep) * h.master_in_slot;
-  float* dst = master + static_cast<int64_t>(rep) * master_slot;
-  const int64_t at = c < h.C ? h.w_off + static_cast<int64_t>(o) * h.C + c : h.b_off + o;
-  dst[at] = fmaf(-lr, tot, src[at]);
-}
-
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
@@ -1435,17 +1420,32 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_conv_update(const ConvArgs& a, ConvPass pass, float* master,
-                              int64_t master_slot, float lr, int n_slots, hipStream_t s) {
-  if (pass != CONV_WGRAD && pass != FC_WGRAD) return hipErrorInvalidValue;
-  const Dims d = pass_dims(a, pass);
-  const int64_t blocks = (d.M * d.N + UW - 1) / UW;
-  if (blocks > 0x7FFFFFFF || n_slots < 1 || a.splits < 1) return hipErrorInvalidValue;
-  const dim3 grid(static_cast<unsigned>(blocks), n_slots), block(256);
-  if (pass == CONV_WGRAD)
-    hipLaunchKernelGGL(conv_update_kernel<CONV_WGRAD>, grid, block, 0, s, a, master, master_slot, lr);
-  else
-    hipLaunchKernelGGL(conv_update_kernel<FC_WGRAD>, grid, block, 0, s, a, master, master_slot, lr);
+hipError_t launch_conv_updates(const UpdateBlock* blocks, int n_blocks, const HeadArgs* head,
+                               const float* master_in, int64_t master_in_slot, const int32_t* order,
+                               float* master, int64_t master_slot, float lr, int n_slots,
+                               hipStream_t s) {
+  if (n_blocks < 1 || n_blocks > MAX_UPDATE_BLOCKS || n_slots < 1) return hipErrorInvalidValue;
+  UpdateAll u{};
+  u.n = n_blocks;
+  u.master_in = master_in;
+  u.master_in_slot = master_in_slot;
+  u.order = order;
+  HeadArgs h{};
+  int64_t total = 0;
+  for (int j = 0; j < n_blocks; ++j) {
+    const UpdateBlock& b = blocks[j];
+    if (b.M < 1 || b.N < 2) return hipErrorInvalidValue;
+    if (b.part ? b.splits < 1 : (!head || head->B < 1 || head->classes != b.M || head->C + 1 != b.N))
+      return hipErrorInvalidValue;
+    u.blk[j] = b;
+    u.first[j] = total;
+    total += (static_cast<int64_t>(b.M) * b.N + UW - 1) / UW;
+  }
+  u.first[n_blocks] = total;
+  if (head) h = *head;
+  if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_update_all_kernel, dim3(static_cast<unsigned>(total), n_slots),
+                     dim3(256), 0, s, u, h, master, master_slot, lr);
   return hipGetLastError();
 }
 
@@ -1480,17 +1480,6 @@ hipError_t launch_conv_head(const HeadArgs& h, int n_slots, hipStream_t s) {
   const size_t lds = (static_cast<size_t>(h.HW) * h.C + 2 * h.C + h.classes) * sizeof(float);
   hipLaunchKernelGGL(conv_head_kernel, dim3(static_cast<unsigned>(h.B), n_slots), dim3(256), lds, s,
                      h);
-  return hipGetLastError();
-}
-
-hipError_t launch_conv_head_update(const HeadArgs& h, float* master, int64_t master_slot,
-                                   float lr, int n_slots, hipStream_t s) {
-  if (n_slots < 1 || h.B < 1 || h.C < 1 || h.classes < 1) return hipErrorInvalidValue;
-  const int64_t MN = static_cast<int64_t>(h.classes) * (h.C + 1);
-  const int64_t blocks = (MN + HW32 - 1) / HW32;
-  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(conv_head_update_kernel, dim3(static_cast<unsigned>(blocks), n_slots),
-                     dim3(256), 0, s, h, master, master_slot, lr);
   return hipGetLastError();
 }
 

@@ -136,8 +136,9 @@ struct oscars_ctx {
   std::vector<float*> cact, cdz;   // [K][max_batch][h][w][c] per conv layer (1..L-1)
   float* pooled = nullptr;         // [K][max_batch][c of layer L-1]
   float* dpooled = nullptr;
-  float* cpart = nullptr;          // weight-gradient partials [K][part slot]
-  int64_t cpart_slot = 0;
+  float* cpart = nullptr;          // weight-gradient partials, one region per layer
+  std::vector<float*> cpart_l;     // layer l's region [K][cpart_slot_l[l]] (l = 1..L; L: the
+  std::vector<int64_t> cpart_slot_l;  // classifier), kept until the step's updates
   int64_t cnn_slot(int l) const {
     return static_cast<int64_t>(max_batch) * img_h[l] * img_w[l] * img_c[l];
   }
@@ -453,8 +454,12 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
     delete c;
     return OSCARS_E_NOMEM;
   }
-  // weight-gradient partials per slot: the largest layer's splits x outputs
-  int64_t part = static_cast<int64_t>(m->classes) * (c->img_c[Lc] + 1);
+  // weight-gradient partials per slot and layer: splits x outputs (all layers'
+  // partials of a step live until its updates, which run after every
+  // backward-data launch)
+  c->cpart_l.assign(Lc + 2, nullptr);
+  c->cpart_slot_l.assign(Lc + 2, 0);
+  c->cpart_slot_l[Lc + 1] = round_up(static_cast<int64_t>(m->classes) * (c->img_c[Lc] + 1), 64);
   for (int l = 1; l <= Lc; ++l) {
     ConvArgs a{};
     a.B = max_batch;
@@ -468,9 +473,10 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
     int splits = 0;
     int64_t per = 0;
     conv_wgrad_ranges(a, &splits, &per);
-    part = std::max<int64_t>(part, static_cast<int64_t>(splits) * a.Co * (9LL * a.C + 1));
+    c->cpart_slot_l[l] = round_up(static_cast<int64_t>(splits) * a.Co * (9LL * a.C + 1), 64);
   }
-  c->cpart_slot = round_up(part, 64);
+  int64_t part_total = 0;
+  for (int l = 1; l <= Lc + 1; ++l) part_total += c->cpart_slot_l[l];
 
   hipError_t e = hipGetDevice(&c->device);
   if (e == hipSuccess) e = scratch_address(c->device, &c->noalloc_scratch);
@@ -491,8 +497,13 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
   c->logits = static_cast<float*>(p);
   if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(K) * c->act_slot(c->L) * 4, &p);
   c->delta[c->L] = p;
-  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(K) * c->cpart_slot * 4, &p);
+  if (e == hipSuccess) e = dev_alloc(c, static_cast<size_t>(K) * part_total * 4, &p);
   c->cpart = static_cast<float*>(p);
+  int64_t part_off = 0;
+  for (int l = 1; l <= Lc + 1 && e == hipSuccess; ++l) {
+    c->cpart_l[l] = c->cpart + part_off;
+    part_off += static_cast<int64_t>(K) * c->cpart_slot_l[l];
+  }
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming);
   if (e == hipSuccess) {
     const int64_t rows = static_cast<int64_t>(K) * kPreTau * max_batch;
@@ -649,12 +660,14 @@ hipError_t cnn_forward(oscars_ctx* c, const float* master_in, int64_t master_in_
 
 // One local step of every active slot of the convolutional model after its
 // forward pass and loss gradient (in c->delta[L]): classifier backward-data
-// and update, pooling backward with the last ReLU mask, then per conv layer
-// (top down) backward-data (masked by the layer below) and the weight update.
-// With `head` (conv_head_kernel ran instead of the pooling, classifier and
-// softmax launches, and already wrote the gradient at the last conv output),
-// the classifier's update alone precedes the conv layers.
-// Backward-data of a layer reads its weights before its update writes them.
+// and weight-gradient partials, pooling backward with the last ReLU mask,
+// then per conv layer (top down) backward-data (masked by the layer below)
+// and its weight-gradient partials; last, the SGD updates of all layers in
+// launches of up to MAX_UPDATE_BLOCKS layers, after every backward-data launch
+// has read the weights they overwrite.  With `head` (conv_head_kernel ran
+// instead of the pooling, classifier and softmax launches and already wrote
+// the gradient at the last conv output), the classifier's update forms its
+// gradient from pooled and delta.
 hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
                         int64_t master_in_slot, const int32_t* order, const void* x,
                         const int32_t* rows, int64_t rows_slot, int B, int ns, float lr,
@@ -663,38 +676,41 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
   const int Cl = c->img_c[L - 1], HW = c->img_h[L - 1] * c->img_w[L - 1];
   const int64_t pslot = static_cast<int64_t>(c->max_batch) * Cl;
   hipError_t e = hipSuccess;
-  if (head) {
-    // conv_head_kernel left the gradient at the last conv output in cdz[L - 1]
-    e = timed(c, OSCARS_KERNEL_WGRAD, [&] {
-      return launch_conv_head_update(*head, replicas, c->n_pad, lr, ns, c->stream);
-    });
-  } else {
+  std::vector<UpdateBlock> upd;
+  {
     ConvArgs a = conv_layer_args(c, L, master_in, master_in_slot, order, B);
-    a.in = c->pooled;
-    a.in_slot = pslot;
-    a.dout = static_cast<const float*>(c->delta[L]);
-    a.dout_slot = c->act_slot(L);
-    a.dout_ld = c->ld[L];
-    a.out = c->dpooled;
-    a.out_slot = pslot;
-    a.out_ld = Cl;
-    e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, FC_DGRAD, ns, c->stream); });
-    a.part = c->cpart;
-    a.part_slot = c->cpart_slot;
-    a.splits = 1;
-    a.k_per_split = B;
-    if (e == hipSuccess)
-      e = timed(c, OSCARS_KERNEL_WGRAD, [&] {
-        hipError_t r = launch_conv(a, FC_WGRAD, ns, c->stream);
-        return r == hipSuccess ? launch_conv_update(a, FC_WGRAD, replicas, c->n_pad, lr, ns, c->stream)
-                               : r;
-      });
+    UpdateBlock u{};
+    u.M = a.Co;
+    u.N = a.C + 1;
+    u.w_off = a.w_off;
+    u.b_off = a.b_off;
+    if (!head) {
+      a.in = c->pooled;
+      a.in_slot = pslot;
+      a.dout = static_cast<const float*>(c->delta[L]);
+      a.dout_slot = c->act_slot(L);
+      a.dout_ld = c->ld[L];
+      a.out = c->dpooled;
+      a.out_slot = pslot;
+      a.out_ld = Cl;
+      e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, FC_DGRAD, ns, c->stream); });
+      a.part = c->cpart_l[L];
+      a.part_slot = c->cpart_slot_l[L];
+      a.splits = 1;
+      a.k_per_split = B;
+      if (e == hipSuccess)
+        e = timed(c, OSCARS_KERNEL_WGRAD, [&] { return launch_conv(a, FC_WGRAD, ns, c->stream); });
+      if (e == hipSuccess)
+        e = timed(c, OSCARS_KERNEL_DGRAD, [&] {
+          return launch_avgpool_backward(c->dpooled, pslot, c->cact[L - 1], c->cnn_slot(L - 1),
+                                         c->cdz[L - 1], B, HW, Cl, ns, c->stream);
+        });
+      u.part = a.part;
+      u.part_slot = a.part_slot;
+      u.splits = 1;
+    }
+    upd.push_back(u);
   }
-  if (e == hipSuccess && !head)
-    e = timed(c, OSCARS_KERNEL_DGRAD, [&] {
-      return launch_avgpool_backward(c->dpooled, pslot, c->cact[L - 1], c->cnn_slot(L - 1),
-                                     c->cdz[L - 1], B, HW, Cl, ns, c->stream);
-    });
   for (int l = L - 1; l >= 1 && e == hipSuccess; --l) {
     ConvArgs a = conv_layer_args(c, l, master_in, master_in_slot, order, B);
     a.dout = c->cdz[l];
@@ -717,12 +733,24 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
       a.gather_slot = rows_slot;
     }
     conv_wgrad_ranges(a, &a.splits, &a.k_per_split);
-    a.part = c->cpart;
-    a.part_slot = c->cpart_slot;
+    a.part = c->cpart_l[l];
+    a.part_slot = c->cpart_slot_l[l];
+    e = timed(c, OSCARS_KERNEL_WGRAD, [&] { return launch_conv(a, CONV_WGRAD, ns, c->stream); });
+    UpdateBlock u{};
+    u.part = a.part;
+    u.part_slot = a.part_slot;
+    u.splits = a.splits;
+    u.M = a.Co;
+    u.N = 9 * a.C + 1;
+    u.w_off = a.w_off;
+    u.b_off = a.b_off;
+    upd.push_back(u);
+  }
+  for (size_t i = 0; i < upd.size() && e == hipSuccess; i += MAX_UPDATE_BLOCKS) {
+    const int n = static_cast<int>(std::min<size_t>(MAX_UPDATE_BLOCKS, upd.size() - i));
     e = timed(c, OSCARS_KERNEL_WGRAD, [&] {
-      hipError_t r = launch_conv(a, CONV_WGRAD, ns, c->stream);
-      return r == hipSuccess ? launch_conv_update(a, CONV_WGRAD, replicas, c->n_pad, lr, ns, c->stream)
-                             : r;
+      return launch_conv_updates(upd.data() + i, n, head, master_in, master_in_slot, order, replicas,
+                                 c->n_pad, lr, ns, c->stream);
     });
   }
   return e;
