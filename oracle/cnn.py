@@ -11,6 +11,11 @@ Readings (the paper fixes no architecture or precision for this build):
   every side, stride s_l, a bias per output channel, then ReLU:
       Z[b, i, j, o] = bias[o] + sum_{r, s, c} Xpad[b, s_l i + r, s_l j + s, c] W[o, r, s, c]
   for i < H_out = (H - 1) // s_l + 1 (likewise j); W is stored [C_out][3][3][C_in];
+* a conv layer l may add the input of the layer before it (A_{l-2}, the
+  output of layer l - 2: the input of a two-layer block) to Z before the
+  ReLU, the identity shortcut of the residual blocks the paper's ResNet is
+  built from: Z_l = conv_l(A_{l-1}) + A_{l-2}; layers l - 1 and l then have
+  stride 1 and layer l as many channels as A_{l-2} (l >= 3);
 * the mean of every channel over all spatial positions of the last conv layer;
 * a fully connected classifier W [classes][C_L] with bias, whose outputs are
   the logits; mean softmax cross-entropy over the batch (as in ``mlp``);
@@ -25,10 +30,11 @@ gradient; with respect to its input it scatters the output gradient back
 through the same kernel taps).
 
 Pinned by tests: the convolution against ``torch.nn.functional.conv2d``
-(float64, NCHW), gradients against central finite differences on a tiny
-network, and one SGD step against ``torch.optim.SGD`` on an
-``nn.Conv2d``/``ReLU``/``AdaptiveAvgPool2d``/``Linear`` stack with
-``CrossEntropyLoss`` (CPU, float64).
+(float64, NCHW), gradients against central finite differences on tiny
+networks (with and without a shortcut), and one SGD step against
+``torch.optim.SGD`` on an ``nn.Conv2d``/``ReLU``/``AdaptiveAvgPool2d``/
+``Linear`` stack with ``CrossEntropyLoss``, with and without shortcuts (CPU,
+float64).
 """
 from __future__ import annotations
 
@@ -79,22 +85,33 @@ def conv_backward(X: np.ndarray, W: np.ndarray, dZ: np.ndarray, stride: int):
     return dXp[:, 1:H + 1, 1:Wd + 1, :], dW, flat.sum(axis=0)
 
 
-def _forward(params: Params, Xb: np.ndarray, image: Sequence[int], strides: Sequence[int]):
+def _skips(skips, n: int) -> List[bool]:
+    return [bool(v) for v in skips] if skips is not None else [False] * n
+
+
+def _forward(params: Params, Xb: np.ndarray, image: Sequence[int], strides: Sequence[int],
+             skips=None):
     H, Wd, C = image
     acts = [np.asarray(Xb, np.float64).reshape(-1, H, Wd, C)]
-    for (W, b), st in zip(params[:-1], strides):
-        acts.append(np.maximum(conv_forward(acts[-1], W, b, st), 0.0))
+    sk = _skips(skips, len(strides))
+    for li, ((W, b), st) in enumerate(zip(params[:-1], strides)):
+        Z = conv_forward(acts[-1], W, b, st)
+        if sk[li]:
+            Z = Z + acts[li - 1]  # the input of layer li - 1 (0-based): the block's input
+        acts.append(np.maximum(Z, 0.0))
     pooled = acts[-1].mean(axis=(1, 2))
     Wf, bf = params[-1]
     return acts, pooled, pooled @ Wf.T + bf
 
 
 def loss_and_grads(params: Params, Xb: np.ndarray, yb: Sequence[int], image: Sequence[int],
-                   strides: Sequence[int]):
+                   strides: Sequence[int], skips=None):
     """Mean softmax cross-entropy and its gradients at ``params`` = [conv
-    layers (W, b) ..., classifier (W, b)].  Returns (loss, grads)."""
+    layers (W, b) ..., classifier (W, b)].  ``skips``: per conv layer, whether
+    it adds its block's input (module docstring).  Returns (loss, grads)."""
     yb = np.asarray(yb, dtype=np.int64)
-    acts, pooled, logits = _forward(params, Xb, image, strides)
+    acts, pooled, logits = _forward(params, Xb, image, strides, skips)
+    sk = _skips(skips, len(strides))
     B = logits.shape[0]
     shift = logits - logits.max(axis=1, keepdims=True)
     expz = np.exp(shift)
@@ -108,8 +125,13 @@ def loss_and_grads(params: Params, Xb: np.ndarray, yb: Sequence[int], image: Seq
     grads[-1] = (delta.T @ pooled, delta.sum(axis=0))
     A = acts[-1]
     dA = np.broadcast_to((delta @ Wf)[:, None, None, :] / (A.shape[1] * A.shape[2]), A.shape)
+    extra = {}  # gradient reaching acts[k] through a shortcut
     for l in range(len(params) - 2, -1, -1):
+        if l + 1 in extra:
+            dA = dA + extra.pop(l + 1)
         dZ = dA * (acts[l + 1] > 0.0)
+        if sk[l]:
+            extra[l - 1] = dZ  # Z_l adds acts[l - 1]
         dX, dW, db = conv_backward(acts[l], params[l][0], dZ, strides[l])
         grads[l] = (dW, db)
         dA = dX
@@ -117,18 +139,18 @@ def loss_and_grads(params: Params, Xb: np.ndarray, yb: Sequence[int], image: Seq
 
 
 def sgd_step(params: Params, Xb: np.ndarray, yb: Sequence[int], lr: float,
-             image: Sequence[int], strides: Sequence[int]):
+             image: Sequence[int], strides: Sequence[int], skips=None):
     """x <- x - lr * g(x).  Returns the new parameters and the loss at x."""
-    loss, grads = loss_and_grads(params, Xb, yb, image, strides)
+    loss, grads = loss_and_grads(params, Xb, yb, image, strides, skips)
     return [(W - lr * dW, b - lr * db) for (W, b), (dW, db) in zip(params, grads)], loss
 
 
 def evaluate(params: Params, X: np.ndarray, y: Sequence[int], image: Sequence[int],
-             strides: Sequence[int]):
+             strides: Sequence[int], skips=None):
     """Held-out summed softmax cross-entropy and the number of rows whose
     label has the largest logit (ties count), as ``mlp.evaluate``."""
     y = np.asarray(y, dtype=np.int64)
-    _, _, logits = _forward(params, X, image, strides)
+    _, _, logits = _forward(params, X, image, strides, skips)
     n = logits.shape[0]
     top = logits.max(axis=1)
     shift = logits - top[:, None]
