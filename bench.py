@@ -103,7 +103,7 @@ def cnn_work(cfg, tau):
                                     "aggregate")}
     H, W, C = cfg.image
     geo = []
-    for co, st in cfg.conv:
+    for co, st, *_ in cfg.conv:
         Ho, Wo = (H - 1) // st + 1, (W - 1) // st + 1
         geo.append((H, W, C, Ho, Wo, co))
         H, W, C = Ho, Wo, co
@@ -223,7 +223,7 @@ def cpu_baseline(cfg, ds, init, tau, budget_s: float):
                 xb = workload.bf16_bits_to_f32(ds.x[rows]) if cfg.dtype == "bf16" else ds.x[rows]
                 if cfg.is_cnn:
                     x, _ = oracle.cnn.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr,
-                                               cfg.image, cfg.strides)
+                                               cfg.image, cfg.strides, cfg.skips)
                 else:
                     x, _ = oracle.sgd_step(x, xb.astype(np.float64), ds.y[rows], cfg.lr,
                                            cfg.dtype == "bf16")

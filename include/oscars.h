@@ -129,7 +129,13 @@ oscars_status oscars_create(oscars_ctx** out, const oscars_model* model, int32_t
  *   conv_strides   host [n_conv]: 1 or 2;
  *   classes   then every channel averaged over all positions, a linear
  *             classifier to `classes` logits (with bias), softmax cross-entropy
- *             averaged over the batch.
+ *             averaged over the batch;
+ *   conv_skip host [n_conv] or NULL (none): nonzero where conv layer l (1-based)
+ *             ends a residual block, the identity shortcut of the paper's
+ *             ResNet: the output of layer l - 2 (the block's input) is added to
+ *             Z before the ReLU.  Such a layer needs l >= 3, stride 1 for
+ *             layers l - 1 and l, as many channels as layer l - 2 and at least
+ *             4 input channels; else OSCARS_E_INVALID.
  * Flat parameter layout of one replica: [W_1 ([C_1][3][3][C_0]), b_1, ...,
  * W_n, b_n, W_fc ([classes][C_n]), b_fc], each segment starting on a
  * 64-element boundary (oscars_layer_offsets: layers 1 .. n_conv + 1).
@@ -142,6 +148,7 @@ typedef struct {
   const int32_t* conv_channels;
   const int32_t* conv_strides;
   int32_t classes;
+  const int32_t* conv_skip;
 } oscars_cnn_model;
 
 /* Create a context for K replicas of a convolutional model (see above), mini-

@@ -49,7 +49,8 @@ class _Model(ctypes.Structure):
 
 class _CnnModel(ctypes.Structure):
     _fields_ = [("height", _i32), ("width", _i32), ("channels", _i32), ("n_conv", _i32),
-                ("conv_channels", _P(_i32)), ("conv_strides", _P(_i32)), ("classes", _i32)]
+                ("conv_channels", _P(_i32)), ("conv_strides", _P(_i32)), ("classes", _i32),
+                ("conv_skip", _P(_i32))]
 
 
 class _Shards(ctypes.Structure):
@@ -247,8 +248,9 @@ def broadcast(global_, replicas, K: int, n: int, ld: int, stream=None):
 class Context:
     """K replicas of a ReLU MLP (dims = (d, h_1, ..., C)) and their workspace;
     or, with ``cnn = (image, conv)``, of the convolutional model: image =
-    (H, W, C), conv = ((out channels, stride), ...), dims = (H W C, classes),
-    fp32 (oscars_create_cnn)."""
+    (H, W, C), conv = ((out channels, stride[, shortcut]), ...), dims =
+    (H W C, classes), fp32 (oscars_create_cnn; shortcut: the layer adds the
+    output of the layer two before it)."""
 
     def __init__(self, dims: Sequence[int], dtype: int, K: int, max_batch: int, stream=None,
                  cnn=None):
@@ -263,14 +265,18 @@ class Context:
             _check(_lib().oscars_create(ctypes.byref(h), ctypes.byref(model), self.K,
                                         int(max_batch), _stream_handle(stream)), "oscars_create")
         else:
-            image, conv = [int(v) for v in cnn[0]], [(int(o), int(st)) for o, st in cnn[1]]
+            image = [int(v) for v in cnn[0]]
+            conv = [(int(c[0]), int(c[1]), int(c[2]) if len(c) > 2 else 0) for c in cnn[1]]
             if self.dtype != FP32 or len(self.dims) != 2 or len(image) != 3:
                 raise ValueError("convolutional models are fp32 with dims (H W C, classes)")
-            self._ch, chp = _arr([o for o, _ in conv], np.int32)
-            self._st, stp = _arr([st for _, st in conv], np.int32)
-            model = _CnnModel(image[0], image[1], image[2], len(conv), chp, stp, self.dims[-1])
+            self._ch, chp = _arr([c[0] for c in conv], np.int32)
+            self._st, stp = _arr([c[1] for c in conv], np.int32)
+            skp = None
+            if any(c[2] for c in conv):
+                self._sk, skp = _arr([c[2] for c in conv], np.int32)
+            model = _CnnModel(image[0], image[1], image[2], len(conv), chp, stp, self.dims[-1], skp)
             self.shapes, cin = [], image[2]
-            for o, _ in conv:
+            for o, *_ in conv:
                 self.shapes.append((o, 3, 3, cin))
                 cin = o
             self.shapes.append((self.dims[-1], cin))

@@ -47,6 +47,9 @@ struct ConvArgs {
   int64_t out_slot, out_ld;
   const float* mask;      // CONV_DGRAD: the input activation (ReLU mask, > 0)
   int64_t mask_slot;
+  const float* skip;      // residual shortcut or nullptr: CONV_FWD adds skip[p][o] to Z before
+  int64_t skip_slot;      // the ReLU (the block's input); CONV_DGRAD adds skip[q][c] to the
+                          // input gradient before the mask (the gradient at the block's end)
   float* part;            // WGRAD: partial sums [slot][split][Co][N] (launch_conv_updates)
   int64_t part_slot;
   int splits;             // WGRAD: number of K ranges (of output pixels, output rows of layers

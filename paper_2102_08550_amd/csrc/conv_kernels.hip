@@ -652,7 +652,8 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       const int row = m0 + wm * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
       if (row >= M || col >= N) continue;
       const int64_t at = wk.offset() + col;
-      a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? acc[i] : 0.0f;
+      const float g = a.skip ? acc[i] + a.skip[z * a.skip_slot + at] : acc[i];
+      a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? g : 0.0f;
     }
     return;
   }
@@ -662,8 +663,10 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     if (row >= M || col >= N) continue;
     const float v = acc[i];
     if constexpr (PASS == CONV_FWD) {
-      const float zv = v + par[a.b_off + col];
-      a.out[z * a.out_slot + static_cast<int64_t>(row) * a.Co + col] = zv > 0.0f ? zv : 0.0f;
+      const int64_t at = static_cast<int64_t>(row) * a.Co + col;
+      float zv = v + par[a.b_off + col];
+      if (a.skip) zv += a.skip[z * a.skip_slot + at];
+      a.out[z * a.out_slot + at] = zv > 0.0f ? zv : 0.0f;
     } else if constexpr (PASS == FC_FWD) {
       a.out[z * a.out_slot + static_cast<int64_t>(row) * a.out_ld + col] = v + par[a.b_off + col];
     } else if constexpr (PASS == FC_DGRAD) {
@@ -769,7 +772,8 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
     const int row = m0 + wave * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
     if (row >= M || col >= N) continue;
     const int64_t at = wk.offset() + col;
-    a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? acc[i] : 0.0f;
+    const float g = a.skip ? acc[i] + a.skip[z * a.skip_slot + at] : acc[i];
+    a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? g : 0.0f;
   }
 }
 
@@ -1306,6 +1310,10 @@ __global__ __launch_bounds__(256) void conv_head_kernel(HeadArgs h) {
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
+  // shortcuts: conv forward and backward-data on the 64 x 64 / 128 x 32 tiles only
+  if (a.skip && (pass == FC_FWD || pass == FC_DGRAD || pass == CONV_WGRAD || pass == FC_WGRAD ||
+                 (pass == CONV_FWD && thin_layer(a))))
+    return hipErrorInvalidValue;
   if (pass == CONV_DGRAD && dgrad_narrow(a)) {
     if (n_slots < 1 || a.cls > 3 || a.B < 1 || a.Co < 1 || (a.stride == 2 && a.cls < -1))
       return hipErrorInvalidValue;

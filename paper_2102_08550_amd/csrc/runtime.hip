@@ -133,6 +133,7 @@ struct oscars_ctx {
   // classifier is layer L.  geometry[l] for l = 0 (the image) .. L-1.
   bool cnn = false;
   std::vector<int> img_h, img_w, img_c, conv_stride;
+  std::vector<int> conv_skip;      // conv layer l adds the output of layer l - 2 (l = 1..L-1)
   std::vector<float*> cact, cdz;   // [K][max_batch][h][w][c] per conv layer (1..L-1)
   float* pooled = nullptr;         // [K][max_batch][c of layer L-1]
   float* dpooled = nullptr;
@@ -394,6 +395,11 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
   for (int l = 0; l < m->n_conv; ++l) {
     if (m->conv_channels[l] < 1 || m->conv_channels[l] > OSCARS_MAX_WIDTH) return OSCARS_E_INVALID;
     if (m->conv_strides[l] != 1 && m->conv_strides[l] != 2) return OSCARS_E_INVALID;
+    // a shortcut at 0-based layer l adds the output of layer l - 2 (1-based l - 1)
+    if (m->conv_skip && m->conv_skip[l] &&
+        (l < 2 || m->conv_strides[l] != 1 || m->conv_strides[l - 1] != 1 ||
+         m->conv_channels[l] != m->conv_channels[l - 2] || m->conv_channels[l - 1] < 4))
+      return OSCARS_E_INVALID;
   }
   oscars_ctx* c = new (std::nothrow) oscars_ctx();
   if (!c) return OSCARS_E_NOMEM;
@@ -413,6 +419,8 @@ oscars_status oscars_create_cnn(oscars_ctx** out, const oscars_cnn_model* m, int
   c->img_w.assign(Lc + 1, 0);
   c->img_c.assign(Lc + 1, 0);
   c->conv_stride.assign(Lc + 1, 1);
+  c->conv_skip.assign(Lc + 2, 0);
+  for (int l = 1; l <= Lc; ++l) c->conv_skip[l] = m->conv_skip && m->conv_skip[l - 1] ? 1 : 0;
   c->img_h[0] = m->height;
   c->img_w[0] = m->width;
   c->img_c[0] = m->channels;
@@ -634,6 +642,10 @@ hipError_t cnn_forward(oscars_ctx* c, const float* master_in, int64_t master_in_
       a.in = c->cact[l - 1];
       a.in_slot = c->cnn_slot(l - 1);
     }
+    if (c->conv_skip[l]) {  // the residual block's input
+      a.skip = c->cact[l - 2];
+      a.skip_slot = c->cnn_slot(l - 2);
+    }
     a.out = c->cact[l];
     a.out_slot = c->cnn_slot(l);
     e = timed(c, OSCARS_KERNEL_FWD, [&] { return launch_conv(a, CONV_FWD, ns, c->stream); });
@@ -720,10 +732,15 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
       a.out_slot = c->cnn_slot(l - 1);
       a.mask = c->cact[l - 1];
       a.mask_slot = c->cnn_slot(l - 1);
+      if (c->conv_skip[l + 1]) {  // layer l + 1 adds this layer's input: its Z gradient too
+        a.skip = c->cdz[l + 1];
+        a.skip_slot = c->cnn_slot(l + 1);
+      }
       // stride 2: the four parity classes of the input pixels in one launch
       a.cls = -1;
       e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, CONV_DGRAD, ns, c->stream); });
       if (e != hipSuccess) break;
+      a.skip = nullptr;
       a.in = c->cact[l - 1];
       a.in_slot = c->cnn_slot(l - 1);
     } else {

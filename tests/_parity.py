@@ -118,7 +118,8 @@ def oracle_step(cfg):
     connected network)."""
     if not cfg.is_cnn:
         return None
-    return lambda p, Xb, yb, lr: oracle.cnn.sgd_step(p, Xb, yb, lr, cfg.image, cfg.strides)
+    return lambda p, Xb, yb, lr: oracle.cnn.sgd_step(p, Xb, yb, lr, cfg.image, cfg.strides,
+                                                             cfg.skips)
 
 
 def oracle_rounds(cfg, ds, init, tau_rounds):

@@ -90,7 +90,7 @@ def make(name: str) -> str:
     step = None
     if cfg.is_cnn:
         step = lambda p, Xb, yb, lr: oracle.cnn.sgd_step(p, Xb, yb, lr, cfg.image,  # noqa: E731
-                                                         cfg.strides)
+                                                         cfg.strides, cfg.skips)
     for r in range(cfg.rounds):
         res = oracle.run_rounds(g, X, ds.y, cfg.K, tau[r:r + 1], cfg.lr, cfg.batch, seed,
                                 cfg.dtype == workload.BF16, steps_done=steps, step=step)

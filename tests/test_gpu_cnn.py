@@ -6,8 +6,8 @@ the oracle, on the same seeded inputs, through the C ABI.
   element by element, within the fp32 tolerance: small images with ragged
   tiles in every dimension, strides 1 and 2, split weight gradients, batch 1,
   a worker idle, the classifier head in one launch and (a last activation too
-  large for it) in separate launches; as local steps + aggregation and as
-  oscars_round.
+  large for it) in separate launches, residual blocks (identity shortcuts);
+  as local steps + aggregation and as oscars_round.
 * Masking independence (grouped == solo, bit for bit) and determinism.
 * The full-size workload (32 x 32 x 3 images, 8 workers, all 5 rounds) in the
   benchmark's launch configuration against the oracle's run stored by
@@ -72,12 +72,20 @@ TRAJ = {
     # x 16 per batch row): pooling, classifier and softmax as separate launches
     "big-head": _cfg("cnn-big-head", (32, 32, 3), ((16, 1),), K=2, n_rows=24, batch=3,
                      tau=(2, 1), rounds=1, seed=46),
+    # residual blocks (the paper's ResNet building block, identity shortcut):
+    # layer 3 adds layer 1's output, layer 6 layer 4's; the blocks'
+    # backward-data on 128 x 32 tiles (8 and 12 input channels)
+    "res": _cfg("cnn-res", (8, 7, 3), ((8, 1), (8, 1), (8, 1, 1), (12, 2), (16, 1), (12, 1, 1)),
+                K=3, n_rows=150, batch=6, tau=(2, 1, 3), rounds=2, seed=49),
+    # a residual block of 40 channels (backward-data on 64 x 64 tiles)
+    "res-wide": _cfg("cnn-res-wide", (6, 5, 4), ((40, 1), (36, 1), (40, 1, 1)), K=2, n_rows=60,
+                     batch=5, tau=(2, 3), rounds=2, seed=50),
     # the full workload's layers on 16 x 16 images, batch 64 (pixels per
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
                            K=4, tau_rule="given", tau_given=(4, 2, 1, 3), rounds=2),
 }
-CASES = [(n, False) for n in TRAJ] + [("small", True), ("c6s", True)]
+CASES = [(n, False) for n in TRAJ] + [("small", True), ("c6s", True), ("res", True)]
 
 
 @pytest.mark.parametrize("name,fused", CASES,
@@ -201,10 +209,11 @@ def test_cnn_full_size_trajectory(P):
         run.close()
 
 
-def test_cnn_evaluate_matches_oracle(P):
+@pytest.mark.parametrize("name", ["small", "res"])
+def test_cnn_evaluate_matches_oracle(P, name):
     import torch
-    cfg = TRAJ["small"]
-    say("cnn evaluate")
+    cfg = TRAJ[name]
+    say(f"cnn evaluate {name}")
     init = workload.gen_init(cfg)
     ctx = P.Context(cfg.dims, P.FP32, cfg.K, cfg.batch, cnn=(cfg.image, cfg.conv))
     try:
@@ -216,7 +225,7 @@ def test_cnn_evaluate_matches_oracle(P):
         loss2, hits2 = ctx.evaluate(params, x, y, noalloc=True)
         ref_loss, ref_hits = oracle.cnn.evaluate(
             [(W.astype(np.float64), b.astype(np.float64)) for W, b in init],
-            ev.x.astype(np.float64), ev.y, cfg.image, cfg.strides)
+            ev.x.astype(np.float64), ev.y, cfg.image, cfg.strides, cfg.skips)
         say(f"  loss {loss} vs {ref_loss}, correct {hits} vs {ref_hits}")
         assert abs(loss - ref_loss) <= FP32_TOL * abs(ref_loss)
         assert abs(hits - ref_hits) <= 1
@@ -228,7 +237,13 @@ def test_cnn_evaluate_matches_oracle(P):
 def test_cnn_create_rejects_bad_models(P):
     for image, conv, classes in (((0, 4, 3), ((8, 1),), 10), ((4, 4, 3), ((8, 3),), 10),
                                  ((4, 4, 3), ((0, 1),), 10), ((4, 4, 3), (), 10),
-                                 ((4, 4, 3), ((8, 1),), 0)):
+                                 ((4, 4, 3), ((8, 1),), 0),
+                                 # shortcuts: at layer 2, across a stride-2 layer, into a
+                                 # different channel count, after a layer of 3 channels
+                                 ((4, 4, 3), ((8, 1), (8, 1, 1)), 10),
+                                 ((4, 4, 3), ((8, 1), (8, 2), (8, 1, 1)), 10),
+                                 ((4, 4, 3), ((8, 1), (8, 1), (12, 1, 1)), 10),
+                                 ((4, 4, 3), ((8, 1), (3, 1), (8, 1, 1)), 10)):
         with pytest.raises((P.OscarsError, ValueError)):
             P.Context((image[0] * image[1] * image[2], classes), P.FP32, 2, 4,
                       cnn=(image, conv))

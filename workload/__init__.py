@@ -63,7 +63,9 @@ class Config:
     staleness_max: int = 4
     mean_scale: float = 1.0  # class means ~ N(0, mean_scale^2 I): smaller overlaps the classes more
     image: Tuple[int, ...] = ()  # convolutional workloads: (H, W, C) of a row
-    conv: Tuple[Tuple[int, int], ...] = ()  # convolutional workloads: (out channels, stride) per 3x3 layer
+    # convolutional workloads: (out channels, stride[, shortcut]) per 3x3 layer; a
+    # shortcut layer adds the output of the layer two before it (residual block)
+    conv: Tuple[Tuple[int, ...], ...] = ()
 
     @property
     def is_cnn(self) -> bool:
@@ -87,7 +89,7 @@ class Config:
     def n_params(self) -> int:
         if self.is_cnn:
             n, cin = 0, self.image[2]
-            for co, _ in self.conv:
+            for co, *_ in self.conv:
                 n += 9 * cin * co + co
                 cin = co
             return n + self.n_classes * cin + self.n_classes
@@ -95,7 +97,13 @@ class Config:
 
     @property
     def strides(self) -> Tuple[int, ...]:
-        return tuple(s for _, s in self.conv)
+        return tuple(c[1] for c in self.conv)
+
+    @property
+    def skips(self):
+        """Per conv layer, whether it ends a residual block (None: no shortcuts)."""
+        sk = tuple(bool(c[2]) if len(c) > 2 else False for c in self.conv)
+        return sk if any(sk) else None
 
 
 # The five workloads the hot path is measured on.  C3/C5 learning rates are not
@@ -203,7 +211,7 @@ def gen_init(cfg: Config) -> List[Tuple[np.ndarray, np.ndarray]]:
     layers = []
     if cfg.is_cnn:
         cin = cfg.image[2]
-        for co, _ in cfg.conv:
+        for co, *_ in cfg.conv:
             a = 1.0 / math.sqrt(9 * cin)
             W = g.uniform(-a, a, size=(co, 3, 3, cin)).astype(np.float32)
             b = g.uniform(-a, a, size=(co,)).astype(np.float32)
