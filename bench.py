@@ -103,6 +103,7 @@ def cnn_work(cfg, tau):
                                     "aggregate")}
     H, W, C = cfg.image
     geo = []
+    skips = list(cfg.skips or [False] * len(cfg.conv)) + [False]
     for co, st, *_ in cfg.conv:
         Ho, Wo = (H - 1) // st + 1, (W - 1) // st + 1
         geo.append((H, W, C, Ho, Wo, co))
@@ -115,10 +116,12 @@ def cnn_work(cfg, tau):
             macs = B * ho * wo * co * 9 * c
             act_in, act_out, wts = B * h * w * c * 4, B * ho * wo * co * 4, (9 * c * co + co) * 4
             work["gemm_fwd"][0] += ns * 2.0 * macs
-            work["gemm_fwd"][1] += ns * (act_in + wts + act_out)
+            # a shortcut layer also reads its block's input (the shape of its output)
+            work["gemm_fwd"][1] += ns * (act_in + wts + act_out * (2 if skips[l] else 1))
             if l > 0:
                 work["gemm_dgrad"][0] += ns * 2.0 * macs
-                work["gemm_dgrad"][1] += ns * (act_out + wts + 2 * act_in)  # reads the mask too
+                # reads the mask too, and, below a shortcut, the shortcut's gradient
+                work["gemm_dgrad"][1] += ns * (act_out + wts + (3 if skips[l + 1] else 2) * act_in)
             work["gemm_wgrad_update"][0] += ns * 2.0 * macs
             work["gemm_wgrad_update"][1] += ns * (act_out + act_in + 2 * wts)
         pooled, act, fc = B * C * 4, B * H * W * C * 4, (C * classes + classes) * 4
@@ -352,9 +355,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5", "c6"],
+    ap.add_argument("--workload", default="c5",
+                    choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"],
                     help="c5 (default): the full round; c4: aggregation-only stress; c6: the "
-                         "convolutional workload")
+                         "convolutional workload; c7: its ResNet-style variant (residual blocks)")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
     ap.add_argument("--backward", default="auto", choices=["auto", "separate", "fused",

@@ -1,10 +1,10 @@
 """Writes the expected values of the full-size trajectory tests: the oracle's
-run of the two bf16 MLP workloads and the convolutional workload over all
-their rounds (Approach, Eq. 4:
+run of the two bf16 MLP workloads and the convolutional workloads (plain and
+ResNet-style) over all their rounds (Approach, Eq. 4:
 every round each worker runs its tau_k local SGD steps from the global model,
 then the 1/K average).
 
-    python tests/golden/make_full_size.py [c3] [c5] [c6]
+    python tests/golden/make_full_size.py [c3] [c5] [c6] [c7]
 
 writes ``tests/golden/full_size_<name>.npz``.  Only ``oracle`` (the
 arithmetic) and ``workload`` (the seeded inputs) are called.  A full copy of
@@ -21,7 +21,7 @@ keeps, per round:
   * ``val_<t>``                [len(CHECK)][len(idx)] values at those indices
                                after the rounds in ``check_rounds`` (float32);
   * ``check_rounds``           1-based round numbers kept.
-Runtime on 8 cores: about three minutes each.
+Runtime on 8 cores: about three minutes each (c7: about twenty).
 """
 from __future__ import annotations
 
@@ -113,5 +113,5 @@ def make(name: str) -> str:
 
 
 if __name__ == "__main__":
-    for n in (sys.argv[1:] or ["c3", "c5", "c6"]):
+    for n in (sys.argv[1:] or ["c3", "c5", "c6", "c7"]):
         print("wrote", make(n), flush=True)

@@ -9,9 +9,9 @@ the oracle, on the same seeded inputs, through the C ABI.
   large for it) in separate launches, residual blocks (identity shortcuts);
   as local steps + aggregation and as oscars_round.
 * Masking independence (grouped == solo, bit for bit) and determinism.
-* The full-size workload (32 x 32 x 3 images, 8 workers, all 5 rounds) in the
-  benchmark's launch configuration against the oracle's run stored by
-  tests/golden/make_full_size.py.
+* The full-size workloads (32 x 32 x 3 images, 8 workers, all 5 rounds; the
+  plain and the ResNet-style network) in the benchmark's launch configuration
+  against the oracle's runs stored by tests/golden/make_full_size.py.
 * Held-out evaluation (and the allocation-free variant) against the oracle."""
 import numpy as np
 import pytest
@@ -84,8 +84,12 @@ TRAJ = {
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
                            K=4, tau_rule="given", tau_given=(4, 2, 1, 3), rounds=2),
+    # the ResNet-style workload's layers likewise
+    "c7s": workload.scaled(workload.C7, image=(16, 16, 3), dims=(768, 10), n_rows=2000, batch=32,
+                           K=4, tau_rule="given", tau_given=(3, 1, 2, 2), rounds=2),
 }
-CASES = [(n, False) for n in TRAJ] + [("small", True), ("c6s", True), ("res", True)]
+CASES = [(n, False) for n in TRAJ] + [("small", True), ("c6s", True), ("res", True),
+                                     ("c7s", True)]
 
 
 @pytest.mark.parametrize("name,fused", CASES,
@@ -152,14 +156,16 @@ def _load_golden(name):
         return {k: z[k] for k in z.files}
 
 
-def test_cnn_full_size_trajectory(P):
-    """C6 at full size, all rounds, oscars_round, against the stored oracle run:
-    aggregate bit for bit with the oracle's tree over the GPU's replicas every
-    round, losses, tensor norms, and elements at the check rounds."""
+@pytest.mark.parametrize("name", ["c6", "c7"])
+def test_cnn_full_size_trajectory(P, name):
+    """C6 and C7 at full size, all rounds, oscars_round, against the stored
+    oracle run: aggregate bit for bit with the oracle's tree over the GPU's
+    replicas every round, losses, tensor norms, and elements at the check
+    rounds."""
     import torch
     from paper_2102_08550_amd.rounds import OscarsRun, tau_schedule
-    cfg = workload.C6
-    gold = _load_golden("c6")
+    cfg = workload.CONFIGS[name]
+    gold = _load_golden(name)
     say(f"full-size {cfg.name}: generating data")
     ds = workload.gen_dataset(cfg)
     init = workload.gen_init(cfg)
@@ -205,7 +211,7 @@ def test_cnn_full_size_trajectory(P):
                 f"{max(entry['norm_rel'].values()):.2e}")
             log["rounds"].append(entry)
     finally:
-        record("full-size-c6", log)
+        record(f"full-size-{name}", log)
         run.close()
 
 

@@ -131,7 +131,18 @@ C6 = Config("cnn-32x32x3-c32-c64s2-c128s2-fp32-K8", (3072, 10), FP32, K=8, n_row
             batch=128, tau_rule="speeds", speeds=(1, 1, 1, 1, 2, 2, 4, 8), lr=0.05, rounds=5,
             seed=6, image=(32, 32, 3), conv=((32, 1), (64, 2), (128, 2)))
 
-CONFIGS = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c6": C6}
+# The same images and workers with a ResNet-style network (the paper's
+# ResNet-101 is built of residual blocks): a 32-channel stem, then three stages
+# of a conv (stride 1, 2, 2) and a two-layer residual block whose second
+# layer adds the stage's first output (identity shortcut), 32 / 64 / 128
+# channels.
+C7 = Config("cnn-res-32x32x3-c32-r32-c64s2-r64-c128s2-r128-fp32-K8", (3072, 10), FP32, K=8,
+            n_rows=50000, batch=128, tau_rule="speeds", speeds=(1, 1, 1, 1, 2, 2, 4, 8), lr=0.05,
+            rounds=5, seed=7, image=(32, 32, 3),
+            conv=((32, 1), (32, 1), (32, 1, 1), (64, 2), (64, 1), (64, 1, 1), (128, 2), (128, 1),
+                  (128, 1, 1)))
+
+CONFIGS = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5, "c6": C6, "c7": C7}
 
 
 def scaled(cfg: Config, **changes) -> Config:
