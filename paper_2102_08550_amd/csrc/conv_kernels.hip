@@ -623,23 +623,35 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   stash(Pi<0>());
   load(kbeg + CK, Pi<1>());
   __syncthreads();
-  auto step = [&](int t, auto P) {  // register set and LDS buffer p = t & 1
+  // a wave whose 32 x 32 block lies wholly past M or N (32-channel layers on
+  // 64 x 64 tiles) skips its products and leaves the MFMA unit to the CU's
+  // other workgroups
+  const bool busy = m0 + wm * 32 < M && n0 + wn * 32 < N;
+  auto step = [&](int t, auto P, auto MUL) {  // register set and LDS buffer p = t & 1
     constexpr int p = decltype(P)::value;
     load(kbeg + (t + 2) * CK, P);
     // MFMA u contracts k = 2u (lanes 0-31) and 2u + 1 (lanes 32-63)
+    if constexpr (decltype(MUL)::value) {
 #pragma unroll
-    for (int u = 0; u < CK / 2; ++u)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][wm * 32 + r],
-                                                 Bs[p][2 * u + h][wn * 32 + r], acc, 0, 0, 0);
+      for (int u = 0; u < CK / 2; ++u)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][wm * 32 + r],
+                                                   Bs[p][2 * u + h][wn * 32 + r], acc, 0, 0, 0);
+    }
     stash(Pi<p ^ 1>());
     __syncthreads();
   };
-  int t = 0;
-  for (; t + 1 < nk; t += 2) {
-    step(t, Pi<0>());
-    step(t + 1, Pi<1>());
-  }
-  if (t < nk) step(t, Pi<0>());
+  auto steps = [&](auto MUL) {
+    int t = 0;
+    for (; t + 1 < nk; t += 2) {
+      step(t, Pi<0>(), MUL);
+      step(t + 1, Pi<1>(), MUL);
+    }
+    if (t < nk) step(t, Pi<0>(), MUL);
+  };
+  if (busy)
+    steps(Pi<1>());
+  else
+    steps(Pi<0>());  // loads, stores and barriers only
 
   // accumulator i of lane (r, h): row 8 (i / 4) + 4 h + i % 4, column r
   const int col = n0 + wn * 32 + r;
