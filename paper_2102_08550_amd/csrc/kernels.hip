@@ -521,7 +521,7 @@ gemm_kernel(GemmArgs g) {
     }
   };
 
-  // After K tile j (counted from kbeg): close the chunk it ends.
+  // After K tile j (counted from kbeg): close the 64-row bias block it ends.
   auto fold = [&](int j, int nk) {
     if constexpr (MODE == GEMM_WGRAD) {
       static_assert(64 % BK == 0, "64-row bias blocks of whole K tiles");
@@ -530,20 +530,24 @@ gemm_kernel(GemmArgs g) {
         dcur = 0.0f;
       }
     }
+  };
+  // After the last K tile of a chunk: its sum into tot.  Called once per
+  // chunk from outside the tile loop (tested inside it, the fold became
+  // selects that ran at every tile).
+  auto fold_chunk = [&](bool first) {
     if constexpr (TOTAL) {
-      if ((j + 1) % TPC == 0 || j + 1 == nk) {
-        const bool first = j < TPC;
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
-          for (int jj = 0; jj < NJ; ++jj) {
-            tot[i][jj] = first ? acc[i][jj] : tot[i][jj] + acc[i][jj];
+        for (int jj = 0; jj < NJ; ++jj) {
+          tot[i][jj] = first ? acc[i][jj] : tot[i][jj] + acc[i][jj];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][jj][r] = 0.0f;
-          }
-      }
+          for (int r = 0; r < 16; ++r) acc[i][jj][r] = 0.0f;
+        }
     }
   };
+  // tiles [j0, chunk_end(j0)): one chunk with chunk totals, else all of K
+  auto chunk_end = [&](int j0, int nk) { return TOTAL ? (nk - j0 < TPC ? nk : j0 + TPC) : nk; };
 
   // Loads past the end of K read zeros, so the loop bodies are straight-line.
   const int nk = (kend - kbeg + BK - 1) / BK;
@@ -555,15 +559,20 @@ gemm_kernel(GemmArgs g) {
     ta.store(lds_a(0), tid);
     tb.store(lds_b(0), tid);
     __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int buf = kt & 1;
-      LOAD_A(ta, kbeg + (kt + 1) * BK);
-      LOAD_B(tb, kbeg + (kt + 1) * BK);
-      compute(buf);
-      fold(kt, nk);
-      ta.store(lds_a(buf ^ 1), tid);
-      tb.store(lds_b(buf ^ 1), tid);
-      __syncthreads();
+    for (int j0 = 0; j0 < nk;) {
+      const int jend = chunk_end(j0, nk);
+      for (int kt = j0; kt < jend; ++kt) {
+        const int buf = kt & 1;
+        LOAD_A(ta, kbeg + (kt + 1) * BK);
+        LOAD_B(tb, kbeg + (kt + 1) * BK);
+        compute(buf);
+        fold(kt, nk);
+        ta.store(lds_a(buf ^ 1), tid);
+        tb.store(lds_b(buf ^ 1), tid);
+        __syncthreads();
+      }
+      fold_chunk(jend <= TPC);
+      j0 = jend;
     }
   } else {
     // ST register stages: while tile j is multiplied out of LDS buffer j & 1,
@@ -580,19 +589,25 @@ gemm_kernel(GemmArgs g) {
     tA[0].store(lds_a(0), tid);
     tB[0].store(lds_b(0), tid);
     __syncthreads();
-    for (int kt = 0; kt < nk; kt += ST) {
+    static_assert(!TOTAL || TPC % ST == 0, "chunks start on register set 0");
+    for (int j0 = 0; j0 < nk;) {
+      const int jend = chunk_end(j0, nk);
+      for (int kt = j0; kt < jend; kt += ST) {
 #pragma unroll
-      for (int u = 0; u < ST; ++u) {
-        const int j = kt + u;
-        if (j >= nk) break;
-        LOAD_A(tA[u], kbeg + (j + ST) * BK);
-        LOAD_B(tB[u], kbeg + (j + ST) * BK);
-        compute(j & 1);
-        fold(j, nk);
-        tA[(u + 1) % ST].store(lds_a((j + 1) & 1), tid);
-        tB[(u + 1) % ST].store(lds_b((j + 1) & 1), tid);
-        __syncthreads();
+        for (int u = 0; u < ST; ++u) {
+          const int j = kt + u;
+          if (j >= jend) break;
+          LOAD_A(tA[u], kbeg + (j + ST) * BK);
+          LOAD_B(tB[u], kbeg + (j + ST) * BK);
+          compute(j & 1);
+          fold(j, nk);
+          tA[(u + 1) % ST].store(lds_a((j + 1) & 1), tid);
+          tB[(u + 1) % ST].store(lds_b((j + 1) & 1), tid);
+          __syncthreads();
+        }
       }
+      fold_chunk(jend <= TPC);
+      j0 = jend;
     }
   }
 #undef LOAD_A
@@ -736,10 +751,12 @@ struct DmaTile {
   static constexpr int P = ROWS * 8 / NTHR;
   static_assert(ROWS * 8 % NTHR == 0 && NTHR % 64 == 0, "whole wave instructions");
   const uint16_t* src[P];
+  const void* zero;  // the zero source, its address taken once
   bool ok[P];
   int kc[P];
   __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* gather,
                                        int row0, int R, int tid) {
+    zero = k_zero16;
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       const int idx = tid + NTHR * p, r = idx >> 3;
@@ -756,7 +773,7 @@ struct DmaTile {
   // (64 w + NTHR p) / 8 .. + 7.
   __device__ __forceinline__ void issue_one(int p, uint32_t* tile, int k0, int ext, int tid) const {
     const bool in = ok[p] && k0 + kc[p] < ext;
-    dma16(in ? static_cast<const void*>(src[p] + k0) : static_cast<const void*>(k_zero16),
+    dma16(in ? static_cast<const void*>(src[p] + k0) : zero,
           tile + (((tid & ~63) + NTHR * p) >> 3) * ROW_U32);
   }
   __device__ __forceinline__ void issue(uint32_t* tile, int k0, int ext, int tid) const {
@@ -902,26 +919,36 @@ gemm_dma_kernel(GemmArgs g) {
         }
       });
     }
-    if constexpr (!SPLIT) {
-      if ((j + 1) % TPC == 0 || j + 1 == nk) {
-        const bool first = j < TPC;
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-          for (int jj = 0; jj < NJ; ++jj) {
-            tot[i][jj] = first ? acc[i][jj] : tot[i][jj] + acc[i][jj];
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][jj][e] = 0.0f;
-          }
-      }
-    }
   };
+  // The steps chunk by chunk (TPC steps each, even: the register-tile index of
+  // a chunk's first step is always that of step 0), the chunk's sum folded into
+  // tot after its last step.  (A fold tested inside every step was turned into
+  // selects the compiler ran at every step: some 400 VALU instructions per 32
+  // MFMAs.)
+  static_assert(TPC % 2 == 0, "chunks of an even number of K tiles");
   int j = 0;
-  for (; j + 1 < nk; j += 2) {
-    step(j, Ic<(NS - 1) & 1>());
-    step(j + 1, Ic<NS & 1>());
+  while (j < nk) {
+    const int jend = nk - j < TPC ? nk : j + TPC;
+    for (; j + 1 < jend; j += 2) {
+      step(j, Ic<(NS - 1) & 1>());
+      step(j + 1, Ic<NS & 1>());
+    }
+    if (j < jend) {
+      step(j, Ic<(NS - 1) & 1>());
+      ++j;
+    }
+    if constexpr (!SPLIT) {
+      const bool first = jend <= TPC;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          tot[i][jj] = first ? acc[i][jj] : tot[i][jj] + acc[i][jj];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[i][jj][e] = 0.0f;
+        }
+    }
   }
-  if (j < nk) step(j, Ic<(NS - 1) & 1>());
   wait_vm<0>();  // nothing streams into LDS past the end of the workgroup
 
   auto mrow = [&](int i, int q) { return m0 + wm * 32 * MI + 32 * i + 8 * q + 4 * h; };
