@@ -23,8 +23,9 @@
 // MFMA 32x32x2, K in steps of 16: later steps' operands are gathered into
 // registers while the current step's MFMAs read LDS (two LDS buffers, one
 // barrier per step; two register sets where the channel counts allow loaders
-// without branches).  Backward-data into at most 32 channels uses 128 x 32
-// tiles, and layers with at most three input channels (layer 1) have a
+// without branches).  Where one side of the GEMM is at most 32 channels
+// (backward-data into, forward into, or backward-weight of 32 channels or
+// fewer) 128 x 32 or 32 x 128 tiles take its place, and layers with at most three input channels (layer 1) have a
 // direct forward and a one-accumulator backward-weight of their own.  The
 // weight-gradient passes split K into ranges, one partial sum per range,
 // which the update kernel adds in a fixed order (eight groups of consecutive
@@ -261,19 +262,23 @@ struct ConvLoader {
   // Forward with channel counts a multiple of 4: four consecutive K of the A
   // row are four channels of one input tap, of the B row four consecutive
   // weights; one 16-byte load each.
-  __device__ __forceinline__ void fwd_vec(int k, const KCursor& kc, float (&ra)[4],
-                                          float (&rb)[4]) const {
+  __device__ __forceinline__ void fwd_a(int k, const KCursor& kc, float (&ra)[4]) const {
     const int rs = kc.q, c = kc.r, r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
     const bool aok = am && k < kend && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
     const f32x4 va =
         *reinterpret_cast<const f32x4*>(aok ? arow + (hi * a.W + wi) * a.C + c : k_conv_zero);
+    for (int e = 0; e < 4; ++e) ra[e] = va[e];
+  }
+  __device__ __forceinline__ void fwd_b(int k, float (&rb)[4]) const {
     const bool bok = bn && k < kend;
     const f32x4 vb = *reinterpret_cast<const f32x4*>(
         bok ? Wt + static_cast<int64_t>(bn_idx) * 9 * a.C + k : k_conv_zero);
-    for (int e = 0; e < 4; ++e) {
-      ra[e] = va[e];
-      rb[e] = vb[e];
-    }
+    for (int e = 0; e < 4; ++e) rb[e] = vb[e];
+  }
+  __device__ __forceinline__ void fwd_vec(int k, const KCursor& kc, float (&ra)[4],
+                                          float (&rb)[4]) const {
+    fwd_a(k, kc, ra);
+    fwd_b(k, rb);
   }
   // Backward-data A with output channels a multiple of 4 (see dgrad_a).
   __device__ __forceinline__ void dgrad_a_vec(int k, const KCursor& kc, float (&ra)[4]) const {
@@ -786,6 +791,201 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
     const int64_t at = wk.offset() + col;
     const float g = a.skip ? acc[i] + a.skip[z * a.skip_slot + at] : acc[i];
     a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? g : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward into at most 32 output channels and backward-weight of at most 32
+// output channels (channel counts multiples of 4, at least 4 input channels),
+// where a 64 x 64 tile would leave half of its waves without products:
+//   forward          128 x 32 tiles (pixels x output channels), the four waves
+//                    stacked along M; each thread gathers two A rows and, in
+//                    the first 128 threads, one weight row, four consecutive K
+//                    each, as conv_gemm_kernel<CONV_FWD, true> does;
+//   backward-weight  32 x 128 tiles (output channels x weight columns), the
+//                    waves side by side along N; each thread takes one K (an
+//                    output pixel) and, as WgradLoader does, four output
+//                    channels (the first eight threads of each K) and two
+//                    groups of four weight columns.
+// Both keep the LDS layout of the 64 x 64 tiles (K steps of CK, [k][row]) and
+// the operand roles of every MFMA, and so every sum is the same.  Two
+// register sets as there: step t + 2 is gathered while step t is multiplied.
+__host__ __device__ inline bool conv_narrow(const ConvArgs& a) {
+  return (a.C & 3) == 0 && (a.Co & 3) == 0 && a.C >= 4 && a.Co <= NN;
+}
+__host__ __device__ inline int64_t fwd_narrow_tiles(const ConvArgs& a) {
+  const Dims d = pass_dims(a, CONV_FWD);
+  return ((d.M + NM - 1) / NM) * ((d.N + NN - 1) / NN);
+}
+__host__ __device__ inline int64_t wgrad_narrow_tiles(const ConvArgs& a) {
+  const Dims d = pass_dims(a, CONV_WGRAD);
+  return ((d.M + NN - 1) / NN) * ((d.N + NM - 1) / NM);
+}
+
+__global__ __launch_bounds__(256) void conv_fwd_narrow_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float As[2][CK][NM + 4];
+  __shared__ __attribute__((aligned(16))) float Bs[2][CK][NN + 4];
+  const Dims d = pass_dims(a, CONV_FWD);
+  const int M = static_cast<int>(d.M), N = static_cast<int>(d.N), K = static_cast<int>(d.K);
+  const int z = blockIdx.y;
+  const int rep = a.order[z];
+  const int gn = (N + NN - 1) / NN;
+  const int tile = blockIdx.x;
+  const int m0 = tile / gn * NM, n0 = (tile - tile / gn * gn) * NN;
+  const float* in = a.in + z * a.in_slot;
+  const int32_t* rows = a.gather ? a.gather + z * a.gather_slot : nullptr;
+  const float* par = a.master_in + static_cast<int64_t>(rep) * a.master_in_slot;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r = lane & 31, h = lane >> 5;
+  // A rows lr and lr + 64, B row lr (threads below 128), K lk .. lk + 3
+  const int lr = tid >> 2, lk = (tid & 3) * 4;
+  const bool bload = tid < NN * CK / 4;
+  const ConvLoader<CONV_FWD> ld0(a, K, m0 + lr, M, n0 + lr, N, in, rows, nullptr, par + a.w_off);
+  const ConvLoader<CONV_FWD> ld1(a, K, m0 + lr + 64, M, n0 + lr, N, in, rows, nullptr,
+                                 par + a.w_off);
+  KCursor ka(lk, a.C);  // stepped along with the loads
+  float ra0[2][4], ra1[2][4], rb[2][4];
+  auto load = [&](int k0, auto P) {
+    constexpr int p = decltype(P)::value;
+    ld0.fwd_a(k0 + lk, ka, ra0[p]);
+    ld1.fwd_a(k0 + lk, ka, ra1[p]);
+    ld0.fwd_b(k0 + lk, rb[p]);  // rows past N (threads from 128 on) read zeros
+    ka.next();
+  };
+  auto stash = [&](auto P) {
+    constexpr int p = decltype(P)::value;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      As[p][lk + e][lr] = ra0[p][e];
+      As[p][lk + e][lr + 64] = ra1[p][e];
+    }
+    if (bload) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Bs[p][lk + e][lr] = rb[p][e];
+    }
+  };
+
+  f32x16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+  const int nk = (K + CK - 1) / CK;
+  load(0, Pi<0>());
+  stash(Pi<0>());
+  load(CK, Pi<1>());
+  __syncthreads();
+  auto step = [&](int t, auto P) {
+    constexpr int p = decltype(P)::value;
+    load((t + 2) * CK, P);
+#pragma unroll
+    for (int u = 0; u < CK / 2; ++u)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][wave * 32 + r],
+                                                 Bs[p][2 * u + h][r], acc, 0, 0, 0);
+    stash(Pi<p ^ 1>());
+    __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < nk; t += 2) {
+    step(t, Pi<0>());
+    step(t + 1, Pi<1>());
+  }
+  if (t < nk) step(t, Pi<0>());
+
+  const int col = n0 + r;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int row = m0 + wave * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+    if (row >= M || col >= N) continue;
+    const int64_t at = static_cast<int64_t>(row) * a.Co + col;
+    float zv = acc[i] + par[a.b_off + col];
+    if (a.skip) zv += a.skip[z * a.skip_slot + at];
+    a.out[z * a.out_slot + at] = zv > 0.0f ? zv : 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float As[2][CK][NN + 4];
+  __shared__ __attribute__((aligned(16))) float Bs[2][CK][NM + 4];
+  const Dims d = pass_dims(a, CONV_WGRAD);
+  const int M = static_cast<int>(d.M), N = static_cast<int>(d.N), K = static_cast<int>(d.K);
+  const int z = blockIdx.y;
+  const int rep = a.order[z];
+  const int gm = (M + NN - 1) / NN, gn = (N + NM - 1) / NM;
+  int tile = blockIdx.x;
+  const int split = tile / (gm * gn);
+  tile -= split * gm * gn;
+  const int m0 = tile / gn * NN, n0 = (tile - tile / gn * gn) * NM;
+  const int kbeg = split * static_cast<int>(a.k_per_split);
+  const int kend = K - kbeg < a.k_per_split ? K : kbeg + static_cast<int>(a.k_per_split);
+  const float* in = a.in + z * a.in_slot;
+  const int32_t* rows = a.gather ? a.gather + z * a.gather_slot : nullptr;
+  const float* dz = a.dout + z * a.dout_slot;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r = lane & 31, h = lane >> 5;
+  // K lk; A rows 4 q .. 4 q + 3 (q below 8); B columns 4 q .. + 3 and 64 + 4 q .. + 3
+  const int lk = tid >> 4, q = tid & 15;
+  const bool aload = q < NN / 4;
+  const WgradLoader w0(a, kend, aload ? m0 + 4 * q : M, M, n0 + 4 * q, N, in, rows, dz, nullptr);
+  const WgradLoader w1(a, kend, M, M, n0 + 64 + 4 * q, N, in, rows, dz, nullptr);
+  PixCursor pc(kbeg + lk, a.Ho, a.Wo);
+  float ra[2][4], rb0[2][4], rb1[2][4];
+  auto load = [&](int k0, auto P) {
+    constexpr int p = decltype(P)::value;
+    float unused[4];
+    w0.fetch(k0 + lk, pc, ra[p], rb0[p]);
+    w1.fetch(k0 + lk, pc, unused, rb1[p]);  // its A rows are past M: zeros, not stored
+    pc.next();
+  };
+  auto stash = [&](auto P) {
+    constexpr int p = decltype(P)::value;
+    if (aload)
+      *reinterpret_cast<f32x4*>(&As[p][lk][4 * q]) = f32x4{ra[p][0], ra[p][1], ra[p][2], ra[p][3]};
+    *reinterpret_cast<f32x4*>(&Bs[p][lk][4 * q]) =
+        f32x4{rb0[p][0], rb0[p][1], rb0[p][2], rb0[p][3]};
+    *reinterpret_cast<f32x4*>(&Bs[p][lk][64 + 4 * q]) =
+        f32x4{rb1[p][0], rb1[p][1], rb1[p][2], rb1[p][3]};
+  };
+
+  f32x16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+  const int nk = (kend - kbeg + CK - 1) / CK;
+  load(kbeg, Pi<0>());
+  stash(Pi<0>());
+  load(kbeg + CK, Pi<1>());
+  __syncthreads();
+  // a wave whose 32 columns lie past N (the last tile) skips its products
+  const bool busy = n0 + wave * 32 < N;
+  auto step = [&](int t, auto P, auto MUL) {
+    constexpr int p = decltype(P)::value;
+    load(kbeg + (t + 2) * CK, P);
+    if constexpr (decltype(MUL)::value) {
+#pragma unroll
+      for (int u = 0; u < CK / 2; ++u)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][r],
+                                                   Bs[p][2 * u + h][wave * 32 + r], acc, 0, 0, 0);
+    }
+    stash(Pi<p ^ 1>());
+    __syncthreads();
+  };
+  auto steps = [&](auto MUL) {
+    int t = 0;
+    for (; t + 1 < nk; t += 2) {
+      step(t, Pi<0>(), MUL);
+      step(t + 1, Pi<1>(), MUL);
+    }
+    if (t < nk) step(t, Pi<0>(), MUL);
+  };
+  if (busy)
+    steps(Pi<1>());
+  else
+    steps(Pi<0>());
+
+  const int col = n0 + wave * 32 + r;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int row = m0 + 8 * (i >> 2) + 4 * h + (i & 3);
+    if (row >= M || col >= N) continue;
+    a.part[z * a.part_slot + (static_cast<int64_t>(split) * M + row) * N + col] = acc[i];
   }
 }
 
@@ -1322,7 +1522,7 @@ __global__ __launch_bounds__(256) void conv_head_kernel(HeadArgs h) {
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
-  // shortcuts: conv forward and backward-data on the 64 x 64 / 128 x 32 tiles only
+  // shortcuts: conv forward and backward-data on the 64 x 64 and narrow tiles only
   if (a.skip && (pass == FC_FWD || pass == FC_DGRAD || pass == CONV_WGRAD || pass == FC_WGRAD ||
                  (pass == CONV_FWD && thin_layer(a))))
     return hipErrorInvalidValue;
@@ -1403,6 +1603,23 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
       case 6: hipLaunchKernelGGL((conv_thin_wgrad_kernel<3, 1>), grid, block, lds, s, a); break;
       default: hipLaunchKernelGGL((conv_thin_wgrad_kernel<3, 2>), grid, block, lds, s, a); break;
     }
+    return hipGetLastError();
+  }
+  if (pass == CONV_FWD && conv_narrow(a)) {
+    const int64_t gx = fwd_narrow_tiles(a);
+    if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_fwd_narrow_kernel, dim3(static_cast<unsigned>(gx), n_slots), dim3(256),
+                       0, s, a);
+    return hipGetLastError();
+  }
+  if (pass == CONV_WGRAD && conv_narrow(a)) {
+    if (a.splits < 1 || a.k_per_split < 1 ||
+        static_cast<int64_t>(a.splits) * a.k_per_split < d.K)
+      return hipErrorInvalidValue;
+    const int64_t gx = wgrad_narrow_tiles(a) * a.splits;
+    if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_wgrad_narrow_kernel, dim3(static_cast<unsigned>(gx), n_slots),
+                       dim3(256), 0, s, a);
     return hipGetLastError();
   }
   int64_t gx = ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
