@@ -513,7 +513,7 @@ def main():
     tau0 = np.asarray(tau_for(0))
     backward_mix = {f"l{l}": {str(ns): ("fused" if fused_path(l, ns) else "separate")
                               for ns in sorted({int((tau0 > j).sum()) for j in range(tau0.max())})}
-                    for l in range(2, len(cfg.dims))}
+                    for l in range(1, len(cfg.dims))}
     mix = backward_mix if args.schedule == "grouped" else {"schedule": "replica"}
 
     def mix_bytes(m):  # the dominant kind's algorithmic bytes per round under mix m

@@ -103,9 +103,9 @@ typedef struct {
  * Allocates, on the current HIP device, the whole device workspace the
  * local steps use: activations, bf16 weight copies, split-K partials, the
  * index table and loss buffer for rounds of up to 64 local steps per worker
- * (with pinned host staging), and, for bf16 models with hidden layers, the
- * scratch replicas on which OSCARS_BACKWARD_AUTO times the backward paths
- * (K x the widest hidden layer, fp32 + bf16; left out where they would take
+ * (with pinned host staging), and, for bf16 models, the scratch replicas
+ * on which OSCARS_BACKWARD_AUTO times the backward paths (K x the widest
+ * layer, fp32 + bf16; left out where they would take
  * more than a quarter of the free device memory, and then nothing is timed).
  * `hip_stream` (a hipStream_t, NULL = null stream) is the stream
  * oscars_local_steps enqueues on.  The context owns its tuning state (GEMM
@@ -389,24 +389,27 @@ oscars_status oscars_set_gemm_tiling(oscars_ctx* ctx, int32_t tiling);
  * pointer. */
 oscars_status oscars_tuning_pending(const oscars_ctx* ctx, int32_t* configurations);
 
-/* Backward pass of the hidden layers (l >= 2) of a bf16 model, per context
- * (a tuning and testing aid).  By default one launch per layer does
+/* Backward pass of the layers of a bf16 model, per context (a tuning and
+ * testing aid).  By default one launch per hidden layer (l >= 2) does
  * backward-data, backward-weight and the SGD update of Eq. 4 (Approach): it
  * rounds the fp32 master it streams for the update to the bf16 weights the
- * forward pass used, so backward-data reads no weights of its own.  Its
- * results are bit-identical to the separate backward-data and update
- * launches, whichever mode runs (a weight that is exactly -0 may come out
- * as +0 in one and -0 in the other).  The bias gradient of every update
- * sums the batch in blocks of 64 rows, block sums left to right.
+ * forward pass used, so backward-data reads no weights of its own.  Layer 1
+ * (no backward-data) may take the same streamed launch for backward-weight
+ * and the update alone.  The results are bit-identical to the separate
+ * backward-data and update launches, whichever mode runs (a weight that is
+ * exactly -0 may come out as +0 in one and -0 in the other).  The bias
+ * gradient of every update sums the batch in blocks of 64 rows, block sums
+ * left to right.
  *   OSCARS_BACKWARD_AUTO (default): the fastest at the first launch of the
- *     configuration (inputs, outputs, batch, active replicas) in this
- *     context of: the fused launch with each feasible number of 1024-output
- *     chunks per workgroup (all; then half, a quarter, ... down to one,
- *     where the context's partial buffer holds the split), and the separate
- *     launches.  Each runs three times there on the scratch replicas
- *     oscars_create allocated, the faster of its last two runs counting; a
- *     later candidate is taken only when it is more than 5% faster than the
- *     earlier pick.
+ *     configuration (inputs, outputs, batch, active replicas, layer 1 or
+ *     hidden) in this context of: the fused launch with each feasible
+ *     number of 1024-output chunks per workgroup (all; then half, a quarter,
+ *     ... down to one, where the context's partial buffer holds the split;
+ *     layer 1 needs no partials), and the separate launches.  Each runs
+ *     three times there on the scratch replicas oscars_create allocated, the
+ *     faster of its last two runs counting; a later candidate is taken only
+ *     when it is more than 5% faster than the earlier pick (the separate
+ *     update comes first for layer 1, last for the hidden layers).
  *     Untimed -- on a stream being captured into a graph, or where
  *     oscars_create left the scratch out --: fused, split over the number of
  *     workgroups per 64-wide input strip that fills the last pass over the
@@ -430,10 +433,11 @@ oscars_status oscars_set_backward(oscars_ctx* ctx, int32_t mode);
 /* The backward path of layer `layer` (1..L) in oscars_local_steps and
  * oscars_round of this context with `replicas` active replicas (1..K) and
  * batch `batch` (1..max_batch): *fused = 1 for the fused launch of
- * backward-data, backward-weight and update, 0 for the separate launches
- * (always for layer 1, fp32 models, OSCARS_BACKWARD_SEPARATE and batches
- * above 256), -1 where OSCARS_BACKWARD_AUTO times configurations and has
- * not timed that one in this context yet.  Returns OSCARS_E_INVALID for an
+ * backward-data (none for layer 1), backward-weight and update, 0 for the
+ * separate launches (always for fp32 models, OSCARS_BACKWARD_SEPARATE,
+ * batches above 256 and layers whose input width is not a multiple of 8),
+ * -1 where OSCARS_BACKWARD_AUTO times configurations and has not timed that
+ * one in this context yet.  Returns OSCARS_E_INVALID for an
  * argument out of range. */
 oscars_status oscars_backward_path(const oscars_ctx* ctx, int32_t layer, int32_t batch,
                                    int32_t replicas, int32_t* fused);

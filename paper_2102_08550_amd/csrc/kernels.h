@@ -127,12 +127,15 @@ bool backward_fusable(const GemmArgs& g);
 bool backward_fused_enabled(int mode);
 // mode: the context's BackwardMode; cps_forced > 0: each workgroup covers
 // that many KCHUNK ranges of outputs (all of them where the partial buffer
-// cannot hold the split); 0: by mode.
+// cannot hold the split); 0: by mode.  dgrad = false: backward-weight and the
+// update only, for layer 1 (GEMM_WGRAD's operands: a = the gathered input
+// rows, b = delta; out, mask and part unused), the same results as
+// GEMM_WGRAD bit for bit (but for the sign of a weight that is exactly -0).
 hipError_t launch_bwd_fused(const GemmArgs& g, int n_slots, hipStream_t s, int mode,
-                            int cps_forced = 0);
+                            int cps_forced = 0, bool dgrad = true);
 // The feasible ranges per workgroup (all chunks first, then halving down to
 // one), at most `max` of them written to cps; returns their number.
-int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max);
+int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max, bool dgrad = true);
 // Backward of hidden bf16 layers (a per-context setting): AUTO (fused, the
 // o chunks split over the workgroup count that best fills the last CU pass,
 // or the separate launches, whichever the caller timed faster for the

@@ -1290,6 +1290,12 @@ __global__ __launch_bounds__(256, MINW) void wgrad_dma_kernel(GemmArgs g) {
 // SPLIT: a workgroup covers `cps` KCHUNK ranges of o and stores the
 // backward-data sum of each as that chunk's partial; splitk_reduce_kernel
 // finishes.
+// DG = false: backward-weight and the update only (layer 1, whose input needs
+// no gradient): no Wq stage, no backward-data products; a split then needs
+// no partials.  The update streams the master the same way, which on the
+// 3072 x 4096 first layer of a 4096-wide MLP moves its bytes faster than the
+// tile kernel (wgrad_dma_kernel), whose workgroups each load their operand
+// tiles, then their master tile, then store it.
 //
 // LDS (144 KB): two delta chunks [256 b][64 o] bf16, two Wq chunks
 // [64 o][64 i] bf16 and the activation strip [256 b][64 i] bf16 (128-byte
@@ -1339,7 +1345,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, kBufWord3);
 }
 
-template <bool SPLIT, int NKS>
+template <bool SPLIT, int NKS, bool DG>
 __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int strips, int nsplit,
                                                              int cps) {
   __shared__ __attribute__((aligned(16))) char smem[144 * 1024 + 2048];
@@ -1369,15 +1375,17 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
   const int nblk = (Bp + 63) / 64;  // 64-row blocks of the bias sum
   static_assert(NKS == 8 || NKS == 16, "batch rows 128 or 256");
 
-  // Activation strip [16 NKS][64] into LDS (all waves), zero from row B on.
+  // Activation strip [16 NKS][64] into LDS (all waves), zero from row B and
+  // from column I on (a row of the layer-1 input is I wide, unpadded).
   {
     const uint16_t* act = static_cast<const uint16_t*>(g.a) + z * g.a_slot;
 #pragma unroll
     for (int p = 0; p < FB_BMAX / 64; ++p) {
       const int row = (tid >> 3) + 64 * p, c = tid & 7;
+      const bool in = row < B && i0 + 8 * c < I;
       if (64 * p < 16 * NKS)
         *reinterpret_cast<u32x4*>(astrip + t128(row, c)) =
-            load16(row < B, act + static_cast<int64_t>(row < B ? row : 0) * g.a_ld + i0 + 8 * c);
+            load16(in, act + static_cast<int64_t>(in ? row : 0) * g.a_ld + (in ? i0 + 8 * c : 0));
     }
   }
   __syncthreads();
@@ -1506,11 +1514,13 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
 #pragma unroll
       for (int p = 0; p < NKS / 2; ++p)
         *reinterpret_cast<u32x4*>(dt + t128((ts >> 3) + 32 * p, ts & 7)) = dreg[d_next][p];
-      char* const wq = wbuf(t + 1);
+      if constexpr (DG) {
+        char* const wq = wbuf(t + 1);
 #pragma unroll
-      for (int p = 0; p < 2; ++p)
-        *reinterpret_cast<u32x4*>(wq + t128(mrow + 32 * p, jx + 4 * sx)) =
-            pair_swap(pack4(mreg[b_next][2 * p]), pack4(mreg[b_next][2 * p + 1]));
+        for (int p = 0; p < 2; ++p)
+          *reinterpret_cast<u32x4*>(wq + t128(mrow + 32 * p, jx + 4 * sx)) =
+              pair_swap(pack4(mreg[b_next][2 * p]), pack4(mreg[b_next][2 * p + 1]));
+      }
       // loads: delta of chunk t + 3, master of chunk t + 4
       load_delta(t + 3, dreg[d_next]);
 #pragma unroll
@@ -1612,7 +1622,7 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
         accw = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr128(astrip, 16 * s, 32 * (wb >> 1), lane),
                                                        tr128(dt, 16 * s, 32 * (wb & 1), lane),
                                                        accw, 0, 0, 0);
-        if (s % (NKS / 4) == 0) {
+        if (DG && s % (NKS / 4) == 0) {
           const int k = s / (NKS / 4);
           const bf16x8 a0 = tr128(wq, 16 * k, 0, lane), a1 = tr128(wq, 16 * k, 32, lane);
           const bf16x8 b0 = row128(dt, 64 * wb + (lane & 31), 2 * k + h);
@@ -1633,7 +1643,7 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
       }
       // end of a KCHUNK range of o: chunk sums left to right, or (SPLIT) the
       // chunk's partial
-      if ((t + 1) % TPC == 0 || t + 1 == tend) {
+      if (DG && ((t + 1) % TPC == 0 || t + 1 == tend)) {
         if constexpr (SPLIT) {
           if (dgrad_wave) {
             float* part = g.part + z * g.part_slot + static_cast<int64_t>(t / TPC) * B * g.out_ld;
@@ -1670,7 +1680,7 @@ __global__ __launch_bounds__(FB_NT, 1) void bwd_fused_kernel(GemmArgs g, int str
     __syncthreads();
   }
 
-  if (SPLIT || !dgrad_wave) return;
+  if (!DG || SPLIT || !dgrad_wave) return;
   // the masks of every group first (loads in flight together; outside the
   // outputs row 0, column 0 is read and not used), then the stores
   f32x4 ea[2][2][4];
@@ -2372,11 +2382,12 @@ bool backward_fused_enabled(int mode) { return mode != BACKWARD_SEPARATE; }
 // CUs best, the largest on ties (a split costs partial traffic and a
 // reduce); measured on MI355X against the other choices at 1 to 8 replicas
 // of 4096 x 4096 layers.
-int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max) {
+int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max, bool dgrad) {
   if (!backward_fusable(g) || n_slots < 1 || max < 1) return 0;
   const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
   const int64_t part_slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
-  const bool can_split = nchunks > 1 && g.part && part_slot * n_slots <= g.part_cap;
+  const bool can_split =
+      nchunks > 1 && (!dgrad || (g.part && part_slot * n_slots <= g.part_cap));
   int n = 0;
   for (int c = nchunks; n < max; c = (c + 1) / 2) {
     cps[n++] = c;
@@ -2386,13 +2397,14 @@ int bwd_fused_splits(const GemmArgs& g, int n_slots, int* cps, int max) {
 }
 
 hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s, int mode,
-                            int cps_forced) {
+                            int cps_forced, bool dgrad) {
   if (!backward_fusable(g_in) || n_slots < 1) return hipErrorInvalidValue;
   GemmArgs g = g_in;
   const int strips = (g.M + FB_TI - 1) / FB_TI;
   const int nchunks = (g.K + KCHUNK - 1) / KCHUNK;
-  g.part_slot = static_cast<int64_t>(nchunks) * g.N * g.out_ld;
-  const bool can_split = nchunks > 1 && g.part && g.part_slot * n_slots <= g.part_cap;
+  g.part_slot = dgrad ? static_cast<int64_t>(nchunks) * g.N * g.out_ld : 0;
+  const bool can_split =
+      nchunks > 1 && (!dgrad || (g.part && g.part_slot * n_slots <= g.part_cap));
   int cps = nchunks;
   if (cps_forced > 0) {
     cps = can_split && cps_forced < nchunks ? cps_forced : nchunks;
@@ -2417,13 +2429,18 @@ hipError_t launch_bwd_fused(const GemmArgs& g_in, int n_slots, hipStream_t s, in
   if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(gx)), block(FB_NT);
   const bool b256 = g.N > 128;  // batch rows summed by backward-weight: 256 or 128
-  if (!split) {
-    if (b256) hipLaunchKernelGGL((bwd_fused_kernel<false, 16>), grid, block, 0, s, g, strips, 1, cps);
-    else hipLaunchKernelGGL((bwd_fused_kernel<false, 8>), grid, block, 0, s, g, strips, 1, cps);
+  if (!dgrad) {  // update only: a split range is a workgroup's own (no partials)
+    if (b256) hipLaunchKernelGGL((bwd_fused_kernel<true, 16, false>), grid, block, 0, s, g, strips, nsplit, cps);
+    else hipLaunchKernelGGL((bwd_fused_kernel<true, 8, false>), grid, block, 0, s, g, strips, nsplit, cps);
     return hipGetLastError();
   }
-  if (b256) hipLaunchKernelGGL((bwd_fused_kernel<true, 16>), grid, block, 0, s, g, strips, nsplit, cps);
-  else hipLaunchKernelGGL((bwd_fused_kernel<true, 8>), grid, block, 0, s, g, strips, nsplit, cps);
+  if (!split) {
+    if (b256) hipLaunchKernelGGL((bwd_fused_kernel<false, 16, true>), grid, block, 0, s, g, strips, 1, cps);
+    else hipLaunchKernelGGL((bwd_fused_kernel<false, 8, true>), grid, block, 0, s, g, strips, 1, cps);
+    return hipGetLastError();
+  }
+  if (b256) hipLaunchKernelGGL((bwd_fused_kernel<true, 16, true>), grid, block, 0, s, g, strips, nsplit, cps);
+  else hipLaunchKernelGGL((bwd_fused_kernel<true, 8, true>), grid, block, 0, s, g, strips, nsplit, cps);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t work = static_cast<int64_t>(g.N) * ((g.M + 3) / 4);

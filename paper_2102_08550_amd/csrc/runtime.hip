@@ -120,7 +120,7 @@ struct oscars_ctx {
   // outputs, batch, replicas): fused with this many 1024-output chunks per
   // workgroup (> 0), or the separate launches (0); timed at the first launch
   // on scratch replicas (cal_*, allocated then).
-  std::map<std::array<int, 4>, int> bwd_fused_choice;
+  std::map<std::array<int, 5>, int> bwd_fused_choice;  // (M, K, N, replicas, backward-data)
   float* cal_master = nullptr;   // [K][cal_layer] fp32: W_l then b_l
   uint16_t* cal_copy = nullptr;  // [K][cal_w] bf16 copies of W_l
   int32_t* cal_order = nullptr;  // [K] = 0 .. K-1
@@ -223,8 +223,8 @@ hipError_t ensure_tables(oscars_ctx* c, int64_t need, int64_t loss_need) {
 // b, bf16 W).  Skipped (no timing: c->cal_off) where it would take more than
 // a quarter of the free device memory.
 hipError_t alloc_calibration(oscars_ctx* c) {
-  if (!c->bf16 || c->L < 2) return hipSuccess;
-  for (int l = 2; l <= c->L; ++l) {
+  if (!c->bf16) return hipSuccess;
+  for (int l = 1; l <= c->L; ++l) {
     const int64_t w = static_cast<int64_t>(c->dims[l]) * c->dims[l - 1];
     c->cal_w = std::max(c->cal_w, round_up(w, 8));
     c->cal_layer = std::max(c->cal_layer, round_up(w + c->dims[l], 8));
@@ -773,25 +773,28 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
   return e;
 }
 
-// Backward of hidden layer l of a bf16 model without a forced mode: at the
-// first launch of each (inputs, outputs, batch, replicas) the fused launch
-// (gf) with every feasible number of output chunks per workgroup (all, then
-// halving down to one), and the separate backward-data + update launches
-// (gd, gw), each run three times on the scratch replicas oscars_create
-// allocated, timed; the fastest of the last two runs of each decides (the
-// earlier candidate on ties).  The real replicas and weight copies are
-// untouched; every candidate writes the delta of the layer below, which the
-// real launch that follows recomputes.  *cps: the chunks per workgroup of the
-// fused launch, or 0 for the separate launches.  On a stream being captured
-// into a graph, or without scratch, nothing is timed: the fused launch with
-// the split its launcher picks (*cps = -1).
-hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const GemmArgs& gd,
+// Backward of layer l of a bf16 model without a forced mode: at the first
+// launch of each (inputs, outputs, batch, replicas, layer 1 or hidden) the
+// fused launch (gf) with every feasible number of output chunks per
+// workgroup (all, then halving down to one), and the separate backward-data
+// + update launches (gd, gw; layer 1: gd == nullptr, the fused launch
+// without backward-data against the update alone), each run three times on
+// the scratch replicas oscars_create allocated, timed; the fastest of the
+// last two runs of each decides (the earlier candidate on ties).  The real
+// replicas and weight copies are untouched; every hidden-layer candidate
+// writes the delta of the layer below, which the real launch that follows
+// recomputes.  *cps: the chunks per workgroup of the fused launch, or 0 for
+// the separate launches.  On a stream being captured into a graph, or
+// without scratch, nothing is timed: the fused launch with the split its
+// launcher picks (*cps = -1).
+hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const GemmArgs* gd,
                            const GemmArgs& gw, int* cps) {
   *cps = -1;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(c->stream, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone)
     return hipSuccess;
-  const std::array<int, 4> key{gf.M, gf.K, gf.N, ns};
+  const bool dgrad = gd != nullptr;
+  const std::array<int, 5> key{gf.M, gf.K, gf.N, ns, dgrad ? 1 : 0};
   auto it = c->bwd_fused_choice.find(key);
   if (it != c->bwd_fused_choice.end()) {
     *cps = it->second;
@@ -814,19 +817,26 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
       a.wcopy_slot = c->cal_w;
     }
   };
-  GemmArgs f = gf, d = gd, w = gw;
+  GemmArgs f = gf, d = dgrad ? *gd : gw, w = gw;
   to_scratch(f);
   to_scratch(d);
   to_scratch(w);
   d.a = c->cal_copy;  // backward-data reads the slots' bf16 weights
   d.a_slot = c->cal_w;
   d.a_by_order = 0;
-  // candidates: fused with each feasible split, then separate (0); three
-  // runs of each, round robin; the first (which also picks the
-  // backward-data tiling) is not counted, the faster of the other two is
+  // candidates: fused with each feasible split, then separate (0) (layer 1:
+  // separate first); three runs of each, round robin; the first (which also
+  // picks the backward-data tiling) is not counted, the faster of the other
+  // two is
   int cand[8];
-  int nc = bwd_fused_splits(f, ns, cand, 7);
-  cand[nc++] = 0;
+  // Layer 1's separate update comes first, so that the streamed launch
+  // replaces it only when faster by the margin (picked first, within the
+  // margin, the streamed launch ran a 4096 x 4096 layer 1 at 3 replicas in
+  // 117 against 96 us for the separate update).
+  int nc = 0;
+  if (!dgrad) cand[nc++] = 0;
+  nc += bwd_fused_splits(f, ns, cand + nc, 7, dgrad);
+  if (dgrad) cand[nc++] = 0;
   float best[8] = {};
   struct TuneNow {  // the separate path's backward-data tiling decided at its first run
     TuneNow() { set_gemm_tune_now(true); }
@@ -837,9 +847,11 @@ hipError_t choose_backward(oscars_ctx* c, int ns, const GemmArgs& gf, const Gemm
       float ms = 0.0f;
       e = hipEventRecord(c->cal_ev[0], c->stream);
       if (cand[i] > 0) {
-        if (e == hipSuccess) e = launch_bwd_fused(f, ns, c->stream, c->backward_mode, cand[i]);
+        if (e == hipSuccess)
+          e = launch_bwd_fused(f, ns, c->stream, c->backward_mode, cand[i], dgrad);
       } else {
-        if (e == hipSuccess) e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream, c->tuner);
+        if (e == hipSuccess && dgrad)
+          e = launch_gemm(d, GEMM_DGRAD, true, ns, c->stream, c->tuner);
         if (e == hipSuccess) e = launch_gemm(w, GEMM_WGRAD, true, ns, c->stream, c->tuner);
       }
       if (e == hipSuccess) e = hipEventRecord(c->cal_ev[1], c->stream);
@@ -1144,7 +1156,8 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
         if (backward_fusable(g)) {
           int cps = -1;  // fused, split by the launcher's rule
           if (c->backward_mode == BACKWARD_AUTO) {
-            e = choose_backward(c, ns, g, dgrad_args(l), wgrad_args(l), &cps);
+            const GemmArgs gd = dgrad_args(l);
+            e = choose_backward(c, ns, g, &gd, wgrad_args(l), &cps);
             if (e != hipSuccess) return hip_fail(e);
           }
           if (cps != 0) {
@@ -1152,6 +1165,40 @@ oscars_status run_local_steps(oscars_ctx* c, float* replicas, const float* start
                       [&] {
                         return launch_bwd_fused(g, ns, c->stream, c->backward_mode,
                                                 cps > 0 ? cps : 0);
+                      });
+            if (e != hipSuccess) return hip_fail(e);
+            continue;
+          }
+        }
+      }
+      if (l == 1 && c->bf16 && backward_fused_enabled(c->backward_mode)) {
+        // layer 1: backward-weight and the update streamed like the fused
+        // backward of the hidden layers, without backward-data
+        GemmArgs g{};
+        g.M = c->dims[0];
+        g.N = B;
+        g.K = c->dims[1];
+        g.a = c->act[0];  // the batch rows the forward pass gathered
+        g.a_ld = c->ld[0];
+        g.a_slot = c->act_slot(0);
+        g.b = c->delta[1];
+        g.b_ld = c->ld[1];
+        g.b_slot = c->act_slot(1);
+        common(g, 1);
+        g.wcopy = c->wcopy;
+        g.wcopy_slot = c->n_pad;
+        g.wcopy_slots = ns_next;  // slots ns_next .. ns-1 take their last step now
+        if (backward_fusable(g)) {
+          int cps = -1;
+          if (c->backward_mode == BACKWARD_AUTO) {
+            e = choose_backward(c, ns, g, nullptr, wgrad_args(1), &cps);
+            if (e != hipSuccess) return hip_fail(e);
+          }
+          if (cps != 0) {
+            e = timed(c, OSCARS_KERNEL_WGRAD,
+                      [&] {
+                        return launch_bwd_fused(g, ns, c->stream, c->backward_mode,
+                                                cps > 0 ? cps : 0, false);
                       });
             if (e != hipSuccess) return hip_fail(e);
             continue;
@@ -1411,7 +1458,7 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
       replicas < 1 || replicas > c->K)
     return OSCARS_E_INVALID;
   *fused = 0;
-  if (layer == 1 || !c->bf16 || !backward_fused_enabled(c->backward_mode)) return OSCARS_OK;
+  if (!c->bf16 || !backward_fused_enabled(c->backward_mode)) return OSCARS_OK;
   GemmArgs g{};
   g.M = c->dims[layer - 1];
   g.N = batch;
@@ -1425,7 +1472,8 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
     *fused = 1;
     return OSCARS_OK;
   }
-  const auto it = c->bwd_fused_choice.find(std::array<int, 4>{g.M, g.K, g.N, replicas});
+  const auto it = c->bwd_fused_choice.find(
+      std::array<int, 5>{g.M, g.K, g.N, replicas, layer > 1 ? 1 : 0});
   *fused = it == c->bwd_fused_choice.end() ? -1 : (it->second > 0 ? 1 : 0);
   return OSCARS_OK;
 }
