@@ -104,6 +104,7 @@ __device__ __forceinline__ void dgrad_tap(const ConvArgs& a, int t, int& r, int&
 // dividing (step = dq D + dr, split once).
 struct KCursor {
   int q, r, D, dq, dr;
+  __device__ KCursor() = default;
   __device__ KCursor(int k0, int D_, int step = CK) : D(D_) {
     q = k0 / D;
     r = k0 - q * D;
@@ -122,14 +123,15 @@ struct KCursor {
 // The same for an output pixel k = (b Ho + i) Wo + j.
 struct PixCursor {
   int b, i, j, Ho, Wo, di, dj;
-  __device__ PixCursor(int k0, int Ho_, int Wo_) : Ho(Ho_), Wo(Wo_) {
+  __device__ PixCursor() = default;
+  __device__ PixCursor(int k0, int Ho_, int Wo_, int step = CK) : Ho(Ho_), Wo(Wo_) {
     const int hw = Ho * Wo;
     b = k0 / hw;
     const int p = k0 - b * hw;
     i = p / Wo;
     j = p - i * Wo;
-    di = CK / Wo;
-    dj = CK - di * Wo;
+    di = step / Wo;
+    dj = step - di * Wo;
   }
   __device__ __forceinline__ void next() {
     j += dj;
@@ -137,7 +139,7 @@ struct PixCursor {
     const bool w = j >= Wo;
     j = w ? j - Wo : j;
     i = w ? i + 1 : i;
-    while (i >= Ho) {  // once at most unless the image has fewer than CK / Wo + 1 rows
+    while (i >= Ho) {  // once at most unless the image has fewer than step / Wo + 1 rows
       i -= Ho;
       ++b;
     }
@@ -524,11 +526,13 @@ __host__ __device__ inline int dgrad_class_at(int i) { return i == 0 ? 3 : i == 
 // ConvLoader does, backward-weight gathers both operands along M and N
 // (WgradLoader), backward-data its weights along N (DgradWeightLoader);
 // otherwise ConvLoader's general gathers along K.
-template <int PASS, bool TR = false>
+template <int PASS, bool TR = false, int HALVES = 1>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   constexpr bool WG = PASS == CONV_WGRAD || PASS == FC_WGRAD;
-  __shared__ __attribute__((aligned(16))) float As[2][CK][CLD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][CK][CLD];
+  static_assert(HALVES == 1 || HALVES == 2, "K per step: CK or 2 CK");
+  constexpr int KS = HALVES * CK;  // K per step (one barrier)
+  __shared__ __attribute__((aligned(16))) float As[2][KS][CLD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][KS][CLD];
   int tile = blockIdx.x, split = 0;
   if constexpr (PASS == CONV_DGRAD) {
     if (a.stride == 2 && a.cls < 0) {
@@ -580,53 +584,72 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   typedef typename std::conditional<TRA, WgradLoader, ConvLoader<PASS>>::type Loader;
   const Loader ld(a, kend, m0 + lr, M, n0 + lrb, N, in, rows, dz, par + a.w_off);
   const DgradWeightLoader wl(a, kend, n0 + lrb, N, par + a.w_off);
-  // the vector loaders' K decode, stepped along with the loads (consecutive K steps)
-  KCursor ka(kbeg + lk, PASS == CONV_FWD ? a.C : a.Co), kb(kbeg + lkb, a.Co);
-  PixCursor pc(TRA ? kbeg + lk : 0, a.Ho > 0 ? a.Ho : 1, a.Wo > 0 ? a.Wo : 1);
-  float ra[2][4], rb[2][4];
+  // the vector loaders' K decode, stepped along with the loads (consecutive K
+  // steps; one cursor per half of a step)
+  const int kdiv = PASS == CONV_FWD ? a.C : a.Co;
+  const int ho = a.Ho > 0 ? a.Ho : 1, wo = a.Wo > 0 ? a.Wo : 1;
+  KCursor ka[HALVES] = {KCursor(kbeg + lk, kdiv, KS)};
+  KCursor kb[HALVES] = {KCursor(kbeg + lkb, a.Co, KS)};
+  PixCursor pc[HALVES] = {PixCursor(TRA ? kbeg + lk : 0, ho, wo, KS)};
+  if constexpr (HALVES == 2) {
+    ka[1] = KCursor(kbeg + CK + lk, kdiv, KS);
+    kb[1] = KCursor(kbeg + CK + lkb, a.Co, KS);
+    pc[1] = PixCursor(TRA ? kbeg + CK + lk : 0, ho, wo, KS);
+  }
+  float ra[2][HALVES][4], rb[2][HALVES][4];
   auto load = [&](int k0, auto P) {
     constexpr int p = decltype(P)::value;
-    if constexpr (TR && PASS == CONV_DGRAD) {
-      ld.dgrad_a_vec(k0 + lk, ka, ra[p]);
-      wl.fetch(k0 + lkb, kb, rb[p]);
-      ka.next();
-      kb.next();
-    } else if constexpr (TR && PASS == CONV_FWD) {
-      ld.fwd_vec(k0 + lk, ka, ra[p], rb[p]);
-      ka.next();
-    } else if constexpr (TRA) {
-      ld.fetch(k0 + lk, pc, ra[p], rb[p]);
-      pc.next();
-    } else {
-      ld.fetch(k0 + lk, ra[p], rb[p]);
+#pragma unroll
+    for (int q = 0; q < HALVES; ++q) {
+      const int kq = k0 + q * CK;
+      if constexpr (TR && PASS == CONV_DGRAD) {
+        ld.dgrad_a_vec(kq + lk, ka[q], ra[p][q]);
+        wl.fetch(kq + lkb, kb[q], rb[p][q]);
+        ka[q].next();
+        kb[q].next();
+      } else if constexpr (TR && PASS == CONV_FWD) {
+        ld.fwd_vec(kq + lk, ka[q], ra[p][q], rb[p][q]);
+        ka[q].next();
+      } else if constexpr (TRA) {
+        ld.fetch(kq + lk, pc[q], ra[p][q], rb[p][q]);
+        pc[q].next();
+      } else {
+        ld.fetch(kq + lk, ra[p][q], rb[p][q]);
+      }
     }
   };
   auto stash = [&](auto P) {
     constexpr int p = decltype(P)::value;  // register set p into LDS buffer p
-    if constexpr (TRA) {
-      *reinterpret_cast<f32x4*>(&As[p][lk][lr]) = f32x4{ra[p][0], ra[p][1], ra[p][2], ra[p][3]};
-    } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) As[p][lk + e][lr] = ra[p][e];
-    }
-    if constexpr (TRB) {
-      *reinterpret_cast<f32x4*>(&Bs[p][lkb][lrb]) = f32x4{rb[p][0], rb[p][1], rb[p][2], rb[p][3]};
-    } else {
+    for (int q = 0; q < HALVES; ++q) {
+      const int kq = q * CK;
+      if constexpr (TRA) {
+        *reinterpret_cast<f32x4*>(&As[p][kq + lk][lr]) =
+            f32x4{ra[p][q][0], ra[p][q][1], ra[p][q][2], ra[p][q][3]};
+      } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) Bs[p][lkb + e][lrb] = rb[p][e];
+        for (int e = 0; e < 4; ++e) As[p][kq + lk + e][lr] = ra[p][q][e];
+      }
+      if constexpr (TRB) {
+        *reinterpret_cast<f32x4*>(&Bs[p][kq + lkb][lrb]) =
+            f32x4{rb[p][q][0], rb[p][q][1], rb[p][q][2], rb[p][q][3]};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Bs[p][kq + lkb + e][lrb] = rb[p][q][e];
+      }
     }
   };
 
   f32x16 acc;
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-  const int nk = (kend - kbeg + CK - 1) / CK;
+  const int nk = (kend - kbeg + KS - 1) / KS;
   // Two register sets: step t + 2 is gathered while step t is multiplied and
   // step t + 1 (gathered a step earlier) goes into the other LDS buffer.
   // Gathers past kend read nothing and give zeros.
   load(kbeg, Pi<0>());
   stash(Pi<0>());
-  load(kbeg + CK, Pi<1>());
+  load(kbeg + KS, Pi<1>());
   __syncthreads();
   // a wave whose 32 x 32 block lies wholly past M or N (32-channel layers on
   // 64 x 64 tiles) skips its products and leaves the MFMA unit to the CU's
@@ -634,11 +657,11 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   const bool busy = m0 + wm * 32 < M && n0 + wn * 32 < N;
   auto step = [&](int t, auto P, auto MUL) {  // register set and LDS buffer p = t & 1
     constexpr int p = decltype(P)::value;
-    load(kbeg + (t + 2) * CK, P);
+    load(kbeg + (t + 2) * KS, P);
     // MFMA u contracts k = 2u (lanes 0-31) and 2u + 1 (lanes 32-63)
     if constexpr (decltype(MUL)::value) {
 #pragma unroll
-      for (int u = 0; u < CK / 2; ++u)
+      for (int u = 0; u < KS / 2; ++u)
         acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][wm * 32 + r],
                                                    Bs[p][2 * u + h][wn * 32 + r], acc, 0, 0, 0);
     }
@@ -1519,6 +1542,37 @@ __global__ __launch_bounds__(256) void conv_head_kernel(HeadArgs h) {
   }
 }
 
+int conv_cu_count() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      cus = v;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
+
+// Launches of at most two workgroups per CU (one or two replicas) take K
+// steps of 32 (one barrier per 16 MFMAs instead of 8): with one or two waves
+// per SIMD nothing else hides a step's fixed cost.  With the vector loaders
+// only (the general gathers spill with two halves).
+template <int PASS, bool TR>
+void launch_conv_gemm(const dim3& grid, hipStream_t s, const ConvArgs& a) {
+  const int64_t wgs = static_cast<int64_t>(grid.x) * grid.y;
+  const bool wide = wgs <= 2LL * conv_cu_count();
+  if constexpr (TR) {
+    if (wide) {
+      hipLaunchKernelGGL((conv_gemm_kernel<PASS, TR, 2>), grid, dim3(256), 0, s, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((conv_gemm_kernel<PASS, TR, 1>), grid, dim3(256), 0, s, a);
+}
+
 }  // namespace
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s) {
@@ -1555,11 +1609,9 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
     if (gx == 0) return hipSuccess;  // no pixels (extents of 1)
     if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (vector_loaders(a))
-      hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, true>),
-                         dim3(static_cast<unsigned>(gx), n_slots), dim3(256), 0, s, a);
+      launch_conv_gemm<CONV_DGRAD, true>(dim3(static_cast<unsigned>(gx), n_slots), s, a);
     else
-      hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, false>),
-                         dim3(static_cast<unsigned>(gx), n_slots), dim3(256), 0, s, a);
+      launch_conv_gemm<CONV_DGRAD, false>(dim3(static_cast<unsigned>(gx), n_slots), s, a);
     return hipGetLastError();
   }
   const Dims d = pass_dims(a, pass);
@@ -1634,25 +1686,25 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   switch (pass) {
     case CONV_FWD:
       if (vector_loaders(a))
-        hipLaunchKernelGGL((conv_gemm_kernel<CONV_FWD, true>), grid, block, 0, s, a);
+        launch_conv_gemm<CONV_FWD, true>(grid, s, a);
       else
-        hipLaunchKernelGGL((conv_gemm_kernel<CONV_FWD, false>), grid, block, 0, s, a);
+        launch_conv_gemm<CONV_FWD, false>(grid, s, a);
       break;
     case CONV_DGRAD:
       if (vector_loaders(a))
-        hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, true>), grid, block, 0, s, a);
+        launch_conv_gemm<CONV_DGRAD, true>(grid, s, a);
       else
-        hipLaunchKernelGGL((conv_gemm_kernel<CONV_DGRAD, false>), grid, block, 0, s, a);
+        launch_conv_gemm<CONV_DGRAD, false>(grid, s, a);
       break;
     case CONV_WGRAD:
       if (vector_loaders(a))
-        hipLaunchKernelGGL((conv_gemm_kernel<CONV_WGRAD, true>), grid, block, 0, s, a);
+        launch_conv_gemm<CONV_WGRAD, true>(grid, s, a);
       else
-        hipLaunchKernelGGL((conv_gemm_kernel<CONV_WGRAD, false>), grid, block, 0, s, a);
+        launch_conv_gemm<CONV_WGRAD, false>(grid, s, a);
       break;
-    case FC_FWD: hipLaunchKernelGGL(conv_gemm_kernel<FC_FWD>, grid, block, 0, s, a); break;
-    case FC_DGRAD: hipLaunchKernelGGL(conv_gemm_kernel<FC_DGRAD>, grid, block, 0, s, a); break;
-    case FC_WGRAD: hipLaunchKernelGGL(conv_gemm_kernel<FC_WGRAD>, grid, block, 0, s, a); break;
+    case FC_FWD: launch_conv_gemm<FC_FWD, false>(grid, s, a); break;
+    case FC_DGRAD: launch_conv_gemm<FC_DGRAD, false>(grid, s, a); break;
+    case FC_WGRAD: launch_conv_gemm<FC_WGRAD, false>(grid, s, a); break;
   }
   return hipGetLastError();
 }
