@@ -46,6 +46,24 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // A compile-time integer passed as an argument (static register indices).
 template <int U> struct Pi { static constexpr int value = U; };
 
+// Schedule of a K step with N MFMAs: each MFMA followed by a share of the
+// step's other work (its next operands' LDS reads, gather address
+// arithmetic, LDS stores, global loads), which then issues while the matrix
+// core runs.  Without it the compiler issued the MFMAs back to back and the
+// rest after them; with one or two waves per SIMD (one or two replicas)
+// nothing else hid that work.
+template <int N>
+__device__ __forceinline__ void interleave() {
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+    __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+  }
+}
+
 constexpr int CT = 64;       // tile rows and columns
 constexpr int CK = 16;       // K per step
 constexpr int CLD = CT + 4;  // LDS row pitch (floats)
@@ -266,13 +284,15 @@ struct ConvLoader {
   // weights; one 16-byte load each.
   __device__ __forceinline__ void fwd_a(int k, const KCursor& kc, float (&ra)[4]) const {
     const int rs = kc.q, c = kc.r, r = rs / 3, hi = ah + r, wi = aw + rs - 3 * r;
-    const bool aok = am && k < kend && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+    // bitwise: every term evaluated, no branch (the short-circuit form became
+    // exec-mask branches that split the K loop into blocks)
+    const bool aok = am & (k < kend) & (hi >= 0) & (hi < a.H) & (wi >= 0) & (wi < a.W);
     const f32x4 va =
         *reinterpret_cast<const f32x4*>(aok ? arow + (hi * a.W + wi) * a.C + c : k_conv_zero);
     for (int e = 0; e < 4; ++e) ra[e] = va[e];
   }
   __device__ __forceinline__ void fwd_b(int k, float (&rb)[4]) const {
-    const bool bok = bn && k < kend;
+    const bool bok = bn & (k < kend);
     const f32x4 vb = *reinterpret_cast<const f32x4*>(
         bok ? Wt + static_cast<int64_t>(bn_idx) * 9 * a.C + k : k_conv_zero);
     for (int e = 0; e < 4; ++e) rb[e] = vb[e];
@@ -289,7 +309,7 @@ struct ConvLoader {
     dgrad_tap_rs(t, r, sc);
     const int ti = ah - r, tj = aw - sc;
     const int i = a.stride == 2 ? ti >> 1 : ti, j = a.stride == 2 ? tj >> 1 : tj;
-    const bool ok = am && k < kend && ti >= 0 && tj >= 0 && i < a.Ho && j < a.Wo;
+    const bool ok = am & (k < kend) & (ti >= 0) & (tj >= 0) & (i < a.Ho) & (j < a.Wo);
     const f32x4 v =
         *reinterpret_cast<const f32x4*>(ok ? arow + (i * a.Wo + j) * a.Co + o : k_conv_zero);
     for (int e = 0; e < 4; ++e) ra[e] = v[e];
@@ -447,7 +467,7 @@ struct DgradWeightLoader {
     const int t = kc.q, o = kc.r;
     int r, sc;
     dgrad_tap(a, t, r, sc);
-    const bool ok = bn && k < kend;
+    const bool ok = bn & (k < kend);
     const f32x4 v = *reinterpret_cast<const f32x4*>(
         ok ? Wt + static_cast<int64_t>(o) * 9 * a.C + (3 * r + sc) * a.C + nq : k_conv_zero);
     for (int e = 0; e < 4; ++e) rb[e] = v[e];
@@ -493,7 +513,7 @@ struct WgradLoader {
     const f32x4 va = *reinterpret_cast<const f32x4*>(
         ok && arow_ok ? dz + static_cast<int64_t>(k) * a.Co + mq : k_conv_zero);
     const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
-    const bool tap_ok = ok && btap && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+    const bool tap_ok = ok & btap & (hi >= 0) & (hi < a.H) & (wi >= 0) & (wi < a.W);
     const float* img = rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
                             : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
     const f32x4 vb = *reinterpret_cast<const f32x4*>(
@@ -666,6 +686,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
                                                    Bs[p][2 * u + h][wn * 32 + r], acc, 0, 0, 0);
     }
     stash(Pi<p ^ 1>());
+    if constexpr (decltype(MUL)::value) interleave<KS / 2>();
     __syncthreads();
   };
   auto steps = [&](auto MUL) {
@@ -801,6 +822,7 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[buf][2 * u + h][wave * 32 + r],
                                                  Bs[buf][2 * u + h][r], acc, 0, 0, 0);
     if (t + 1 < nk) stash(buf ^ 1);
+    interleave<CK / 2>();
     __syncthreads();
   }
 
@@ -904,6 +926,7 @@ __global__ __launch_bounds__(256) void conv_fwd_narrow_kernel(ConvArgs a) {
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[p][2 * u + h][wave * 32 + r],
                                                  Bs[p][2 * u + h][r], acc, 0, 0, 0);
     stash(Pi<p ^ 1>());
+    interleave<CK / 2>();
     __syncthreads();
   };
   int t = 0;
@@ -988,6 +1011,7 @@ __global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
                                                    Bs[p][2 * u + h][wave * 32 + r], acc, 0, 0, 0);
     }
     stash(Pi<p ^ 1>());
+    if constexpr (decltype(MUL)::value) interleave<CK / 2>();
     __syncthreads();
   };
   auto steps = [&](auto MUL) {
