@@ -138,9 +138,11 @@ struct KCursor {
   }
 };
 
-// The same for an output pixel k = (b Ho + i) Wo + j.
+// The same for an output pixel k = (b Ho + i) Wo + j: a step of `step`
+// pixels is db whole images and a remainder of di rows and dj columns, so
+// that each coordinate wraps at most once per step (no loop, no branch).
 struct PixCursor {
-  int b, i, j, Ho, Wo, di, dj;
+  int b, i, j, Ho, Wo, db, di, dj;
   __device__ PixCursor() = default;
   __device__ PixCursor(int k0, int Ho_, int Wo_, int step = CK) : Ho(Ho_), Wo(Wo_) {
     const int hw = Ho * Wo;
@@ -148,19 +150,21 @@ struct PixCursor {
     const int p = k0 - b * hw;
     i = p / Wo;
     j = p - i * Wo;
-    di = step / Wo;
-    dj = step - di * Wo;
+    db = step / hw;
+    const int rest = step - db * hw;
+    di = rest / Wo;
+    dj = rest - di * Wo;
   }
   __device__ __forceinline__ void next() {
     j += dj;
     i += di;
-    const bool w = j >= Wo;
-    j = w ? j - Wo : j;
-    i = w ? i + 1 : i;
-    while (i >= Ho) {  // once at most unless the image has fewer than step / Wo + 1 rows
-      i -= Ho;
-      ++b;
-    }
+    b += db;
+    const bool wj = j >= Wo;
+    j = wj ? j - Wo : j;
+    i = wj ? i + 1 : i;
+    const bool wi = i >= Ho;
+    i = wi ? i - Ho : i;
+    b = wi ? b + 1 : b;
   }
 };
 
@@ -482,6 +486,7 @@ struct DgradWeightLoader {
 // both: one 16-byte load each.  With Cin a multiple of 4 a column group lies
 // inside one tap, or is the bias column's group (column 9 Cin: ones) or past
 // the end.
+template <bool GATHER>
 struct WgradLoader {
   const ConvArgs& a;
   int kend;
@@ -514,8 +519,14 @@ struct WgradLoader {
         ok && arow_ok ? dz + static_cast<int64_t>(k) * a.Co + mq : k_conv_zero);
     const int hi = a.stride * i + br - 1, wi = a.stride * j + bs - 1;
     const bool tap_ok = ok & btap & (hi >= 0) & (hi < a.H) & (wi >= 0) & (wi < a.W);
-    const float* img = rows ? in + static_cast<int64_t>(rows[b]) * a.in_ld
-                            : in + static_cast<int64_t>(b) * a.H * a.W * a.C;
+    // the gathered case is a template parameter: a branch on `rows` here made
+    // the compiler wait for every load in flight (the next steps' too) before
+    // each LDS store
+    const float* img;
+    if constexpr (GATHER)
+      img = in + static_cast<int64_t>(rows[b]) * a.in_ld;
+    else
+      img = in + static_cast<int64_t>(b) * a.H * a.W * a.C;
     const f32x4 vb = *reinterpret_cast<const f32x4*>(
         tap_ok ? img + (hi * a.W + wi) * a.C + bc : k_conv_zero);
     for (int e = 0; e < 4; ++e) {
@@ -546,7 +557,7 @@ __host__ __device__ inline int dgrad_class_at(int i) { return i == 0 ? 3 : i == 
 // ConvLoader does, backward-weight gathers both operands along M and N
 // (WgradLoader), backward-data its weights along N (DgradWeightLoader);
 // otherwise ConvLoader's general gathers along K.
-template <int PASS, bool TR = false, int HALVES = 1>
+template <int PASS, bool TR = false, int HALVES = 1, bool GATHER = false>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   constexpr bool WG = PASS == CONV_WGRAD || PASS == FC_WGRAD;
   static_assert(HALVES == 1 || HALVES == 2, "K per step: CK or 2 CK");
@@ -601,7 +612,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   const int lk = TRA ? tid >> 4 : (tid & 3) * 4;
   const int lrb = TRB ? 4 * (tid & 15) : tid >> 2;
   const int lkb = TRB ? tid >> 4 : (tid & 3) * 4;
-  typedef typename std::conditional<TRA, WgradLoader, ConvLoader<PASS>>::type Loader;
+  typedef typename std::conditional<TRA, WgradLoader<GATHER>, ConvLoader<PASS>>::type Loader;
   const Loader ld(a, kend, m0 + lr, M, n0 + lrb, N, in, rows, dz, par + a.w_off);
   const DgradWeightLoader wl(a, kend, n0 + lrb, N, par + a.w_off);
   // the vector loaders' K decode, stepped along with the loads (consecutive K
@@ -948,6 +959,7 @@ __global__ __launch_bounds__(256) void conv_fwd_narrow_kernel(ConvArgs a) {
   }
 }
 
+template <bool GATHER>
 __global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) float As[2][CK][NN + 4];
   __shared__ __attribute__((aligned(16))) float Bs[2][CK][NM + 4];
@@ -970,8 +982,9 @@ __global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
   // K lk; A rows 4 q .. 4 q + 3 (q below 8); B columns 4 q .. + 3 and 64 + 4 q .. + 3
   const int lk = tid >> 4, q = tid & 15;
   const bool aload = q < NN / 4;
-  const WgradLoader w0(a, kend, aload ? m0 + 4 * q : M, M, n0 + 4 * q, N, in, rows, dz, nullptr);
-  const WgradLoader w1(a, kend, M, M, n0 + 64 + 4 * q, N, in, rows, dz, nullptr);
+  const WgradLoader<GATHER> w0(a, kend, aload ? m0 + 4 * q : M, M, n0 + 4 * q, N, in, rows, dz,
+                              nullptr);
+  const WgradLoader<GATHER> w1(a, kend, M, M, n0 + 64 + 4 * q, N, in, rows, dz, nullptr);
   PixCursor pc(kbeg + lk, a.Ho, a.Wo);
   float ra[2][4], rb0[2][4], rb1[2][4];
   auto load = [&](int k0, auto P) {
@@ -1588,6 +1601,12 @@ template <int PASS, bool TR>
 void launch_conv_gemm(const dim3& grid, hipStream_t s, const ConvArgs& a) {
   const int64_t wgs = static_cast<int64_t>(grid.x) * grid.y;
   const bool wide = wgs <= 2LL * conv_cu_count();
+  if constexpr (PASS == CONV_WGRAD && TR) {
+    if (a.gather) {  // gathered dataset rows (a first layer with four or more channels)
+      hipLaunchKernelGGL((conv_gemm_kernel<PASS, TR, 1, true>), grid, dim3(256), 0, s, a);
+      return;
+    }
+  }
   if constexpr (TR) {
     if (wide) {
       hipLaunchKernelGGL((conv_gemm_kernel<PASS, TR, 2>), grid, dim3(256), 0, s, a);
@@ -1694,8 +1713,12 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
       return hipErrorInvalidValue;
     const int64_t gx = wgrad_narrow_tiles(a) * a.splits;
     if (gx > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(conv_wgrad_narrow_kernel, dim3(static_cast<unsigned>(gx), n_slots),
-                       dim3(256), 0, s, a);
+    if (a.gather)
+      hipLaunchKernelGGL(conv_wgrad_narrow_kernel<true>, dim3(static_cast<unsigned>(gx), n_slots),
+                         dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(conv_wgrad_narrow_kernel<false>, dim3(static_cast<unsigned>(gx), n_slots),
+                         dim3(256), 0, s, a);
     return hipGetLastError();
   }
   int64_t gx = ((d.M + CT - 1) / CT) * ((d.N + CT - 1) / CT);
