@@ -1201,13 +1201,16 @@ __device__ __forceinline__ void thin_stage(const ConvArgs& a, int z, int r0, int
       const int e = e0 + 256 * u;
       const int col = ec.r;
       const int64_t off = src_s[e < n_stage ? ec.q : 0];
-      const bool ok = e < n_stage && off >= 0 && col >= CIN && col < (a.W + 1) * CIN;
+      // bitwise: no branch, so that the eight loads stay in flight together
+      const bool ok = (e < n_stage) & (off >= 0) & (col >= CIN) & (col < (a.W + 1) * CIN);
       v[u] = *(ok ? in + off + (col - CIN) : k_conv_zero);  // staged column 0: padding
       ec.next();
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (e0 + 256 * u < n_stage) x_s[e0 + 256 * u] = v[u];
+    for (int u = 0; u < 8; ++u) {  // past the rows: the spare float after them
+      const int e = e0 + 256 * u;
+      x_s[e < n_stage ? e : n_stage] = v[u];
+    }
   }
   __syncthreads();
 }
@@ -1251,7 +1254,7 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
     const float* base = dz + (prow + 32 * jb + h) * M + l32;
 #pragma unroll
     for (int u = 0; u < UB; ++u)
-      av[qs][u] = *(mrow && 2 * u < jlim ? base + static_cast<int64_t>(2 * u) * M : k_conv_zero);
+      av[qs][u] = *((mrow & (2 * u < jlim)) ? base + static_cast<int64_t>(2 * u) * M : k_conv_zero);
   };
   auto mul = [&](int t, auto P) {
     constexpr int qs = decltype(P)::value;
@@ -1259,7 +1262,10 @@ __global__ __launch_bounds__(256) void conv_thin_wgrad_kernel(ConvArgs a) {
     const float* xrow = x_s + q * 3 * per_row + (STRIDE * (32 * jb + h)) * CIN + tap_off;
     float bv[UB];
 #pragma unroll
-    for (int u = 0; u < UB; ++u) bv[u] = ntap ? xrow[2 * STRIDE * CIN * u] : bconst;
+    for (int u = 0; u < UB; ++u) {
+      const float xv = xrow[2 * STRIDE * CIN * u];  // read by every lane (tap_off 0 past the taps)
+      bv[u] = ntap ? xv : bconst;
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u)
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[qs][u], bv[u], acc, 0, 0, 0);
@@ -1339,7 +1345,7 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_rows_kernel(ConvArgs a) {
     for (int e = 0; e < 16; ++e) {
       const int pj = 8 * (e >> 2) + 4 * h + (e & 3);
       const float v = acc[e] + bias;
-      if (pj < jlim && col_ok) orow[pj * a.Co] = v > 0.0f ? v : 0.0f;
+      if ((pj < jlim) & col_ok) orow[pj * a.Co] = v > 0.0f ? v : 0.0f;
     }
   }
 }
@@ -1662,7 +1668,8 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
   if (pass == CONV_FWD && thin_wgrad(a)) {
     const int R = thin_rows_per_range(a, THIN_FWD_PIXELS);
     const dim3 grid(static_cast<unsigned>((a.B * a.Ho + R - 1) / R), n_slots), block(256);
-    const size_t lds = static_cast<size_t>(thin_stage_floats(a, THIN_FWD_PIXELS)) * sizeof(float);
+    // staged rows and one spare float (the target of stores past the rows)
+    const size_t lds = static_cast<size_t>(thin_stage_floats(a, THIN_FWD_PIXELS) + 1) * sizeof(float);
     switch (2 * a.C + (a.stride == 2 ? 1 : 0)) {
       case 2: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<1, 1>), grid, block, lds, s, a); break;
       case 3: hipLaunchKernelGGL((conv_thin_fwd_rows_kernel<1, 2>), grid, block, lds, s, a); break;
@@ -1688,7 +1695,7 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
     const int R = thin_rows_per_range(a);
     if (a.k_per_split != R || a.splits != (a.B * a.Ho + R - 1) / R) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(a.splits), n_slots), block(256);
-    const size_t lds = static_cast<size_t>(thin_stage_floats(a)) * sizeof(float);
+    const size_t lds = static_cast<size_t>(thin_stage_floats(a) + 1) * sizeof(float);
     const int key = 2 * a.C + (a.stride == 2 ? 1 : 0);
     switch (key) {
       case 2: hipLaunchKernelGGL((conv_thin_wgrad_kernel<1, 1>), grid, block, lds, s, a); break;
