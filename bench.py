@@ -88,7 +88,7 @@ def head_fused(hw, c, classes):
     return hw * c + 2 * c + classes <= 12288
 
 
-def cnn_work(cfg, tau):
+def cnn_work(cfg, tau, fused_path=None):
     """Algorithmic FLOPs and bytes of one round of the convolutional workload
     (oscars_round), per kind: conv layers as implicit GEMMs (2 FLOPs per
     multiply-add of every kernel tap; bytes: input, weights and output once),
@@ -100,7 +100,7 @@ def cnn_work(cfg, tau):
     B = cfg.batch
     tau = np.asarray(tau)
     work = {k: [0.0, 0.0] for k in ("gemm_fwd", "gemm_dgrad", "gemm_wgrad_update", "softmax_ce",
-                                    "aggregate")}
+                                    "aggregate", "gemm_bwd_fused")}
     H, W, C = cfg.image
     geo = []
     skips = list(cfg.skips or [False] * len(cfg.conv)) + [False]
@@ -118,12 +118,19 @@ def cnn_work(cfg, tau):
             work["gemm_fwd"][0] += ns * 2.0 * macs
             # a shortcut layer also reads its block's input (the shape of its output)
             work["gemm_fwd"][1] += ns * (act_in + wts + act_out * (2 if skips[l] else 1))
+            # backward-data and backward-weight of conv layer l + 1 in one launch
+            # (fused_path, the library's choice: one or two replicas), booked as
+            # gemm_bwd_fused; the update stays with gemm_wgrad_update
+            pair = l > 0 and fused_path is not None and fused_path(l + 1, ns)
+            dk = "gemm_bwd_fused" if pair else "gemm_dgrad"
+            wk = "gemm_bwd_fused" if pair else "gemm_wgrad_update"
             if l > 0:
-                work["gemm_dgrad"][0] += ns * 2.0 * macs
+                work[dk][0] += ns * 2.0 * macs
                 # reads the mask too, and, below a shortcut, the shortcut's gradient
-                work["gemm_dgrad"][1] += ns * (act_out + wts + (3 if skips[l + 1] else 2) * act_in)
-            work["gemm_wgrad_update"][0] += ns * 2.0 * macs
-            work["gemm_wgrad_update"][1] += ns * (act_out + act_in + 2 * wts)
+                work[dk][1] += ns * (act_out + wts + (3 if skips[l + 1] else 2) * act_in)
+            work[wk][0] += ns * 2.0 * macs
+            work[wk][1] += ns * (act_out + act_in)
+            work["gemm_wgrad_update"][1] += ns * 2 * wts
         pooled, act, fc = B * C * 4, B * H * W * C * 4, (C * classes + classes) * 4
         if head_fused(H * W, C, classes):
             # one launch (booked as softmax_ce): the last activation read once, pooled,
@@ -457,7 +464,7 @@ def main():
         tau = tau_for(s)
         do_round(tau)
         samples_w += int(np.sum(tau)) * cfg.batch
-        for kname, (fl, by) in (cnn_work(cfg, tau) if cfg.is_cnn
+        for kname, (fl, by) in (cnn_work(cfg, tau, fused_path) if cfg.is_cnn
                                 else gemm_work(cfg, tau, fused_path)).items():
             a = work_w.setdefault(kname, [0.0, 0.0])
             a[0] += fl
@@ -480,7 +487,7 @@ def main():
             run.ctx.profile_begin([dom_kind])
         do_round(tau)
         if s == args.steps - 1:
-            work_tot = cnn_work(cfg, tau) if cfg.is_cnn else gemm_work(cfg, tau, fused_path)
+            work_tot = cnn_work(cfg, tau, fused_path) if cfg.is_cnn else gemm_work(cfg, tau, fused_path)
         samples += int(np.sum(tau)) * cfg.batch
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -513,12 +520,12 @@ def main():
     tau0 = np.asarray(tau_for(0))
     backward_mix = {f"l{l}": {str(ns): ("fused" if fused_path(l, ns) else "separate")
                               for ns in sorted({int((tau0 > j).sum()) for j in range(tau0.max())})}
-                    for l in range(1, len(cfg.dims))}
+                    for l in range(1, (len(cfg.conv) + 2) if cfg.is_cnn else len(cfg.dims))}
     mix = backward_mix if args.schedule == "grouped" else {"schedule": "replica"}
 
     def mix_bytes(m):  # the dominant kind's algorithmic bytes per round under mix m
         if cfg.is_cnn:
-            return cnn_work(cfg, tau0)[dom][1]
+            return cnn_work(cfg, tau0, fused_path)[dom][1]
         path = lambda l, ns: m.get(f"l{l}", {}).get(str(ns), "fused") == "fused"  # noqa: E731
         return gemm_work(cfg, tau0, path)[dom][1]
     roof["traffic"] = pmc_traffic(dom, args.workload, d["bytes_per_launch"], mix, mix_bytes)

@@ -434,11 +434,13 @@ oscars_status oscars_set_backward(oscars_ctx* ctx, int32_t mode);
  * oscars_round of this context with `replicas` active replicas (1..K) and
  * batch `batch` (1..max_batch): *fused = 1 for the fused launch of
  * backward-data (none for layer 1), backward-weight and update, 0 for the
- * separate launches (always for fp32 models, OSCARS_BACKWARD_SEPARATE,
+ * separate launches (always for fp32 MLPs, OSCARS_BACKWARD_SEPARATE,
  * batches above 256 and layers whose input width is not a multiple of 8),
  * -1 where OSCARS_BACKWARD_AUTO times configurations and has not timed that
- * one in this context yet.  Returns OSCARS_E_INVALID for an
- * argument out of range. */
+ * one in this context yet.  Convolutional contexts: 1 where backward-data
+ * and backward-weight of a conv layer (2..L-1, channel counts multiples of
+ * 4) share one launch (the updates follow in their own launch), else 0.
+ * Returns OSCARS_E_INVALID for an argument out of range. */
 oscars_status oscars_backward_path(const oscars_ctx* ctx, int32_t layer, int32_t batch,
                                    int32_t replicas, int32_t* fused);
 

@@ -59,6 +59,13 @@ struct ConvArgs {
 
 hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_t s);
 
+// CONV_DGRAD of d and CONV_WGRAD of w (the same layer; each as launch_conv
+// takes it) in one launch, where that applies: channel counts multiples of 4
+// and no gathered rows (conv_pair_fits; otherwise hipErrorInvalidValue and
+// nothing launched).
+bool conv_pair_fits(const ConvArgs& d, const ConvArgs& w, int n_slots);
+hipError_t launch_conv_pair(const ConvArgs& d, const ConvArgs& w, int n_slots, hipStream_t s);
+
 // Output pixels per weight-gradient range of the 64 x 64 conv tiles.
 constexpr int CONV_WGRAD_PIXELS = 256;
 

@@ -557,14 +557,17 @@ __host__ __device__ inline int dgrad_class_at(int i) { return i == 0 ? 3 : i == 
 // ConvLoader does, backward-weight gathers both operands along M and N
 // (WgradLoader), backward-data its weights along N (DgradWeightLoader);
 // otherwise ConvLoader's general gathers along K.
-template <int PASS, bool TR = false, int HALVES = 1, bool GATHER = false>
-__global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
+// One tile of the GEMM; `lds` holds 4 HALVES CK CLD floats (conv_gemm_kernel,
+// conv_bwd_pair_kernel).
+template <int PASS, bool TR, int HALVES, bool GATHER>
+__device__ __forceinline__ void conv_gemm_tile(ConvArgs a, int tile, float* lds) {
   constexpr bool WG = PASS == CONV_WGRAD || PASS == FC_WGRAD;
   static_assert(HALVES == 1 || HALVES == 2, "K per step: CK or 2 CK");
   constexpr int KS = HALVES * CK;  // K per step (one barrier)
-  __shared__ __attribute__((aligned(16))) float As[2][KS][CLD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][KS][CLD];
-  int tile = blockIdx.x, split = 0;
+  typedef float Stage[2][KS][CLD];
+  Stage& As = *reinterpret_cast<Stage*>(lds);
+  Stage& Bs = *reinterpret_cast<Stage*>(lds + 2 * KS * CLD);
+  int split = 0;
   if constexpr (PASS == CONV_DGRAD) {
     if (a.stride == 2 && a.cls < 0) {
       // all four parity classes in one launch: the workgroup's class and its
@@ -749,6 +752,12 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
 }
 
+template <int PASS, bool TR = false, int HALVES = 1, bool GATHER = false>
+__global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float lds[4 * HALVES * CK * CLD];
+  conv_gemm_tile<PASS, TR, HALVES, GATHER>(a, blockIdx.x, lds);
+}
+
 // ---------------------------------------------------------------------------
 // Backward-data with at most 32 input channels (a multiple of 4): 128 x 32
 // tiles, the four waves stacked along M, where a 64 x 64 tile would leave half
@@ -767,10 +776,12 @@ __host__ __device__ inline int64_t dgrad_narrow_tiles(const ConvArgs& a) {
   return ((d.M + NM - 1) / NM) * ((d.N + NN - 1) / NN);
 }
 
-__global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
-  __shared__ __attribute__((aligned(16))) float As[2][CK][NM + 4];
-  __shared__ __attribute__((aligned(16))) float Bs[2][CK][NN + 4];
-  int tile = blockIdx.x;
+// `lds` holds 2 CK (NM + NN + 8) floats.
+__device__ __forceinline__ void conv_dgrad_narrow_tile(ConvArgs a, int tile, float* lds) {
+  typedef float StageA[2][CK][NM + 4];
+  typedef float StageB[2][CK][NN + 4];
+  StageA& As = *reinterpret_cast<StageA*>(lds);
+  StageB& Bs = *reinterpret_cast<StageB*>(lds + 2 * CK * (NM + 4));
   if (a.stride == 2 && a.cls < 0) {
     int i = 0;
     for (; i < 4; ++i) {
@@ -848,6 +859,11 @@ __global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
     const float g = a.skip ? acc[i] + a.skip[z * a.skip_slot + at] : acc[i];
     a.out[z * a.out_slot + at] = a.mask[z * a.mask_slot + at] > 0.0f ? g : 0.0f;
   }
+}
+
+__global__ __launch_bounds__(256) void conv_dgrad_narrow_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float lds[2 * CK * (NM + NN + 8)];
+  conv_dgrad_narrow_tile(a, blockIdx.x, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -959,16 +975,18 @@ __global__ __launch_bounds__(256) void conv_fwd_narrow_kernel(ConvArgs a) {
   }
 }
 
+// `lds` holds 2 CK (NM + NN + 8) floats.
 template <bool GATHER>
-__global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
-  __shared__ __attribute__((aligned(16))) float As[2][CK][NN + 4];
-  __shared__ __attribute__((aligned(16))) float Bs[2][CK][NM + 4];
+__device__ __forceinline__ void conv_wgrad_narrow_tile(ConvArgs a, int tile, float* lds) {
+  typedef float StageA[2][CK][NN + 4];
+  typedef float StageB[2][CK][NM + 4];
+  StageA& As = *reinterpret_cast<StageA*>(lds);
+  StageB& Bs = *reinterpret_cast<StageB*>(lds + 2 * CK * (NN + 4));
   const Dims d = pass_dims(a, CONV_WGRAD);
   const int M = static_cast<int>(d.M), N = static_cast<int>(d.N), K = static_cast<int>(d.K);
   const int z = blockIdx.y;
   const int rep = a.order[z];
   const int gm = (M + NN - 1) / NN, gn = (N + NM - 1) / NM;
-  int tile = blockIdx.x;
   const int split = tile / (gm * gn);
   tile -= split * gm * gn;
   const int m0 = tile / gn * NN, n0 = (tile - tile / gn * gn) * NM;
@@ -1046,6 +1064,38 @@ __global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
     const int row = m0 + 8 * (i >> 2) + 4 * h + (i & 3);
     if (row >= M || col >= N) continue;
     a.part[z * a.part_slot + (static_cast<int64_t>(split) * M + row) * N + col] = acc[i];
+  }
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(256) void conv_wgrad_narrow_kernel(ConvArgs a) {
+  __shared__ __attribute__((aligned(16))) float lds[2 * CK * (NM + NN + 8)];
+  conv_wgrad_narrow_tile<GATHER>(a, blockIdx.x, lds);
+}
+
+// Backward-data and backward-weight of one layer in one launch: the first nd
+// workgroups take backward-data tiles, the others backward-weight tiles.  The
+// two read the layer's output gradient and nothing that the other writes;
+// with one or two replicas either launch alone leaves most of every CU idle,
+// and with more the two kinds of tiles share the CUs better than in turn.
+// DN / WN: the 128 x 32 backward-data / 32 x 128 backward-weight tiles, else
+// the 64 x 64 ones (vector loaders, K steps of CK).
+template <bool DN, bool WN>
+__global__ __launch_bounds__(256) void conv_bwd_pair_kernel(ConvArgs d, ConvArgs w, int nd) {
+  constexpr int DF = DN ? 2 * CK * (NM + NN + 8) : 4 * CK * CLD;
+  constexpr int WF = WN ? 2 * CK * (NM + NN + 8) : 4 * CK * CLD;
+  __shared__ __attribute__((aligned(16))) float lds[DF > WF ? DF : WF];
+  const int b = blockIdx.x;
+  if (b < nd) {
+    if constexpr (DN)
+      conv_dgrad_narrow_tile(d, b, lds);
+    else
+      conv_gemm_tile<CONV_DGRAD, true, 1, false>(d, b, lds);
+  } else {
+    if constexpr (WN)
+      conv_wgrad_narrow_tile<false>(w, b - nd, lds);
+    else
+      conv_gemm_tile<CONV_WGRAD, true, 1, false>(w, b - nd, lds);
   }
 }
 
@@ -1760,6 +1810,65 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
     case FC_DGRAD: launch_conv_gemm<FC_DGRAD, false>(grid, s, a); break;
     case FC_WGRAD: launch_conv_gemm<FC_WGRAD, false>(grid, s, a); break;
   }
+  return hipGetLastError();
+}
+
+namespace {
+// Tiles of the two launches conv_bwd_pair_kernel joins, or false where it
+// does not apply (channel counts for the vector loaders, no gathered rows).
+// Joined at every replica count: on C6 / C7 rounds 2.65 / 14.4 ms against
+// 2.67 / 14.6 with the pair only up to twelve workgroups per CU, and 2.75 /
+// 15.2 ms with two launches everywhere.
+bool conv_pair_plan(const ConvArgs& d, const ConvArgs& w, int n_slots, bool* dn, bool* wn,
+                    int64_t* nd, int64_t* nw) {
+  if (n_slots < 1 || !vector_loaders(d) || !vector_loaders(w) || d.gather || w.gather ||
+      thin_layer(w) || d.B < 1 || d.cls > 3 || (d.stride == 2 && d.cls < -1) || w.splits < 1 ||
+      w.k_per_split < 1)
+    return false;
+  const Dims dw = pass_dims(w, CONV_WGRAD);
+  if (static_cast<int64_t>(w.splits) * w.k_per_split < dw.K) return false;
+  *dn = dgrad_narrow(d);
+  int64_t t = 0;
+  const bool all = d.stride == 2 && d.cls < 0;
+  for (int i = 0; i < (all ? 4 : 1); ++i) {
+    ConvArgs ac = d;
+    if (all) ac.cls = i;
+    if (*dn) {
+      t += dgrad_narrow_tiles(ac);
+    } else if (d.stride == 2) {
+      t += dgrad_class_tiles(ac, ac.cls);
+    } else {
+      const Dims dd = pass_dims(ac, CONV_DGRAD);
+      t += ((dd.M + CT - 1) / CT) * ((dd.N + CT - 1) / CT);
+    }
+  }
+  *nd = t;
+  *wn = conv_narrow(w);
+  *nw = (*wn ? wgrad_narrow_tiles(w) : ((dw.M + CT - 1) / CT) * ((dw.N + CT - 1) / CT)) * w.splits;
+  return *nd > 0 && *nw > 0 && *nd + *nw <= 0x7FFFFFFF;
+}
+}  // namespace
+
+bool conv_pair_fits(const ConvArgs& d, const ConvArgs& w, int n_slots) {
+  bool dn, wn;
+  int64_t nd, nw;
+  return conv_pair_plan(d, w, n_slots, &dn, &wn, &nd, &nw);
+}
+
+hipError_t launch_conv_pair(const ConvArgs& d, const ConvArgs& w, int n_slots, hipStream_t s) {
+  bool dn, wn;
+  int64_t nd, nw;
+  if (!conv_pair_plan(d, w, n_slots, &dn, &wn, &nd, &nw)) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(nd + nw), n_slots), block(256);
+  const int ndi = static_cast<int>(nd);
+  if (dn && wn)
+    hipLaunchKernelGGL((conv_bwd_pair_kernel<true, true>), grid, block, 0, s, d, w, ndi);
+  else if (dn)
+    hipLaunchKernelGGL((conv_bwd_pair_kernel<true, false>), grid, block, 0, s, d, w, ndi);
+  else if (wn)
+    hipLaunchKernelGGL((conv_bwd_pair_kernel<false, true>), grid, block, 0, s, d, w, ndi);
+  else
+    hipLaunchKernelGGL((conv_bwd_pair_kernel<false, false>), grid, block, 0, s, d, w, ndi);
   return hipGetLastError();
 }
 

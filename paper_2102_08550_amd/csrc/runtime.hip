@@ -727,20 +727,18 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
     ConvArgs a = conv_layer_args(c, l, master_in, master_in_slot, order, B);
     a.dout = c->cdz[l];
     a.dout_slot = c->cnn_slot(l);
+    ConvArgs ad = a;  // backward-data (l > 1)
     if (l > 1) {
-      a.out = c->cdz[l - 1];
-      a.out_slot = c->cnn_slot(l - 1);
-      a.mask = c->cact[l - 1];
-      a.mask_slot = c->cnn_slot(l - 1);
+      ad.out = c->cdz[l - 1];
+      ad.out_slot = c->cnn_slot(l - 1);
+      ad.mask = c->cact[l - 1];
+      ad.mask_slot = c->cnn_slot(l - 1);
       if (c->conv_skip[l + 1]) {  // layer l + 1 adds this layer's input: its Z gradient too
-        a.skip = c->cdz[l + 1];
-        a.skip_slot = c->cnn_slot(l + 1);
+        ad.skip = c->cdz[l + 1];
+        ad.skip_slot = c->cnn_slot(l + 1);
       }
       // stride 2: the four parity classes of the input pixels in one launch
-      a.cls = -1;
-      e = timed(c, OSCARS_KERNEL_DGRAD, [&] { return launch_conv(a, CONV_DGRAD, ns, c->stream); });
-      if (e != hipSuccess) break;
-      a.skip = nullptr;
+      ad.cls = -1;
       a.in = c->cact[l - 1];
       a.in_slot = c->cnn_slot(l - 1);
     } else {
@@ -752,7 +750,18 @@ hipError_t cnn_backward(oscars_ctx* c, float* replicas, const float* master_in,
     conv_wgrad_ranges(a, &a.splits, &a.k_per_split);
     a.part = c->cpart_l[l];
     a.part_slot = c->cpart_slot_l[l];
-    e = timed(c, OSCARS_KERNEL_WGRAD, [&] { return launch_conv(a, CONV_WGRAD, ns, c->stream); });
+    if (l > 1 && conv_pair_fits(ad, a, ns)) {
+      // one or two replicas: backward-data and backward-weight in one launch
+      e = timed(c, OSCARS_KERNEL_BWD_FUSED,
+                [&] { return launch_conv_pair(ad, a, ns, c->stream); });
+    } else {
+      if (l > 1) {
+        e = timed(c, OSCARS_KERNEL_DGRAD,
+                  [&] { return launch_conv(ad, CONV_DGRAD, ns, c->stream); });
+        if (e != hipSuccess) break;
+      }
+      e = timed(c, OSCARS_KERNEL_WGRAD, [&] { return launch_conv(a, CONV_WGRAD, ns, c->stream); });
+    }
     UpdateBlock u{};
     u.part = a.part;
     u.part_slot = a.part_slot;
@@ -1458,6 +1467,16 @@ oscars_status oscars_backward_path(const oscars_ctx* c, int32_t layer, int32_t b
       replicas < 1 || replicas > c->K)
     return OSCARS_E_INVALID;
   *fused = 0;
+  if (c->cnn) {
+    // conv layers 2 .. L - 1: backward-data and backward-weight in one launch
+    if (layer < 2 || layer >= c->L) return OSCARS_OK;
+    ConvArgs a = conv_layer_args(c, layer, nullptr, 0, nullptr, batch);
+    ConvArgs ad = a;
+    ad.cls = -1;
+    conv_wgrad_ranges(a, &a.splits, &a.k_per_split);
+    *fused = conv_pair_fits(ad, a, replicas) ? 1 : 0;
+    return OSCARS_OK;
+  }
   if (!c->bf16 || !backward_fused_enabled(c->backward_mode)) return OSCARS_OK;
   GemmArgs g{};
   g.M = c->dims[layer - 1];
