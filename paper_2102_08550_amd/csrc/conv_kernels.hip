@@ -1198,7 +1198,7 @@ __global__ __launch_bounds__(256) void conv_thin_fwd_kernel(ConvArgs a) {
 // waves' sums are added in wave order.
 constexpr int THIN_WG_PIXELS = 512;   // a range's pixel slots (rows x padded width) at most
 // The forward's workgroups take the same ranges (ranges of 128 or 256 pixel
-// slots, more workgroups, ran the C6 layer 1 slower over a round).
+// slots, more workgroups, ran the first layer of a 32 x 32 x 3 network slower over a round).
 constexpr int THIN_FWD_PIXELS = THIN_WG_PIXELS;
 constexpr int THIN_STAGE_MAX = 11264;  // staged floats at most (44 KB, with red: under 64 KB)
 
@@ -1816,9 +1816,10 @@ hipError_t launch_conv(const ConvArgs& a, ConvPass pass, int n_slots, hipStream_
 namespace {
 // Tiles of the two launches conv_bwd_pair_kernel joins, or false where it
 // does not apply (channel counts for the vector loaders, no gathered rows).
-// Joined at every replica count: on C6 / C7 rounds 2.65 / 14.4 ms against
-// 2.67 / 14.6 with the pair only up to twelve workgroups per CU, and 2.75 /
-// 15.2 ms with two launches everywhere.
+// Joined at every replica count: on the CIFAR-shaped networks of 3 and 9
+// conv layers (K = 8) a round took 2.65 / 14.4 ms, against 2.67 / 14.6 ms with
+// the pair only up to twelve workgroups per CU and 2.75 / 15.2 ms with two
+// launches everywhere.
 bool conv_pair_plan(const ConvArgs& d, const ConvArgs& w, int n_slots, bool* dn, bool* wn,
                     int64_t* nd, int64_t* nw) {
   if (n_slots < 1 || !vector_loaders(d) || !vector_loaders(w) || d.gather || w.gather ||
