@@ -80,6 +80,11 @@ TRAJ = {
     # a residual block of 40 channels (backward-data on 64 x 64 tiles)
     "res-wide": _cfg("cnn-res-wide", (6, 5, 4), ((40, 1), (36, 1), (40, 1, 1)), K=2, n_rows=60,
                      batch=5, tau=(2, 3), rounds=2, seed=50),
+    # channel counts that are not multiples of 4 after layer 1 (6, 10, 7):
+    # every pass on the general gathers, backward-data and backward-weight as
+    # two launches, stride-2 backward-data on them
+    "odd-ch": _cfg("cnn-odd-ch", (9, 8, 3), ((6, 1), (10, 2), (7, 1)), K=3, n_rows=90, batch=5,
+                   tau=(2, 1, 3), rounds=2, seed=51),
     # the full workload's layers on 16 x 16 images, batch 64 (pixels per
     # weight-gradient range: several ranges per layer)
     "c6s": workload.scaled(workload.C6, image=(16, 16, 3), dims=(768, 10), n_rows=3000, batch=64,
