@@ -590,24 +590,35 @@ gemm_kernel(GemmArgs g) {
     tB[0].store(lds_b(0), tid);
     __syncthreads();
     static_assert(!TOTAL || TPC % ST == 0, "chunks start on register set 0");
-    for (int j0 = 0; j0 < nk;) {
-      const int jend = chunk_end(j0, nk);
+    auto tile_step = [&](int j, auto uc) {
+      constexpr int u = decltype(uc)::value;
+      LOAD_A(tA[u], kbeg + (j + ST) * BK);
+      LOAD_B(tB[u], kbeg + (j + ST) * BK);
+      compute(j & 1);
+      fold(j, nk);
+      tA[(u + 1) % ST].store(lds_a((j + 1) & 1), tid);
+      tB[(u + 1) % ST].store(lds_b((j + 1) & 1), tid);
+      __syncthreads();
+    };
+    // Whole groups of ST tiles in the loops (no exit between the tiles of a
+    // group, so every path into the loop header has the same loads in
+    // flight: with an exit after any tile the compiler waited for every load
+    // at the header, halving the prefetch distance); a last tile of K that
+    // does not fill a group comes after.
+    static_assert(ST == 2, "two register sets");
+    const int nkg = nk - nk % ST;
+    for (int j0 = 0; j0 < nkg;) {
+      const int jc = chunk_end(j0, nk), jend = jc < nkg ? jc : nkg;
       for (int kt = j0; kt < jend; kt += ST) {
-#pragma unroll
-        for (int u = 0; u < ST; ++u) {
-          const int j = kt + u;
-          if (j >= jend) break;
-          LOAD_A(tA[u], kbeg + (j + ST) * BK);
-          LOAD_B(tB[u], kbeg + (j + ST) * BK);
-          compute(j & 1);
-          fold(j, nk);
-          tA[(u + 1) % ST].store(lds_a((j + 1) & 1), tid);
-          tB[(u + 1) % ST].store(lds_b((j + 1) & 1), tid);
-          __syncthreads();
-        }
+        tile_step(kt, Ic<0>());
+        tile_step(kt + 1, Ic<1>());
       }
-      fold_chunk(jend <= TPC);
+      if (jend == jc) fold_chunk(jend <= TPC);
       j0 = jend;
+    }
+    if (nkg < nk) {
+      tile_step(nkg, Ic<0>());
+      fold_chunk(nk <= TPC);
     }
   }
 #undef LOAD_A
